@@ -1,0 +1,8 @@
+"""MI355X-native fp32 convolution training passes (forward, backward-data,
+backward-weight) behind a C ABI (include/miconv.h), with a thin ctypes
+binding.  The library is loaded on first use; see ``miconv.lib``."""
+from .miconv import (MiconvError, conv_bwd_data, conv_bwd_weight, conv_fwd, lib,
+                     output_size, workspace_size, PASS_FWD, PASS_BWD_DATA, PASS_BWD_WEIGHT)
+
+__all__ = ["MiconvError", "conv_fwd", "conv_bwd_data", "conv_bwd_weight", "lib",
+           "output_size", "workspace_size", "PASS_FWD", "PASS_BWD_DATA", "PASS_BWD_WEIGHT"]

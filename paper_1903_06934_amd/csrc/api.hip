@@ -1,0 +1,474 @@
+// C ABI of the convolution library (declared in include/miconv.h): argument
+// validation, output geometry, workspace layout, kernel selection and
+// launches on the caller's stream.
+#include <atomic>
+#include <stddef.h>
+#include <stdint.h>
+#include <string.h>
+
+#include "../../include/miconv.h"
+#include "internal.h"
+
+namespace miconv {
+
+FastDiv make_fastdiv(uint32_t d)
+{
+    uint32_t s = 0;
+    while ((1ull << s) < d)
+        s++;
+    uint64_t m = ((1ull << 32) * ((1ull << s) - d)) / d + 1;
+    FastDiv f;
+    f.mul = (uint32_t)m;
+    f.shift = s;
+    f.d = d;
+    return f;
+}
+
+namespace {
+
+constexpr long long kMaxElems = 2147483647LL;  // 2^31 - 1
+constexpr size_t kAlign = 256;                  // sub-buffer alignment inside ws
+constexpr int kBK = 16;                         // reduction slice of every GEMM kernel
+constexpr int kTargetWorkgroups = 1024;         // 4 per CU on 256 CUs
+
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+struct Geom {
+    int N, C, H, W, K, R, S, st, pad, G, P, Q, Cg, Kg;
+};
+
+int out_extent(int in, int filt, int stride, int pad)
+{
+    long long span = (long long)in + 2LL * pad - filt;
+    if (span < 0)
+        return 0;
+    long long o = span / stride + 1;
+    return o > kMaxElems ? 0 : (int)o;
+}
+
+int make_geom(int N, int C, int H, int W, int K, int R, int S, int stride, int pad, int group,
+              Geom *g)
+{
+    if (N < 1 || C < 1 || H < 1 || W < 1 || K < 1 || R < 1 || S < 1 || stride < 1 || pad < 0 ||
+        group < 1)
+        return MICONV_ERR_SHAPE;
+    if (C % group || K % group)
+        return MICONV_ERR_SHAPE;
+    // Spatial extents are kept below 2^15 so that packed (r, s) and
+    // per-axis coordinates fit the kernels' 16-bit fields.
+    if (H > 32767 || W > 32767 || R > 32767 || S > 32767 || pad > 32767)
+        return MICONV_ERR_SHAPE;
+    // Groups index the third grid dimension.
+    if (group > 65535)
+        return MICONV_ERR_SHAPE;
+    int P = out_extent(H, R, stride, pad), Q = out_extent(W, S, stride, pad);
+    if (P < 1 || Q < 1)
+        return MICONV_ERR_SHAPE;
+    long long nx = (long long)N * C * H * W, ny = (long long)N * K * P * Q;
+    long long nw = (long long)K * (C / group) * R * S;
+    if (nx > kMaxElems || ny > kMaxElems || nw > kMaxElems)
+        return MICONV_ERR_SHAPE;
+    *g = Geom{N, C, H, W, K, R, S, stride, pad, group, P, Q, C / group, K / group};
+    return MICONV_OK;
+}
+
+struct Range {
+    const void *p;
+    size_t bytes;
+    bool written;
+};
+
+bool overlap(const Range &a, const Range &b)
+{
+    if (!a.p || !b.p || !a.bytes || !b.bytes)
+        return false;
+    uintptr_t a0 = (uintptr_t)a.p, b0 = (uintptr_t)b.p;
+    return a0 < b0 + b.bytes && b0 < a0 + a.bytes;
+}
+
+// Null, alignment, workspace and aliasing checks, in that order.
+int check_buffers(const Range *r, int n, const bool *required, const void *ws, size_t ws_bytes,
+                  size_t ws_need)
+{
+    for (int i = 0; i < n; i++)
+        if (required[i] && !r[i].p)
+            return MICONV_ERR_NULL;
+    for (int i = 0; i < n; i++)
+        if (r[i].p && ((uintptr_t)r[i].p % 16))
+            return MICONV_ERR_ALIGN;
+    if (ws_need) {
+        if (!ws || ws_bytes < ws_need)
+            return MICONV_ERR_WORKSPACE;
+        if ((uintptr_t)ws % 16)
+            return MICONV_ERR_ALIGN;
+    }
+    Range all[8];
+    int m = 0;
+    for (int i = 0; i < n; i++)
+        all[m++] = r[i];
+    if (ws_need)
+        all[m++] = Range{ws, ws_need, true};
+    for (int i = 0; i < m; i++)
+        for (int j = i + 1; j < m; j++)
+            if ((all[i].written || all[j].written) && overlap(all[i], all[j]))
+                return MICONV_ERR_ALIAS;
+    return MICONV_OK;
+}
+
+int check_device()
+{
+    static std::atomic<int> cache[64];  // 0 unknown, 1 gfx950, 2 other
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0)
+        return MICONV_ERR_DEVICE;
+    if (dev < 64) {
+        int c = cache[dev].load(std::memory_order_relaxed);
+        if (c)
+            return c == 1 ? MICONV_OK : MICONV_ERR_DEVICE;
+    }
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, dev) != hipSuccess)
+        return MICONV_ERR_DEVICE;
+    bool ok = strncmp(prop.gcnArchName, "gfx950", 6) == 0;
+    if (dev < 64)
+        cache[dev].store(ok ? 1 : 2, std::memory_order_relaxed);
+    return ok ? MICONV_OK : MICONV_ERR_DEVICE;
+}
+
+// ------------------------------------------------------------ kernel choice
+int gemm_tiles(int M, int Ncol, int bm, int bn)
+{
+    return ((M + bm - 1) / bm) * ((Ncol + bn - 1) / bn);
+}
+
+// Larger tiles reuse each loaded element more; fall back to 64x64 when the
+// large tiling would leave the chip short of workgroups.
+int pick_img_tile(int M, long long Ncol, int G)
+{
+    if (M > 64 && (long long)gemm_tiles(M, (int)Ncol, 128, 128) * G >= 2 * 256)
+        return TILE_128x128;
+    return TILE_64x64;
+}
+
+// ------------------------------------------------------------ fwd plan
+size_t fwd_ws(const Geom &g) { return align_up((size_t)g.K * g.Cg * g.R * g.S * sizeof(float)); }
+
+// ------------------------------------------------------------ bwd-data plan
+// Stride phase (ph, pw): input pixels h = ph + st*i, w = pw + st*j; the taps
+// that reach them are r = r0 + st*rr (rr < nr), s = s0 + st*ss (ss < ns),
+// with r0 = (ph + pad) mod st, and p = i + dh - rr where dh = (ph + pad - r0) / st.
+struct Axis {
+    int n;   // pixels of the phase along the axis
+    int t0;  // first tap
+    int nt;  // taps
+    int d;   // offset dh / dw
+};
+
+Axis phase_axis(int in, int filt, int st, int pad, int ph)
+{
+    Axis a;
+    a.n = ph < in ? (in - ph + st - 1) / st : 0;
+    a.t0 = (ph + pad) % st;
+    a.nt = a.t0 < filt ? (filt - a.t0 + st - 1) / st : 0;
+    a.d = (ph + pad - a.t0) / st;
+    return a;
+}
+
+size_t bwd_data_ws(const Geom &g)
+{
+    size_t total = 0;
+    for (int ph = 0; ph < g.st; ph++)
+        for (int pw = 0; pw < g.st; pw++) {
+            Axis ah = phase_axis(g.H, g.R, g.st, g.pad, ph);
+            Axis aw = phase_axis(g.W, g.S, g.st, g.pad, pw);
+            total += align_up((size_t)g.K * g.Cg * ah.nt * aw.nt * sizeof(float));
+        }
+    return total;
+}
+
+// ------------------------------------------------------------ bwd-weight plan
+struct WgradPlan {
+    int tile, nsplit, chunk, bias_chunks;
+    size_t part_bytes, bias_bytes;
+};
+
+WgradPlan wgrad_plan(const Geom &g)
+{
+    WgradPlan p;
+    int M = g.Kg, Ncol = g.Cg * g.R * g.S;
+    long long Kred = (long long)g.N * g.P * g.Q;
+    p.tile = (M > 64 && Ncol > 64) ? TILE_128x128 : TILE_64x64;
+    int bm = p.tile == TILE_128x128 ? 128 : 64;
+    long long tiles = (long long)gemm_tiles(M, Ncol, bm, bm) * g.G;
+    long long ns = (kTargetWorkgroups + tiles - 1) / tiles;
+    long long max_ns = Kred / (kBK * 8);
+    if (ns > max_ns)
+        ns = max_ns;
+    if (ns < 1)
+        ns = 1;
+    long long chunk = (Kred + ns - 1) / ns;
+    chunk = (chunk + kBK - 1) / kBK * kBK;
+    p.chunk = (int)chunk;
+    p.nsplit = (int)((Kred + chunk - 1) / chunk);
+    p.part_bytes = p.nsplit > 1 ? align_up((size_t)p.nsplit * g.K * Ncol * sizeof(float)) : 0;
+    long long bc = (1024 + g.K - 1) / g.K;
+    long long bmax = (Kred + 4095) / 4096;
+    if (bc > bmax)
+        bc = bmax;
+    if (bc < 1)
+        bc = 1;
+    p.bias_chunks = (int)bc;
+    p.bias_bytes = align_up((size_t)g.K * bc * sizeof(float));
+    return p;
+}
+
+int launch_status(hipError_t e) { return e == hipSuccess ? MICONV_OK : MICONV_ERR_LAUNCH; }
+
+}  // namespace
+}  // namespace miconv
+
+using namespace miconv;
+
+extern "C" {
+
+int conv_output_size(int H, int W, int R, int S, int stride, int pad, int *P, int *Q)
+{
+    if (!P || !Q)
+        return MICONV_ERR_NULL;
+    if (H < 1 || W < 1 || R < 1 || S < 1 || stride < 1 || pad < 0)
+        return MICONV_ERR_SHAPE;
+    int p = out_extent(H, R, stride, pad), q = out_extent(W, S, stride, pad);
+    if (p < 1 || q < 1)
+        return MICONV_ERR_SHAPE;
+    *P = p;
+    *Q = q;
+    return MICONV_OK;
+}
+
+size_t conv_workspace_size(int pass, int N, int C, int H, int W, int K, int R, int S,
+                           int stride, int pad, int group)
+{
+    Geom g;
+    if (make_geom(N, C, H, W, K, R, S, stride, pad, group, &g) != MICONV_OK)
+        return 0;
+    switch (pass) {
+    case MICONV_PASS_FWD:
+        return fwd_ws(g);
+    case MICONV_PASS_BWD_DATA:
+        return bwd_data_ws(g);
+    case MICONV_PASS_BWD_WEIGHT: {
+        WgradPlan p = wgrad_plan(g);
+        return p.part_bytes + p.bias_bytes;
+    }
+    default:
+        return 0;
+    }
+}
+
+const char *conv_error_string(int status)
+{
+    switch (status) {
+    case MICONV_OK: return "success";
+    case MICONV_ERR_SHAPE: return "invalid shape, stride, padding or group";
+    case MICONV_ERR_NULL: return "a required pointer is NULL";
+    case MICONV_ERR_WORKSPACE: return "workspace missing or smaller than conv_workspace_size()";
+    case MICONV_ERR_ALIAS: return "an output overlaps an input, another output or the workspace";
+    case MICONV_ERR_ALIGN: return "a tensor or workspace pointer is not 16-byte aligned";
+    case MICONV_ERR_DEVICE: return "no current HIP device, or it is not gfx950";
+    case MICONV_ERR_LAUNCH: return "kernel launch failed";
+    case MICONV_ERR_PASS: return "unknown pass id";
+    default: return "unknown status";
+    }
+}
+
+int conv_fwd(int N, int C, int H, int W, int K, int R, int S, int stride, int pad, int group,
+             const float *x, const float *w, const float *b, float *y, void *ws, size_t ws_bytes,
+             hipStream_t stream)
+{
+    Geom g;
+    int st = make_geom(N, C, H, W, K, R, S, stride, pad, group, &g);
+    if (st != MICONV_OK)
+        return st;
+    const size_t fb = sizeof(float);
+    Range r[4] = {{x, (size_t)N * C * H * W * fb, false},
+                  {w, (size_t)K * g.Cg * R * S * fb, false},
+                  {b, (size_t)K * fb, false},
+                  {y, (size_t)N * K * g.P * g.Q * fb, true}};
+    bool req[4] = {true, true, false, true};
+    size_t need = fwd_ws(g);
+    if ((st = check_buffers(r, 4, req, ws, ws_bytes, need)) != MICONV_OK)
+        return st;
+    if ((st = check_device()) != MICONV_OK)
+        return st;
+    (void)hipGetLastError();
+
+    float *wp = (float *)ws;
+    hipError_t e = launch_pack_fwd(w, wp, K, g.Cg, R, S, group, stream);
+    if (e != hipSuccess)
+        return MICONV_ERR_LAUNCH;
+
+    ImgGemmArgs a;
+    a.M = g.Kg;
+    a.Ncol = N * g.P * g.Q;
+    a.Kred = g.Cg * R * S;
+    a.A = wp;
+    a.a_gstride = (long long)a.Kred * a.M;
+    a.src = x;
+    a.cin = g.Cg;
+    a.src_h = H;
+    a.src_w = W;
+    a.src_hw = H * W;
+    a.src_img_stride = (long long)C * H * W;
+    a.col_hw = make_fastdiv(g.P * g.Q);
+    a.col_w = make_fastdiv(g.Q);
+    a.cstep = stride;
+    a.coff_h = -pad;
+    a.coff_w = -pad;
+    a.tsign = 1;
+    a.k_cin = make_fastdiv(g.Cg);
+    a.k_tw = make_fastdiv(S);
+    a.out = y;
+    a.bias = b;
+    a.out_img_stride = (long long)K * g.P * g.Q;
+    a.out_hw = g.P * g.Q;
+    a.out_w = g.Q;
+    a.ostep = 1;
+    a.ooff_h = 0;
+    a.ooff_w = 0;
+    int tile = pick_img_tile(a.M, a.Ncol, group);
+    bool fast = g.Cg % kBK == 0;
+    return launch_status(launch_img_gemm(a, group, tile, fast, stream));
+}
+
+int conv_bwd_data(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+                  int group, const float *dy, const float *w, float *dx, void *ws,
+                  size_t ws_bytes, hipStream_t stream)
+{
+    Geom g;
+    int st = make_geom(N, C, H, W, K, R, S, stride, pad, group, &g);
+    if (st != MICONV_OK)
+        return st;
+    const size_t fb = sizeof(float);
+    Range r[3] = {{dy, (size_t)N * K * g.P * g.Q * fb, false},
+                  {w, (size_t)K * g.Cg * R * S * fb, false},
+                  {dx, (size_t)N * C * H * W * fb, true}};
+    bool req[3] = {true, true, true};
+    size_t need = bwd_data_ws(g);
+    if ((st = check_buffers(r, 3, req, ws, ws_bytes, need)) != MICONV_OK)
+        return st;
+    if ((st = check_device()) != MICONV_OK)
+        return st;
+    (void)hipGetLastError();
+
+    char *wsp = (char *)ws;
+    for (int ph = 0; ph < stride; ph++)
+        for (int pw = 0; pw < stride; pw++) {
+            Axis ah = phase_axis(H, R, stride, pad, ph);
+            Axis aw = phase_axis(W, S, stride, pad, pw);
+            size_t bytes = align_up((size_t)K * g.Cg * ah.nt * aw.nt * fb);
+            float *wr = (float *)wsp;
+            wsp += bytes;
+            if (ah.n == 0 || aw.n == 0)
+                continue;
+            hipError_t e = launch_pack_bwd_phase(w, wr, K, g.Cg, R, S, group, ah.t0, aw.t0,
+                                                 ah.nt, aw.nt, stride, stream);
+            if (e != hipSuccess)
+                return MICONV_ERR_LAUNCH;
+            ImgGemmArgs a;
+            a.M = g.Cg;
+            a.Ncol = N * ah.n * aw.n;
+            a.Kred = ah.nt * aw.nt * g.Kg;
+            a.A = wr;
+            a.a_gstride = (long long)a.Kred * a.M;
+            a.src = dy;
+            a.cin = g.Kg;
+            a.src_h = g.P;
+            a.src_w = g.Q;
+            a.src_hw = g.P * g.Q;
+            a.src_img_stride = (long long)K * g.P * g.Q;
+            a.col_hw = make_fastdiv(ah.n * aw.n);
+            a.col_w = make_fastdiv(aw.n);
+            a.cstep = 1;
+            a.coff_h = ah.d;
+            a.coff_w = aw.d;
+            a.tsign = -1;
+            a.k_cin = make_fastdiv(g.Kg);
+            a.k_tw = make_fastdiv(aw.nt > 0 ? aw.nt : 1);
+            a.out = dx;
+            a.bias = nullptr;
+            a.out_img_stride = (long long)C * H * W;
+            a.out_hw = H * W;
+            a.out_w = W;
+            a.ostep = stride;
+            a.ooff_h = ph;
+            a.ooff_w = pw;
+            int tile = pick_img_tile(a.M, a.Ncol, group);
+            bool fast = g.Kg % kBK == 0;
+            if ((st = launch_status(launch_img_gemm(a, group, tile, fast, stream))) != MICONV_OK)
+                return st;
+        }
+    return MICONV_OK;
+}
+
+int conv_bwd_weight(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+                    int group, const float *x, const float *dy, float *dw, float *db, void *ws,
+                    size_t ws_bytes, hipStream_t stream)
+{
+    Geom g;
+    int st = make_geom(N, C, H, W, K, R, S, stride, pad, group, &g);
+    if (st != MICONV_OK)
+        return st;
+    const size_t fb = sizeof(float);
+    Range r[4] = {{x, (size_t)N * C * H * W * fb, false},
+                  {dy, (size_t)N * K * g.P * g.Q * fb, false},
+                  {dw, (size_t)K * g.Cg * R * S * fb, true},
+                  {db, (size_t)K * fb, true}};
+    bool req[4] = {true, true, true, false};
+    WgradPlan p = wgrad_plan(g);
+    size_t need = p.part_bytes + p.bias_bytes;
+    if ((st = check_buffers(r, 4, req, ws, ws_bytes, need)) != MICONV_OK)
+        return st;
+    if ((st = check_device()) != MICONV_OK)
+        return st;
+    (void)hipGetLastError();
+
+    WgradArgs a;
+    a.M = g.Kg;
+    a.Ncol = g.Cg * R * S;
+    a.Kred = N * g.P * g.Q;
+    a.dy = dy;
+    a.x = x;
+    a.K = K;
+    a.C = C;
+    a.H = H;
+    a.W = W;
+    a.HW = H * W;
+    a.PQ = g.P * g.Q;
+    a.stride = stride;
+    a.pad = pad;
+    a.Kg = g.Kg;
+    a.Cg = g.Cg;
+    a.pix_pq = make_fastdiv(g.P * g.Q);
+    a.pix_q = make_fastdiv(g.Q);
+    a.n_rs = make_fastdiv(R * S);
+    a.n_s = make_fastdiv(S);
+    a.chunk = p.chunk;
+    float *part = (float *)ws;
+    a.out = p.nsplit > 1 ? part : dw;
+    a.split_stride = (long long)K * a.Ncol;
+    if ((st = launch_status(launch_wgrad_gemm(a, group, p.nsplit, p.tile, stream))) != MICONV_OK)
+        return st;
+    if (p.nsplit > 1 &&
+        (st = launch_status(launch_splitk_reduce(part, p.nsplit, a.split_stride,
+                                                 (long long)K * a.Ncol, dw, stream))) != MICONV_OK)
+        return st;
+    if (db) {
+        float *bpart = (float *)((char *)ws + p.part_bytes);
+        if ((st = launch_status(launch_bias_grad(dy, N, K, g.P * g.Q, p.bias_chunks, bpart, db,
+                                                 stream))) != MICONV_OK)
+            return st;
+    }
+    return MICONV_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,103 @@
+// Internal declarations shared by the C-ABI layer (api.hip) and the kernels
+// (conv_kernels.hip).  Not installed; the public interface is miconv.h.
+#pragma once
+
+#include <stdint.h>
+#include <hip/hip_runtime.h>
+
+namespace miconv {
+
+// Division by a run-time constant d (1 <= d < 2^31) for dividends n < 2^31:
+// q = (mulhi(n, mul) + n) >> shift, with shift = ceil(log2 d) and
+// mul = floor(2^32 (2^shift - d) / d) + 1 (Granlund & Montgomery, 1994).
+struct FastDiv {
+    uint32_t mul;
+    uint32_t shift;
+    uint32_t d;
+};
+
+__host__ __device__ inline uint32_t fast_div(uint32_t n, FastDiv f)
+{
+    uint32_t hi = (uint32_t)(((uint64_t)n * f.mul) >> 32);
+    return (hi + n) >> f.shift;
+}
+
+FastDiv make_fastdiv(uint32_t d);
+
+// ---------------------------------------------------------------------------
+// Implicit GEMM whose columns are pixels of an image-like output and whose
+// B operand gathers from an image-like source.  Used for the forward pass
+// (source x, columns = output pixels, taps = filter taps) and for each stride
+// phase of the backward-data pass (source dy, columns = the input pixels of
+// one phase, taps = the filter taps of that phase).
+//
+// Per group g (grid z):  out[g] (M x Ncol) = A[g] (M x Kred) * B[g] (Kred x Ncol)
+//   A[g][m][k]  = Ap[g * Kred * M + k * M + m]          (packed, k-major)
+//   k           = tap * cin + ch,  tap = tr * taps_w + ts
+//   column n    = (img, ci, cj) over  N x col_h x col_w
+//   B[g][k][n]  = src[img][g * cin + ch][hy][wx] or 0 outside the source, with
+//                 hy = ci * cstep + coff_h + tsign * tr,
+//                 wx = cj * cstep + coff_w + tsign * ts
+//   out[img][g * M + m][ci * ostep + ooff_h][cj * ostep + ooff_w] = C + bias
+// ---------------------------------------------------------------------------
+struct ImgGemmArgs {
+    int M, Ncol, Kred;
+    const float *A;
+    long long a_gstride;  // Kred * M
+    const float *src;
+    int cin;              // source channels per group
+    int src_h, src_w, src_hw;
+    long long src_img_stride;
+    FastDiv col_hw, col_w;  // d = col_h * col_w, col_w
+    int cstep, coff_h, coff_w, tsign;
+    FastDiv k_cin, k_tw;    // d = cin, taps_w
+    float *out;
+    const float *bias;      // may be null
+    long long out_img_stride;
+    int out_hw, out_w;
+    int ostep, ooff_h, ooff_w;
+};
+
+// ---------------------------------------------------------------------------
+// Backward-weight GEMM, per group g (grid z) and split s (grid y):
+//   out[s][g][m][n] = sum over pixels pix in split s of
+//                     dy[img][g*Kg + m][p][q] * x[img][g*Cg + c][p*st - pad + r][q*st - pad + s']
+//   m in [0, Kg),  n = c * R * S + r * S + s'  in [0, Cg R S),
+//   pix = img * P * Q + p * Q + q in [s * chunk, min((s+1) * chunk, N P Q)).
+// ---------------------------------------------------------------------------
+struct WgradArgs {
+    int M, Ncol, Kred;
+    const float *dy;
+    const float *x;
+    int K, C, H, W, HW, PQ, stride, pad, Kg, Cg;
+    FastDiv pix_pq, pix_q;  // d = P * Q, Q
+    FastDiv n_rs, n_s;      // d = R * S, S
+    int chunk;
+    float *out;
+    long long split_stride;  // G * M * Ncol
+};
+
+enum TileCfg { TILE_128x128 = 0, TILE_64x64 = 1 };
+
+hipError_t launch_img_gemm(const ImgGemmArgs &a, int groups, int tile, bool fast,
+                           hipStream_t stream);
+hipError_t launch_wgrad_gemm(const WgradArgs &a, int groups, int nsplit, int tile,
+                             hipStream_t stream);
+
+// wp[g][(r*S + s)*Cg + c][k] = w[g*Kg + k][c][r][s]
+hipError_t launch_pack_fwd(const float *w, float *wp, int K, int Cg, int R, int S, int G,
+                           hipStream_t stream);
+// One stride phase of the backward-data filter:
+// wr[g][(rr*ns + ss)*Kg + k][c] = w[g*Kg + k][c][r0 + st*rr][s0 + st*ss]
+hipError_t launch_pack_bwd_phase(const float *w, float *wr, int K, int Cg, int R, int S,
+                                 int G, int r0, int s0, int nr, int ns, int stride,
+                                 hipStream_t stream);
+// out[i] = sum_{s < nsplit} part[s * stride + i], in order of s.
+hipError_t launch_splitk_reduce(const float *part, int nsplit, long long stride,
+                                long long count, float *out, hipStream_t stream);
+// Two-stage bias gradient: part[k][j] = partial sums of dy over chunk j of
+// the N*P*Q positions of channel k, then db[k] = sum_j part[k][j] in order.
+hipError_t launch_bias_grad(const float *dy, int N, int K, int PQ, int nchunk, float *part,
+                            float *db, hipStream_t stream);
+
+}  // namespace miconv

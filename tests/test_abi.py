@@ -1,0 +1,137 @@
+"""The C-ABI library on the CPU: it loads, exports every function that
+include/miconv.h declares, computes geometry and workspace sizes on the
+host, and rejects bad arguments before touching any device.  No kernel runs
+here: the pointers below are fake device addresses that the library never
+dereferences, because every check fails first."""
+import os
+import re
+
+import pytest
+
+import paper_1903_06934_amd as m
+from paper_1903_06934_amd import build as libbuild
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "miconv.h")
+
+OK, SHAPE, NULL, WS, ALIAS, ALIGN, DEVICE = 0, -1, -2, -3, -4, -5, -6
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(libbuild.LIBRARY):
+        libbuild.build()
+    return m.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b([a-z_][a-z0-9_]*)\s*\(", text)) - {"sizeof", "defined"})
+
+
+def test_exports_every_declared_function(L):
+    names = declared_functions()
+    assert set(names) == {"conv_output_size", "conv_workspace_size", "conv_fwd",
+                          "conv_bwd_data", "conv_bwd_weight", "conv_error_string"}
+    for n in names:
+        assert hasattr(L, n), n
+
+
+@pytest.mark.parametrize("n_in,f,st,pad,want", [
+    (227, 11, 4, 0, 55), (224, 7, 2, 3, 112), (56, 1, 2, 0, 28), (224, 3, 1, 1, 224),
+    (27, 5, 1, 2, 27), (13, 3, 1, 1, 13), (4, 3, 2, 1, 2), (5, 2, 3, 0, 2), (3, 5, 1, 1, 1),
+    (1, 1, 1, 0, 1)])
+def test_output_size(L, n_in, f, st, pad, want):
+    assert m.output_size(n_in, n_in, f, f, st, pad) == (want, want)
+    assert m.output_size(n_in, 7, f, 1, st, pad)[0] == want
+
+
+@pytest.mark.parametrize("args", [(3, 3, 5, 5, 1, 0), (0, 3, 1, 1, 1, 0), (3, 3, 1, 1, 0, 0),
+                                  (3, 3, 1, 1, 1, -1), (3, 3, 0, 1, 1, 0)])
+def test_output_size_rejects(L, args):
+    import ctypes
+    P, Q = ctypes.c_int(-7), ctypes.c_int(-7)
+    assert L.conv_output_size(*args, ctypes.byref(P), ctypes.byref(Q)) == SHAPE
+    assert (P.value, Q.value) == (-7, -7)
+    assert L.conv_output_size(5, 5, 3, 3, 1, 0, None, ctypes.byref(Q)) == NULL
+
+
+def test_error_strings(L):
+    for s in range(-8, 1):
+        assert L.conv_error_string(s)
+    assert L.conv_error_string(12345) == b"unknown status"
+
+
+GOOD = (2, 16, 32, 32, 32, 3, 3, 1, 1, 1)
+BAD_SHAPES = [
+    (0, 16, 32, 32, 32, 3, 3, 1, 1, 1), (2, 16, 32, 32, 32, 3, 3, 0, 1, 1),
+    (2, 16, 32, 32, 32, 3, 3, 1, -1, 1), (2, 15, 32, 32, 32, 3, 3, 1, 1, 2),
+    (2, 16, 32, 32, 30, 3, 3, 1, 1, 4), (2, 16, 2, 2, 32, 5, 5, 1, 0, 1),
+    (2048, 1024, 64, 64, 8, 1, 1, 1, 0, 1),  # x above 2^31 - 1 elements
+]
+
+X, W_, B, Y, WSP = 0x10000000, 0x20000000, 0x28000000, 0x30000000, 0x40000000
+
+
+def test_workspace_sizes(L):
+    for p in (0, 1, 2):
+        assert m.workspace_size(p, GOOD) > 0
+        for bad in BAD_SHAPES:
+            assert m.workspace_size(p, bad) == 0
+    assert m.workspace_size(3, GOOD) == 0
+    # one packed filter per pass; stride phases partition the taps
+    assert m.workspace_size(0, GOOD) == 32 * 16 * 9 * 4
+    assert m.workspace_size(1, (2, 4, 9, 9, 8, 3, 3, 2, 1, 1)) >= 8 * 4 * 9 * 4
+
+
+@pytest.mark.parametrize("shape", BAD_SHAPES)
+def test_bad_shapes(L, shape):
+    assert L.conv_fwd(*shape, X, W_, None, Y, WSP, 1 << 30, None) == SHAPE
+    assert L.conv_bwd_data(*shape, Y, W_, X, WSP, 1 << 30, None) == SHAPE
+    assert L.conv_bwd_weight(*shape, X, Y, W_, None, WSP, 1 << 30, None) == SHAPE
+
+
+def test_fwd_checks(L):
+    ws = m.workspace_size(0, GOOD)
+    f = lambda *a: L.conv_fwd(*GOOD, *a, None)
+    assert f(None, W_, B, Y, WSP, ws) == NULL
+    assert f(X, None, B, Y, WSP, ws) == NULL
+    assert f(X, W_, B, None, WSP, ws) == NULL
+    assert f(X + 4, W_, B, Y, WSP, ws) == ALIGN
+    assert f(X, W_, B + 8, Y, WSP, ws) == ALIGN
+    assert f(X, W_, B, Y, WSP, ws - 1) == WS
+    assert f(X, W_, B, Y, None, ws) == WS
+    assert f(X, W_, B, Y, WSP + 4, ws) == ALIGN
+    assert f(X, W_, B, X + 64, WSP, ws) == ALIAS          # y overlaps x
+    assert f(X, W_, B, Y, Y + 256, ws) == ALIAS           # ws overlaps y
+    assert f(X, W_, B, Y, W_, ws) == ALIAS                # ws overlaps w
+    # inputs may overlap each other
+    assert f(X, X, None, Y, WSP, ws) in (OK, DEVICE)
+
+
+def test_bwd_checks(L):
+    ws = m.workspace_size(1, GOOD)
+    g = lambda *a: L.conv_bwd_data(*GOOD, *a, None)
+    assert g(None, W_, X, WSP, ws) == NULL
+    assert g(Y, W_, None, WSP, ws) == NULL
+    assert g(Y, W_, X, WSP, ws - 4) == WS
+    assert g(Y, W_, Y + 16, WSP, ws) == ALIAS
+    ws = m.workspace_size(2, GOOD)
+    h = lambda *a: L.conv_bwd_weight(*GOOD, *a, None)
+    assert h(X, Y, None, B, WSP, ws) == NULL
+    assert h(X, None, W_, B, WSP, ws) == NULL
+    assert h(X, Y, W_, W_ + 16, WSP, ws) == ALIAS        # db overlaps dw
+    assert h(X, Y, W_, X, WSP, ws) == ALIAS              # db overlaps x
+    assert h(X, Y, W_, None, WSP, 0) == WS
+    assert h(X, Y, W_ + 4, None, WSP, ws) == ALIGN
+
+
+def test_device_check_without_gpu(L):
+    """On a host without a gfx950 device, a well-formed call reports
+    MICONV_ERR_DEVICE (and launches nothing)."""
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    ws = m.workspace_size(0, GOOD)
+    assert L.conv_fwd(*GOOD, X, W_, B, Y, WSP, ws, None) == DEVICE
