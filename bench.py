@@ -1,0 +1,334 @@
+#!/usr/bin/env python3
+"""Benchmark: fp32 convolution training passes on one MI355X.
+
+A step is one pass of the whole hot path over one batch of synthetic input:
+the forward pass of every layer of a conv stack, then, in reverse layer
+order, the backward-weight (+ bias) and backward-data passes (the network's
+first layer skips backward-data, whose result no layer would use).  Every
+layer occurs as many times as the stack lists it.
+
+Default workload: the AlexNet-shaped stack, batch 128, input 3x227x227.
+Printed: ONE JSON line with images/s of the stack (value), TFLOP/s per pass
+(2 N K P Q (C/G) R S flops per pass, divided by the device time of the
+whole library call), the roofline fraction of the dominant kernel, and the
+CPU oracle timed on a bounded sample of the same workload.
+
+All inputs are resident in device memory before the timed region; the timed
+region contains only the library's calls on torch's current stream.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "fp32 conv TFLOP/s per pass (fwd/bwdD/bwdW) + images/s conv stack"
+PEAK_TFLOPS = 157.3   # MI355X dense fp32 MFMA
+PEAK_GBS = 8000.0     # MI355X HBM3E
+PASSES = ("fwd", "bwd_data", "bwd_weight")
+
+WORKLOAD_NAMES = {
+    0: "single conv layer N=2 C=16 32x32 K=32 3x3 s1 p1 (all three passes)",
+    1: "AlexNet-shaped conv stack fwd+bwd, batch 128, input 3x227x227 (5 conv layers)",
+    2: "VGG-16-shaped conv stack fwd+bwd, batch 32, input 3x224x224 (13 conv layers)",
+    3: "ResNet-50-shaped bottleneck conv set fwd+bwd, batch 64 (stem, 4 stages, projections)",
+    4: "GoogLeNet-inception-shaped conv set fwd+bwd, batch 64 (3 modules on 28x28/14x14)",
+}
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="1", help="0-4, or 'all' (one JSON line each)")
+    ap.add_argument("--reps", type=int, default=20, help="timed repeats per layer and pass")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="target CPU time of the oracle sample (0 disables it)")
+    ap.add_argument("--flush", action="store_true",
+                    help="write a 512 MiB buffer between per-layer repeats (cold caches)")
+    return ap.parse_args()
+
+
+def flops_of(L):
+    return 2.0 * L.N * L.K * L.P * L.Q * (L.C // L.group) * L.R * L.S
+
+
+def bytes_of(L, p):
+    """Compulsory HBM bytes of one pass (each tensor read or written once)."""
+    x = L.N * L.C * L.H * L.W
+    y = L.N * L.K * L.P * L.Q
+    w = L.K * (L.C // L.group) * L.R * L.S
+    if p == "fwd":
+        n = x + w + L.K + y
+    elif p == "bwd_data":
+        n = y + w + x
+    else:
+        n = x + y + w + L.K
+    return 4.0 * n
+
+
+class HipEvents:
+    """Raw HIP events (for the library's timing hook)."""
+
+    def __init__(self):
+        self.hip = ctypes.CDLL("libamdhip64.so")
+        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float),
+                                                 ctypes.c_void_p, ctypes.c_void_p]
+        self.hip.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+
+    def create(self):
+        e = ctypes.c_void_p()
+        assert self.hip.hipEventCreate(ctypes.byref(e)) == 0
+        return e
+
+    def elapsed_ms(self, a, b):
+        assert self.hip.hipEventSynchronize(b) == 0
+        ms = ctypes.c_float()
+        assert self.hip.hipEventElapsedTime(ctypes.byref(ms), a, b) == 0
+        return ms.value
+
+    def destroy(self, e):
+        self.hip.hipEventDestroy(e)
+
+
+class LayerRun:
+    """Device buffers and prepared library calls of one layer."""
+
+    def __init__(self, cfg, li, L, stream):
+        import numpy as np
+        import torch
+        import workloads
+        import paper_1903_06934_amd as m
+
+        self.L = L
+        d = workloads.layer_inputs(cfg, li, L)
+        dev = torch.device("cuda")
+        t = {k: torch.from_numpy(np.ascontiguousarray(v)).to(dev) for k, v in d.items()}
+        self.t = t
+        self.y = torch.empty((L.N, L.K, L.P, L.Q), dtype=torch.float32, device=dev)
+        self.dx = torch.empty((L.N, L.C, L.H, L.W), dtype=torch.float32, device=dev)
+        self.dw = torch.empty_like(t["w"])
+        self.db = torch.empty_like(t["b"])
+        shape = L.shape
+        self.ws = {}
+        for pid in (0, 1, 2):
+            n = m.workspace_size(pid, shape)
+            self.ws[pid] = torch.empty(max(n, 256), dtype=torch.uint8, device=dev)
+        lib = m.lib()
+        ws = lambda pid: (self.ws[pid].data_ptr(), self.ws[pid].numel())
+        self.calls = {
+            "fwd": (lib.conv_fwd, shape + (t["x"].data_ptr(), t["w"].data_ptr(),
+                                           t["b"].data_ptr(), self.y.data_ptr()) + ws(0) + (stream,)),
+            "bwd_data": (lib.conv_bwd_data, shape + (t["dy"].data_ptr(), t["w"].data_ptr(),
+                                                     self.dx.data_ptr()) + ws(1) + (stream,)),
+            "bwd_weight": (lib.conv_bwd_weight, shape + (t["x"].data_ptr(), t["dy"].data_ptr(),
+                                                         self.dw.data_ptr(), self.db.data_ptr())
+                           + ws(2) + (stream,)),
+        }
+
+    def run(self, p):
+        fn, args = self.calls[p]
+        st = fn(*args)
+        if st != 0:
+            import paper_1903_06934_amd as m
+            raise m.MiconvError(st, f"{p} {self.L.name}")
+
+
+def stack_step(runs):
+    for r in runs:
+        for _ in range(r.L.count):
+            r.run("fwd")
+    for r in reversed(runs):
+        for _ in range(r.L.count):
+            r.run("bwd_weight")
+            if not r.L.first:
+                r.run("bwd_data")
+
+
+def time_call(fn, reps, flush_buf=None):
+    """Median and min device ms of fn() over reps, torch events on the
+    current stream (the stream the library launches on)."""
+    import torch
+    ts = []
+    for _ in range(reps):
+        if flush_buf is not None:
+            flush_buf.add_(1.0)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        fn()
+        b.record()
+        b.synchronize()
+        ts.append(a.elapsed_time(b))
+    return statistics.median(ts), min(ts)
+
+
+def kernel_time(run, p, reps, hev):
+    """Average device ms of the pass's GEMM kernel(s) alone, from the
+    library's timing hook (events recorded around the GEMM launches)."""
+    import torch
+    import paper_1903_06934_amd as m
+    lib = m.lib()
+    a, b = hev.create(), hev.create()
+    ts = []
+    try:
+        assert lib.conv_set_timing_events(a, b) == 0
+        for _ in range(reps):
+            run.run(p)
+            ts.append(hev.elapsed_ms(a, b))
+    finally:
+        lib.conv_set_timing_events(None, None)
+        torch.cuda.synchronize()
+        hev.destroy(a)
+        hev.destroy(b)
+    return sum(ts) / len(ts)
+
+
+def cpu_baseline(cfg, layers, target_s):
+    """The oracle (fp64 loop nests, all host threads) on a batch slice of
+    the same stack: images/s on the host."""
+    import oracle
+    import workloads
+    o = oracle.default()
+
+    def run_stack(n):
+        secs = 0.0
+        for li, L in enumerate(layers):
+            Ls = L.with_batch(n)
+            d = workloads.layer_inputs(cfg, li, Ls)
+            t0 = time.perf_counter()
+            for _ in range(L.count):
+                o.conv_fwd(Ls.shape, d["x"], d["w"], d["b"])
+                o.conv_bwd_weight(Ls.shape, d["x"], d["dy"])
+                if not L.first:
+                    o.conv_bwd_data(Ls.shape, d["dy"], d["w"])
+            secs += time.perf_counter() - t0
+        return secs
+
+    # Calibrate on one image, then size the sample to the target time.
+    t1 = run_stack(1)
+    n = max(1, min(layers[0].N, int(target_s / max(t1, 1e-6))))
+    if n == 1:
+        secs = t1
+    else:
+        secs = run_stack(n)
+    return {"value": n / secs, "unit": "img/s", "cores": o.num_threads(), "kind": "oracle",
+            "sample": f"the same stack at batch {n} of {layers[0].N}, every layer and pass "
+                      f"(fp64 direct loop nests; input generation not timed), {secs:.1f} s"}
+
+
+def bench_config(cfg, args, with_cpu):
+    import torch
+    import workloads
+
+    name, layers = workloads.config(cfg)
+    stream = torch.cuda.current_stream().cuda_stream
+    runs = [LayerRun(cfg, li, L, stream) for li, L in enumerate(layers)]
+    torch.cuda.synchronize()
+    N = layers[0].N
+
+    for _ in range(args.warmup):
+        stack_step(runs)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        stack_step(runs)
+    e1.record()
+    torch.cuda.synchronize()
+    step_ms = e0.elapsed_time(e1) / args.steps
+
+    flush = torch.empty(128 << 20, dtype=torch.float32, device="cuda") if args.flush else None
+    per = []
+    tot = {p: [0.0, 0.0] for p in PASSES}
+    for r in runs:
+        L = r.L
+        for p in PASSES:
+            med, mn = time_call(lambda: r.run(p), args.reps, flush)
+            F = flops_of(L)
+            B = bytes_of(L, p)
+            t_roof = max(F / (PEAK_TFLOPS * 1e12), B / (PEAK_GBS * 1e9)) * 1e3
+            in_stack = not (p == "bwd_data" and L.first)
+            per.append({"layer": L.name, "pass": p, "count": L.count, "in_stack": in_stack,
+                        "ms": round(med, 4), "ms_min": round(mn, 4),
+                        "tflops": round(F / med / 1e9, 2), "gbs": round(B / med / 1e6, 1),
+                        "roof_frac": round(t_roof / med, 3)})
+            if in_stack:
+                tot[p][0] += F * L.count
+                tot[p][1] += med * L.count
+
+    # Dominant kernel: the GEMM of the (layer, pass) with the largest share
+    # of the step.
+    dom = max((x for x in per if x["in_stack"]), key=lambda x: x["ms"] * x["count"])
+    hev = HipEvents()
+    drun = next(r for r in runs if r.L.name == dom["layer"])
+    k_ms = kernel_time(drun, dom["pass"], args.reps, hev)
+    F = flops_of(drun.L)
+    ai = F / bytes_of(drun.L, dom["pass"])
+    ridge = PEAK_TFLOPS * 1e12 / (PEAK_GBS * 1e9)
+    if ai >= ridge:
+        ach = F / k_ms / 1e9
+        roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(ach / PEAK_TFLOPS, 4), "traffic": None}
+    else:
+        ach = bytes_of(drun.L, dom["pass"]) / k_ms / 1e6
+        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_GBS,
+                "unit": "GB/s", "frac": round(ach / PEAK_GBS, 4), "traffic": None}
+    roof.update({"kernel": f"{dom['pass']} GEMM of {dom['layer']}",
+                 "kernel_ms": round(k_ms, 4), "flops_per_launch": F,
+                 "bytes_per_launch": bytes_of(drun.L, dom["pass"])})
+
+    line = {
+        "metric": METRIC,
+        "value": round(N * args.steps / (step_ms * args.steps / 1e3), 2),
+        "unit": "img/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(step_ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": WORKLOAD_NAMES[cfg], "name": name, "global_batch": N,
+                   "layers": len(layers), "parallelism": "single GPU"},
+        "tflops_per_pass": {p: round(tot[p][0] / tot[p][1] / 1e9, 2) if tot[p][1] else None
+                            for p in PASSES},
+        "stack_tflops": round(sum(v[0] for v in tot.values()) / (step_ms * 1e9), 2),
+        "roofline": roof,
+        "per_layer": per,
+    }
+    if with_cpu:
+        line["cpu_baseline"] = cpu_baseline(cfg, layers, args.cpu_seconds)
+    del runs
+    torch.cuda.empty_cache()
+    return line
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the multi-GPU "
+              "data-parallel path is a design, not part of this build.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    import paper_1903_06934_amd as m
+    m.lib()
+    cfgs = [0, 1, 2, 3, 4] if args.config == "all" else [int(args.config)]
+    for cfg in cfgs:
+        line = bench_config(cfg, args, with_cpu=args.cpu_seconds > 0 and cfg == cfgs[0])
+        print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

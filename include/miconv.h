@@ -121,6 +121,20 @@ int conv_bwd_weight(int N, int C, int H, int W, int K, int R, int S, int stride,
                     int group, const float *x, const float *dy, float *dw, float *db,
                     void *ws, size_t ws_bytes, hipStream_t stream);
 
+/*
+ * Benchmark instrumentation; not needed to compute anything.  After this
+ * call, every conv_fwd / conv_bwd_data / conv_bwd_weight made by the calling
+ * thread records `before` on its stream immediately before the launch of the
+ * pass's first implicit-GEMM kernel and `after` immediately after its last
+ * one, so hipEventElapsedTime(before, after) is the GEMM kernels' device
+ * time without the filter packing, split-K reduction and bias-gradient
+ * kernels around them (for a strided conv_bwd_data it spans every stride
+ * phase, packing in between included).  Pass two NULLs to stop.  The events
+ * are created and owned by the caller.  Returns MICONV_OK, or
+ * MICONV_ERR_NULL if exactly one of the two is NULL.
+ */
+int conv_set_timing_events(hipEvent_t before, hipEvent_t after);
+
 /* Static, NUL-terminated description of a status code (never NULL). */
 const char *conv_error_string(int status);
 

@@ -224,6 +224,17 @@ WgradPlan wgrad_plan(const Geom &g)
 
 int launch_status(hipError_t e) { return e == hipSuccess ? MICONV_OK : MICONV_ERR_LAUNCH; }
 
+// Caller-owned timing events of conv_set_timing_events, per calling thread.
+struct TimingEvents {
+    hipEvent_t before = nullptr, after = nullptr;
+};
+thread_local TimingEvents tl_events;
+
+hipError_t mark(hipEvent_t ev, hipStream_t stream)
+{
+    return ev ? hipEventRecord(ev, stream) : hipSuccess;
+}
+
 }  // namespace
 }  // namespace miconv
 
@@ -263,6 +274,15 @@ size_t conv_workspace_size(int pass, int N, int C, int H, int W, int K, int R, i
     default:
         return 0;
     }
+}
+
+int conv_set_timing_events(hipEvent_t before, hipEvent_t after)
+{
+    if ((before == nullptr) != (after == nullptr))
+        return MICONV_ERR_NULL;
+    tl_events.before = before;
+    tl_events.after = after;
+    return MICONV_OK;
 }
 
 const char *conv_error_string(int status)
@@ -337,7 +357,11 @@ int conv_fwd(int N, int C, int H, int W, int K, int R, int S, int stride, int pa
     a.ooff_w = 0;
     int tile = pick_img_tile(a.M, a.Ncol, group);
     bool fast = g.Cg % kBK == 0;
-    return launch_status(launch_img_gemm(a, group, tile, fast, stream));
+    if (mark(tl_events.before, stream) != hipSuccess)
+        return MICONV_ERR_LAUNCH;
+    if ((st = launch_status(launch_img_gemm(a, group, tile, fast, stream))) != MICONV_OK)
+        return st;
+    return launch_status(mark(tl_events.after, stream));
 }
 
 int conv_bwd_data(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
@@ -361,6 +385,7 @@ int conv_bwd_data(int N, int C, int H, int W, int K, int R, int S, int stride, i
     (void)hipGetLastError();
 
     char *wsp = (char *)ws;
+    bool marked = false;
     for (int ph = 0; ph < stride; ph++)
         for (int pw = 0; pw < stride; pw++) {
             Axis ah = phase_axis(H, R, stride, pad, ph);
@@ -404,10 +429,13 @@ int conv_bwd_data(int N, int C, int H, int W, int K, int R, int S, int stride, i
             a.ooff_w = pw;
             int tile = pick_img_tile(a.M, a.Ncol, group);
             bool fast = g.Kg % kBK == 0;
+            if (!marked && mark(tl_events.before, stream) != hipSuccess)
+                return MICONV_ERR_LAUNCH;
+            marked = true;
             if ((st = launch_status(launch_img_gemm(a, group, tile, fast, stream))) != MICONV_OK)
                 return st;
         }
-    return MICONV_OK;
+    return launch_status(mark(tl_events.after, stream));
 }
 
 int conv_bwd_weight(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
@@ -456,8 +484,12 @@ int conv_bwd_weight(int N, int C, int H, int W, int K, int R, int S, int stride,
     float *part = (float *)ws;
     a.out = p.nsplit > 1 ? part : dw;
     a.split_stride = (long long)K * a.Ncol;
+    if (mark(tl_events.before, stream) != hipSuccess)
+        return MICONV_ERR_LAUNCH;
     if ((st = launch_status(launch_wgrad_gemm(a, group, p.nsplit, p.tile, stream))) != MICONV_OK)
         return st;
+    if (mark(tl_events.after, stream) != hipSuccess)
+        return MICONV_ERR_LAUNCH;
     if (p.nsplit > 1 &&
         (st = launch_status(launch_splitk_reduce(part, p.nsplit, a.split_stride,
                                                  (long long)K * a.Ncol, dw, stream))) != MICONV_OK)

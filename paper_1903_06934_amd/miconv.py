@@ -53,6 +53,8 @@ def lib():
     L.conv_bwd_data.restype = _I
     L.conv_bwd_weight.argtypes = geo + [_P, _P, _P, _P, _P, _Z, _P]
     L.conv_bwd_weight.restype = _I
+    L.conv_set_timing_events.argtypes = [_P, _P]
+    L.conv_set_timing_events.restype = _I
     L.conv_error_string.argtypes = [_I]
     L.conv_error_string.restype = ctypes.c_char_p
     _lib = L

@@ -3,6 +3,7 @@ include/miconv.h declares, computes geometry and workspace sizes on the
 host, and rejects bad arguments before touching any device.  No kernel runs
 here: the pointers below are fake device addresses that the library never
 dereferences, because every check fails first."""
+import ctypes
 import os
 import re
 
@@ -33,7 +34,8 @@ def declared_functions():
 def test_exports_every_declared_function(L):
     names = declared_functions()
     assert set(names) == {"conv_output_size", "conv_workspace_size", "conv_fwd",
-                          "conv_bwd_data", "conv_bwd_weight", "conv_error_string"}
+                          "conv_bwd_data", "conv_bwd_weight", "conv_error_string",
+                          "conv_set_timing_events"}
     for n in names:
         assert hasattr(L, n), n
 
@@ -55,6 +57,13 @@ def test_output_size_rejects(L, args):
     assert L.conv_output_size(*args, ctypes.byref(P), ctypes.byref(Q)) == SHAPE
     assert (P.value, Q.value) == (-7, -7)
     assert L.conv_output_size(5, 5, 3, 3, 1, 0, None, ctypes.byref(Q)) == NULL
+
+
+def test_timing_events_arguments(L):
+    L.conv_set_timing_events.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+    assert L.conv_set_timing_events(None, None) == OK
+    assert L.conv_set_timing_events(0x1000, None) == NULL
+    assert L.conv_set_timing_events(None, 0x1000) == NULL
 
 
 def test_error_strings(L):

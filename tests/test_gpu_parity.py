@@ -135,10 +135,12 @@ def test_config_layer_full_batch_sampled(cfg, li):
     assert_within(dx.ravel()[idx], v, a, "bwd_data")
     del dx
     dw, db = gpu_bwd_weight(shape, d["x"], d["dy"])
-    if dw.size * N * L.P * L.Q <= 4e9:
+    npq = N * L.P * L.Q                     # products per dw element
+    if dw.size * npq <= 2e9:
         idx = np.arange(dw.size)
     else:
-        idx = sample_indices(dw.shape, rng, groups=1, channel_axis=0)
+        count = int(min(2048, max(128, 1e9 / npq)))
+        idx = sample_indices(dw.shape, rng, count=count, groups=1, channel_axis=0)
     v, a = oracle.conv_bwd_weight_at(shape, d["x"], d["dy"], idx)
     assert_within(dw.ravel()[idx], v, a, "bwd_weight")
     v, a = oracle.bias_grad(d["dy"])

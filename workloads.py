@@ -7,8 +7,12 @@ convolution's arithmetic lives here, so neither the oracle nor the HIP
 library depends on it.
 
 Recipe (used for every config):
-  * seeds: ``numpy.random.default_rng([1903, cfg, layer, t])`` with
-    t = 0 for x, 1 for w, 2 for b, 3 for dy;
+  * each tensor is drawn in consecutive chunks of 2^22 elements of its
+    row-major order; chunk j of tensor t of layer ``layer`` of configuration
+    ``cfg`` comes from ``numpy.random.default_rng([1903, cfg, layer, t, j])``
+    with t = 0 for x, 1 for w, 2 for b, 3 for dy (chunks are drawn on
+    parallel threads; the values do not depend on the thread count, and a
+    smaller batch gives exactly the leading images of the full batch);
   * values are drawn in float64 and rounded once to float32 (round to
     nearest even); the float32 arrays are the canonical inputs to both sides;
   * x, dy ~ N(0, 1);
@@ -22,9 +26,13 @@ synthetic values, no dataset and no trained weights.
 """
 from __future__ import annotations
 
+import os
+from concurrent.futures import ThreadPoolExecutor
 from dataclasses import dataclass, replace
 
 import numpy as np
+
+CHUNK = 1 << 22
 
 
 @dataclass(frozen=True)
@@ -134,16 +142,33 @@ def config(cfg: int):
     return CONFIGS[cfg]
 
 
-def _rng(cfg, layer, t):
-    return np.random.default_rng([1903, cfg, layer, t])
+def _draw(key, shape, fill):
+    """float32 array of ``shape`` whose chunk j is ``fill(rng_j, n)`` (float64
+    draws, rounded to float32) with rng_j = default_rng([1903, *key, j])."""
+    out = np.empty(shape, dtype=np.float32)
+    flat = out.reshape(-1)
+    total = flat.size
+
+    def one(j):
+        n = min(CHUNK, total - j * CHUNK)
+        flat[j * CHUNK:j * CHUNK + n] = fill(np.random.default_rng([1903, *key, j]), n)
+
+    nchunks = (total + CHUNK - 1) // CHUNK
+    if nchunks <= 1:
+        for j in range(nchunks):
+            one(j)
+    else:
+        with ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 1, nchunks)) as ex:
+            list(ex.map(one, range(nchunks)))
+    return out
 
 
-def _normal(rng, shape):
-    return rng.standard_normal(size=shape, dtype=np.float64).astype(np.float32)
+def _normal(key, shape):
+    return _draw(key, shape, lambda rng, n: rng.standard_normal(n, dtype=np.float64))
 
 
-def _uniform(rng, lim, shape):
-    return rng.uniform(-lim, lim, size=shape).astype(np.float32)
+def _uniform(key, lim, shape):
+    return _draw(key, shape, lambda rng, n: rng.uniform(-lim, lim, n))
 
 
 def weight_limit(C, K, R, S, group, init):
@@ -164,14 +189,14 @@ def make_inputs(shape, P, Q, seed=(0, 0), init="he", tensors=("x", "w", "b", "dy
     cfg, li = seed
     out = {}
     if "x" in tensors:
-        out["x"] = _normal(_rng(cfg, li, 0), (N, C, H, W))
+        out["x"] = _normal((cfg, li, 0), (N, C, H, W))
     if "w" in tensors:
         lim = weight_limit(C, K, R, S, group, init)
-        out["w"] = _uniform(_rng(cfg, li, 1), lim, (K, C // group, R, S))
+        out["w"] = _uniform((cfg, li, 1), lim, (K, C // group, R, S))
     if "b" in tensors:
-        out["b"] = _uniform(_rng(cfg, li, 2), 0.1, (K,))
+        out["b"] = _uniform((cfg, li, 2), 0.1, (K,))
     if "dy" in tensors:
-        out["dy"] = _normal(_rng(cfg, li, 3), (N, K, P, Q))
+        out["dy"] = _normal((cfg, li, 3), (N, K, P, Q))
     return out
 
 
