@@ -52,8 +52,10 @@ extern "C" {
 typedef enum miconv_status {
     MICONV_OK = 0,
     MICONV_ERR_SHAPE = -1,     /* a dim < 1, pad < 0, stride < 1, C or K not divisible by
-                                  group, P or Q < 1, a tensor above 2^31 - 1 elements,
-                                  H, W, R, S or pad above 32767, or group above 65535 */
+                                  group, P or Q < 1, a tensor above 2^31 - 1 elements, one
+                                  image (C*H*W or K*P*Q) or the filter bank above 2^29 - 1
+                                  elements, H, W, R, S or pad above 32767, or group above
+                                  65535 */
     MICONV_ERR_NULL = -2,      /* a required pointer is NULL */
     MICONV_ERR_WORKSPACE = -3, /* ws_bytes below conv_workspace_size(), or ws NULL when
                                   a workspace is needed */

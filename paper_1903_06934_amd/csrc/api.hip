@@ -6,7 +6,7 @@
 #include <stdint.h>
 #include <string.h>
 
-#include "../../include/miconv.h"
+#include "miconv.h"
 #include "internal.h"
 
 namespace miconv {
@@ -27,6 +27,7 @@ FastDiv make_fastdiv(uint32_t d)
 namespace {
 
 constexpr long long kMaxElems = 2147483647LL;  // 2^31 - 1
+constexpr long long kMaxChunkElems = (1LL << 29) - 1;  // per launch, per source tensor
 constexpr size_t kAlign = 256;                  // sub-buffer alignment inside ws
 constexpr int kBK = 16;                         // reduction slice of every GEMM kernel
 constexpr int kTargetWorkgroups = 1024;         // 4 per CU on 256 CUs
@@ -67,6 +68,12 @@ int make_geom(int N, int C, int H, int W, int K, int R, int S, int stride, int p
     long long nx = (long long)N * C * H * W, ny = (long long)N * K * P * Q;
     long long nw = (long long)K * (C / group) * R * S;
     if (nx > kMaxElems || ny > kMaxElems || nw > kMaxElems)
+        return MICONV_ERR_SHAPE;
+    // Kernels address the images of one launch, and the packed filter bank,
+    // with byte offsets below 2^31: one image and the filters must each stay
+    // below 2^29 elements.
+    if ((long long)C * H * W > kMaxChunkElems || (long long)K * P * Q > kMaxChunkElems ||
+        nw > kMaxChunkElems)
         return MICONV_ERR_SHAPE;
     *g = Geom{N, C, H, W, K, R, S, stride, pad, group, P, Q, C / group, K / group};
     return MICONV_OK;
@@ -141,13 +148,30 @@ int gemm_tiles(int M, int Ncol, int bm, int bn)
     return ((M + bm - 1) / bm) * ((Ncol + bn - 1) / bn);
 }
 
-// Larger tiles reuse each loaded element more; fall back to 64x64 when the
-// large tiling would leave the chip short of workgroups.
-int pick_img_tile(int M, long long Ncol, int G)
+// Tile choice for the image GEMM.  Measured on MI355X across the layers of
+// the five benchmark stacks: the kernel is limited by latency hiding rather
+// than by MFMA issue, so the 64x64 tile (4 waves of 32x32, many workgroups
+// per CU) is best or within ~2% almost everywhere; 64x128 gains a little when
+// there are at least 8 of its tiles per CU; layers with a per-element tap
+// decode (channels per group not a multiple of the slice depth) prefer
+// 128x128 when M > 64.
+int pick_img_tile(int M, long long Ncol, int G, bool fast)
 {
-    if (M > 64 && (long long)gemm_tiles(M, (int)Ncol, 128, 128) * G >= 2 * 256)
-        return TILE_128x128;
-    return TILE_64x64;
+    if (!fast)
+        return M > 64 ? IMG_128x128 : IMG_64x64;
+    long long t64x128 = (long long)((M + 63) / 64) * ((Ncol + 127) / 128) * G;
+    return t64x128 >= 8 * 256 ? IMG_64x128 : IMG_64x64;
+}
+
+// Images per launch so that every source view stays below 2^29 elements.
+int images_per_launch(const Geom &g)
+{
+    long long per = (long long)g.C * g.H * g.W;
+    long long pery = (long long)g.K * g.P * g.Q;
+    if (pery > per)
+        per = pery;
+    long long n = kMaxChunkElems / per;
+    return (int)(n < g.N ? n : g.N);
 }
 
 // ------------------------------------------------------------ fwd plan
@@ -187,8 +211,12 @@ size_t bwd_data_ws(const Geom &g)
 }
 
 // ------------------------------------------------------------ bwd-weight plan
+// The reduction over N*P*Q pixels is cut into fixed-length splits (a
+// multiple of the 16-pixel slice) so that about kTargetWorkgroups
+// workgroups run; each split writes its own partial dw, summed afterwards in
+// split order.  Launches never straddle a batch chunk (images_per_launch).
 struct WgradPlan {
-    int tile, nsplit, chunk, bias_chunks;
+    int tile, chunk, nsplit, nb, bias_chunks;
     size_t part_bytes, bias_bytes;
 };
 
@@ -196,7 +224,7 @@ WgradPlan wgrad_plan(const Geom &g)
 {
     WgradPlan p;
     int M = g.Kg, Ncol = g.Cg * g.R * g.S;
-    long long Kred = (long long)g.N * g.P * g.Q;
+    long long PQ = (long long)g.P * g.Q, Kred = (long long)g.N * PQ;
     p.tile = (M > 64 && Ncol > 64) ? TILE_128x128 : TILE_64x64;
     int bm = p.tile == TILE_128x128 ? 128 : 64;
     long long tiles = (long long)gemm_tiles(M, Ncol, bm, bm) * g.G;
@@ -209,7 +237,13 @@ WgradPlan wgrad_plan(const Geom &g)
     long long chunk = (Kred + ns - 1) / ns;
     chunk = (chunk + kBK - 1) / kBK * kBK;
     p.chunk = (int)chunk;
-    p.nsplit = (int)((Kred + chunk - 1) / chunk);
+    p.nb = images_per_launch(g);
+    long long total = 0;
+    for (int n0 = 0; n0 < g.N; n0 += p.nb) {
+        long long n = g.N - n0 < p.nb ? g.N - n0 : p.nb;
+        total += (n * PQ + chunk - 1) / chunk;
+    }
+    p.nsplit = (int)total;
     p.part_bytes = p.nsplit > 1 ? align_up((size_t)p.nsplit * g.K * Ncol * sizeof(float)) : 0;
     long long bc = (1024 + g.K - 1) / g.K;
     long long bmax = (Kred + 4095) / 4096;
@@ -323,22 +357,22 @@ int conv_fwd(int N, int C, int H, int W, int K, int R, int S, int stride, int pa
     (void)hipGetLastError();
 
     float *wp = (float *)ws;
-    hipError_t e = launch_pack_fwd(w, wp, K, g.Cg, R, S, group, stream);
-    if (e != hipSuccess)
+    if (launch_pack_fwd(w, wp, K, g.Cg, R, S, group, stream) != hipSuccess)
         return MICONV_ERR_LAUNCH;
 
+    const int nb = images_per_launch(g);
+    const long long xi = (long long)C * H * W, yi = (long long)K * g.P * g.Q;
     ImgGemmArgs a;
     a.M = g.Kg;
-    a.Ncol = N * g.P * g.Q;
     a.Kred = g.Cg * R * S;
+    a.groups = group;
     a.A = wp;
-    a.a_gstride = (long long)a.Kred * a.M;
-    a.src = x;
+    a.a_bytes = (uint32_t)((size_t)K * a.Kred * fb);
     a.cin = g.Cg;
     a.src_h = H;
     a.src_w = W;
     a.src_hw = H * W;
-    a.src_img_stride = (long long)C * H * W;
+    a.src_img_words = (uint32_t)xi;
     a.col_hw = make_fastdiv(g.P * g.Q);
     a.col_w = make_fastdiv(g.Q);
     a.cstep = stride;
@@ -347,20 +381,26 @@ int conv_fwd(int N, int C, int H, int W, int K, int R, int S, int stride, int pa
     a.tsign = 1;
     a.k_cin = make_fastdiv(g.Cg);
     a.k_tw = make_fastdiv(S);
-    a.out = y;
     a.bias = b;
-    a.out_img_stride = (long long)K * g.P * g.Q;
+    a.out_img_stride = yi;
     a.out_hw = g.P * g.Q;
     a.out_w = g.Q;
     a.ostep = 1;
     a.ooff_h = 0;
     a.ooff_w = 0;
-    int tile = pick_img_tile(a.M, a.Ncol, group);
-    bool fast = g.Cg % kBK == 0;
+    const bool fast = g.Cg % kBK == 0;
     if (mark(tl_events.before, stream) != hipSuccess)
         return MICONV_ERR_LAUNCH;
-    if ((st = launch_status(launch_img_gemm(a, group, tile, fast, stream))) != MICONV_OK)
-        return st;
+    for (int n0 = 0; n0 < N; n0 += nb) {
+        const int n = N - n0 < nb ? N - n0 : nb;
+        a.Ncol = n * g.P * g.Q;
+        a.src = x + n0 * xi;
+        a.src_bytes = (uint32_t)(n * xi * (long long)fb);
+        a.out = y + n0 * yi;
+        int tile = pick_img_tile(a.M, a.Ncol, group, fast);
+        if ((st = launch_status(launch_img_gemm(a, tile, fast, stream))) != MICONV_OK)
+            return st;
+    }
     return launch_status(mark(tl_events.after, stream));
 }
 
@@ -384,6 +424,8 @@ int conv_bwd_data(int N, int C, int H, int W, int K, int R, int S, int stride, i
         return st;
     (void)hipGetLastError();
 
+    const int nb = images_per_launch(g);
+    const long long xi = (long long)C * H * W, yi = (long long)K * g.P * g.Q;
     char *wsp = (char *)ws;
     bool marked = false;
     for (int ph = 0; ph < stride; ph++)
@@ -395,22 +437,20 @@ int conv_bwd_data(int N, int C, int H, int W, int K, int R, int S, int stride, i
             wsp += bytes;
             if (ah.n == 0 || aw.n == 0)
                 continue;
-            hipError_t e = launch_pack_bwd_phase(w, wr, K, g.Cg, R, S, group, ah.t0, aw.t0,
-                                                 ah.nt, aw.nt, stride, stream);
-            if (e != hipSuccess)
+            if (launch_pack_bwd_phase(w, wr, K, g.Cg, R, S, group, ah.t0, aw.t0, ah.nt, aw.nt,
+                                      stride, stream) != hipSuccess)
                 return MICONV_ERR_LAUNCH;
             ImgGemmArgs a;
             a.M = g.Cg;
-            a.Ncol = N * ah.n * aw.n;
             a.Kred = ah.nt * aw.nt * g.Kg;
+            a.groups = group;
             a.A = wr;
-            a.a_gstride = (long long)a.Kred * a.M;
-            a.src = dy;
+            a.a_bytes = (uint32_t)((size_t)C * a.Kred * fb);
             a.cin = g.Kg;
             a.src_h = g.P;
             a.src_w = g.Q;
             a.src_hw = g.P * g.Q;
-            a.src_img_stride = (long long)K * g.P * g.Q;
+            a.src_img_words = (uint32_t)yi;
             a.col_hw = make_fastdiv(ah.n * aw.n);
             a.col_w = make_fastdiv(aw.n);
             a.cstep = 1;
@@ -419,21 +459,27 @@ int conv_bwd_data(int N, int C, int H, int W, int K, int R, int S, int stride, i
             a.tsign = -1;
             a.k_cin = make_fastdiv(g.Kg);
             a.k_tw = make_fastdiv(aw.nt > 0 ? aw.nt : 1);
-            a.out = dx;
             a.bias = nullptr;
-            a.out_img_stride = (long long)C * H * W;
+            a.out_img_stride = xi;
             a.out_hw = H * W;
             a.out_w = W;
             a.ostep = stride;
             a.ooff_h = ph;
             a.ooff_w = pw;
-            int tile = pick_img_tile(a.M, a.Ncol, group);
-            bool fast = g.Kg % kBK == 0;
+            const bool fast = g.Kg % kBK == 0;
             if (!marked && mark(tl_events.before, stream) != hipSuccess)
                 return MICONV_ERR_LAUNCH;
             marked = true;
-            if ((st = launch_status(launch_img_gemm(a, group, tile, fast, stream))) != MICONV_OK)
-                return st;
+            for (int n0 = 0; n0 < N; n0 += nb) {
+                const int n = N - n0 < nb ? N - n0 : nb;
+                a.Ncol = n * ah.n * aw.n;
+                a.src = dy + n0 * yi;
+                a.src_bytes = (uint32_t)(n * yi * (long long)fb);
+                a.out = dx + n0 * xi;
+                int tile = pick_img_tile(a.M, a.Ncol, group, fast);
+                if ((st = launch_status(launch_img_gemm(a, tile, fast, stream))) != MICONV_OK)
+                    return st;
+            }
         }
     return launch_status(mark(tl_events.after, stream));
 }
@@ -460,34 +506,44 @@ int conv_bwd_weight(int N, int C, int H, int W, int K, int R, int S, int stride,
         return st;
     (void)hipGetLastError();
 
+    const long long xi = (long long)C * H * W, yi = (long long)K * g.P * g.Q;
     WgradArgs a;
     a.M = g.Kg;
     a.Ncol = g.Cg * R * S;
-    a.Kred = N * g.P * g.Q;
-    a.dy = dy;
-    a.x = x;
-    a.K = K;
-    a.C = C;
+    a.groups = group;
+    a.dy_img_words = (uint32_t)yi;
+    a.x_img_words = (uint32_t)xi;
+    a.Cg = g.Cg;
     a.H = H;
     a.W = W;
     a.HW = H * W;
     a.PQ = g.P * g.Q;
     a.stride = stride;
     a.pad = pad;
-    a.Kg = g.Kg;
-    a.Cg = g.Cg;
     a.pix_pq = make_fastdiv(g.P * g.Q);
     a.pix_q = make_fastdiv(g.Q);
     a.n_rs = make_fastdiv(R * S);
     a.n_s = make_fastdiv(S);
     a.chunk = p.chunk;
-    float *part = (float *)ws;
-    a.out = p.nsplit > 1 ? part : dw;
     a.split_stride = (long long)K * a.Ncol;
+    const bool vec = a.PQ % 4 == 0;
+    float *part = (float *)ws;
     if (mark(tl_events.before, stream) != hipSuccess)
         return MICONV_ERR_LAUNCH;
-    if ((st = launch_status(launch_wgrad_gemm(a, group, p.nsplit, p.tile, stream))) != MICONV_OK)
-        return st;
+    int split0 = 0;
+    for (int n0 = 0; n0 < N; n0 += p.nb) {
+        const int n = N - n0 < p.nb ? N - n0 : p.nb;
+        a.Kred = n * a.PQ;
+        a.nsplit = (a.Kred + p.chunk - 1) / p.chunk;
+        a.dy = dy + n0 * yi;
+        a.x = x + n0 * xi;
+        a.dy_bytes = (uint32_t)(n * yi * (long long)fb);
+        a.x_bytes = (uint32_t)(n * xi * (long long)fb);
+        a.out = p.nsplit > 1 ? part + (long long)split0 * a.split_stride : dw;
+        if ((st = launch_status(launch_wgrad_gemm(a, p.tile, vec, stream))) != MICONV_OK)
+            return st;
+        split0 += a.nsplit;
+    }
     if (mark(tl_events.after, stream) != hipSuccess)
         return MICONV_ERR_LAUNCH;
     if (p.nsplit > 1 &&

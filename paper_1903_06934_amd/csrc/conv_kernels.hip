@@ -48,96 +48,170 @@ __device__ __forceinline__ void mfma_slice(const float (*As)[LDA], const float (
 }
 
 // ---------------------------------------------------------------------------
-// Forward / backward-data implicit GEMM (see ImgGemmArgs).
-// FAST: cin % BK == 0, so every BK slice of the reduction lies inside one
-// filter tap and the tap's (tr, ts) and the spatial bounds test are uniform
-// over the slice; otherwise each element decodes its own (tap, channel).
+// Operand staging: buffer loads that write straight into LDS.
+//
+// `buffer_load_dword ... lds` moves one dword per lane from a buffer into LDS
+// at (M0 + 4 * lane): a wave fills 64 consecutive words of an LDS row, with no
+// register staging and no ds_write.  A lane whose byte offset lies outside the
+// buffer's range reads 0 (hardware range checking), which is how padding,
+// ragged tiles and the reduction tail are zero-filled without branches.
+// Every buffer a launch reads is below 2^31 bytes, so a valid offset never
+// has bit 31 set and OR-ing bit 31 into an offset makes it out of range
+// (for every dword of a multi-dword load too).
 // ---------------------------------------------------------------------------
-template <int BM, int BN, int BK, int WM, int WN, bool FAST>
+#define LDS_AS __attribute__((address_space(3)))
+
+constexpr uint32_t kOob = 0x80000000u;  // beyond any buffer of < 2^31 bytes
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *p, uint32_t bytes)
+{
+    // Raw buffer (stride 0), dword 3 = 0x00020000 for the gfx9 family.
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)bytes,
+                                             0x00020000);
+}
+
+__device__ __forceinline__ void lds_load(__amdgpu_buffer_rsrc_t r, float *lds_row, uint32_t voff)
+{
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (LDS_AS void *)lds_row, 4, voff, 0, 0, 0);
+}
+
+// Out-of-range bit for a lane whose element is absent.
+__device__ __forceinline__ uint32_t oob_mask(bool ok) { return ok ? 0u : kOob; }
+
+// Workgroup id -> tile id, so that the workgroups the dispatcher sends to
+// one XCD (hardware ids congruent mod 8) own a contiguous range of tiles:
+// neighbouring tiles share operand rows in that XCD's L2.
+__device__ __forceinline__ int xcd_tile(int hw, int total)
+{
+    int xcd = hw & 7, idx = hw >> 3;
+    int per = total >> 3, rem = total & 7;
+    return xcd * per + min(xcd, rem) + idx;
+}
+
+// ---------------------------------------------------------------------------
+// Forward / backward-data implicit GEMM (see ImgGemmArgs).
+//
+// Workgroup = WM x WN waves computing a BM x BN tile; each wave owns a
+// (BM/WM) x (BN/WN) block of 32x32 MFMA accumulators.  Slices of BK rows of
+// the reduction are staged through a double-buffered LDS tile shared by the
+// workgroup (rows optionally padded by PAD words; measured: no padding is
+// best, the extra LDS costs more occupancy than the rare bank conflict).  Per slice a wave first reads
+// all its MFMA operands from LDS into registers, then issues its share of the
+// loads of the next slice into the other buffer, then runs its MFMAs, so the
+// loads overlap the MFMAs; one barrier per slice.
+//
+// A wave-load fills one LDS row segment of 64 words: for A, 64 consecutive
+// output rows m of one reduction row k (the packed filter is k-major, so the
+// load is coalesced); for B, 64 consecutive output columns (pixels) of one
+// reduction row k (coalesced along the pixel row).  k is the same for the
+// whole wave, so the (tap, channel) decode of k is scalar work.
+// FAST: cin % BK == 0, so a slice lies inside one filter tap; the spatial
+// bounds test and offset are then computed once per slice and column.
+// ---------------------------------------------------------------------------
+template <int BM, int BN, int BK, int WM, int WN, int PAD, bool FAST>
 __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArgs a)
 {
-    constexpr int NT = 64 * WM * WN;
-    constexpr int FM = BM / WM / 32, FN = BN / WN / 32;
-    constexpr int APT = BM * BK / NT, BPT = BN * BK / NT;
-    constexpr int AKS = NT / BM, BKS = NT / BN;
-    constexpr int LDA = BM, LDB = BN;
-    static_assert(NT % BM == 0 && NT % BN == 0, "loader mapping");
-    static_assert(APT * AKS == BK && BPT * BKS == BK, "loader mapping");
+    constexpr int NW = WM * WN;
+    constexpr int TM = BM / WM, TN = BN / WN;
+    constexpr int FM = TM / 32, FN = TN / 32;
+    constexpr int HA = BM / 64, HB = BN / 64;          // 64-wide segments per row
+    constexpr int LA = BK * HA / NW, LB = BK * HB / NW;  // wave-loads per slice
+    constexpr int LDA = BM + PAD, LDB = BN + PAD;
+    static_assert(BM % 64 == 0 && BN % 64 == 0 && TM % 32 == 0 && TN % 32 == 0, "tile");
+    static_assert((BK * HA) % NW == 0 && (BK * HB) % NW == 0, "loads per wave");
 
     __shared__ float As[2][BK][LDA];
     __shared__ float Bs[2][BK][LDB];
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int wm = wave % WM, wn = wave / WM;
-    const int g = blockIdx.z;
     const int mtiles = (a.M + BM - 1) / BM;
-    const int mt = blockIdx.x % mtiles, nt = blockIdx.x / mtiles;
+    const int ntiles = (a.Ncol + BN - 1) / BN;
+    const int tiles = mtiles * ntiles;
+    const int lin = xcd_tile(blockIdx.x, tiles * a.groups);
+    const int g = lin / tiles, tile = lin - g * tiles;
+    const int mt = tile % mtiles, nt = tile / mtiles;
     const int m0 = mt * BM, n0 = nt * BN;
 
-    // A loader: thread -> (m = tid % BM, k = tid / BM + AKS * i); coalesced along m.
-    const int a_m = tid % BM, a_k = tid / BM;
-    const bool a_mok = m0 + a_m < a.M;
-    const float *Ag = a.A + (long long)g * a.a_gstride + m0 + a_m;
+    const __amdgpu_buffer_rsrc_t rA = make_rsrc(a.A, a.a_bytes);
+    const __amdgpu_buffer_rsrc_t rB = make_rsrc(a.src, a.src_bytes);
 
-    // B loader: thread -> (n = tid % BN, k = tid / BN + BKS * i); coalesced along n.
-    const int b_n = tid % BN, b_k = tid / BN;
-    const int col = n0 + b_n;
-    const bool colok = col < a.Ncol;
-    int hb = 0, wb = 0;
-    const float *sb = a.src;
-    {
-        uint32_t c = colok ? (uint32_t)col : 0u;
+    // Per-lane A offsets (byte offset of row m within a packed row), masked.
+    uint32_t a_off[HA];
+#pragma unroll
+    for (int h = 0; h < HA; h++) {
+        int m = m0 + 64 * h + lane;
+        a_off[h] = (uint32_t)(m * 4) | oob_mask(m < a.M);
+    }
+    const uint32_t a_gbase = (uint32_t)g * (uint32_t)a.Kred * (uint32_t)a.M * 4u;
+
+    // Per-lane B column data: image base offset, base coordinates, validity.
+    uint32_t b_base[HB];
+    int b_hb[HB], b_wb[HB];
+    bool b_ok[HB];
+#pragma unroll
+    for (int h = 0; h < HB; h++) {
+        int n = n0 + 64 * h + lane;
+        b_ok[h] = n < a.Ncol;
+        uint32_t c = b_ok[h] ? (uint32_t)n : 0u;
         uint32_t img = fast_div(c, a.col_hw);
         uint32_t rem = c - img * a.col_hw.d;
         uint32_t ci = fast_div(rem, a.col_w);
         uint32_t cj = rem - ci * a.col_w.d;
-        hb = (int)ci * a.cstep + a.coff_h;
-        wb = (int)cj * a.cstep + a.coff_w;
-        sb = a.src + (long long)img * a.src_img_stride + (long long)g * a.cin * a.src_hw;
+        b_hb[h] = (int)ci * a.cstep + a.coff_h;
+        b_wb[h] = (int)cj * a.cstep + a.coff_w;
+        b_base[h] = (img * a.src_img_words + (uint32_t)g * a.cin * a.src_hw) * 4u;
     }
 
-    float ra[APT], rb[BPT];
-
-    auto load_slice = [&](int k0) {
+    auto issue = [&](int k0, int buf) {
 #pragma unroll
-        for (int i = 0; i < APT; i++) {
-            int k = k0 + a_k + AKS * i;
-            ra[i] = (a_mok && k < a.Kred) ? Ag[(long long)k * a.M] : 0.f;
+        for (int j = 0; j < LA; j++) {
+            const int li = wave + NW * j, kk = li / HA, h = li % HA;
+            const int k = k0 + kk;
+            const uint32_t row = a_gbase + (uint32_t)k * (uint32_t)a.M * 4u;
+            lds_load(rA, &As[buf][kk][64 * h], (row + a_off[h]) | oob_mask(k < a.Kred));
         }
         if constexpr (FAST) {
-            uint32_t tap = fast_div((uint32_t)k0, a.k_cin);
-            int ch0 = k0 - (int)(tap * a.k_cin.d);
-            uint32_t tr = fast_div(tap, a.k_tw);
-            int ts = (int)(tap - tr * a.k_tw.d);
-            int hy = hb + a.tsign * (int)tr, wx = wb + a.tsign * ts;
-            bool ok = colok && (unsigned)hy < (unsigned)a.src_h && (unsigned)wx < (unsigned)a.src_w;
-            long long off = (long long)(ch0 + b_k) * a.src_hw + (long long)hy * a.src_w + wx;
+            const uint32_t tap = fast_div((uint32_t)k0, a.k_cin);
+            const int ch0 = k0 - (int)(tap * a.k_cin.d);
+            const uint32_t tr = fast_div(tap, a.k_tw);
+            const int ts = (int)(tap - tr * a.k_tw.d);
+            uint32_t sp[HB], msk[HB];
 #pragma unroll
-            for (int i = 0; i < BPT; i++)
-                rb[i] = ok ? sb[off + (long long)(BKS * i) * a.src_hw] : 0.f;
+            for (int h = 0; h < HB; h++) {
+                int hy = b_hb[h] + a.tsign * (int)tr, wx = b_wb[h] + a.tsign * ts;
+                bool ok = b_ok[h] && (unsigned)hy < (unsigned)a.src_h &&
+                          (unsigned)wx < (unsigned)a.src_w;
+                sp[h] = b_base[h] + ((uint32_t)ch0 * (uint32_t)a.src_hw +
+                                     (uint32_t)(hy * a.src_w + wx)) * 4u;
+                msk[h] = oob_mask(ok);
+            }
+#pragma unroll
+            for (int j = 0; j < LB; j++) {
+                const int li = wave + NW * j, kk = li / HB, h = li % HB;
+                lds_load(rB, &Bs[buf][kk][64 * h],
+                         (sp[h] + (uint32_t)kk * (uint32_t)a.src_hw * 4u) | msk[h]);
+            }
         } else {
 #pragma unroll
-            for (int i = 0; i < BPT; i++) {
-                int k = k0 + b_k + BKS * i;
-                uint32_t kc = k < a.Kred ? (uint32_t)k : 0u;
-                uint32_t tap = fast_div(kc, a.k_cin);
-                int ch = (int)(kc - tap * a.k_cin.d);
-                uint32_t tr = fast_div(tap, a.k_tw);
-                int ts = (int)(tap - tr * a.k_tw.d);
-                int hy = hb + a.tsign * (int)tr, wx = wb + a.tsign * ts;
-                bool ok = colok && k < a.Kred && (unsigned)hy < (unsigned)a.src_h &&
+            for (int j = 0; j < LB; j++) {
+                const int li = wave + NW * j, kk = li / HB, h = li % HB;
+                const int k = k0 + kk;
+                const bool kok = k < a.Kred;
+                const uint32_t kc = kok ? (uint32_t)k : 0u;
+                const uint32_t tap = fast_div(kc, a.k_cin);
+                const int ch = (int)(kc - tap * a.k_cin.d);
+                const uint32_t tr = fast_div(tap, a.k_tw);
+                const int ts = (int)(tap - tr * a.k_tw.d);
+                int hy = b_hb[h] + a.tsign * (int)tr, wx = b_wb[h] + a.tsign * ts;
+                bool ok = kok && b_ok[h] && (unsigned)hy < (unsigned)a.src_h &&
                           (unsigned)wx < (unsigned)a.src_w;
-                rb[i] = ok ? sb[(long long)ch * a.src_hw + (long long)hy * a.src_w + wx] : 0.f;
+                uint32_t off = b_base[h] + ((uint32_t)ch * (uint32_t)a.src_hw +
+                                            (uint32_t)(hy * a.src_w + wx)) * 4u;
+                lds_load(rB, &Bs[buf][kk][64 * h], off | oob_mask(ok));
             }
         }
-    };
-    auto store_slice = [&](int buf) {
-#pragma unroll
-        for (int i = 0; i < APT; i++)
-            As[buf][a_k + AKS * i][a_m] = ra[i];
-#pragma unroll
-        for (int i = 0; i < BPT; i++)
-            Bs[buf][b_k + BKS * i][b_n] = rb[i];
     };
 
     f32x16 acc[FM][FN];
@@ -149,20 +223,36 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
             for (int v = 0; v < 16; v++)
                 acc[i][j][v] = 0.f;
 
+    const int kr = lane >> 5, lc = lane & 31;
     const int nslices = (a.Kred + BK - 1) / BK;
-    if (nslices > 0) {
-        load_slice(0);
-        store_slice(0);
-    }
-    __syncthreads();
+    if (nslices > 0)
+        issue(0, 0);
     for (int t = 0; t < nslices; t++) {
         const int buf = t & 1;
-        if (t + 1 < nslices)
-            load_slice((t + 1) * BK);
-        mfma_slice<BM, BN, BK, WM, WN, LDA, LDB>(As[buf], Bs[buf], acc, lane, wm, wn);
-        if (t + 1 < nslices)
-            store_slice(buf ^ 1);
+        // Slice t has landed in LDS for every wave, and every wave is done
+        // reading buffer buf ^ 1 (slice t - 1).
+        __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
+        float af[BK / 2][FM], bf[BK / 2][FN];
+#pragma unroll
+        for (int s = 0; s < BK / 2; s++) {
+#pragma unroll
+            for (int i = 0; i < FM; i++)
+                af[s][i] = As[buf][2 * s + kr][wm * TM + i * 32 + lc];
+#pragma unroll
+            for (int j = 0; j < FN; j++)
+                bf[s][j] = Bs[buf][2 * s + kr][wn * TN + j * 32 + lc];
+        }
+        if (t + 1 < nslices)
+            issue((t + 1) * BK, buf ^ 1);
+#pragma unroll
+        for (int s = 0; s < BK / 2; s++)
+#pragma unroll
+            for (int i = 0; i < FM; i++)
+#pragma unroll
+                for (int j = 0; j < FN; j++)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[s][i], bf[s][j],
+                                                                    acc[i][j], 0, 0, 0);
     }
 
     // Epilogue: + bias, scatter columns back to image coordinates.
@@ -170,7 +260,7 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
     bool nok[FN];
 #pragma unroll
     for (int j = 0; j < FN; j++) {
-        int n = n0 + wn * (BN / WN) + j * 32 + (lane & 31);
+        int n = n0 + wn * TN + j * 32 + lc;
         nok[j] = n < a.Ncol;
         uint32_t c = nok[j] ? (uint32_t)n : 0u;
         uint32_t img = fast_div(c, a.col_hw);
@@ -184,7 +274,7 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
     for (int i = 0; i < FM; i++)
 #pragma unroll
         for (int v = 0; v < 16; v++) {
-            int m = m0 + wm * (BM / WM) + i * 32 + acc_row(v, lane);
+            int m = m0 + wm * TM + i * 32 + acc_row(v, lane);
             if (m >= a.M)
                 continue;
             int oc = g * a.M + m;
@@ -198,89 +288,166 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
 }
 
 // ---------------------------------------------------------------------------
-// Backward-weight GEMM (see WgradArgs).  The reduction runs over pixels, so
-// both operands are loaded with lanes along the pixel index (coalesced along
-// q) and transposed into the k-major LDS tiles; the per-column filter tap
-// decode (c, r, s) is computed once per workgroup into an LDS table.
+// Backward-weight GEMM (see WgradArgs).
+//
+// The reduction runs over pixels, and both operands are contiguous along the
+// pixel index in HBM (dy rows; x rows for the gathered columns), so lanes load
+// along pixels (coalesced) and LDS keeps each operand row pixel-contiguous:
+// As[m][k], Bs[n][k].  Within a BK-deep slice, pixel kk sits at position
+// (kk & 1) * BK/2 + kk / 2, so the 8 pixels a lane consumes over the slice's
+// 8 MFMA steps (kk = 2 s + lane / 32) are contiguous: two ds_read_b128 per
+// 32-row block and slice.  Operands are staged through registers: the
+// loads of slice t + 1 are issued before the MFMAs of slice t and written to
+// the other LDS buffer after them; one barrier per slice.  Loads are raw
+// buffer loads, so out-of-range elements (padding, ragged tiles, the end of
+// the split) read 0 without branches.  VEC: P*Q % 4 == 0, so four
+// consecutive pixels of one dy row are one aligned float4.
 // ---------------------------------------------------------------------------
-template <int BM, int BN, int BK, int WM, int WN>
+// The raw buffer-load builtins return bit patterns: reinterpret, never convert.
+__device__ __forceinline__ float buf_load(__amdgpu_buffer_rsrc_t r, uint32_t voff)
+{
+    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, voff, 0, 0));
+}
+
+__device__ __forceinline__ float4 buf_load4(__amdgpu_buffer_rsrc_t r, uint32_t voff)
+{
+    typedef float f32x4 __attribute__((ext_vector_type(4)));
+    f32x4 v = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, 0, 0));
+    return make_float4(v[0], v[1], v[2], v[3]);
+}
+
+template <int BM, int BN, int WM, int WN, bool VEC>
 __global__ __launch_bounds__(64 * WM * WN) void wgrad_gemm_kernel(const WgradArgs a)
 {
-    constexpr int NT = 64 * WM * WN;
-    constexpr int FM = BM / WM / 32, FN = BN / WN / 32;
-    constexpr int RS = NT / BK;  // rows covered per loader pass
-    constexpr int APT = BM / RS, BPT = BN / RS;
-    constexpr int LDA = BM + 4, LDB = BN + 4;
-    static_assert(NT % BK == 0 && BM % RS == 0 && BN % RS == 0, "loader mapping");
+    constexpr int BK = 16, NT = 64 * WM * WN;
+    constexpr int TM = BM / WM, TN = BN / WN, FM = TM / 32, FN = TN / 32;
+    constexpr int KP = BK + 4;                 // row stride (words), keeps b128 rows aligned
+    constexpr int G4 = BK / 4;                 // 4-pixel groups per slice
+    constexpr int RA = BM * G4 / NT, RB = BN * G4 / NT;  // 4-pixel groups per thread
+    static_assert((BM * G4) % NT == 0 && (BN * G4) % NT == 0, "loader mapping");
 
-    __shared__ float As[2][BK][LDA];
-    __shared__ float Bs[2][BK][LDB];
-    __shared__ int2 ctab[BN];
+    // 16-byte aligned: rows are written as float2 and read as float4.
+    __shared__ __attribute__((aligned(16))) float As[2][BM][KP];
+    __shared__ __attribute__((aligned(16))) float Bs[2][BN][KP];
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave % WM, wn = wave / WM;
-    const int g = blockIdx.z, split = blockIdx.y;
-    const int mtiles = (a.M + BM - 1) / BM;
-    const int mt = blockIdx.x % mtiles, nt = blockIdx.x / mtiles;
+    const int mtiles = (a.M + BM - 1) / BM, ntiles = (a.Ncol + BN - 1) / BN;
+    const int tiles = mtiles * ntiles;
+    const int lin = xcd_tile(blockIdx.x, tiles * a.groups * a.nsplit);
+    const int split = lin / (tiles * a.groups);
+    const int rest = lin - split * tiles * a.groups;
+    const int g = rest / tiles, tile = rest - g * tiles;
+    const int mt = tile % mtiles, nt = tile / mtiles;
     const int m0 = mt * BM, n0 = nt * BN;
     const int kbeg = split * a.chunk;
     const int kend = min(a.Kred, kbeg + a.chunk);
 
-    for (int n = tid; n < BN; n += NT) {
-        int col = n0 + n;
-        int2 e = make_int2(-1, 0);
-        if (col < a.Ncol) {
-            uint32_t c = fast_div((uint32_t)col, a.n_rs);
-            uint32_t rs = col - c * a.n_rs.d;
-            uint32_t r = fast_div(rs, a.n_s);
-            uint32_t s = rs - r * a.n_s.d;
-            e = make_int2((int)(c * a.HW + r * a.W + s), (int)((r << 16) | s));
-        }
-        ctab[n] = e;
+    const __amdgpu_buffer_rsrc_t rdy = make_rsrc(a.dy, a.dy_bytes);
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(a.x, a.x_bytes);
+
+    // Loader mapping: thread -> 4-pixel group q4 (same for A and B) and rows
+    // row = tid / G4 + (NT / G4) * i.
+    const int q4 = tid % G4, row0 = tid / G4;
+    constexpr int RSTEP = NT / G4;
+    uint32_t a_row[RA];  // byte offset of dy row (g*Kg + m) within an image, masked
+#pragma unroll
+    for (int i = 0; i < RA; i++) {
+        int m = m0 + row0 + RSTEP * i;
+        a_row[i] = ((uint32_t)(g * a.M + m) * (uint32_t)a.PQ * 4u) | oob_mask(m < a.M);
     }
-    __syncthreads();
-
-    // Loader: thread -> (pixel kk = tid % BK, row = tid / BK + RS * i).
-    const int kk = tid % BK, rrow = tid / BK;
-    const float *dyg = a.dy + (long long)g * a.Kg * a.PQ;
-    const float *xg = a.x + (long long)g * a.Cg * a.HW;
-    int2 ce[BPT];
+    uint32_t b_col[RB];  // byte offset of x[., g*Cg + c][r][s] within an image, masked
+    int b_r[RB], b_s[RB];
 #pragma unroll
-    for (int i = 0; i < BPT; i++)
-        ce[i] = ctab[rrow + RS * i];
+    for (int i = 0; i < RB; i++) {
+        int n = n0 + row0 + RSTEP * i;
+        bool ok = n < a.Ncol;
+        uint32_t nc = ok ? (uint32_t)n : 0u;
+        uint32_t c = fast_div(nc, a.n_rs);
+        uint32_t rs = nc - c * a.n_rs.d;
+        uint32_t r = fast_div(rs, a.n_s);
+        uint32_t s_ = rs - r * a.n_s.d;
+        b_r[i] = (int)r;
+        b_s[i] = (int)s_;
+        b_col[i] = ((uint32_t)(g * a.Cg + c) * (uint32_t)a.HW * 4u) | oob_mask(ok);
+    }
 
-    float ra[APT], rb[BPT];
+    float ra[RA][4], rb[RB][4];
     auto load_slice = [&](int k0) {
-        int pix = k0 + kk;
-        bool ok = pix < kend;
-        uint32_t pc = ok ? (uint32_t)pix : 0u;
-        uint32_t img = fast_div(pc, a.pix_pq);
-        uint32_t pq = pc - img * a.pix_pq.d;
-        uint32_t p = fast_div(pq, a.pix_q);
-        uint32_t q = pq - p * a.pix_q.d;
-        long long abase = (long long)img * a.K * a.PQ + pq;
+        const int pix = k0 + 4 * q4;
+        // A: dy[img][g*Kg + m][pq .. pq+3]
+        if constexpr (VEC) {
+            const bool ok = pix < kend;  // the whole group shares one image row
+            const uint32_t pc = ok ? (uint32_t)pix : 0u;
+            const uint32_t img = fast_div(pc, a.pix_pq);
+            const uint32_t pq = pc - img * a.pix_pq.d;
+            const uint32_t base = (img * (uint32_t)a.dy_img_words + pq) * 4u | oob_mask(ok);
 #pragma unroll
-        for (int i = 0; i < APT; i++) {
-            int m = m0 + rrow + RS * i;
-            ra[i] = (ok && m < a.M) ? dyg[abase + (long long)m * a.PQ] : 0.f;
+            for (int i = 0; i < RA; i++) {
+                float4 v = buf_load4(rdy, (base + a_row[i]) | (a_row[i] & kOob) | (base & kOob));
+                ra[i][0] = v.x;
+                ra[i][1] = v.y;
+                ra[i][2] = v.z;
+                ra[i][3] = v.w;
+            }
         }
-        int h0 = (int)p * a.stride - a.pad, w0 = (int)q * a.stride - a.pad;
-        long long xbase = (long long)img * a.C * a.HW + (long long)h0 * a.W + w0;
+        // per-pixel decode (needed by B, and by A when not vectorised)
+        int pimg[4], pp[4], pq_[4];
+        bool pok[4];
 #pragma unroll
-        for (int i = 0; i < BPT; i++) {
-            int r = ce[i].y >> 16, s = ce[i].y & 0xffff;
-            bool okb = ok && ce[i].x >= 0 && (unsigned)(h0 + r) < (unsigned)a.H &&
-                       (unsigned)(w0 + s) < (unsigned)a.W;
-            rb[i] = okb ? xg[xbase + ce[i].x] : 0.f;
+        for (int e = 0; e < 4; e++) {
+            const int px = pix + e;
+            pok[e] = px < kend;
+            const uint32_t pc = pok[e] ? (uint32_t)px : 0u;
+            const uint32_t img = fast_div(pc, a.pix_pq);
+            const uint32_t pq = pc - img * a.pix_pq.d;
+            const uint32_t p = fast_div(pq, a.pix_q);
+            pimg[e] = (int)img;
+            pq_[e] = (int)pq;
+            pp[e] = (int)p;
+        }
+        if constexpr (!VEC) {
+#pragma unroll
+            for (int e = 0; e < 4; e++) {
+                const uint32_t base = ((uint32_t)pimg[e] * (uint32_t)a.dy_img_words +
+                                       (uint32_t)pq_[e]) * 4u | oob_mask(pok[e]);
+#pragma unroll
+                for (int i = 0; i < RA; i++)
+                    ra[i][e] = buf_load(rdy, (base + a_row[i]) | (a_row[i] & kOob) | (base & kOob));
+            }
+        }
+        // B: x[img][g*Cg + c][p*st - pad + r][q*st - pad + s]
+#pragma unroll
+        for (int e = 0; e < 4; e++) {
+            const int q = pq_[e] - pp[e] * (int)a.pix_q.d;
+            const int h0 = pp[e] * a.stride - a.pad, w0 = q * a.stride - a.pad;
+            const uint32_t ibase = (uint32_t)pimg[e] * (uint32_t)a.x_img_words * 4u;
+#pragma unroll
+            for (int i = 0; i < RB; i++) {
+                const int h = h0 + b_r[i], w = w0 + b_s[i];
+                const bool ok = pok[e] && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
+                const uint32_t off = ibase + b_col[i] + (uint32_t)(h * a.W + w) * 4u;
+                rb[i][e] = buf_load(rx, off | oob_mask(ok) | (b_col[i] & kOob));
+            }
         }
     };
+    // Pixel kk = 4 q4 + e goes to position (kk & 1) * BK/2 + kk / 2: the even
+    // pixels (e = 0, 2) are adjacent, and so are the odd ones (e = 1, 3).
     auto store_slice = [&](int buf) {
+        const int pe = 2 * q4, po = BK / 2 + 2 * q4;
 #pragma unroll
-        for (int i = 0; i < APT; i++)
-            As[buf][kk][rrow + RS * i] = ra[i];
+        for (int i = 0; i < RA; i++) {
+            float *rowp = &As[buf][row0 + RSTEP * i][0];
+            *(float2 *)&rowp[pe] = make_float2(ra[i][0], ra[i][2]);
+            *(float2 *)&rowp[po] = make_float2(ra[i][1], ra[i][3]);
+        }
 #pragma unroll
-        for (int i = 0; i < BPT; i++)
-            Bs[buf][kk][rrow + RS * i] = rb[i];
+        for (int i = 0; i < RB; i++) {
+            float *rowp = &Bs[buf][row0 + RSTEP * i][0];
+            *(float2 *)&rowp[pe] = make_float2(rb[i][0], rb[i][2]);
+            *(float2 *)&rowp[po] = make_float2(rb[i][1], rb[i][3]);
+        }
     };
 
     f32x16 acc[FM][FN];
@@ -292,6 +459,7 @@ __global__ __launch_bounds__(64 * WM * WN) void wgrad_gemm_kernel(const WgradArg
             for (int v = 0; v < 16; v++)
                 acc[i][j][v] = 0.f;
 
+    const int kr = lane >> 5, lc = lane & 31;
     const int nslices = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
     if (nslices > 0) {
         load_slice(kbeg);
@@ -302,7 +470,33 @@ __global__ __launch_bounds__(64 * WM * WN) void wgrad_gemm_kernel(const WgradArg
         const int buf = t & 1;
         if (t + 1 < nslices)
             load_slice(kbeg + (t + 1) * BK);
-        mfma_slice<BM, BN, BK, WM, WN, LDA, LDB>(As[buf], Bs[buf], acc, lane, wm, wn);
+        float4 af[FM][2], bf[FN][2];
+#pragma unroll
+        for (int i = 0; i < FM; i++) {
+            const float *rowp = &As[buf][wm * TM + i * 32 + lc][kr * (BK / 2)];
+            af[i][0] = *(const float4 *)&rowp[0];
+            af[i][1] = *(const float4 *)&rowp[4];
+        }
+#pragma unroll
+        for (int j = 0; j < FN; j++) {
+            const float *rowp = &Bs[buf][wn * TN + j * 32 + lc][kr * (BK / 2)];
+            bf[j][0] = *(const float4 *)&rowp[0];
+            bf[j][1] = *(const float4 *)&rowp[4];
+        }
+#pragma unroll
+        for (int s = 0; s < BK / 2; s++) {
+#pragma unroll
+            for (int i = 0; i < FM; i++) {
+                const float4 &av = af[i][s >> 2];
+                const float aval = (s & 3) == 0 ? av.x : (s & 3) == 1 ? av.y : (s & 3) == 2 ? av.z : av.w;
+#pragma unroll
+                for (int j = 0; j < FN; j++) {
+                    const float4 &bv = bf[j][s >> 2];
+                    const float bval = (s & 3) == 0 ? bv.x : (s & 3) == 1 ? bv.y : (s & 3) == 2 ? bv.z : bv.w;
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(aval, bval, acc[i][j], 0, 0, 0);
+                }
+            }
+        }
         if (t + 1 < nslices)
             store_slice(buf ^ 1);
         __syncthreads();
@@ -313,12 +507,12 @@ __global__ __launch_bounds__(64 * WM * WN) void wgrad_gemm_kernel(const WgradArg
     for (int i = 0; i < FM; i++)
 #pragma unroll
         for (int v = 0; v < 16; v++) {
-            int m = m0 + wm * (BM / WM) + i * 32 + acc_row(v, lane);
+            int m = m0 + wm * TM + i * 32 + acc_row(v, lane);
             if (m >= a.M)
                 continue;
 #pragma unroll
             for (int j = 0; j < FN; j++) {
-                int n = n0 + wn * (BN / WN) + j * 32 + (lane & 31);
+                int n = n0 + wn * TN + j * 32 + lc;
                 if (n < a.Ncol)
                     outg[(long long)m * a.Ncol + n] = acc[i][j][v];
             }
@@ -435,42 +629,56 @@ __global__ void bias_grad_final_kernel(const float *__restrict__ part, int K, in
 // ---------------------------------------------------------------------------
 // Launchers.
 // ---------------------------------------------------------------------------
-template <int BM, int BN, int BK, int WM, int WN, bool FAST>
-static hipError_t img_launch(const ImgGemmArgs &a, int groups, hipStream_t stream)
+template <int BM, int BN, int BK, int WM, int WN, int PAD>
+static hipError_t img_launch(const ImgGemmArgs &a, bool fast, hipStream_t stream)
 {
     int tiles = ((a.M + BM - 1) / BM) * ((a.Ncol + BN - 1) / BN);
-    dim3 grid(tiles, 1, groups);
-    hipLaunchKernelGGL((img_gemm_kernel<BM, BN, BK, WM, WN, FAST>), grid, dim3(64 * WM * WN), 0,
-                       stream, a);
+    dim3 grid(tiles * a.groups);
+    if (fast)
+        hipLaunchKernelGGL((img_gemm_kernel<BM, BN, BK, WM, WN, PAD, true>), grid,
+                           dim3(64 * WM * WN), 0, stream, a);
+    else
+        hipLaunchKernelGGL((img_gemm_kernel<BM, BN, BK, WM, WN, PAD, false>), grid,
+                           dim3(64 * WM * WN), 0, stream, a);
     return hipGetLastError();
 }
 
-hipError_t launch_img_gemm(const ImgGemmArgs &a, int groups, int tile, bool fast,
-                           hipStream_t stream)
+#ifndef MICONV_IMG_BK
+#define MICONV_IMG_BK 16
+#endif
+#ifndef MICONV_IMG_PAD
+#define MICONV_IMG_PAD 0
+#endif
+
+hipError_t launch_img_gemm(const ImgGemmArgs &a, int tile, bool fast, hipStream_t stream)
 {
-    if (tile == TILE_128x128)
-        return fast ? img_launch<128, 128, 16, 2, 2, true>(a, groups, stream)
-                    : img_launch<128, 128, 16, 2, 2, false>(a, groups, stream);
-    return fast ? img_launch<64, 64, 16, 2, 2, true>(a, groups, stream)
-                : img_launch<64, 64, 16, 2, 2, false>(a, groups, stream);
+    constexpr int K = MICONV_IMG_BK, P = MICONV_IMG_PAD;
+    switch (tile) {
+    case IMG_128x128: return img_launch<128, 128, K, 2, 2, P>(a, fast, stream);
+    case IMG_64x128: return img_launch<64, 128, K, 2, 2, P>(a, fast, stream);
+    default: return img_launch<64, 64, K, 2, 2, P>(a, fast, stream);
+    }
 }
 
-template <int BM, int BN, int BK, int WM, int WN>
-static hipError_t wgrad_launch(const WgradArgs &a, int groups, int nsplit, hipStream_t stream)
+template <int BM, int BN, int WM, int WN>
+static hipError_t wgrad_launch(const WgradArgs &a, bool vec, hipStream_t stream)
 {
     int tiles = ((a.M + BM - 1) / BM) * ((a.Ncol + BN - 1) / BN);
-    dim3 grid(tiles, nsplit, groups);
-    hipLaunchKernelGGL((wgrad_gemm_kernel<BM, BN, BK, WM, WN>), grid, dim3(64 * WM * WN), 0,
-                       stream, a);
+    dim3 grid(tiles * a.groups * a.nsplit);
+    if (vec)
+        hipLaunchKernelGGL((wgrad_gemm_kernel<BM, BN, WM, WN, true>), grid, dim3(64 * WM * WN),
+                           0, stream, a);
+    else
+        hipLaunchKernelGGL((wgrad_gemm_kernel<BM, BN, WM, WN, false>), grid, dim3(64 * WM * WN),
+                           0, stream, a);
     return hipGetLastError();
 }
 
-hipError_t launch_wgrad_gemm(const WgradArgs &a, int groups, int nsplit, int tile,
-                             hipStream_t stream)
+hipError_t launch_wgrad_gemm(const WgradArgs &a, int tile, bool vec, hipStream_t stream)
 {
     if (tile == TILE_128x128)
-        return wgrad_launch<128, 128, 16, 2, 2>(a, groups, nsplit, stream);
-    return wgrad_launch<64, 64, 16, 2, 2>(a, groups, nsplit, stream);
+        return wgrad_launch<128, 128, 2, 2>(a, vec, stream);
+    return wgrad_launch<64, 64, 2, 2>(a, vec, stream);
 }
 
 static unsigned blocks_for(long long total, int nt)

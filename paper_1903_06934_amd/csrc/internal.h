@@ -41,13 +41,14 @@ FastDiv make_fastdiv(uint32_t d);
 //   out[img][g * M + m][ci * ostep + ooff_h][cj * ostep + ooff_w] = C + bias
 // ---------------------------------------------------------------------------
 struct ImgGemmArgs {
-    int M, Ncol, Kred;
+    int M, Ncol, Kred, groups;
     const float *A;
-    long long a_gstride;  // Kred * M
+    uint32_t a_bytes;     // groups * Kred * M * 4 (< 2^31)
     const float *src;
+    uint32_t src_bytes;   // bytes of the source images this launch reads (< 2^31)
     int cin;              // source channels per group
     int src_h, src_w, src_hw;
-    long long src_img_stride;
+    uint32_t src_img_words;  // words per source image
     FastDiv col_hw, col_w;  // d = col_h * col_w, col_w
     int cstep, coff_h, coff_w, tsign;
     FastDiv k_cin, k_tw;    // d = cin, taps_w
@@ -59,17 +60,21 @@ struct ImgGemmArgs {
 };
 
 // ---------------------------------------------------------------------------
-// Backward-weight GEMM, per group g (grid z) and split s (grid y):
+// Backward-weight GEMM, per split s and group g (both folded into the 1-D grid):
 //   out[s][g][m][n] = sum over pixels pix in split s of
 //                     dy[img][g*Kg + m][p][q] * x[img][g*Cg + c][p*st - pad + r][q*st - pad + s']
 //   m in [0, Kg),  n = c * R * S + r * S + s'  in [0, Cg R S),
-//   pix = img * P * Q + p * Q + q in [s * chunk, min((s+1) * chunk, N P Q)).
+//   pix = img * P * Q + p * Q + q in [s * chunk, min((s+1) * chunk, Kred)),
+// where img counts from the launch's first image (dy and x point there).
 // ---------------------------------------------------------------------------
 struct WgradArgs {
-    int M, Ncol, Kred;
+    int M, Ncol, Kred, groups, nsplit;
     const float *dy;
     const float *x;
-    int K, C, H, W, HW, PQ, stride, pad, Kg, Cg;
+    uint32_t dy_bytes, x_bytes;      // bytes of this launch's images (< 2^31)
+    uint32_t dy_img_words, x_img_words;
+    int Cg;                          // input channels per group
+    int H, W, HW, PQ, stride, pad;
     FastDiv pix_pq, pix_q;  // d = P * Q, Q
     FastDiv n_rs, n_s;      // d = R * S, S
     int chunk;
@@ -77,12 +82,12 @@ struct WgradArgs {
     long long split_stride;  // G * M * Ncol
 };
 
+// Image-GEMM tile shapes (BM x BN; every shape runs 4 waves).
+enum ImgTile { IMG_128x128 = 0, IMG_64x128, IMG_64x64 };
 enum TileCfg { TILE_128x128 = 0, TILE_64x64 = 1 };
 
-hipError_t launch_img_gemm(const ImgGemmArgs &a, int groups, int tile, bool fast,
-                           hipStream_t stream);
-hipError_t launch_wgrad_gemm(const WgradArgs &a, int groups, int nsplit, int tile,
-                             hipStream_t stream);
+hipError_t launch_img_gemm(const ImgGemmArgs &a, int tile, bool fast, hipStream_t stream);
+hipError_t launch_wgrad_gemm(const WgradArgs &a, int tile, bool vec, hipStream_t stream);
 
 // wp[g][(r*S + s)*Cg + c][k] = w[g*Kg + k][c][r][s]
 hipError_t launch_pack_fwd(const float *w, float *wp, int K, int Cg, int R, int S, int G,
