@@ -216,7 +216,7 @@ size_t bwd_data_ws(const Geom &g)
 // workgroups run; each split writes its own partial dw, summed afterwards in
 // split order.  Launches never straddle a batch chunk (images_per_launch).
 struct WgradPlan {
-    int tile, chunk, nsplit, nb, bias_chunks;
+    int tile, slice, chunk, nsplit, nb, bias_chunks;
     size_t part_bytes, bias_bytes;
 };
 
@@ -225,17 +225,28 @@ WgradPlan wgrad_plan(const Geom &g)
     WgradPlan p;
     int M = g.Kg, Ncol = g.Cg * g.R * g.S;
     long long PQ = (long long)g.P * g.Q, Kred = (long long)g.N * PQ;
-    p.tile = (M > 64 && Ncol > 64) ? TILE_128x128 : TILE_64x64;
-    int bm = p.tile == TILE_128x128 ? 128 : 64;
-    long long tiles = (long long)gemm_tiles(M, Ncol, bm, bm) * g.G;
+    long long tiles;
+    if (g.Cg >= 32) {
+        // Tap-uniform tiles, 64 rows of K/G x 64 channels of one tap (the
+        // 64x64 shape measured fastest on every layer of the five stacks).
+        p.tile = WG_TAP_64x64;
+        tiles = (long long)((M + 63) / 64) * g.R * g.S * ((g.Cg + 63) / 64) * g.G;
+        p.slice = 64;
+    } else {
+        // Few channels per group: pack (c, r, s) into the columns instead.
+        p.tile = (M > 64 && Ncol > 64) ? WG_128x128 : WG_64x64;
+        int bm = p.tile == WG_128x128 ? 128 : 64;
+        tiles = (long long)gemm_tiles(M, Ncol, bm, bm) * g.G;
+        p.slice = kBK;
+    }
     long long ns = (kTargetWorkgroups + tiles - 1) / tiles;
-    long long max_ns = Kred / (kBK * 8);
+    long long max_ns = Kred / (p.slice * 8);
     if (ns > max_ns)
         ns = max_ns;
     if (ns < 1)
         ns = 1;
     long long chunk = (Kred + ns - 1) / ns;
-    chunk = (chunk + kBK - 1) / kBK * kBK;
+    chunk = (chunk + p.slice - 1) / p.slice * p.slice;
     p.chunk = (int)chunk;
     p.nb = images_per_launch(g);
     long long total = 0;

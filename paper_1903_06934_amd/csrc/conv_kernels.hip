@@ -520,6 +520,153 @@ __global__ __launch_bounds__(64 * WM * WN) void wgrad_gemm_kernel(const WgradArg
 }
 
 // ---------------------------------------------------------------------------
+// Backward-weight GEMM with tap-uniform tiles (same WgradArgs; requires the
+// columns of a tile to share one filter tap).
+//
+// dw columns are taken in (tap, channel) order: a workgroup tile owns one tap
+// t = r S + s and BN consecutive channels, so its B operand is x shifted by
+// (r, s) — for a given pixel, the BN rows of B are BN channels at one
+// spatial position.  A slice of the reduction is 64 consecutive pixels; lane
+// l owns pixel k0 + l of the slice and computes, once per slice, the byte
+// offset of its dy element (row m0) and of its x element (channel c0, shifted
+// by the tap), or an out-of-range offset when the pixel is outside the split
+// or the image.  Every row of the A (dy) and B (x) tiles is then one
+// direct-to-LDS wave-load whose offset is that base plus a row stride: one
+// VALU add.  Rows past K/G or C/G read neighbouring data (or zeros) and are
+// simply not stored.
+//
+// LDS holds each row pixel-contiguous (64 words + 4 of padding, so the
+// ds_read_b128 of 16 consecutive rows hit distinct banks).  MFMA step s
+// (0..31) takes pixel s from the first half of the slice in lanes 0-31 and
+// pixel 32 + s in lanes 32-63, so a lane's 32 operands of a row are
+// contiguous: 8 ds_read_b128.  The tile is single-buffered: after a barrier
+// every wave copies its operands of the slice into registers, a second
+// barrier frees the LDS, the next slice's loads are issued, and the slice's
+// MFMAs run while they land.
+// ---------------------------------------------------------------------------
+template <int BM, int BN, int WM, int WN>
+__global__ __launch_bounds__(64 * WM * WN) void wgrad_tap_kernel(const WgradArgs a)
+{
+    constexpr int BK = 64, LDR = BK + 4;
+    constexpr int NW = WM * WN, TM = BM / WM, TN = BN / WN, FM = TM / 32, FN = TN / 32;
+    static_assert(BM % NW == 0 && BN % NW == 0, "rows per wave");
+
+    __shared__ __attribute__((aligned(16))) float L[(BM + BN) * LDR];
+
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wm = wave % WM, wn = wave / WM;
+    const int RS = (int)a.n_rs.d;
+    const int cblocks = (a.Cg + BN - 1) / BN;
+    const int mtiles = (a.M + BM - 1) / BM, ntiles = RS * cblocks;
+    const int tiles = mtiles * ntiles;
+    const int lin = xcd_tile(blockIdx.x, tiles * a.groups * a.nsplit);
+    const int split = lin / (tiles * a.groups);
+    const int rest = lin - split * tiles * a.groups;
+    const int g = rest / tiles, tile = rest - g * tiles;
+    const int mt = tile % mtiles, nt = tile / mtiles;
+    const int tap = nt / cblocks, c0 = (nt - tap * cblocks) * BN;
+    const int r = (int)fast_div((uint32_t)tap, a.n_s), s_ = tap - r * (int)a.n_s.d;
+    const int m0 = mt * BM;
+    const int kbeg = split * a.chunk;
+    const int kend = min(a.Kred, kbeg + a.chunk);
+
+    const __amdgpu_buffer_rsrc_t rdy = make_rsrc(a.dy, a.dy_bytes);
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(a.x, a.x_bytes);
+    const uint32_t a_rowstep = (uint32_t)a.PQ * 4u, b_rowstep = (uint32_t)a.HW * 4u;
+    const uint32_t a_row0 = (uint32_t)(g * a.M + m0) * a_rowstep;
+    const uint32_t b_row0 = (uint32_t)(g * a.Cg + c0) * b_rowstep;
+
+    auto issue = [&](int k0) {
+        const int pix = k0 + lane;
+        const bool pok = pix < kend;
+        const uint32_t pc = pok ? (uint32_t)pix : 0u;
+        const uint32_t img = fast_div(pc, a.pix_pq);
+        const uint32_t pq = pc - img * a.pix_pq.d;
+        const uint32_t p = fast_div(pq, a.pix_q);
+        const int q = (int)(pq - p * a.pix_q.d);
+        const int h = (int)p * a.stride - a.pad + r, w = q * a.stride - a.pad + s_;
+        const bool xok = pok && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
+        const uint32_t abase = pok ? (img * a.dy_img_words + pq) * 4u + a_row0 : kOob;
+        const uint32_t bbase =
+            xok ? (img * a.x_img_words + (uint32_t)(h * a.W + w)) * 4u + b_row0 : kOob;
+#pragma unroll
+        for (int i = 0; i < BM / NW; i++) {
+            const int j = wave + NW * i;
+            lds_load(rdy, &L[j * LDR], abase + (uint32_t)j * a_rowstep);
+        }
+#pragma unroll
+        for (int i = 0; i < BN / NW; i++) {
+            const int j = wave + NW * i;
+            lds_load(rx, &L[(BM + j) * LDR], bbase + (uint32_t)j * b_rowstep);
+        }
+    };
+
+    f32x16 acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; i++)
+#pragma unroll
+        for (int j = 0; j < FN; j++)
+#pragma unroll
+            for (int v = 0; v < 16; v++)
+                acc[i][j][v] = 0.f;
+
+    const int kr = lane >> 5, lc = lane & 31;
+    const int nslices = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
+    if (nslices > 0)
+        issue(kbeg);
+    for (int t = 0; t < nslices; t++) {
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();  // slice t is in LDS
+        float4 af[FM][8], bf[FN][8];
+#pragma unroll
+        for (int i = 0; i < FM; i++) {
+            const float *rowp = &L[(wm * TM + i * 32 + lc) * LDR + kr * 32];
+#pragma unroll
+            for (int u = 0; u < 8; u++)
+                af[i][u] = *(const float4 *)&rowp[4 * u];
+        }
+#pragma unroll
+        for (int j = 0; j < FN; j++) {
+            const float *rowp = &L[(BM + wn * TN + j * 32 + lc) * LDR + kr * 32];
+#pragma unroll
+            for (int u = 0; u < 8; u++)
+                bf[j][u] = *(const float4 *)&rowp[4 * u];
+        }
+        __syncthreads();  // every wave holds its operands: the tile is free
+        if (t + 1 < nslices)
+            issue(kbeg + (t + 1) * BK);
+#pragma unroll
+        for (int u = 0; u < 8; u++)
+#pragma unroll
+            for (int e = 0; e < 4; e++)
+#pragma unroll
+                for (int i = 0; i < FM; i++)
+#pragma unroll
+                    for (int j = 0; j < FN; j++)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(
+                            af[i][u][e], bf[j][u][e], acc[i][j], 0, 0, 0);
+    }
+
+    // Column (c0 + col) of the tile is dw[k][c0 + col][r][s]: stride R*S.
+    float *outg = a.out + (long long)split * a.split_stride + (long long)g * a.M * a.Ncol;
+#pragma unroll
+    for (int i = 0; i < FM; i++)
+#pragma unroll
+        for (int v = 0; v < 16; v++) {
+            int m = m0 + wm * TM + i * 32 + acc_row(v, lane);
+            if (m >= a.M)
+                continue;
+#pragma unroll
+            for (int j = 0; j < FN; j++) {
+                int c = c0 + wn * TN + j * 32 + lc;
+                if (c < a.Cg)
+                    outg[(long long)m * a.Ncol + (long long)c * RS + tap] = acc[i][j][v];
+            }
+        }
+}
+
+// ---------------------------------------------------------------------------
 // Filter packing.
 // ---------------------------------------------------------------------------
 __global__ void pack_fwd_kernel(const float *__restrict__ w, float *__restrict__ wp, int Kg,
@@ -674,11 +821,24 @@ static hipError_t wgrad_launch(const WgradArgs &a, bool vec, hipStream_t stream)
     return hipGetLastError();
 }
 
+template <int BM, int BN, int WM, int WN>
+static hipError_t wgrad_tap_launch(const WgradArgs &a, hipStream_t stream)
+{
+    int RS = (int)a.n_rs.d;
+    int tiles = ((a.M + BM - 1) / BM) * RS * ((a.Cg + BN - 1) / BN);
+    hipLaunchKernelGGL((wgrad_tap_kernel<BM, BN, WM, WN>), dim3(tiles * a.groups * a.nsplit),
+                       dim3(64 * WM * WN), 0, stream, a);
+    return hipGetLastError();
+}
+
 hipError_t launch_wgrad_gemm(const WgradArgs &a, int tile, bool vec, hipStream_t stream)
 {
-    if (tile == TILE_128x128)
-        return wgrad_launch<128, 128, 2, 2>(a, vec, stream);
-    return wgrad_launch<64, 64, 2, 2>(a, vec, stream);
+    switch (tile) {
+    case WG_128x128: return wgrad_launch<128, 128, 2, 2>(a, vec, stream);
+    case WG_TAP_128x64: return wgrad_tap_launch<128, 64, 2, 2>(a, stream);
+    case WG_TAP_64x64: return wgrad_tap_launch<64, 64, 2, 2>(a, stream);
+    default: return wgrad_launch<64, 64, 2, 2>(a, vec, stream);
+    }
 }
 
 static unsigned blocks_for(long long total, int nt)

@@ -84,7 +84,9 @@ struct WgradArgs {
 
 // Image-GEMM tile shapes (BM x BN; every shape runs 4 waves).
 enum ImgTile { IMG_128x128 = 0, IMG_64x128, IMG_64x64 };
-enum TileCfg { TILE_128x128 = 0, TILE_64x64 = 1 };
+// Backward-weight kernels: packed (c, r, s) columns, or tap-uniform tiles
+// (BM rows of K/G x BN channels of one tap).
+enum WgradTile { WG_128x128 = 0, WG_64x64, WG_TAP_128x64, WG_TAP_64x64 };
 
 hipError_t launch_img_gemm(const ImgGemmArgs &a, int tile, bool fast, hipStream_t stream);
 hipError_t launch_wgrad_gemm(const WgradArgs &a, int tile, bool vec, hipStream_t stream);
