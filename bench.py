@@ -55,6 +55,10 @@ def parse():
                     help="target CPU time of the oracle sample (0 disables it)")
     ap.add_argument("--flush", action="store_true",
                     help="write a 512 MiB buffer between per-layer repeats (cold caches)")
+    ap.add_argument("--profile-pass", default=None, metavar="CFG:LAYER:PASS",
+                    help="only run one layer pass --reps times (for rocprofv3), print nothing else")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only copy 1 GiB device-to-device 3 times (HBM counter calibration)")
     return ap.parse_args()
 
 
@@ -194,6 +198,29 @@ def kernel_time(run, p, reps, hev):
     return sum(ts) / len(ts)
 
 
+TRAFFIC_DIR = os.path.join(ROOT, "profiles")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_1903_06934_amd", "csrc", "conv_kernels.hip")
+
+
+def measured_traffic(cfg, layer, p):
+    """HBM bytes per launch of the (cfg, layer, pass) GEMM from a committed
+    rocprofv3 counter summary (profiles/traffic_*.txt), if one exists for
+    exactly this workload and the kernel source has not changed since."""
+    import glob
+    import hashlib
+    sha = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
+    for f in sorted(glob.glob(os.path.join(TRAFFIC_DIR, "traffic_*.txt"))):
+        kv = {}
+        for line in open(f):
+            if ":" in line and not line.startswith(("#", " ")):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+        if (kv.get("workload") == f"{cfg}:{layer}:{p}" and kv.get("kernel_source_sha256") == sha
+                and "traffic_bytes_per_launch" in kv):
+            return float(kv["traffic_bytes_per_launch"])
+    return None
+
+
 def cpu_baseline(cfg, layers, target_s):
     """The oracle (fp64 loop nests, all host threads) on a batch slice of
     the same stack: images/s on the host."""
@@ -284,6 +311,7 @@ def bench_config(cfg, args, with_cpu):
         ach = bytes_of(drun.L, dom["pass"]) / k_ms / 1e6
         roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_GBS,
                 "unit": "GB/s", "frac": round(ach / PEAK_GBS, 4), "traffic": None}
+    roof["traffic"] = measured_traffic(cfg, dom["layer"], dom["pass"])
     roof.update({"kernel": f"{dom['pass']} GEMM of {dom['layer']}",
                  "kernel_ms": round(k_ms, 4), "flops_per_launch": F,
                  "bytes_per_launch": bytes_of(drun.L, dom["pass"])})
@@ -324,6 +352,26 @@ def main():
     torch.cuda.set_device(0)
     import paper_1903_06934_amd as m
     m.lib()
+    if args.copy_calibration:
+        x = torch.ones(1 << 28, device="cuda")
+        y = torch.empty_like(x)
+        for _ in range(3):
+            y.copy_(x)
+        torch.cuda.synchronize()
+        print("copied 1 GiB device-to-device 3 times", flush=True)
+        return
+    if args.profile_pass:
+        import workloads
+        cfg, lname, p = args.profile_pass.split(":")
+        cfg = int(cfg)
+        layers = workloads.config(cfg)[1]
+        li = [L.name for L in layers].index(lname)
+        run = LayerRun(cfg, li, layers[li], torch.cuda.current_stream().cuda_stream)
+        for _ in range(args.reps):
+            run.run(p)
+        torch.cuda.synchronize()
+        print(f"ran {args.profile_pass} x{args.reps}", flush=True)
+        return
     cfgs = [0, 1, 2, 3, 4] if args.config == "all" else [int(args.config)]
     for cfg in cfgs:
         line = bench_config(cfg, args, with_cpu=args.cpu_seconds > 0 and cfg == cfgs[0])

@@ -216,7 +216,8 @@ size_t bwd_data_ws(const Geom &g)
 // workgroups run; each split writes its own partial dw, summed afterwards in
 // split order.  Launches never straddle a batch chunk (images_per_launch).
 struct WgradPlan {
-    int tile, slice, chunk, nsplit, nb, bias_chunks;
+    int tile, slice, chunk, nsplit, nb;
+    bool via_part;
     size_t part_bytes, bias_bytes;
 };
 
@@ -255,15 +256,11 @@ WgradPlan wgrad_plan(const Geom &g)
         total += (n * PQ + chunk - 1) / chunk;
     }
     p.nsplit = (int)total;
-    p.part_bytes = p.nsplit > 1 ? align_up((size_t)p.nsplit * g.K * Ncol * sizeof(float)) : 0;
-    long long bc = (1024 + g.K - 1) / g.K;
-    long long bmax = (Kred + 4095) / 4096;
-    if (bc > bmax)
-        bc = bmax;
-    if (bc < 1)
-        bc = 1;
-    p.bias_chunks = (int)bc;
-    p.bias_bytes = align_up((size_t)g.K * bc * sizeof(float));
+    // Tap-uniform tiles always go through the partial buffer (the reduction
+    // also reorders columns); packed tiles write dw directly when unsplit.
+    p.via_part = p.tile >= WG_TAP_128x64 || p.nsplit > 1;
+    p.part_bytes = p.via_part ? align_up((size_t)p.nsplit * g.K * Ncol * sizeof(float)) : 0;
+    p.bias_bytes = align_up((size_t)p.nsplit * g.K * sizeof(float));
     return p;
 }
 
@@ -537,8 +534,11 @@ int conv_bwd_weight(int N, int C, int H, int W, int K, int R, int S, int stride,
     a.n_s = make_fastdiv(S);
     a.chunk = p.chunk;
     a.split_stride = (long long)K * a.Ncol;
-    const bool vec = a.PQ % 4 == 0;
+    a.K = K;
     float *part = (float *)ws;
+    float *db_part = (float *)((char *)ws + p.part_bytes);
+    a.db_part = db ? db_part : nullptr;
+    const bool vec = a.PQ % 4 == 0;
     if (mark(tl_events.before, stream) != hipSuccess)
         return MICONV_ERR_LAUNCH;
     int split0 = 0;
@@ -550,23 +550,24 @@ int conv_bwd_weight(int N, int C, int H, int W, int K, int R, int S, int stride,
         a.x = x + n0 * xi;
         a.dy_bytes = (uint32_t)(n * yi * (long long)fb);
         a.x_bytes = (uint32_t)(n * xi * (long long)fb);
-        a.out = p.nsplit > 1 ? part + (long long)split0 * a.split_stride : dw;
+        a.out = p.via_part ? part + (long long)split0 * a.split_stride : dw;
+        if (db)
+            a.db_part = db_part + (long long)split0 * K;
         if ((st = launch_status(launch_wgrad_gemm(a, p.tile, vec, stream))) != MICONV_OK)
             return st;
         split0 += a.nsplit;
     }
     if (mark(tl_events.after, stream) != hipSuccess)
         return MICONV_ERR_LAUNCH;
-    if (p.nsplit > 1 &&
-        (st = launch_status(launch_splitk_reduce(part, p.nsplit, a.split_stride,
-                                                 (long long)K * a.Ncol, dw, stream))) != MICONV_OK)
-        return st;
-    if (db) {
-        float *bpart = (float *)((char *)ws + p.part_bytes);
-        if ((st = launch_status(launch_bias_grad(dy, N, K, g.P * g.Q, p.bias_chunks, bpart, db,
+    const bool tap_order = p.tile >= WG_TAP_128x64;
+    if (p.via_part &&
+        (st = launch_status(launch_splitk_reduce(part, p.nsplit, a.split_stride, K * a.Ncol, dw,
+                                                 tap_order ? R * S : 0, tap_order ? g.Cg : 0,
                                                  stream))) != MICONV_OK)
-            return st;
-    }
+        return st;
+    if (db && (st = launch_status(launch_splitk_reduce(db_part, p.nsplit, K, K, db, 0, 0,
+                                                       stream))) != MICONV_OK)
+        return st;
     return MICONV_OK;
 }
 

@@ -459,6 +459,13 @@ __global__ __launch_bounds__(64 * WM * WN) void wgrad_gemm_kernel(const WgradArg
             for (int v = 0; v < 16; v++)
                 acc[i][j][v] = 0.f;
 
+    // Bias gradient: the workgroups of the first column tile also sum the dy
+    // rows they stage (thread -> row tid / TPR, BK / TPR slice positions).
+    constexpr int TPR = NT / BM;
+    const bool do_bias = a.db_part != nullptr && nt == 0;
+    const int brow = tid / TPR, bpart = tid % TPR;
+    float bsum = 0.f;
+
     const int kr = lane >> 5, lc = lane & 31;
     const int nslices = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
     if (nslices > 0) {
@@ -470,6 +477,17 @@ __global__ __launch_bounds__(64 * WM * WN) void wgrad_gemm_kernel(const WgradArg
         const int buf = t & 1;
         if (t + 1 < nslices)
             load_slice(kbeg + (t + 1) * BK);
+        if (do_bias) {
+            const float *rowp = &As[buf][brow][bpart * (BK / TPR)];
+#pragma unroll
+            for (int u = 0; u < BK / TPR; u += 4) {
+                float4 v = *(const float4 *)&rowp[u];
+                bsum += v.x;
+                bsum += v.y;
+                bsum += v.z;
+                bsum += v.w;
+            }
+        }
         float4 af[FM][2], bf[FN][2];
 #pragma unroll
         for (int i = 0; i < FM; i++) {
@@ -500,6 +518,15 @@ __global__ __launch_bounds__(64 * WM * WN) void wgrad_gemm_kernel(const WgradArg
         if (t + 1 < nslices)
             store_slice(buf ^ 1);
         __syncthreads();
+    }
+
+    if (do_bias) {
+#pragma unroll
+        for (int off = 1; off < TPR; off <<= 1)
+            bsum += __shfl_xor(bsum, off, 64);
+        const int m = m0 + brow;
+        if (bpart == 0 && m < a.M)
+            a.db_part[(long long)split * a.K + g * a.M + m] = bsum;
     }
 
     float *outg = a.out + (long long)split * a.split_stride + (long long)g * a.M * a.Ncol;
@@ -611,6 +638,13 @@ __global__ __launch_bounds__(64 * WM * WN) void wgrad_tap_kernel(const WgradArgs
             for (int v = 0; v < 16; v++)
                 acc[i][j][v] = 0.f;
 
+    // Bias gradient: the workgroups of tap 0 and the first channel block also
+    // sum the dy rows they stage (thread -> row tid / TPR, 64 / TPR pixels).
+    constexpr int TPR = 64 * NW / BM;
+    const bool do_bias = a.db_part != nullptr && tap == 0 && c0 == 0;
+    const int brow = threadIdx.x / TPR, bpart = threadIdx.x % TPR;
+    float bsum = 0.f;
+
     const int kr = lane >> 5, lc = lane & 31;
     const int nslices = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
     if (nslices > 0)
@@ -618,6 +652,17 @@ __global__ __launch_bounds__(64 * WM * WN) void wgrad_tap_kernel(const WgradArgs
     for (int t = 0; t < nslices; t++) {
         __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();  // slice t is in LDS
+        if (do_bias) {
+            const float *rowp = &L[brow * LDR + bpart * (BK / TPR)];
+#pragma unroll
+            for (int u = 0; u < BK / TPR; u += 4) {
+                float4 v = *(const float4 *)&rowp[u];
+                bsum += v.x;
+                bsum += v.y;
+                bsum += v.z;
+                bsum += v.w;
+            }
+        }
         float4 af[FM][8], bf[FN][8];
 #pragma unroll
         for (int i = 0; i < FM; i++) {
@@ -648,8 +693,20 @@ __global__ __launch_bounds__(64 * WM * WN) void wgrad_tap_kernel(const WgradArgs
                             af[i][u][e], bf[j][u][e], acc[i][j], 0, 0, 0);
     }
 
-    // Column (c0 + col) of the tile is dw[k][c0 + col][r][s]: stride R*S.
-    float *outg = a.out + (long long)split * a.split_stride + (long long)g * a.M * a.Ncol;
+    if (do_bias) {
+        // Fixed butterfly over the TPR threads of a row.
+#pragma unroll
+        for (int off = 1; off < TPR; off <<= 1)
+            bsum += __shfl_xor(bsum, off, 64);
+        const int m = m0 + brow;
+        if (bpart == 0 && m < a.M)
+            a.db_part[(long long)split * a.K + g * a.M + m] = bsum;
+    }
+
+    // Partial dw in tile order [split][g*Kg + m][tap][c] (coalesced along c);
+    // the reduction kernel moves it to dw[k][c][r][s].
+    float *outg = a.out + (long long)split * a.split_stride + (long long)g * a.M * a.Ncol +
+                  (long long)tap * a.Cg;
 #pragma unroll
     for (int i = 0; i < FM; i++)
 #pragma unroll
@@ -661,7 +718,7 @@ __global__ __launch_bounds__(64 * WM * WN) void wgrad_tap_kernel(const WgradArgs
             for (int j = 0; j < FN; j++) {
                 int c = c0 + wn * TN + j * 32 + lc;
                 if (c < a.Cg)
-                    outg[(long long)m * a.Ncol + (long long)c * RS + tap] = acc[i][j][v];
+                    outg[(long long)m * a.Ncol + c] = acc[i][j][v];
             }
         }
 }
@@ -705,72 +762,45 @@ __global__ void pack_bwd_phase_kernel(const float *__restrict__ w, float *__rest
 }
 
 // ---------------------------------------------------------------------------
-// Deterministic split-K reduction: fixed order over splits.
+// Deterministic split-K reduction.  out[dst(i)] = sum over s < nsplit of
+// part[s * stride + i].  A block handles 32 consecutive elements with 8
+// threads each: thread j sums splits j, j + 8, j + 16, ... in order, and the
+// 8 partial sums are then added in the order j = 0..7, so the result depends
+// only on nsplit.  dst is the identity, or (tap_cg > 0) the move from the
+// tap-uniform kernel's [k][tap][c] order to dw's [k][c][tap] order.
 // ---------------------------------------------------------------------------
-__global__ void splitk_reduce_kernel(const float *__restrict__ part, int nsplit,
-                                     long long stride, long long count, float *__restrict__ out)
-{
-    for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < count;
-         i += (long long)gridDim.x * blockDim.x) {
-        float s = part[i];
-        for (int k = 1; k < nsplit; k++)
-            s += part[(long long)k * stride + i];
-        out[i] = s;
-    }
-}
+constexpr int RED_E = 32, RED_J = 8;
 
-// ---------------------------------------------------------------------------
-// Bias gradient, stage 1: workgroup (k = blockIdx.x, chunk j = blockIdx.y)
-// sums dy[img][k][pq] over flat positions e = img*PQ + pq in its chunk.
-// Each thread sums a strided sequence, then a fixed butterfly over the
-// wavefront and a fixed-order sum over the waves: deterministic.
-// ---------------------------------------------------------------------------
-constexpr int BIAS_NT = 256;
-
-__device__ __forceinline__ float wave_sum(float v)
+__global__ __launch_bounds__(RED_E * RED_J) void splitk_reduce_kernel(
+    const float *__restrict__ part, int nsplit, long long stride, int count,
+    float *__restrict__ out, int taps, int tap_cg)
 {
+    __shared__ float sh[RED_J][RED_E];
+    const int e = threadIdx.x % RED_E, j = threadIdx.x / RED_E;
+    for (int base = blockIdx.x * RED_E; base < count; base += gridDim.x * RED_E) {
+        const int i = base + e;
+        float s = 0.f;
+        if (i < count)
+            for (int k = j; k < nsplit; k += RED_J)
+                s += part[(long long)k * stride + i];
+        sh[j][e] = s;
+        __syncthreads();
+        if (j == 0 && i < count) {
+            float t = sh[0][e];
 #pragma unroll
-    for (int off = 32; off >= 1; off >>= 1)
-        v += __shfl_xor(v, off, 64);
-    return v;
-}
-
-__global__ __launch_bounds__(BIAS_NT) void bias_grad_partial_kernel(
-    const float *__restrict__ dy, int N, int K, int PQ, int nchunk, float *__restrict__ part)
-{
-    __shared__ float wsum[BIAS_NT / 64];
-    const int k = blockIdx.x, j = blockIdx.y;
-    const long long total = (long long)N * PQ;
-    const long long per = (total + nchunk - 1) / nchunk;
-    const long long e0 = (long long)j * per;
-    const long long e1 = min(total, e0 + per);
-    float s = 0.f;
-    for (long long e = e0 + threadIdx.x; e < e1; e += BIAS_NT) {
-        long long img = e / PQ, pq = e - img * PQ;
-        s += dy[(img * K + k) * PQ + pq];
+            for (int jj = 1; jj < RED_J; jj++)
+                t += sh[jj][e];
+            int d = i;
+            if (tap_cg > 0) {
+                int per = taps * tap_cg;
+                int k = i / per, rem = i - k * per;
+                int tap = rem / tap_cg, c = rem - tap * tap_cg;
+                d = k * per + c * taps + tap;
+            }
+            out[d] = t;
+        }
+        __syncthreads();
     }
-    s = wave_sum(s);
-    if ((threadIdx.x & 63) == 0)
-        wsum[threadIdx.x >> 6] = s;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        float t = wsum[0];
-        for (int i = 1; i < BIAS_NT / 64; i++)
-            t += wsum[i];
-        part[(long long)k * nchunk + j] = t;
-    }
-}
-
-__global__ void bias_grad_final_kernel(const float *__restrict__ part, int K, int nchunk,
-                                       float *__restrict__ db)
-{
-    int k = blockIdx.x * blockDim.x + threadIdx.x;
-    if (k >= K)
-        return;
-    float s = part[(long long)k * nchunk];
-    for (int j = 1; j < nchunk; j++)
-        s += part[(long long)k * nchunk + j];
-    db[k] = s;
 }
 
 // ---------------------------------------------------------------------------
@@ -867,27 +897,14 @@ hipError_t launch_pack_bwd_phase(const float *w, float *wr, int K, int Cg, int R
     return hipGetLastError();
 }
 
-hipError_t launch_splitk_reduce(const float *part, int nsplit, long long stride,
-                                long long count, float *out, hipStream_t stream)
+hipError_t launch_splitk_reduce(const float *part, int nsplit, long long stride, int count,
+                                float *out, int taps, int tap_cg, hipStream_t stream)
 {
-    long long blocks = (count + 255) / 256;
+    long long blocks = (count + RED_E - 1) / RED_E;
     if (blocks > 65536)
         blocks = 65536;
-    hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, part,
-                       nsplit, stride, count, out);
-    return hipGetLastError();
-}
-
-hipError_t launch_bias_grad(const float *dy, int N, int K, int PQ, int nchunk, float *part,
-                            float *db, hipStream_t stream)
-{
-    hipLaunchKernelGGL(bias_grad_partial_kernel, dim3(K, nchunk), dim3(BIAS_NT), 0, stream, dy,
-                       N, K, PQ, nchunk, part);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess)
-        return e;
-    hipLaunchKernelGGL(bias_grad_final_kernel, dim3((K + 255) / 256), dim3(256), 0, stream, part,
-                       K, nchunk, db);
+    hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)blocks), dim3(RED_E * RED_J), 0,
+                       stream, part, nsplit, stride, count, out, taps, tap_cg);
     return hipGetLastError();
 }
 

@@ -80,6 +80,8 @@ struct WgradArgs {
     int chunk;
     float *out;
     long long split_stride;  // G * M * Ncol
+    int K;                   // all filters (G * M): the stride of db_part
+    float *db_part;          // [split][K] partial bias gradients, or null
 };
 
 // Image-GEMM tile shapes (BM x BN; every shape runs 4 waves).
@@ -99,12 +101,9 @@ hipError_t launch_pack_fwd(const float *w, float *wp, int K, int Cg, int R, int 
 hipError_t launch_pack_bwd_phase(const float *w, float *wr, int K, int Cg, int R, int S,
                                  int G, int r0, int s0, int nr, int ns, int stride,
                                  hipStream_t stream);
-// out[i] = sum_{s < nsplit} part[s * stride + i], in order of s.
-hipError_t launch_splitk_reduce(const float *part, int nsplit, long long stride,
-                                long long count, float *out, hipStream_t stream);
-// Two-stage bias gradient: part[k][j] = partial sums of dy over chunk j of
-// the N*P*Q positions of channel k, then db[k] = sum_j part[k][j] in order.
-hipError_t launch_bias_grad(const float *dy, int N, int K, int PQ, int nchunk, float *part,
-                            float *db, hipStream_t stream);
+// out[dst(i)] = sum over s < nsplit of part[s * stride + i] for i < count, in a
+// fixed order; dst = identity, or (tap_cg > 0) [k][tap][c] -> [k][c][tap].
+hipError_t launch_splitk_reduce(const float *part, int nsplit, long long stride, int count,
+                                float *out, int taps, int tap_cg, hipStream_t stream);
 
 }  // namespace miconv
