@@ -174,8 +174,61 @@ int images_per_launch(const Geom &g)
     return (int)(n < g.N ? n : g.N);
 }
 
+// Split-K for the image GEMM.  With fewer than four tiles per CU the MFMA
+// pipes starve for latency hiding; the reduction is then cut into splits of
+// at least 8 slices so that ~8 workgroups per CU run, each split writes an
+// output-shaped partial slab, and a fixed-order reduction adds them (and the
+// bias).  The slabs cost about (nsplit + 1) output passes of HBM traffic, so
+// the reduction must be deep enough to amortise them: Kred >= 600 (nsplit + 1).
+// Only for single-launch problems (no batch chunking).
+struct ImgPlan {
+    int tile, nsplit, kchunk;
+};
+
+ImgPlan img_plan(int M, long long Ncol, int Kred, int G, bool fast, bool allow_split)
+{
+    ImgPlan p;
+    p.tile = pick_img_tile(M, Ncol, G, fast);
+    p.nsplit = 1;
+    p.kchunk = Kred;
+    if (!allow_split)
+        return p;
+    const int bm = p.tile == IMG_128x128 ? 128 : 64, bn = p.tile == IMG_64x64 ? 64 : 128;
+    long long tiles = (long long)((M + bm - 1) / bm) * ((Ncol + bn - 1) / bn) * G;
+    long long slices = (Kred + kBK - 1) / kBK;
+    if (tiles >= 4 * 256 || slices < 16)
+        return p;
+    long long ns = (8 * 256 + tiles - 1) / tiles;
+    if (ns > slices / 8)
+        ns = slices / 8;
+    if (ns > Kred / 600 - 1)
+        ns = Kred / 600 - 1;
+    if (ns < 2)
+        return p;
+    p.kchunk = (int)((slices + ns - 1) / ns) * kBK;
+    p.nsplit = (Kred + p.kchunk - 1) / p.kchunk;
+    return p;
+}
+
 // ------------------------------------------------------------ fwd plan
-size_t fwd_ws(const Geom &g) { return align_up((size_t)g.K * g.Cg * g.R * g.S * sizeof(float)); }
+size_t fwd_pack_bytes(const Geom &g)
+{
+    return align_up((size_t)g.K * g.Cg * g.R * g.S * sizeof(float));
+}
+
+ImgPlan fwd_plan(const Geom &g)
+{
+    return img_plan(g.Kg, (long long)g.N * g.P * g.Q, g.Cg * g.R * g.S, g.G, g.Cg % kBK == 0,
+                    images_per_launch(g) >= g.N);
+}
+
+size_t fwd_ws(const Geom &g)
+{
+    ImgPlan p = fwd_plan(g);
+    size_t part = p.nsplit > 1 ? align_up((size_t)p.nsplit * g.N * g.K * g.P * g.Q * sizeof(float))
+                               : 0;
+    return fwd_pack_bytes(g) + part;
+}
 
 // ------------------------------------------------------------ bwd-data plan
 // Stride phase (ph, pw): input pixels h = ph + st*i, w = pw + st*j; the taps
@@ -198,7 +251,7 @@ Axis phase_axis(int in, int filt, int st, int pad, int ph)
     return a;
 }
 
-size_t bwd_data_ws(const Geom &g)
+size_t bwd_data_pack_bytes(const Geom &g)
 {
     size_t total = 0;
     for (int ph = 0; ph < g.st; ph++)
@@ -208,6 +261,21 @@ size_t bwd_data_ws(const Geom &g)
             total += align_up((size_t)g.K * g.Cg * ah.nt * aw.nt * sizeof(float));
         }
     return total;
+}
+
+// Split-K only for stride 1 (one phase covering all of dx).
+ImgPlan bwd_data_plan(const Geom &g)
+{
+    return img_plan(g.Cg, (long long)g.N * g.H * g.W, g.Kg * g.R * g.S, g.G, g.Kg % kBK == 0,
+                    g.st == 1 && images_per_launch(g) >= g.N);
+}
+
+size_t bwd_data_ws(const Geom &g)
+{
+    ImgPlan p = bwd_data_plan(g);
+    size_t part = p.nsplit > 1 ? align_up((size_t)p.nsplit * g.N * g.C * g.H * g.W * sizeof(float))
+                               : 0;
+    return bwd_data_pack_bytes(g) + part;
 }
 
 // ------------------------------------------------------------ bwd-weight plan
@@ -397,6 +465,8 @@ int conv_fwd(int N, int C, int H, int W, int K, int R, int S, int stride, int pa
     a.ooff_h = 0;
     a.ooff_w = 0;
     const bool fast = g.Cg % kBK == 0;
+    const ImgPlan plan = fwd_plan(g);
+    float *part = (float *)((char *)ws + fwd_pack_bytes(g));
     if (mark(tl_events.before, stream) != hipSuccess)
         return MICONV_ERR_LAUNCH;
     for (int n0 = 0; n0 < N; n0 += nb) {
@@ -404,12 +474,21 @@ int conv_fwd(int N, int C, int H, int W, int K, int R, int S, int stride, int pa
         a.Ncol = n * g.P * g.Q;
         a.src = x + n0 * xi;
         a.src_bytes = (uint32_t)(n * xi * (long long)fb);
-        a.out = y + n0 * yi;
-        int tile = pick_img_tile(a.M, a.Ncol, group, fast);
+        a.out = plan.nsplit > 1 ? part : y + n0 * yi;
+        a.nsplit = plan.nsplit;
+        a.kchunk = plan.kchunk;
+        a.split_stride = (long long)N * yi;
+        int tile = n == N ? plan.tile : pick_img_tile(a.M, a.Ncol, group, fast);
         if ((st = launch_status(launch_img_gemm(a, tile, fast, stream))) != MICONV_OK)
             return st;
     }
-    return launch_status(mark(tl_events.after, stream));
+    if (mark(tl_events.after, stream) != hipSuccess)
+        return MICONV_ERR_LAUNCH;
+    if (plan.nsplit > 1)
+        return launch_status(launch_splitk_bias_reduce(part, plan.nsplit, (long long)N * yi,
+                                                       (int)(N * yi), b, g.P * g.Q, K, y,
+                                                       stream));
+    return MICONV_OK;
 }
 
 int conv_bwd_data(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
@@ -434,6 +513,8 @@ int conv_bwd_data(int N, int C, int H, int W, int K, int R, int S, int stride, i
 
     const int nb = images_per_launch(g);
     const long long xi = (long long)C * H * W, yi = (long long)K * g.P * g.Q;
+    const ImgPlan plan = bwd_data_plan(g);  // nsplit > 1 only for stride 1
+    float *part = (float *)((char *)ws + bwd_data_pack_bytes(g));
     char *wsp = (char *)ws;
     bool marked = false;
     for (int ph = 0; ph < stride; ph++)
@@ -483,13 +564,22 @@ int conv_bwd_data(int N, int C, int H, int W, int K, int R, int S, int stride, i
                 a.Ncol = n * ah.n * aw.n;
                 a.src = dy + n0 * yi;
                 a.src_bytes = (uint32_t)(n * yi * (long long)fb);
-                a.out = dx + n0 * xi;
-                int tile = pick_img_tile(a.M, a.Ncol, group, fast);
+                a.out = plan.nsplit > 1 ? part : dx + n0 * xi;
+                a.nsplit = plan.nsplit;
+                a.kchunk = plan.nsplit > 1 ? plan.kchunk : a.Kred;
+                a.split_stride = (long long)N * xi;
+                int tile = stride == 1 && n == N ? plan.tile : pick_img_tile(a.M, a.Ncol, group, fast);
                 if ((st = launch_status(launch_img_gemm(a, tile, fast, stream))) != MICONV_OK)
                     return st;
             }
         }
-    return launch_status(mark(tl_events.after, stream));
+    if (mark(tl_events.after, stream) != hipSuccess)
+        return MICONV_ERR_LAUNCH;
+    if (plan.nsplit > 1)
+        return launch_status(launch_splitk_bias_reduce(part, plan.nsplit, (long long)N * xi,
+                                                       (int)(N * xi), nullptr, 1, 1, dx,
+                                                       stream));
+    return MICONV_OK;
 }
 
 int conv_bwd_weight(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,

@@ -129,10 +129,14 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
     const int mtiles = (a.M + BM - 1) / BM;
     const int ntiles = (a.Ncol + BN - 1) / BN;
     const int tiles = mtiles * ntiles;
-    const int lin = xcd_tile(blockIdx.x, tiles * a.groups);
-    const int g = lin / tiles, tile = lin - g * tiles;
+    const int lin = xcd_tile(blockIdx.x, tiles * a.groups * a.nsplit);
+    const int split = lin / (tiles * a.groups);
+    const int rest = lin - split * tiles * a.groups;
+    const int g = rest / tiles, tile = rest - g * tiles;
     const int mt = tile % mtiles, nt = tile / mtiles;
     const int m0 = mt * BM, n0 = nt * BN;
+    const int kbeg = split * a.kchunk;
+    const int kend = min(a.Kred, kbeg + a.kchunk);
 
     const __amdgpu_buffer_rsrc_t rA = make_rsrc(a.A, a.a_bytes);
     const __amdgpu_buffer_rsrc_t rB = make_rsrc(a.src, a.src_bytes);
@@ -170,7 +174,7 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
             const int li = wave + NW * j, kk = li / HA, h = li % HA;
             const int k = k0 + kk;
             const uint32_t row = a_gbase + (uint32_t)k * (uint32_t)a.M * 4u;
-            lds_load(rA, &As[buf][kk][64 * h], (row + a_off[h]) | oob_mask(k < a.Kred));
+            lds_load(rA, &As[buf][kk][64 * h], (row + a_off[h]) | oob_mask(k < kend));
         }
         if constexpr (FAST) {
             const uint32_t tap = fast_div((uint32_t)k0, a.k_cin);
@@ -198,7 +202,7 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
             for (int j = 0; j < LB; j++) {
                 const int li = wave + NW * j, kk = li / HB, h = li % HB;
                 const int k = k0 + kk;
-                const bool kok = k < a.Kred;
+                const bool kok = k < kend;
                 const uint32_t kc = kok ? (uint32_t)k : 0u;
                 const uint32_t tap = fast_div(kc, a.k_cin);
                 const int ch = (int)(kc - tap * a.k_cin.d);
@@ -224,9 +228,9 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
                 acc[i][j][v] = 0.f;
 
     const int kr = lane >> 5, lc = lane & 31;
-    const int nslices = (a.Kred + BK - 1) / BK;
+    const int nslices = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
     if (nslices > 0)
-        issue(0, 0);
+        issue(kbeg, 0);
     for (int t = 0; t < nslices; t++) {
         const int buf = t & 1;
         // Slice t has landed in LDS for every wave, and every wave is done
@@ -244,7 +248,7 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
                 bf[s][j] = Bs[buf][2 * s + kr][wn * TN + j * 32 + lc];
         }
         if (t + 1 < nslices)
-            issue((t + 1) * BK, buf ^ 1);
+            issue(kbeg + (t + 1) * BK, buf ^ 1);
 #pragma unroll
         for (int s = 0; s < BK / 2; s++)
 #pragma unroll
@@ -255,7 +259,10 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
                                                                     acc[i][j], 0, 0, 0);
     }
 
-    // Epilogue: + bias, scatter columns back to image coordinates.
+    // Epilogue: + bias, scatter columns back to image coordinates (a split
+    // writes its partial sums, without bias, to its own output-shaped slab).
+    float *const out = a.nsplit > 1 ? a.out + (long long)split * a.split_stride : a.out;
+    const float *const bias = a.nsplit > 1 ? nullptr : a.bias;
     long long obase[FN];
     bool nok[FN];
 #pragma unroll
@@ -278,12 +285,12 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
             if (m >= a.M)
                 continue;
             int oc = g * a.M + m;
-            float bv = a.bias ? a.bias[oc] : 0.f;
+            float bv = bias ? bias[oc] : 0.f;
             long long choff = (long long)oc * a.out_hw;
 #pragma unroll
             for (int j = 0; j < FN; j++)
                 if (nok[j])
-                    a.out[obase[j] + choff] = acc[i][j][v] + bv;
+                    out[obase[j] + choff] = acc[i][j][v] + bv;
         }
 }
 
@@ -810,7 +817,7 @@ template <int BM, int BN, int BK, int WM, int WN, int PAD>
 static hipError_t img_launch(const ImgGemmArgs &a, bool fast, hipStream_t stream)
 {
     int tiles = ((a.M + BM - 1) / BM) * ((a.Ncol + BN - 1) / BN);
-    dim3 grid(tiles * a.groups);
+    dim3 grid(tiles * a.groups * a.nsplit);
     if (fast)
         hipLaunchKernelGGL((img_gemm_kernel<BM, BN, BK, WM, WN, PAD, true>), grid,
                            dim3(64 * WM * WN), 0, stream, a);
@@ -894,6 +901,51 @@ hipError_t launch_pack_bwd_phase(const float *w, float *wr, int K, int Cg, int R
         return hipSuccess;
     hipLaunchKernelGGL(pack_bwd_phase_kernel, dim3(blocks_for(total, 256)), dim3(256), 0,
                        stream, w, wr, K / G, Cg, R, S, r0, s0, nr, ns, stride, total);
+    return hipGetLastError();
+}
+
+// Split-K reduction of the image GEMM: same fixed order as splitk_reduce_kernel
+// (8 threads per element, strided over splits, combined in thread order),
+// then + bias of the element's channel.
+__global__ __launch_bounds__(RED_E * RED_J) void splitk_bias_reduce_kernel(
+    const float *__restrict__ part, int nsplit, long long stride, int count,
+    const float *__restrict__ bias, FastDiv hw, FastDiv K, float *__restrict__ out)
+{
+    __shared__ float sh[RED_J][RED_E];
+    const int e = threadIdx.x % RED_E, j = threadIdx.x / RED_E;
+    for (int base = blockIdx.x * RED_E; base < count; base += gridDim.x * RED_E) {
+        const int i = base + e;
+        float s = 0.f;
+        if (i < count)
+            for (int k = j; k < nsplit; k += RED_J)
+                s += part[(long long)k * stride + i];
+        sh[j][e] = s;
+        __syncthreads();
+        if (j == 0 && i < count) {
+            float t = sh[0][e];
+#pragma unroll
+            for (int jj = 1; jj < RED_J; jj++)
+                t += sh[jj][e];
+            if (bias) {
+                const uint32_t q = fast_div((uint32_t)i, hw);
+                t += bias[q - fast_div(q, K) * K.d];
+            }
+            out[i] = t;
+        }
+        __syncthreads();
+    }
+}
+
+hipError_t launch_splitk_bias_reduce(const float *part, int nsplit, long long stride, int count,
+                                     const float *bias, int hw, int K, float *out,
+                                     hipStream_t stream)
+{
+    long long blocks = (count + RED_E - 1) / RED_E;
+    if (blocks > 65536)
+        blocks = 65536;
+    hipLaunchKernelGGL(splitk_bias_reduce_kernel, dim3((unsigned)blocks), dim3(RED_E * RED_J), 0,
+                       stream, part, nsplit, stride, count, bias, make_fastdiv(hw),
+                       make_fastdiv(K), out);
     return hipGetLastError();
 }
 

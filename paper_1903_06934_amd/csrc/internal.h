@@ -57,6 +57,10 @@ struct ImgGemmArgs {
     long long out_img_stride;
     int out_hw, out_w;
     int ostep, ooff_h, ooff_w;
+    // Split-K: split s covers reduction rows [s * kchunk, min((s+1) * kchunk, Kred))
+    // and, when nsplit > 1, writes its partial sums (no bias) to out + s * split_stride.
+    int nsplit, kchunk;
+    long long split_stride;
 };
 
 // ---------------------------------------------------------------------------
@@ -105,5 +109,10 @@ hipError_t launch_pack_bwd_phase(const float *w, float *wr, int K, int Cg, int R
 // fixed order; dst = identity, or (tap_cg > 0) [k][tap][c] -> [k][c][tap].
 hipError_t launch_splitk_reduce(const float *part, int nsplit, long long stride, int count,
                                 float *out, int taps, int tap_cg, hipStream_t stream);
+// out[i] = sum over s < nsplit of part[s * stride + i] in a fixed order,
+// + bias[(i / hw) % K] if bias is given, for i < count.
+hipError_t launch_splitk_bias_reduce(const float *part, int nsplit, long long stride, int count,
+                                     const float *bias, int hw, int K, float *out,
+                                     hipStream_t stream);
 
 }  // namespace miconv
