@@ -148,17 +148,17 @@ int gemm_tiles(int M, int Ncol, int bm, int bn)
     return ((M + bm - 1) / bm) * ((Ncol + bn - 1) / bn);
 }
 
-// Tile choice for the image GEMM.  Measured on MI355X across the layers of
-// the five benchmark stacks: the kernel is limited by latency hiding rather
-// than by MFMA issue, so the 64x64 tile (4 waves of 32x32, many workgroups
-// per CU) is best or within ~2% almost everywhere; 64x128 gains a little when
-// there are at least 8 of its tiles per CU; layers with a per-element tap
-// decode (channels per group not a multiple of the slice depth) prefer
-// 128x128 when M > 64.
+// Tile choice for the image GEMM, from measured sweeps on MI355X across the
+// layers of the five benchmark stacks.  The kernel is limited by latency
+// hiding rather than by MFMA issue: the 64x64 tile (4 waves of 32x32
+// accumulators, many workgroups per CU) is best or tied on most layers,
+// 64x128 gains a few percent when it still has >= 8 tiles per CU, and is
+// also best for the layers with a per-element tap decode (channels per group
+// not a multiple of 16: 3-channel first layers).
 int pick_img_tile(int M, long long Ncol, int G, bool fast)
 {
     if (!fast)
-        return M > 64 ? IMG_128x128 : IMG_64x64;
+        return IMG_64x128;
     long long t64x128 = (long long)((M + 63) / 64) * ((Ncol + 127) / 128) * G;
     return t64x128 >= 8 * 256 ? IMG_64x128 : IMG_64x64;
 }
@@ -433,7 +433,7 @@ int conv_fwd(int N, int C, int H, int W, int K, int R, int S, int stride, int pa
     (void)hipGetLastError();
 
     float *wp = (float *)ws;
-    if (launch_pack_fwd(w, wp, K, g.Cg, R, S, group, stream) != hipSuccess)
+    if (launch_pack_fwd(w, wp, K, g.Cg, R, S, group, g.Cg % kBK == 0, stream) != hipSuccess)
         return MICONV_ERR_LAUNCH;
 
     const int nb = images_per_launch(g);
@@ -457,6 +457,7 @@ int conv_fwd(int N, int C, int H, int W, int K, int R, int S, int stride, int pa
     a.tsign = 1;
     a.k_cin = make_fastdiv(g.Cg);
     a.k_tw = make_fastdiv(S);
+    a.k_taps = make_fastdiv(R * S);
     a.bias = b;
     a.out_img_stride = yi;
     a.out_hw = g.P * g.Q;
@@ -527,7 +528,7 @@ int conv_bwd_data(int N, int C, int H, int W, int K, int R, int S, int stride, i
             if (ah.n == 0 || aw.n == 0)
                 continue;
             if (launch_pack_bwd_phase(w, wr, K, g.Cg, R, S, group, ah.t0, aw.t0, ah.nt, aw.nt,
-                                      stride, stream) != hipSuccess)
+                                      stride, g.Kg % kBK == 0, stream) != hipSuccess)
                 return MICONV_ERR_LAUNCH;
             ImgGemmArgs a;
             a.M = g.Cg;
@@ -548,6 +549,7 @@ int conv_bwd_data(int N, int C, int H, int W, int K, int R, int S, int stride, i
             a.tsign = -1;
             a.k_cin = make_fastdiv(g.Kg);
             a.k_tw = make_fastdiv(aw.nt > 0 ? aw.nt : 1);
+            a.k_taps = make_fastdiv(ah.nt * aw.nt > 0 ? ah.nt * aw.nt : 1);
             a.bias = nullptr;
             a.out_img_stride = xi;
             a.out_hw = H * W;

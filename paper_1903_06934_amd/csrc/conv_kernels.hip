@@ -108,7 +108,7 @@ __device__ __forceinline__ int xcd_tile(int hw, int total)
 // FAST: cin % BK == 0, so a slice lies inside one filter tap; the spatial
 // bounds test and offset are then computed once per slice and column.
 // ---------------------------------------------------------------------------
-template <int BM, int BN, int BK, int WM, int WN, int PAD, bool FAST>
+template <int BM, int BN, int BK, int WM, int WN, int PAD, bool FAST, int NST>
 __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArgs a)
 {
     constexpr int NW = WM * WN;
@@ -118,10 +118,15 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
     constexpr int LA = BK * HA / NW, LB = BK * HB / NW;  // wave-loads per slice
     constexpr int LDA = BM + PAD, LDB = BN + PAD;
     static_assert(BM % 64 == 0 && BN % 64 == 0 && TM % 32 == 0 && TN % 32 == 0, "tile");
-    static_assert((BK * HA) % NW == 0 && (BK * HB) % NW == 0, "loads per wave");
+    static_assert(BK % NW == 0, "reduction rows per wave");
+    static_assert(!FAST || BK == 16, "the FAST reduction order packs 16-channel blocks");
+    static_assert(NST == 2 || NST == 3, "pipeline depth");
 
-    __shared__ float As[2][BK][LDA];
-    __shared__ float Bs[2][BK][LDB];
+    // One distinct array per pipeline stage, so that the compiler's alias
+    // analysis can tell an in-flight direct-to-LDS load from a read of
+    // another stage's buffer (it would otherwise wait for every load).
+    __shared__ float As0[BK][LDA], As1[BK][LDA], As2[NST == 3 ? BK : 1][LDA];
+    __shared__ float Bs0[BK][LDB], Bs1[BK][LDB], Bs2[NST == 3 ? BK : 1][LDB];
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -168,17 +173,22 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
         b_base[h] = (img * a.src_img_words + (uint32_t)g * a.cin * a.src_hw) * 4u;
     }
 
-    auto issue = [&](int k0, int buf) {
+    auto issue = [&](int k0, float (*Ad)[LDA], float (*Bd)[LDB]) {
+        // Wave-load j: LDS row kk = wave + NW * (j / HA), 64-wide segment h = j % HA
+        // (h is a compile-time index, so the per-lane arrays stay in registers).
 #pragma unroll
         for (int j = 0; j < LA; j++) {
-            const int li = wave + NW * j, kk = li / HA, h = li % HA;
+            const int kk = wave + NW * (j / HA), h = j % HA;
             const int k = k0 + kk;
             const uint32_t row = a_gbase + (uint32_t)k * (uint32_t)a.M * 4u;
-            lds_load(rA, &As[buf][kk][64 * h], (row + a_off[h]) | oob_mask(k < kend));
+            lds_load(rA, &Ad[kk][64 * h], (row + a_off[h]) | oob_mask(k < kend));
         }
         if constexpr (FAST) {
-            const uint32_t tap = fast_div((uint32_t)k0, a.k_cin);
-            const int ch0 = k0 - (int)(tap * a.k_cin.d);
+            // Slice k0 / 16 = cb * taps + tap covers channels 16 cb .. 16 cb + 15.
+            const uint32_t sl = (uint32_t)k0 / 16u;
+            const uint32_t cb = fast_div(sl, a.k_taps);
+            const uint32_t tap = sl - cb * a.k_taps.d;
+            const int ch0 = (int)cb * 16;
             const uint32_t tr = fast_div(tap, a.k_tw);
             const int ts = (int)(tap - tr * a.k_tw.d);
             uint32_t sp[HB], msk[HB];
@@ -193,14 +203,14 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
             }
 #pragma unroll
             for (int j = 0; j < LB; j++) {
-                const int li = wave + NW * j, kk = li / HB, h = li % HB;
-                lds_load(rB, &Bs[buf][kk][64 * h],
+                const int kk = wave + NW * (j / HB), h = j % HB;
+                lds_load(rB, &Bd[kk][64 * h],
                          (sp[h] + (uint32_t)kk * (uint32_t)a.src_hw * 4u) | msk[h]);
             }
         } else {
 #pragma unroll
             for (int j = 0; j < LB; j++) {
-                const int li = wave + NW * j, kk = li / HB, h = li % HB;
+                const int kk = wave + NW * (j / HB), h = j % HB;
                 const int k = k0 + kk;
                 const bool kok = k < kend;
                 const uint32_t kc = kok ? (uint32_t)k : 0u;
@@ -213,7 +223,7 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
                           (unsigned)wx < (unsigned)a.src_w;
                 uint32_t off = b_base[h] + ((uint32_t)ch * (uint32_t)a.src_hw +
                                             (uint32_t)(hy * a.src_w + wx)) * 4u;
-                lds_load(rB, &Bs[buf][kk][64 * h], off | oob_mask(ok));
+                lds_load(rB, &Bd[kk][64 * h], off | oob_mask(ok));
             }
         }
     };
@@ -229,26 +239,20 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
 
     const int kr = lane >> 5, lc = lane & 31;
     const int nslices = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
-    if (nslices > 0)
-        issue(kbeg, 0);
-    for (int t = 0; t < nslices; t++) {
-        const int buf = t & 1;
-        // Slice t has landed in LDS for every wave, and every wave is done
-        // reading buffer buf ^ 1 (slice t - 1).
-        __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();
+
+    // Operands of one slice -> registers, then MFMAs.
+    auto compute = [&](float (*Ac)[LDA], float (*Bc)[LDB], auto &&between) {
         float af[BK / 2][FM], bf[BK / 2][FN];
 #pragma unroll
         for (int s = 0; s < BK / 2; s++) {
 #pragma unroll
             for (int i = 0; i < FM; i++)
-                af[s][i] = As[buf][2 * s + kr][wm * TM + i * 32 + lc];
+                af[s][i] = Ac[2 * s + kr][wm * TM + i * 32 + lc];
 #pragma unroll
             for (int j = 0; j < FN; j++)
-                bf[s][j] = Bs[buf][2 * s + kr][wn * TN + j * 32 + lc];
+                bf[s][j] = Bc[2 * s + kr][wn * TN + j * 32 + lc];
         }
-        if (t + 1 < nslices)
-            issue(kbeg + (t + 1) * BK, buf ^ 1);
+        between();  // issue later slices' loads once this slice's reads are out
 #pragma unroll
         for (int s = 0; s < BK / 2; s++)
 #pragma unroll
@@ -257,6 +261,63 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
                 for (int j = 0; j < FN; j++)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[s][i], bf[s][j],
                                                                     acc[i][j], 0, 0, 0);
+    };
+
+    if constexpr (NST == 2) {
+        // Two stages: slice t + 1 loads while slice t computes; one barrier
+        // per slice (every wave's loads of slice t landed, and every wave is
+        // done reading the buffer about to be refilled).
+        auto stage = [&](int t, float (*Ac)[LDA], float (*Bc)[LDB], float (*An)[LDA],
+                         float (*Bn)[LDB]) {
+            __builtin_amdgcn_s_waitcnt(0);
+            __syncthreads();
+            compute(Ac, Bc, [&] {
+                if (t + 1 < nslices)
+                    issue(kbeg + (t + 1) * BK, An, Bn);
+            });
+        };
+        if (nslices > 0)
+            issue(kbeg, As0, Bs0);
+        for (int t = 0; t < nslices; t += 2) {
+            stage(t, As0, Bs0, As1, Bs1);
+            if (t + 1 < nslices)
+                stage(t + 1, As1, Bs1, As0, Bs0);
+        }
+    } else {
+        // Three stages: slices t + 1 and t + 2 are in flight while slice t
+        // computes.  Before the barrier a wave waits only until its own loads
+        // of slice t are done (vmcnt counts down in issue order, and the
+        // LA + LB loads of slice t + 1 may stay outstanding); a raw s_barrier
+        // (no fence, which would wait for every load) then publishes the
+        // slice, and the compiler barriers keep LDS accesses on their side.
+        constexpr int LPS = LA + LB;
+        constexpr int WAIT_NEXT = (LPS & 15) | (((LPS >> 4) & 3) << 14) | (7 << 4) | (15 << 8);
+        static_assert(LPS < 64, "vmcnt range");
+        auto stage = [&](int t, float (*Ac)[LDA], float (*Bc)[LDB], float (*An)[LDA],
+                         float (*Bn)[LDB]) {
+            if (t + 1 < nslices)
+                __builtin_amdgcn_s_waitcnt(WAIT_NEXT);
+            else
+                __builtin_amdgcn_s_waitcnt(0);
+            __asm__ volatile("" ::: "memory");
+            __builtin_amdgcn_s_barrier();
+            __asm__ volatile("" ::: "memory");
+            compute(Ac, Bc, [&] {
+                if (t + 2 < nslices)
+                    issue(kbeg + (t + 2) * BK, An, Bn);
+            });
+        };
+        if (nslices > 0)
+            issue(kbeg, As0, Bs0);
+        if (nslices > 1)
+            issue(kbeg + BK, As1, Bs1);
+        for (int t = 0; t < nslices; t += 3) {
+            stage(t, As0, Bs0, As2, Bs2);
+            if (t + 1 < nslices)
+                stage(t + 1, As1, Bs1, As0, Bs0);
+            if (t + 2 < nslices)
+                stage(t + 2, As2, Bs2, As1, Bs1);
+        }
     }
 
     // Epilogue: + bias, scatter columns back to image coordinates (a split
@@ -734,36 +795,51 @@ __global__ __launch_bounds__(64 * WM * WN) void wgrad_tap_kernel(const WgradArgs
 // Filter packing.
 // ---------------------------------------------------------------------------
 __global__ void pack_fwd_kernel(const float *__restrict__ w, float *__restrict__ wp, int Kg,
-                                int Cg, int R, int S, long long total)
+                                int Cg, int R, int S, int cblock, long long total)
 {
     long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= total)
         return;
-    // i = ((g * R*S*Cg) + (r*S + s)*Cg + c) * Kg + k
+    // i = (g * R*S*Cg + kk) * Kg + k
     int k = (int)(i % Kg);
     long long t = i / Kg;
-    int c = (int)(t % Cg);
-    t /= Cg;
-    int rs = (int)(t % (R * S));
-    int g = (int)(t / (R * S));
+    int kk = (int)(t % ((long long)R * S * Cg));
+    int g = (int)(t / ((long long)R * S * Cg));
+    int c, rs;
+    if (cblock) {  // kk = (cb * RS + rs) * 16 + ci
+        int ci = kk % 16, sl = kk / 16;
+        rs = sl % (R * S);
+        c = (sl / (R * S)) * 16 + ci;
+    } else {       // kk = rs * Cg + c
+        c = kk % Cg;
+        rs = kk / Cg;
+    }
     int r = rs / S, s = rs % S;
     wp[i] = w[(((long long)(g * Kg + k) * Cg + c) * R + r) * S + s];
 }
 
 __global__ void pack_bwd_phase_kernel(const float *__restrict__ w, float *__restrict__ wr,
                                       int Kg, int Cg, int R, int S, int r0, int s0, int nr,
-                                      int ns, int stride, long long total)
+                                      int ns, int stride, int cblock, long long total)
 {
     long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= total)
         return;
-    // i = ((g * nr*ns + rr*ns + ss) * Kg + k) * Cg + c
+    // i = (g * nr*ns*Kg + kk) * Cg + c
     int c = (int)(i % Cg);
     long long t = i / Cg;
-    int k = (int)(t % Kg);
-    t /= Kg;
-    int tap = (int)(t % (nr * ns));
-    int g = (int)(t / (nr * ns));
+    int ntap = nr * ns;
+    int kk = (int)(t % ((long long)ntap * Kg));
+    int g = (int)(t / ((long long)ntap * Kg));
+    int k, tap;
+    if (cblock) {  // kk = (kb * ntap + tap) * 16 + ki
+        int ki = kk % 16, sl = kk / 16;
+        tap = sl % ntap;
+        k = (sl / ntap) * 16 + ki;
+    } else {       // kk = tap * Kg + k
+        k = kk % Kg;
+        tap = kk / Kg;
+    }
     int r = r0 + stride * (tap / ns), s = s0 + stride * (tap % ns);
     wr[i] = w[(((long long)(g * Kg + k) * Cg + c) * R + r) * S + s];
 }
@@ -813,16 +889,21 @@ __global__ __launch_bounds__(RED_E * RED_J) void splitk_reduce_kernel(
 // ---------------------------------------------------------------------------
 // Launchers.
 // ---------------------------------------------------------------------------
+#ifndef MICONV_IMG_NST
+#define MICONV_IMG_NST 3
+#endif
+
 template <int BM, int BN, int BK, int WM, int WN, int PAD>
 static hipError_t img_launch(const ImgGemmArgs &a, bool fast, hipStream_t stream)
 {
+    constexpr int NST = MICONV_IMG_NST;
     int tiles = ((a.M + BM - 1) / BM) * ((a.Ncol + BN - 1) / BN);
     dim3 grid(tiles * a.groups * a.nsplit);
     if (fast)
-        hipLaunchKernelGGL((img_gemm_kernel<BM, BN, BK, WM, WN, PAD, true>), grid,
+        hipLaunchKernelGGL((img_gemm_kernel<BM, BN, BK, WM, WN, PAD, true, NST>), grid,
                            dim3(64 * WM * WN), 0, stream, a);
     else
-        hipLaunchKernelGGL((img_gemm_kernel<BM, BN, BK, WM, WN, PAD, false>), grid,
+        hipLaunchKernelGGL((img_gemm_kernel<BM, BN, BK, WM, WN, PAD, false, NST>), grid,
                            dim3(64 * WM * WN), 0, stream, a);
     return hipGetLastError();
 }
@@ -884,23 +965,24 @@ static unsigned blocks_for(long long total, int nt)
 }
 
 hipError_t launch_pack_fwd(const float *w, float *wp, int K, int Cg, int R, int S, int G,
-                           hipStream_t stream)
+                           bool cblock, hipStream_t stream)
 {
     long long total = (long long)K * Cg * R * S;
     hipLaunchKernelGGL(pack_fwd_kernel, dim3(blocks_for(total, 256)), dim3(256), 0, stream, w,
-                       wp, K / G, Cg, R, S, total);
+                       wp, K / G, Cg, R, S, cblock ? 1 : 0, total);
     return hipGetLastError();
 }
 
 hipError_t launch_pack_bwd_phase(const float *w, float *wr, int K, int Cg, int R, int S,
-                                 int G, int r0, int s0, int nr, int ns, int stride,
+                                 int G, int r0, int s0, int nr, int ns, int stride, bool cblock,
                                  hipStream_t stream)
 {
     long long total = (long long)K * Cg * nr * ns;
     if (total == 0)
         return hipSuccess;
     hipLaunchKernelGGL(pack_bwd_phase_kernel, dim3(blocks_for(total, 256)), dim3(256), 0,
-                       stream, w, wr, K / G, Cg, R, S, r0, s0, nr, ns, stride, total);
+                       stream, w, wr, K / G, Cg, R, S, r0, s0, nr, ns, stride, cblock ? 1 : 0,
+                       total);
     return hipGetLastError();
 }
 

@@ -33,7 +33,11 @@ FastDiv make_fastdiv(uint32_t d);
 //
 // Per group g (grid z):  out[g] (M x Ncol) = A[g] (M x Kred) * B[g] (Kred x Ncol)
 //   A[g][m][k]  = Ap[g * Kred * M + k * M + m]          (packed, k-major)
-//   k           = tap * cin + ch,  tap = tr * taps_w + ts
+//   k           = tap * cin + ch (general), or, when cin % 16 == 0 (FAST),
+//                 (cb * taps + tap) * 16 + ci with ch = 16 cb + ci: the taps of a
+//                 16-channel block are consecutive, so the source rows a
+//                 workgroup re-reads tap after tap stay in cache;
+//   tap         = tr * taps_w + ts
 //   column n    = (img, ci, cj) over  N x col_h x col_w
 //   B[g][k][n]  = src[img][g * cin + ch][hy][wx] or 0 outside the source, with
 //                 hy = ci * cstep + coff_h + tsign * tr,
@@ -52,6 +56,7 @@ struct ImgGemmArgs {
     FastDiv col_hw, col_w;  // d = col_h * col_w, col_w
     int cstep, coff_h, coff_w, tsign;
     FastDiv k_cin, k_tw;    // d = cin, taps_w
+    FastDiv k_taps;         // d = taps (FAST order)
     float *out;
     const float *bias;      // may be null
     long long out_img_stride;
@@ -97,14 +102,16 @@ enum WgradTile { WG_128x128 = 0, WG_64x64, WG_TAP_128x64, WG_TAP_64x64 };
 hipError_t launch_img_gemm(const ImgGemmArgs &a, int tile, bool fast, hipStream_t stream);
 hipError_t launch_wgrad_gemm(const WgradArgs &a, int tile, bool vec, hipStream_t stream);
 
-// wp[g][(r*S + s)*Cg + c][k] = w[g*Kg + k][c][r][s]
+// wp[g][kk][k] = w[g*Kg + k][c][r][s] with kk = (r*S + s)*Cg + c, or, if
+// cblock (Cg % 16 == 0), kk = ((c / 16) * R*S + r*S + s) * 16 + c % 16.
 hipError_t launch_pack_fwd(const float *w, float *wp, int K, int Cg, int R, int S, int G,
-                           hipStream_t stream);
-// One stride phase of the backward-data filter:
-// wr[g][(rr*ns + ss)*Kg + k][c] = w[g*Kg + k][c][r0 + st*rr][s0 + st*ss]
+                           bool cblock, hipStream_t stream);
+// One stride phase of the backward-data filter: wr[g][kk][c] =
+// w[g*Kg + k][c][r0 + st*rr][s0 + st*ss] with tap = rr*ns + ss and kk = tap*Kg + k,
+// or, if cblock (Kg % 16 == 0), kk = ((k / 16) * nr*ns + tap) * 16 + k % 16.
 hipError_t launch_pack_bwd_phase(const float *w, float *wr, int K, int Cg, int R, int S,
                                  int G, int r0, int s0, int nr, int ns, int stride,
-                                 hipStream_t stream);
+                                 bool cblock, hipStream_t stream);
 // out[dst(i)] = sum over s < nsplit of part[s * stride + i] for i < count, in a
 // fixed order; dst = identity, or (tap_cg > 0) [k][tap][c] -> [k][c][tap].
 hipError_t launch_splitk_reduce(const float *part, int nsplit, long long stride, int count,
