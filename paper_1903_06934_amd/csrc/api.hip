@@ -157,10 +157,27 @@ int gemm_tiles(int M, int Ncol, int bm, int bn)
 // not a multiple of 16: 3-channel first layers).
 int pick_img_tile(int M, long long Ncol, int G, bool fast)
 {
+    // Row counts that a 64-row tile would leave partly empty.
+    if (M <= 16)
+        return IMG_16x128;
+    if (M <= 32)
+        return IMG_32x128;
+    if (M <= 48)
+        return IMG_48x128;
+    if (M > 64 && M <= 96)
+        return IMG_96x128;
     if (!fast)
         return IMG_64x128;
     long long t64x128 = (long long)((M + 63) / 64) * ((Ncol + 127) / 128) * G;
     return t64x128 >= 8 * 256 ? IMG_64x128 : IMG_64x64;
+}
+
+void img_tile_dims(int tile, int &bm, int &bn)
+{
+    static const int dims[][2] = {{128, 128}, {64, 128}, {64, 64}, {16, 128},
+                                  {32, 128}, {48, 128}, {96, 128}};
+    bm = dims[tile][0];
+    bn = dims[tile][1];
 }
 
 // Images per launch so that every source view stays below 2^29 elements.
@@ -193,7 +210,8 @@ ImgPlan img_plan(int M, long long Ncol, int Kred, int G, bool fast, bool allow_s
     p.kchunk = Kred;
     if (!allow_split)
         return p;
-    const int bm = p.tile == IMG_128x128 ? 128 : 64, bn = p.tile == IMG_64x64 ? 64 : 128;
+    int bm, bn;
+    img_tile_dims(p.tile, bm, bn);
     long long tiles = (long long)((M + bm - 1) / bm) * ((Ncol + bn - 1) / bn) * G;
     long long slices = (Kred + kBK - 1) / kBK;
     if (tiles >= 4 * 256 || slices < 16)

@@ -23,6 +23,41 @@ __device__ __forceinline__ int acc_row(int v, int lane)
     return 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
 }
 
+// v_mfma_f32_16x16x4f32: A (16 x 4): lane l holds A[l % 16][l / 16];
+// B (4 x 16): B[l / 16][l % 16]; D (16 x 16): lane l, register v holds
+// D[4 (l / 16) + v][l % 16].
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+template <int MF>
+__device__ __forceinline__ int acc_row_mf(int v, int lane)
+{
+    if constexpr (MF == 32)
+        return 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+    else
+        return 4 * (lane >> 4) + v;
+}
+
+template <int MF>
+struct MfmaAcc;
+template <>
+struct MfmaAcc<32> {
+    typedef f32x16 T;
+    static constexpr int NV = 16;
+    static __device__ __forceinline__ T mma(float a, float b, T c)
+    {
+        return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+    }
+};
+template <>
+struct MfmaAcc<16> {
+    typedef f32x4 T;
+    static constexpr int NV = 4;
+    static __device__ __forceinline__ T mma(float a, float b, T c)
+    {
+        return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+    }
+};
+
 template <int BM, int BN, int BK, int WM, int WN, int LDA, int LDB>
 __device__ __forceinline__ void mfma_slice(const float (*As)[LDA], const float (*Bs)[LDB],
                                            f32x16 (&acc)[BM / WM / 32][BN / WN / 32],
@@ -108,16 +143,21 @@ __device__ __forceinline__ int xcd_tile(int hw, int total)
 // FAST: cin % BK == 0, so a slice lies inside one filter tap; the spatial
 // bounds test and offset are then computed once per slice and column.
 // ---------------------------------------------------------------------------
-template <int BM, int BN, int BK, int WM, int WN, int PAD, bool FAST, int NST>
+template <int BM, int BN, int BK, int WM, int WN, int PAD, bool FAST, int NST, int MF>
 __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArgs a)
 {
+    // MF: MFMA shape, 32 (v_mfma_f32_32x32x2f32) or 16 (v_mfma_f32_16x16x4f32,
+    // for tiles of 16 or 48 rows).  A wave-load always fills 64 words, so a
+    // tile narrower than 64 rows stages a 64-wide A row and uses BM of it.
+    typedef MfmaAcc<MF> Mf;
     constexpr int NW = WM * WN;
     constexpr int TM = BM / WM, TN = BN / WN;
-    constexpr int FM = TM / 32, FN = TN / 32;
-    constexpr int HA = BM / 64, HB = BN / 64;          // 64-wide segments per row
+    constexpr int FM = TM / MF, FN = TN / MF;
+    constexpr int KS = 64 / MF;                        // reduction rows per MFMA
+    constexpr int HA = (BM + 63) / 64, HB = BN / 64;   // 64-wide segments per row
     constexpr int LA = BK * HA / NW, LB = BK * HB / NW;  // wave-loads per slice
-    constexpr int LDA = BM + PAD, LDB = BN + PAD;
-    static_assert(BM % 64 == 0 && BN % 64 == 0 && TM % 32 == 0 && TN % 32 == 0, "tile");
+    constexpr int LDA = 64 * HA + PAD, LDB = BN + PAD;
+    static_assert(BN % 64 == 0 && TM % MF == 0 && TN % MF == 0 && BK % KS == 0, "tile");
     static_assert(BK % NW == 0, "reduction rows per wave");
     static_assert(!FAST || BK == 16, "the FAST reduction order packs 16-channel blocks");
     static_assert(NST == 2 || NST == 3, "pipeline depth");
@@ -228,39 +268,38 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
         }
     };
 
-    f32x16 acc[FM][FN];
+    typename Mf::T acc[FM][FN];
 #pragma unroll
     for (int i = 0; i < FM; i++)
 #pragma unroll
         for (int j = 0; j < FN; j++)
 #pragma unroll
-            for (int v = 0; v < 16; v++)
+            for (int v = 0; v < Mf::NV; v++)
                 acc[i][j][v] = 0.f;
 
-    const int kr = lane >> 5, lc = lane & 31;
+    const int kr = lane / MF, lc = lane % MF;
     const int nslices = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
 
     // Operands of one slice -> registers, then MFMAs.
     auto compute = [&](float (*Ac)[LDA], float (*Bc)[LDB], auto &&between) {
-        float af[BK / 2][FM], bf[BK / 2][FN];
+        float af[BK / KS][FM], bf[BK / KS][FN];
 #pragma unroll
-        for (int s = 0; s < BK / 2; s++) {
+        for (int s = 0; s < BK / KS; s++) {
 #pragma unroll
             for (int i = 0; i < FM; i++)
-                af[s][i] = Ac[2 * s + kr][wm * TM + i * 32 + lc];
+                af[s][i] = Ac[KS * s + kr][wm * TM + i * MF + lc];
 #pragma unroll
             for (int j = 0; j < FN; j++)
-                bf[s][j] = Bc[2 * s + kr][wn * TN + j * 32 + lc];
+                bf[s][j] = Bc[KS * s + kr][wn * TN + j * MF + lc];
         }
         between();  // issue later slices' loads once this slice's reads are out
 #pragma unroll
-        for (int s = 0; s < BK / 2; s++)
+        for (int s = 0; s < BK / KS; s++)
 #pragma unroll
             for (int i = 0; i < FM; i++)
 #pragma unroll
                 for (int j = 0; j < FN; j++)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[s][i], bf[s][j],
-                                                                    acc[i][j], 0, 0, 0);
+                    acc[i][j] = Mf::mma(af[s][i], bf[s][j], acc[i][j]);
     };
 
     if constexpr (NST == 2) {
@@ -328,7 +367,7 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
     bool nok[FN];
 #pragma unroll
     for (int j = 0; j < FN; j++) {
-        int n = n0 + wn * TN + j * 32 + lc;
+        int n = n0 + wn * TN + j * MF + lc;
         nok[j] = n < a.Ncol;
         uint32_t c = nok[j] ? (uint32_t)n : 0u;
         uint32_t img = fast_div(c, a.col_hw);
@@ -341,8 +380,8 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
 #pragma unroll
     for (int i = 0; i < FM; i++)
 #pragma unroll
-        for (int v = 0; v < 16; v++) {
-            int m = m0 + wm * TM + i * 32 + acc_row(v, lane);
+        for (int v = 0; v < Mf::NV; v++) {
+            int m = m0 + wm * TM + i * MF + acc_row_mf<MF>(v, lane);
             if (m >= a.M)
                 continue;
             int oc = g * a.M + m;
@@ -893,17 +932,17 @@ __global__ __launch_bounds__(RED_E * RED_J) void splitk_reduce_kernel(
 #define MICONV_IMG_NST 3
 #endif
 
-template <int BM, int BN, int BK, int WM, int WN, int PAD>
+template <int BM, int BN, int BK, int WM, int WN, int PAD, int MF = 32>
 static hipError_t img_launch(const ImgGemmArgs &a, bool fast, hipStream_t stream)
 {
     constexpr int NST = MICONV_IMG_NST;
     int tiles = ((a.M + BM - 1) / BM) * ((a.Ncol + BN - 1) / BN);
     dim3 grid(tiles * a.groups * a.nsplit);
     if (fast)
-        hipLaunchKernelGGL((img_gemm_kernel<BM, BN, BK, WM, WN, PAD, true, NST>), grid,
+        hipLaunchKernelGGL((img_gemm_kernel<BM, BN, BK, WM, WN, PAD, true, NST, MF>), grid,
                            dim3(64 * WM * WN), 0, stream, a);
     else
-        hipLaunchKernelGGL((img_gemm_kernel<BM, BN, BK, WM, WN, PAD, false, NST>), grid,
+        hipLaunchKernelGGL((img_gemm_kernel<BM, BN, BK, WM, WN, PAD, false, NST, MF>), grid,
                            dim3(64 * WM * WN), 0, stream, a);
     return hipGetLastError();
 }
@@ -921,6 +960,12 @@ hipError_t launch_img_gemm(const ImgGemmArgs &a, int tile, bool fast, hipStream_
     switch (tile) {
     case IMG_128x128: return img_launch<128, 128, K, 2, 2, P>(a, fast, stream);
     case IMG_64x128: return img_launch<64, 128, K, 2, 2, P>(a, fast, stream);
+    // Narrow tiles: one wave row of 1 x 4 waves; rows of the 16x16 MFMA are
+    // padded by 16 words so its four 16-lane groups read distinct banks.
+    case IMG_16x128: return img_launch<16, 128, K, 1, 4, 16, 16>(a, fast, stream);
+    case IMG_32x128: return img_launch<32, 128, K, 1, 4, P>(a, fast, stream);
+    case IMG_48x128: return img_launch<48, 128, K, 1, 4, 16, 16>(a, fast, stream);
+    case IMG_96x128: return img_launch<96, 128, K, 2, 2, 16, 16>(a, fast, stream);
     default: return img_launch<64, 64, K, 2, 2, P>(a, fast, stream);
     }
 }

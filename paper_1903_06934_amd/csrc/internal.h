@@ -94,7 +94,8 @@ struct WgradArgs {
 };
 
 // Image-GEMM tile shapes (BM x BN; every shape runs 4 waves).
-enum ImgTile { IMG_128x128 = 0, IMG_64x128, IMG_64x64 };
+enum ImgTile { IMG_128x128 = 0, IMG_64x128, IMG_64x64, IMG_16x128, IMG_32x128, IMG_48x128,
+              IMG_96x128 };
 // Backward-weight kernels: packed (c, r, s) columns, or tap-uniform tiles
 // (BM rows of K/G x BN channels of one tap).
 enum WgradTile { WG_128x128 = 0, WG_64x64, WG_TAP_128x64, WG_TAP_64x64 };

@@ -82,6 +82,12 @@ TILE_SHAPES = [
     (8, 32, 64, 64, 200, 3, 3, 1, 1, 1),   # fwd 128-tile, channel-aligned, ragged M
     (16, 96, 64, 64, 64, 3, 3, 1, 1, 1),   # bwd-data 128-tile
     (8, 3, 128, 128, 96, 3, 3, 1, 1, 1),   # fwd 128-tile, per-element tap decode
+    # Narrow-row tiles (16, 32, 48 and 96 rows), with ragged rows and columns.
+    (4, 64, 20, 20, 80, 3, 3, 1, 1, 1),    # fwd M = 80 (96-row tile)
+    (4, 80, 21, 21, 40, 3, 3, 1, 1, 1),    # fwd M = 40 (48), bwd-data M = 80, tap decode
+    (4, 32, 24, 24, 12, 3, 3, 1, 1, 1),    # fwd M = 12 (16), bwd-data M = 32, tap decode
+    (4, 96, 15, 15, 64, 5, 5, 1, 2, 2),    # bwd-data M = 48 over groups
+    (3, 48, 11, 11, 96, 5, 5, 2, 2, 1),    # bwd-data M = 48, stride phases
 ]
 
 
