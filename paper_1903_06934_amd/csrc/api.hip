@@ -31,6 +31,13 @@ constexpr long long kMaxChunkElems = (1LL << 29) - 1;  // per launch, per source
 constexpr size_t kAlign = 256;                  // sub-buffer alignment inside ws
 constexpr int kBK = 16;                         // reduction slice of every GEMM kernel
 constexpr int kTargetWorkgroups = 1024;         // 4 per CU on 256 CUs
+// Tap-uniform backward-weight tiles: six fit on a CU at once, and about
+// three rounds of them measured best, as long as a split keeps at least
+// kTapMinSlices slices (shorter splits cost more in partial sums than they
+// gain in balance) -- unless that would leave fewer than kTargetWorkgroups
+// workgroups (small layers), where splits go down to 8 slices.
+constexpr int kTapTargetWorkgroups = 4096;
+constexpr int kTapMinSlices = 24;
 
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
@@ -298,8 +305,8 @@ size_t bwd_data_ws(const Geom &g)
 
 // ------------------------------------------------------------ bwd-weight plan
 // The reduction over N*P*Q pixels is cut into fixed-length splits (a
-// multiple of the 16-pixel slice) so that about kTargetWorkgroups
-// workgroups run; each split writes its own partial dw, summed afterwards in
+// multiple of the slice) so that about kTargetWorkgroups (packed tiles) or
+// kTapTargetWorkgroups (tap-uniform tiles) workgroups run; each split writes its own partial dw, summed afterwards in
 // split order.  Launches never straddle a batch chunk (images_per_launch).
 struct WgradPlan {
     int tile, slice, chunk, nsplit, nb;
@@ -312,12 +319,18 @@ WgradPlan wgrad_plan(const Geom &g)
     WgradPlan p;
     int M = g.Kg, Ncol = g.Cg * g.R * g.S;
     long long PQ = (long long)g.P * g.Q, Kred = (long long)g.N * PQ;
-    long long tiles;
-    if (g.Cg >= 32) {
-        // Tap-uniform tiles, 64 rows of K/G x 64 channels of one tap (the
-        // 64x64 shape measured fastest on every layer of the five stacks).
-        p.tile = WG_TAP_64x64;
-        tiles = (long long)((M + 63) / 64) * g.R * g.S * ((g.Cg + 63) / 64) * g.G;
+    long long tiles, target = kTargetWorkgroups, min_slices = 8;
+    if (g.Cg >= 32 || g.Cg == 16) {
+        // Tap-uniform tiles of 64 rows of K/G by 32 channels of one tap, by
+        // 48 channels when C/G is a multiple of 48 but not of 64, or by 16 for
+        // 16 channels, so that no column stays idle.  Small tiles measured
+        // fastest on every layer of the five stacks: six fit on a CU.
+        const int bm = 64;
+        const int bn = g.Cg == 16 ? 16 : (g.Cg % 64 != 0 && g.Cg % 48 == 0) ? 48 : 32;
+        p.tile = bn == 16 ? WG_TAP_64x16 : bn == 48 ? WG_TAP_64x48 : WG_TAP_64x32;
+        tiles = (long long)((M + bm - 1) / bm) * g.R * g.S * ((g.Cg + bn - 1) / bn) * g.G;
+        target = kTapTargetWorkgroups;
+        min_slices = kTapMinSlices;
         p.slice = 64;
     } else {
         // Few channels per group: pack (c, r, s) into the columns instead.
@@ -326,8 +339,12 @@ WgradPlan wgrad_plan(const Geom &g)
         tiles = (long long)gemm_tiles(M, Ncol, bm, bm) * g.G;
         p.slice = kBK;
     }
-    long long ns = (kTargetWorkgroups + tiles - 1) / tiles;
-    long long max_ns = Kred / (p.slice * 8);
+    long long ns = (target + tiles - 1) / tiles;
+    long long long_ns = Kred / (p.slice * min_slices);
+    long long fill_ns = (kTargetWorkgroups + tiles - 1) / tiles;
+    long long max_ns = long_ns > fill_ns ? long_ns : fill_ns;
+    if (max_ns > Kred / (p.slice * 8))
+        max_ns = Kred / (p.slice * 8);
     if (ns > max_ns)
         ns = max_ns;
     if (ns < 1)
@@ -344,7 +361,7 @@ WgradPlan wgrad_plan(const Geom &g)
     p.nsplit = (int)total;
     // Tap-uniform tiles always go through the partial buffer (the reduction
     // also reorders columns); packed tiles write dw directly when unsplit.
-    p.via_part = p.tile >= WG_TAP_128x64 || p.nsplit > 1;
+    p.via_part = p.tile >= WG_TAP_64x32 || p.nsplit > 1;
     p.part_bytes = p.via_part ? align_up((size_t)p.nsplit * g.K * Ncol * sizeof(float)) : 0;
     p.bias_bytes = align_up((size_t)p.nsplit * g.K * sizeof(float));
     return p;
@@ -669,7 +686,7 @@ int conv_bwd_weight(int N, int C, int H, int W, int K, int R, int S, int stride,
     }
     if (mark(tl_events.after, stream) != hipSuccess)
         return MICONV_ERR_LAUNCH;
-    const bool tap_order = p.tile >= WG_TAP_128x64;
+    const bool tap_order = p.tile >= WG_TAP_64x32;
     if (p.via_part &&
         (st = launch_status(launch_splitk_reduce(part, p.nsplit, a.split_stride, K * a.Ncol, dw,
                                                  tap_order ? R * S : 0, tap_order ? g.Cg : 0,

@@ -670,20 +670,25 @@ __global__ __launch_bounds__(64 * WM * WN) void wgrad_gemm_kernel(const WgradArg
 // simply not stored.
 //
 // LDS holds each row pixel-contiguous (64 words + 4 of padding, so the
-// ds_read_b128 of 16 consecutive rows hit distinct banks).  MFMA step s
-// (0..31) takes pixel s from the first half of the slice in lanes 0-31 and
-// pixel 32 + s in lanes 32-63, so a lane's 32 operands of a row are
-// contiguous: 8 ds_read_b128.  The tile is single-buffered: after a barrier
+// ds_read_b128 of 16 consecutive rows hit distinct banks).  With the 32x32x2
+// MFMA, step s (0..31) takes pixel s from the first half of the slice in
+// lanes 0-31 and pixel 32 + s in lanes 32-63, so a lane's 32 operands of a
+// row are contiguous: 8 ds_read_b128.  With the 16x16x4 MFMA (MF = 16) the
+// four 16-lane groups take the four quarters of the slice, 16 contiguous
+// operands each: 4 ds_read_b128.  The tile is single-buffered: after a barrier
 // every wave copies its operands of the slice into registers, a second
 // barrier frees the LDS, the next slice's loads are issued, and the slice's
 // MFMAs run while they land.
 // ---------------------------------------------------------------------------
-template <int BM, int BN, int WM, int WN>
+template <int BM, int BN, int WM, int WN, int MF>
 __global__ __launch_bounds__(64 * WM * WN) void wgrad_tap_kernel(const WgradArgs a)
 {
+    typedef MfmaAcc<MF> Mf;
     constexpr int BK = 64, LDR = BK + 4;
-    constexpr int NW = WM * WN, TM = BM / WM, TN = BN / WN, FM = TM / 32, FN = TN / 32;
+    constexpr int NW = WM * WN, TM = BM / WM, TN = BN / WN, FM = TM / MF, FN = TN / MF;
+    constexpr int PB = BK * MF / 64;  // pixels of the slice per lane group
     static_assert(BM % NW == 0 && BN % NW == 0, "rows per wave");
+    static_assert(TM % MF == 0 && TN % MF == 0, "tile");
 
     __shared__ __attribute__((aligned(16))) float L[(BM + BN) * LDR];
 
@@ -736,13 +741,13 @@ __global__ __launch_bounds__(64 * WM * WN) void wgrad_tap_kernel(const WgradArgs
         }
     };
 
-    f32x16 acc[FM][FN];
+    typename Mf::T acc[FM][FN];
 #pragma unroll
     for (int i = 0; i < FM; i++)
 #pragma unroll
         for (int j = 0; j < FN; j++)
 #pragma unroll
-            for (int v = 0; v < 16; v++)
+            for (int v = 0; v < Mf::NV; v++)
                 acc[i][j][v] = 0.f;
 
     // Bias gradient: the workgroups of tap 0 and the first channel block also
@@ -752,7 +757,7 @@ __global__ __launch_bounds__(64 * WM * WN) void wgrad_tap_kernel(const WgradArgs
     const int brow = threadIdx.x / TPR, bpart = threadIdx.x % TPR;
     float bsum = 0.f;
 
-    const int kr = lane >> 5, lc = lane & 31;
+    const int kr = lane / MF, lc = lane % MF;
     const int nslices = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
     if (nslices > 0)
         issue(kbeg);
@@ -770,34 +775,33 @@ __global__ __launch_bounds__(64 * WM * WN) void wgrad_tap_kernel(const WgradArgs
                 bsum += v.w;
             }
         }
-        float4 af[FM][8], bf[FN][8];
+        float4 af[FM][PB / 4], bf[FN][PB / 4];
 #pragma unroll
         for (int i = 0; i < FM; i++) {
-            const float *rowp = &L[(wm * TM + i * 32 + lc) * LDR + kr * 32];
+            const float *rowp = &L[(wm * TM + i * MF + lc) * LDR + kr * PB];
 #pragma unroll
-            for (int u = 0; u < 8; u++)
+            for (int u = 0; u < PB / 4; u++)
                 af[i][u] = *(const float4 *)&rowp[4 * u];
         }
 #pragma unroll
         for (int j = 0; j < FN; j++) {
-            const float *rowp = &L[(BM + wn * TN + j * 32 + lc) * LDR + kr * 32];
+            const float *rowp = &L[(BM + wn * TN + j * MF + lc) * LDR + kr * PB];
 #pragma unroll
-            for (int u = 0; u < 8; u++)
+            for (int u = 0; u < PB / 4; u++)
                 bf[j][u] = *(const float4 *)&rowp[4 * u];
         }
         __syncthreads();  // every wave holds its operands: the tile is free
         if (t + 1 < nslices)
             issue(kbeg + (t + 1) * BK);
 #pragma unroll
-        for (int u = 0; u < 8; u++)
+        for (int u = 0; u < PB / 4; u++)
 #pragma unroll
             for (int e = 0; e < 4; e++)
 #pragma unroll
                 for (int i = 0; i < FM; i++)
 #pragma unroll
                     for (int j = 0; j < FN; j++)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(
-                            af[i][u][e], bf[j][u][e], acc[i][j], 0, 0, 0);
+                        acc[i][j] = Mf::mma(af[i][u][e], bf[j][u][e], acc[i][j]);
     }
 
     if (do_bias) {
@@ -817,13 +821,13 @@ __global__ __launch_bounds__(64 * WM * WN) void wgrad_tap_kernel(const WgradArgs
 #pragma unroll
     for (int i = 0; i < FM; i++)
 #pragma unroll
-        for (int v = 0; v < 16; v++) {
-            int m = m0 + wm * TM + i * 32 + acc_row(v, lane);
+        for (int v = 0; v < Mf::NV; v++) {
+            int m = m0 + wm * TM + i * MF + acc_row_mf<MF>(v, lane);
             if (m >= a.M)
                 continue;
 #pragma unroll
             for (int j = 0; j < FN; j++) {
-                int c = c0 + wn * TN + j * 32 + lc;
+                int c = c0 + wn * TN + j * MF + lc;
                 if (c < a.Cg)
                     outg[(long long)m * a.Ncol + c] = acc[i][j][v];
             }
@@ -984,12 +988,12 @@ static hipError_t wgrad_launch(const WgradArgs &a, bool vec, hipStream_t stream)
     return hipGetLastError();
 }
 
-template <int BM, int BN, int WM, int WN>
+template <int BM, int BN, int WM, int WN, int MF = 32>
 static hipError_t wgrad_tap_launch(const WgradArgs &a, hipStream_t stream)
 {
     int RS = (int)a.n_rs.d;
     int tiles = ((a.M + BM - 1) / BM) * RS * ((a.Cg + BN - 1) / BN);
-    hipLaunchKernelGGL((wgrad_tap_kernel<BM, BN, WM, WN>), dim3(tiles * a.groups * a.nsplit),
+    hipLaunchKernelGGL((wgrad_tap_kernel<BM, BN, WM, WN, MF>), dim3(tiles * a.groups * a.nsplit),
                        dim3(64 * WM * WN), 0, stream, a);
     return hipGetLastError();
 }
@@ -998,8 +1002,9 @@ hipError_t launch_wgrad_gemm(const WgradArgs &a, int tile, bool vec, hipStream_t
 {
     switch (tile) {
     case WG_128x128: return wgrad_launch<128, 128, 2, 2>(a, vec, stream);
-    case WG_TAP_128x64: return wgrad_tap_launch<128, 64, 2, 2>(a, stream);
-    case WG_TAP_64x64: return wgrad_tap_launch<64, 64, 2, 2>(a, stream);
+    case WG_TAP_64x32: return wgrad_tap_launch<64, 32, 2, 2, 16>(a, stream);
+    case WG_TAP_64x48: return wgrad_tap_launch<64, 48, 4, 1, 16>(a, stream);
+    case WG_TAP_64x16: return wgrad_tap_launch<64, 16, 4, 1, 16>(a, stream);
     default: return wgrad_launch<64, 64, 2, 2>(a, vec, stream);
     }
 }

@@ -98,7 +98,8 @@ enum ImgTile { IMG_128x128 = 0, IMG_64x128, IMG_64x64, IMG_16x128, IMG_32x128, I
               IMG_96x128 };
 // Backward-weight kernels: packed (c, r, s) columns, or tap-uniform tiles
 // (BM rows of K/G x BN channels of one tap).
-enum WgradTile { WG_128x128 = 0, WG_64x64, WG_TAP_128x64, WG_TAP_64x64 };
+// Every tap-uniform shape follows WG_TAP_64x32.
+enum WgradTile { WG_128x128 = 0, WG_64x64, WG_TAP_64x32, WG_TAP_64x48, WG_TAP_64x16 };
 
 hipError_t launch_img_gemm(const ImgGemmArgs &a, int tile, bool fast, hipStream_t stream);
 hipError_t launch_wgrad_gemm(const WgradArgs &a, int tile, bool vec, hipStream_t stream);
