@@ -157,12 +157,10 @@ int gemm_tiles(int M, int Ncol, int bm, int bn)
 
 // Tile choice for the image GEMM, from measured sweeps on MI355X across the
 // layers of the five benchmark stacks.  The kernel is limited by latency
-// hiding rather than by MFMA issue: the 64x64 tile (4 waves of 32x32
-// accumulators, many workgroups per CU) is best or tied on most layers,
-// 64x128 gains a few percent when it still has >= 8 tiles per CU, and is
-// also best for the layers with a per-element tap decode (channels per group
-// not a multiple of 16: 3-channel first layers).
-int pick_img_tile(int M, long long Ncol, int G, bool fast)
+// hiding rather than by MFMA issue: the 64x64 tile of four 16x64 waves on the
+// 16x16x4 MFMA (small accumulators, many workgroups per CU) is best or tied
+// on most layers, including those with a per-element tap decode.
+int pick_img_tile(int M, long long Ncol, int G)
 {
     // Row counts that a 64-row tile would leave partly empty.
     if (M <= 16)
@@ -173,15 +171,17 @@ int pick_img_tile(int M, long long Ncol, int G, bool fast)
         return IMG_48x128;
     if (M > 64 && M <= 96)
         return IMG_96x128;
-    if (!fast)
-        return IMG_64x128;
-    long long t64x128 = (long long)((M + 63) / 64) * ((Ncol + 127) / 128) * G;
-    return t64x128 >= 8 * 256 ? IMG_64x128 : IMG_64x64;
+    // 128x64 halves the gathered-operand loads per MFMA; it pays when it
+    // leaves no row empty and still gives 4 tiles per CU.
+    long long t128 = (long long)((M + 127) / 128) * ((Ncol + 63) / 64) * G;
+    if (M % 128 == 0 && t128 >= 4 * 256)
+        return IMG_128x64;
+    return IMG_64x64;
 }
 
 void img_tile_dims(int tile, int &bm, int &bn)
 {
-    static const int dims[][2] = {{128, 128}, {64, 128}, {64, 64}, {16, 128},
+    static const int dims[][2] = {{64, 64}, {128, 64}, {16, 128},
                                   {32, 128}, {48, 128}, {96, 128}};
     bm = dims[tile][0];
     bn = dims[tile][1];
@@ -209,10 +209,10 @@ struct ImgPlan {
     int tile, nsplit, kchunk;
 };
 
-ImgPlan img_plan(int M, long long Ncol, int Kred, int G, bool fast, bool allow_split)
+ImgPlan img_plan(int M, long long Ncol, int Kred, int G, bool allow_split)
 {
     ImgPlan p;
-    p.tile = pick_img_tile(M, Ncol, G, fast);
+    p.tile = pick_img_tile(M, Ncol, G);
     p.nsplit = 1;
     p.kchunk = Kred;
     if (!allow_split)
@@ -243,7 +243,7 @@ size_t fwd_pack_bytes(const Geom &g)
 
 ImgPlan fwd_plan(const Geom &g)
 {
-    return img_plan(g.Kg, (long long)g.N * g.P * g.Q, g.Cg * g.R * g.S, g.G, g.Cg % kBK == 0,
+    return img_plan(g.Kg, (long long)g.N * g.P * g.Q, g.Cg * g.R * g.S, g.G,
                     images_per_launch(g) >= g.N);
 }
 
@@ -291,7 +291,7 @@ size_t bwd_data_pack_bytes(const Geom &g)
 // Split-K only for stride 1 (one phase covering all of dx).
 ImgPlan bwd_data_plan(const Geom &g)
 {
-    return img_plan(g.Cg, (long long)g.N * g.H * g.W, g.Kg * g.R * g.S, g.G, g.Kg % kBK == 0,
+    return img_plan(g.Cg, (long long)g.N * g.H * g.W, g.Kg * g.R * g.S, g.G,
                     g.st == 1 && images_per_launch(g) >= g.N);
 }
 
@@ -514,7 +514,7 @@ int conv_fwd(int N, int C, int H, int W, int K, int R, int S, int stride, int pa
         a.nsplit = plan.nsplit;
         a.kchunk = plan.kchunk;
         a.split_stride = (long long)N * yi;
-        int tile = n == N ? plan.tile : pick_img_tile(a.M, a.Ncol, group, fast);
+        int tile = n == N ? plan.tile : pick_img_tile(a.M, a.Ncol, group);
         if ((st = launch_status(launch_img_gemm(a, tile, fast, stream))) != MICONV_OK)
             return st;
     }
@@ -605,7 +605,7 @@ int conv_bwd_data(int N, int C, int H, int W, int K, int R, int S, int stride, i
                 a.nsplit = plan.nsplit;
                 a.kchunk = plan.nsplit > 1 ? plan.kchunk : a.Kred;
                 a.split_stride = (long long)N * xi;
-                int tile = stride == 1 && n == N ? plan.tile : pick_img_tile(a.M, a.Ncol, group, fast);
+                int tile = stride == 1 && n == N ? plan.tile : pick_img_tile(a.M, a.Ncol, group);
                 if ((st = launch_status(launch_img_gemm(a, tile, fast, stream))) != MICONV_OK)
                     return st;
             }

@@ -962,15 +962,16 @@ hipError_t launch_img_gemm(const ImgGemmArgs &a, int tile, bool fast, hipStream_
 {
     constexpr int K = MICONV_IMG_BK, P = MICONV_IMG_PAD;
     switch (tile) {
-    case IMG_128x128: return img_launch<128, 128, K, 2, 2, P>(a, fast, stream);
-    case IMG_64x128: return img_launch<64, 128, K, 2, 2, P>(a, fast, stream);
+    // 128x64: four waves of 32 rows x 64 columns (32x32x2 MFMA).
+    case IMG_128x64: return img_launch<128, 64, K, 4, 1, P>(a, fast, stream);
     // Narrow tiles: one wave row of 1 x 4 waves; rows of the 16x16 MFMA are
     // padded by 16 words so its four 16-lane groups read distinct banks.
     case IMG_16x128: return img_launch<16, 128, K, 1, 4, 16, 16>(a, fast, stream);
     case IMG_32x128: return img_launch<32, 128, K, 1, 4, P>(a, fast, stream);
     case IMG_48x128: return img_launch<48, 128, K, 1, 4, 16, 16>(a, fast, stream);
     case IMG_96x128: return img_launch<96, 128, K, 2, 2, 16, 16>(a, fast, stream);
-    default: return img_launch<64, 64, K, 2, 2, P>(a, fast, stream);
+    // 64x64: four waves of 16 rows x 64 columns (16x16x4 MFMA).
+    default: return img_launch<64, 64, K, 4, 1, 16, 16>(a, fast, stream);
     }
 }
 

@@ -77,11 +77,13 @@ def test_edge_shapes(shape):
     full_parity(shape)
 
 
-# Shapes large enough that the dispatcher picks the 128x128 tiles.
+# Shapes for each image-GEMM tile: 128x64 needs 128-row multiples and at
+# least 1024 tiles; the others cover ragged rows and columns.
 TILE_SHAPES = [
-    (8, 32, 64, 64, 200, 3, 3, 1, 1, 1),   # fwd 128-tile, channel-aligned, ragged M
-    (16, 96, 64, 64, 64, 3, 3, 1, 1, 1),   # bwd-data 128-tile
-    (8, 3, 128, 128, 96, 3, 3, 1, 1, 1),   # fwd 128-tile, per-element tap decode
+    (16, 32, 65, 63, 128, 3, 3, 1, 1, 1),  # fwd 128x64, ragged columns
+    (16, 128, 63, 65, 16, 3, 3, 1, 1, 1),  # bwd-data 128x64, ragged columns
+    (8, 32, 64, 64, 200, 3, 3, 1, 1, 1),   # fwd 64x64, channel-aligned, ragged M
+    (8, 3, 128, 128, 96, 3, 3, 1, 1, 1),   # fwd 96-row tile, per-element tap decode
     # Narrow-row tiles (16, 32, 48 and 96 rows), with ragged rows and columns.
     (4, 64, 20, 20, 80, 3, 3, 1, 1, 1),    # fwd M = 80 (96-row tile)
     (4, 80, 21, 21, 40, 3, 3, 1, 1, 1),    # fwd M = 40 (48), bwd-data M = 80, tap decode
