@@ -157,32 +157,33 @@ int gemm_tiles(int M, int Ncol, int bm, int bn)
 
 // Tile choice for the image GEMM, from measured sweeps on MI355X across the
 // layers of the five benchmark stacks.  The kernel is limited by latency
-// hiding rather than by MFMA issue: the 64x64 tile of four 16x64 waves on the
-// 16x16x4 MFMA (small accumulators, many workgroups per CU) is best or tied
-// on most layers, including those with a per-element tap decode.
+// hiding rather than by MFMA issue: the 64x64 tile (small accumulators, six
+// workgroups per CU) is best or tied on most layers; narrower tiles serve
+// row counts that would leave 64-row tiles partly empty, and the 128-wide
+// variants (fewer gathered-operand loads per MFMA) pay only when they still
+// give 4 workgroups per CU without a split reduction.
 int pick_img_tile(int M, long long Ncol, int G)
 {
-    // Row counts that a 64-row tile would leave partly empty.
+    auto tiles = [&](int bm, int bn) {
+        return (long long)((M + bm - 1) / bm) * ((Ncol + bn - 1) / bn) * G;
+    };
     if (M <= 16)
         return IMG_16x128;
     if (M <= 32)
-        return IMG_32x128;
+        return IMG_32x64;
     if (M <= 48)
-        return IMG_48x128;
+        return tiles(48, 128) >= 4 * 256 ? IMG_48x128 : IMG_48x64;
     if (M > 64 && M <= 96)
-        return IMG_96x128;
-    // 128x64 halves the gathered-operand loads per MFMA; it pays when it
-    // leaves no row empty and still gives 4 tiles per CU.
-    long long t128 = (long long)((M + 127) / 128) * ((Ncol + 63) / 64) * G;
-    if (M % 128 == 0 && t128 >= 4 * 256)
+        return tiles(96, 128) >= 4 * 256 ? IMG_96x128 : IMG_96x64;
+    if (M % 128 == 0 && tiles(128, 64) >= 4 * 256)
         return IMG_128x64;
     return IMG_64x64;
 }
 
 void img_tile_dims(int tile, int &bm, int &bn)
 {
-    static const int dims[][2] = {{64, 64}, {128, 64}, {16, 128},
-                                  {32, 128}, {48, 128}, {96, 128}};
+    static const int dims[][2] = {{64, 64}, {128, 64}, {16, 128}, {32, 64},
+                                  {48, 64}, {48, 128}, {96, 64},  {96, 128}};
     bm = dims[tile][0];
     bn = dims[tile][1];
 }

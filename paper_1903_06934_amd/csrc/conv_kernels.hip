@@ -280,17 +280,19 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
     const int kr = lane / MF, lc = lane % MF;
     const int nslices = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
 
-    // Operands of one slice -> registers, then MFMAs.
+    // Operands of one slice -> registers, then MFMAs.  MFMA step s takes
+    // reduction row kr * (BK / KS) + s in lane group kr: with rows of
+    // 64 + 4 words, the KS groups of one ds_read then hit distinct banks.
     auto compute = [&](float (*Ac)[LDA], float (*Bc)[LDB], auto &&between) {
         float af[BK / KS][FM], bf[BK / KS][FN];
 #pragma unroll
         for (int s = 0; s < BK / KS; s++) {
 #pragma unroll
             for (int i = 0; i < FM; i++)
-                af[s][i] = Ac[KS * s + kr][wm * TM + i * MF + lc];
+                af[s][i] = Ac[kr * (BK / KS) + s][wm * TM + i * MF + lc];
 #pragma unroll
             for (int j = 0; j < FN; j++)
-                bf[s][j] = Bc[KS * s + kr][wn * TN + j * MF + lc];
+                bf[s][j] = Bc[kr * (BK / KS) + s][wn * TN + j * MF + lc];
         }
         between();  // issue later slices' loads once this slice's reads are out
 #pragma unroll
@@ -954,24 +956,23 @@ static hipError_t img_launch(const ImgGemmArgs &a, bool fast, hipStream_t stream
 #ifndef MICONV_IMG_BK
 #define MICONV_IMG_BK 16
 #endif
-#ifndef MICONV_IMG_PAD
-#define MICONV_IMG_PAD 0
-#endif
 
 hipError_t launch_img_gemm(const ImgGemmArgs &a, int tile, bool fast, hipStream_t stream)
 {
-    constexpr int K = MICONV_IMG_BK, P = MICONV_IMG_PAD;
+    constexpr int K = MICONV_IMG_BK;
     switch (tile) {
-    // 128x64: four waves of 32 rows x 64 columns (32x32x2 MFMA).
-    case IMG_128x64: return img_launch<128, 64, K, 4, 1, P>(a, fast, stream);
-    // Narrow tiles: one wave row of 1 x 4 waves; rows of the 16x16 MFMA are
-    // padded by 16 words so its four 16-lane groups read distinct banks.
-    case IMG_16x128: return img_launch<16, 128, K, 1, 4, 16, 16>(a, fast, stream);
-    case IMG_32x128: return img_launch<32, 128, K, 1, 4, P>(a, fast, stream);
-    case IMG_48x128: return img_launch<48, 128, K, 1, 4, 16, 16>(a, fast, stream);
-    case IMG_96x128: return img_launch<96, 128, K, 2, 2, 16, 16>(a, fast, stream);
-    // 64x64: four waves of 16 rows x 64 columns (16x16x4 MFMA).
-    default: return img_launch<64, 64, K, 4, 1, 16, 16>(a, fast, stream);
+    // Every shape runs on the 16x16x4 MFMA with LDS rows padded by 4 words,
+    // so that its four 16-lane groups, which read rows 4 apart, hit distinct
+    // banks.  Waves: 4 x 1 (each wave a 16- or 32-row band across the tile),
+    // 2 x 2, or 1 x 4 (each wave a column band).
+    case IMG_128x64: return img_launch<128, 64, K, 4, 1, 4, 16>(a, fast, stream);
+    case IMG_16x128: return img_launch<16, 128, K, 1, 4, 4, 16>(a, fast, stream);
+    case IMG_32x64: return img_launch<32, 64, K, 2, 2, 4, 16>(a, fast, stream);
+    case IMG_48x64: return img_launch<48, 64, K, 1, 4, 4, 16>(a, fast, stream);
+    case IMG_48x128: return img_launch<48, 128, K, 1, 4, 4, 16>(a, fast, stream);
+    case IMG_96x64: return img_launch<96, 64, K, 2, 2, 4, 16>(a, fast, stream);
+    case IMG_96x128: return img_launch<96, 128, K, 2, 2, 4, 16>(a, fast, stream);
+    default: return img_launch<64, 64, K, 4, 1, 4, 16>(a, fast, stream);
     }
 }
 

@@ -94,7 +94,10 @@ struct WgradArgs {
 };
 
 // Image-GEMM tile shapes (BM x BN; every shape runs 4 waves).
-enum ImgTile { IMG_64x64 = 0, IMG_128x64, IMG_16x128, IMG_32x128, IMG_48x128, IMG_96x128 };
+enum ImgTile {
+    IMG_64x64 = 0, IMG_128x64, IMG_16x128, IMG_32x64, IMG_48x64, IMG_48x128, IMG_96x64,
+    IMG_96x128
+};
 // Backward-weight kernels: packed (c, r, s) columns, or tap-uniform tiles
 // (BM rows of K/G x BN channels of one tap).
 // Every tap-uniform shape follows WG_TAP_64x32.
