@@ -30,6 +30,7 @@ constexpr long long kMaxElems = 2147483647LL;  // 2^31 - 1
 constexpr long long kMaxChunkElems = (1LL << 29) - 1;  // per launch, per source tensor
 constexpr size_t kAlign = 256;                  // sub-buffer alignment inside ws
 constexpr int kBK = 16;                         // reduction slice of every GEMM kernel
+constexpr int kNumCUs = 256;                    // MI355X: 8 XCDs x 32 CUs
 constexpr int kTargetWorkgroups = 1024;         // 4 per CU on 256 CUs
 // Tap-uniform backward-weight tiles: six fit on a CU at once, and about
 // three rounds of them measured best, as long as a split keeps at least
@@ -155,14 +156,25 @@ int gemm_tiles(int M, int Ncol, int bm, int bn)
     return ((M + bm - 1) / bm) * ((Ncol + bn - 1) / bn);
 }
 
+// Fraction of the CUs' workgroup slots kept busy when `tiles` equal
+// workgroups are dealt out over 256 CUs: tiles / (256 * ceil(tiles / 256)).
+double cu_balance(long long tiles)
+{
+    long long rounds = (tiles + kNumCUs - 1) / kNumCUs;
+    return rounds > 0 ? (double)tiles / (double)(rounds * kNumCUs) : 1.0;
+}
+
 // Tile choice for the image GEMM, from measured sweeps on MI355X across the
-// layers of the five benchmark stacks.  The kernel is limited by latency
-// hiding rather than by MFMA issue: the 64x64 tile (small accumulators, six
-// workgroups per CU) is best or tied on most layers; narrower tiles serve
-// row counts that would leave 64-row tiles partly empty, and the 128-wide
-// variants (fewer gathered-operand loads per MFMA) pay only when they still
-// give 4 workgroups per CU without a split reduction.
-int pick_img_tile(int M, long long Ncol, int G)
+// layers of the five benchmark stacks.  The 64x64 tile (small accumulators,
+// six workgroups per CU) is the default.  Row counts that would leave a
+// 64-row tile partly empty take 16-, 32-, 48- or 96-row tiles (128 columns
+// wide when that still gives 4 tiles per CU).  The 128x64 tile halves the
+// gathered-operand loads per MFMA and runs about 5 % faster per tile when it
+// leaves no row empty and the reduction is not trivially short; it is taken
+// when it gives every CU a workgroup and does not leave noticeably more CU
+// slots idle in the last round than the 64x64 tiles would (a 2.3-per-CU deal
+// against 4.6 lost 10 %).
+int pick_img_tile(int M, long long Ncol, int Kred, int G)
 {
     auto tiles = [&](int bm, int bn) {
         return (long long)((M + bm - 1) / bm) * ((Ncol + bn - 1) / bn) * G;
@@ -172,10 +184,11 @@ int pick_img_tile(int M, long long Ncol, int G)
     if (M <= 32)
         return IMG_32x64;
     if (M <= 48)
-        return tiles(48, 128) >= 4 * 256 ? IMG_48x128 : IMG_48x64;
+        return tiles(48, 128) >= 4 * kNumCUs ? IMG_48x128 : IMG_48x64;
     if (M > 64 && M <= 96)
-        return tiles(96, 128) >= 4 * 256 ? IMG_96x128 : IMG_96x64;
-    if (M % 128 == 0 && tiles(128, 64) >= 4 * 256)
+        return tiles(96, 128) >= 4 * kNumCUs ? IMG_96x128 : IMG_96x64;
+    if (M % 128 == 0 && Kred >= 256 && tiles(128, 64) >= kNumCUs &&
+        1.05 * cu_balance(tiles(128, 64)) >= cu_balance(tiles(64, 64)))
         return IMG_128x64;
     return IMG_64x64;
 }
@@ -199,13 +212,18 @@ int images_per_launch(const Geom &g)
     return (int)(n < g.N ? n : g.N);
 }
 
-// Split-K for the image GEMM.  With fewer than four tiles per CU the MFMA
-// pipes starve for latency hiding; the reduction is then cut into splits of
-// at least 8 slices so that ~8 workgroups per CU run, each split writes an
-// output-shaped partial slab, and a fixed-order reduction adds them (and the
-// bias).  The slabs cost about (nsplit + 1) output passes of HBM traffic, so
-// the reduction must be deep enough to amortise them: Kred >= 600 (nsplit + 1).
-// Only for single-launch problems (no batch chunking).
+// Split-K for the image GEMM.  With fewer than 640 tiles (2.5 per CU) the
+// MFMA pipes starve for latency hiding; a deep reduction (>= kSplitMinRows)
+// is then cut into splits of at least kSplitRows rows so that ~8 workgroups
+// per CU run, each split writes an output-shaped partial slab, and a
+// fixed-order reduction adds them (and the bias).  The slabs cost about
+// 2 nsplit + 1 output passes of HBM traffic: measured, splitting reductions
+// of 2304 rows or fewer lost up to a fifth, while 3200 rows and more at
+// 200-600 tiles gained 6-23 %.  Only for single-launch problems (no batch
+// chunking).
+constexpr int kSplitMinRows = 3072;
+constexpr int kSplitRows = 768;
+
 struct ImgPlan {
     int tile, nsplit, kchunk;
 };
@@ -213,22 +231,22 @@ struct ImgPlan {
 ImgPlan img_plan(int M, long long Ncol, int Kred, int G, bool allow_split)
 {
     ImgPlan p;
-    p.tile = pick_img_tile(M, Ncol, G);
+    p.tile = pick_img_tile(M, Ncol, Kred, G);
     p.nsplit = 1;
     p.kchunk = Kred;
-    if (!allow_split)
+    if (!allow_split || Kred < kSplitMinRows)
         return p;
     int bm, bn;
     img_tile_dims(p.tile, bm, bn);
     long long tiles = (long long)((M + bm - 1) / bm) * ((Ncol + bn - 1) / bn) * G;
     long long slices = (Kred + kBK - 1) / kBK;
-    if (tiles >= 4 * 256 || slices < 16)
+    if (tiles >= 640)
         return p;
-    long long ns = (8 * 256 + tiles - 1) / tiles;
+    long long ns = (8 * kNumCUs + tiles - 1) / tiles;
     if (ns > slices / 8)
         ns = slices / 8;
-    if (ns > Kred / 600 - 1)
-        ns = Kred / 600 - 1;
+    if (ns > Kred / kSplitRows)
+        ns = Kred / kSplitRows;
     if (ns < 2)
         return p;
     p.kchunk = (int)((slices + ns - 1) / ns) * kBK;
@@ -515,7 +533,7 @@ int conv_fwd(int N, int C, int H, int W, int K, int R, int S, int stride, int pa
         a.nsplit = plan.nsplit;
         a.kchunk = plan.kchunk;
         a.split_stride = (long long)N * yi;
-        int tile = n == N ? plan.tile : pick_img_tile(a.M, a.Ncol, group);
+        int tile = n == N ? plan.tile : pick_img_tile(a.M, a.Ncol, a.Kred, group);
         if ((st = launch_status(launch_img_gemm(a, tile, fast, stream))) != MICONV_OK)
             return st;
     }
@@ -606,7 +624,7 @@ int conv_bwd_data(int N, int C, int H, int W, int K, int R, int S, int stride, i
                 a.nsplit = plan.nsplit;
                 a.kchunk = plan.nsplit > 1 ? plan.kchunk : a.Kred;
                 a.split_stride = (long long)N * xi;
-                int tile = stride == 1 && n == N ? plan.tile : pick_img_tile(a.M, a.Ncol, group);
+                int tile = stride == 1 && n == N ? plan.tile : pick_img_tile(a.M, a.Ncol, a.Kred, group);
                 if ((st = launch_status(launch_img_gemm(a, tile, fast, stream))) != MICONV_OK)
                     return st;
             }
