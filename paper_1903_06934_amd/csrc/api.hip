@@ -333,6 +333,8 @@ struct WgradPlan {
     size_t part_bytes, bias_bytes;
 };
 
+bool is_tap_tile(int tile) { return tile <= WG_TAP_64x16; }
+
 WgradPlan wgrad_plan(const Geom &g)
 {
     WgradPlan p;
@@ -352,11 +354,14 @@ WgradPlan wgrad_plan(const Geom &g)
         min_slices = kTapMinSlices;
         p.slice = 64;
     } else {
-        // Few channels per group: pack (c, r, s) into the columns instead.
-        p.tile = (M > 64 && Ncol > 64) ? WG_128x128 : WG_64x64;
-        int bm = p.tile == WG_128x128 ? 128 : 64;
-        tiles = (long long)gemm_tiles(M, Ncol, bm, bm) * g.G;
-        p.slice = kBK;
+        // Few channels per group: the same one-pixel-per-lane kernel with
+        // (c, r, s) packed into the columns, 96 rows for 65-96 filters.
+        const int bm = (M > 64 && M <= 96) ? 96 : 64, bn = Ncol <= 32 ? 32 : 64;
+        p.tile = bm == 96 ? WG_PIX_96x64 : bn == 32 ? WG_PIX_64x32 : WG_PIX_64x64;
+        tiles = (long long)gemm_tiles(M, Ncol, bm, bn) * g.G;
+        target = kTapTargetWorkgroups;
+        min_slices = kTapMinSlices;
+        p.slice = 64;
     }
     long long ns = (target + tiles - 1) / tiles;
     long long long_ns = Kred / (p.slice * min_slices);
@@ -380,7 +385,7 @@ WgradPlan wgrad_plan(const Geom &g)
     p.nsplit = (int)total;
     // Tap-uniform tiles always go through the partial buffer (the reduction
     // also reorders columns); packed tiles write dw directly when unsplit.
-    p.via_part = p.tile >= WG_TAP_64x32 || p.nsplit > 1;
+    p.via_part = is_tap_tile(p.tile) || p.nsplit > 1;
     p.part_bytes = p.via_part ? align_up((size_t)p.nsplit * g.K * Ncol * sizeof(float)) : 0;
     p.bias_bytes = align_up((size_t)p.nsplit * g.K * sizeof(float));
     return p;
@@ -684,7 +689,6 @@ int conv_bwd_weight(int N, int C, int H, int W, int K, int R, int S, int stride,
     float *part = (float *)ws;
     float *db_part = (float *)((char *)ws + p.part_bytes);
     a.db_part = db ? db_part : nullptr;
-    const bool vec = a.PQ % 4 == 0;
     if (mark(tl_events.before, stream) != hipSuccess)
         return MICONV_ERR_LAUNCH;
     int split0 = 0;
@@ -699,13 +703,13 @@ int conv_bwd_weight(int N, int C, int H, int W, int K, int R, int S, int stride,
         a.out = p.via_part ? part + (long long)split0 * a.split_stride : dw;
         if (db)
             a.db_part = db_part + (long long)split0 * K;
-        if ((st = launch_status(launch_wgrad_gemm(a, p.tile, vec, stream))) != MICONV_OK)
+        if ((st = launch_status(launch_wgrad_gemm(a, p.tile, stream))) != MICONV_OK)
             return st;
         split0 += a.nsplit;
     }
     if (mark(tl_events.after, stream) != hipSuccess)
         return MICONV_ERR_LAUNCH;
-    const bool tap_order = p.tile >= WG_TAP_64x32;
+    const bool tap_order = is_tap_tile(p.tile);
     if (p.via_part &&
         (st = launch_status(launch_splitk_reduce(part, p.nsplit, a.split_stride, K * a.Ncol, dw,
                                                  tap_order ? R * S : 0, tap_order ? g.Cg : 0,

@@ -2,13 +2,11 @@
 // MFMA, filter packing, split-K reduction and the bias gradient.
 //
 // GEMM core: a workgroup of WM x WN waves computes a BM x BN tile of C with
-// v_mfma_f32_32x32x2f32 (each wave owns a (BM/WM) x (BN/WN) sub-tile made of
-// 32x32 accumulator blocks).  The reduction dimension is walked in BK-deep
-// slices that are staged through LDS in a double buffer: while the MFMAs
-// consume slice t from LDS, the global loads of slice t+1 are in flight in
-// registers; one barrier per slice.  LDS holds both operands k-major
-// (As[k][m], Bs[k][n]) so that the 32 lanes of an MFMA operand read 32
-// consecutive words.
+// v_mfma_f32_16x16x4f32 (each wave owns a (BM/WM) x (BN/WN) sub-tile made of
+// 16x16 accumulator blocks; the 32x32x2 shape is also described below).
+// Operands go from HBM straight into LDS with buffer_load_dword ... lds (no
+// register staging); out-of-range elements read zero through the buffer
+// range check, so padding and ragged tiles need no branches.
 #include "internal.h"
 
 namespace miconv {
@@ -18,11 +16,6 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 // v_mfma_f32_32x32x2f32 operand layout (64 lanes):
 //   A (32 x 2): lane l holds A[l % 32][l / 32];  B (2 x 32): B[l / 32][l % 32]
 //   D (32 x 32): lane l, register v holds D[8 (v / 4) + 4 (l / 32) + v % 4][l % 32]
-__device__ __forceinline__ int acc_row(int v, int lane)
-{
-    return 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-}
-
 // v_mfma_f32_16x16x4f32: A (16 x 4): lane l holds A[l % 16][l / 16];
 // B (4 x 16): B[l / 16][l % 16]; D (16 x 16): lane l, register v holds
 // D[4 (l / 16) + v][l % 16].
@@ -58,29 +51,6 @@ struct MfmaAcc<16> {
     }
 };
 
-template <int BM, int BN, int BK, int WM, int WN, int LDA, int LDB>
-__device__ __forceinline__ void mfma_slice(const float (*As)[LDA], const float (*Bs)[LDB],
-                                           f32x16 (&acc)[BM / WM / 32][BN / WN / 32],
-                                           int lane, int wm, int wn)
-{
-    constexpr int FM = BM / WM / 32, FN = BN / WN / 32;
-    const int kr = lane >> 5, lc = lane & 31;
-#pragma unroll
-    for (int kk = 0; kk < BK; kk += 2) {
-        float af[FM], bf[FN];
-#pragma unroll
-        for (int i = 0; i < FM; i++)
-            af[i] = As[kk + kr][wm * (BM / WM) + i * 32 + lc];
-#pragma unroll
-        for (int j = 0; j < FN; j++)
-            bf[j] = Bs[kk + kr][wn * (BN / WN) + j * 32 + lc];
-#pragma unroll
-        for (int i = 0; i < FM; i++)
-#pragma unroll
-            for (int j = 0; j < FN; j++)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i], bf[j], acc[i][j], 0, 0, 0);
-    }
-}
 
 // ---------------------------------------------------------------------------
 // Operand staging: buffer loads that write straight into LDS.
@@ -397,269 +367,10 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
 }
 
 // ---------------------------------------------------------------------------
-// Backward-weight GEMM (see WgradArgs).
+// Backward-weight GEMM with one pixel per lane (same WgradArgs).
 //
-// The reduction runs over pixels, and both operands are contiguous along the
-// pixel index in HBM (dy rows; x rows for the gathered columns), so lanes load
-// along pixels (coalesced) and LDS keeps each operand row pixel-contiguous:
-// As[m][k], Bs[n][k].  Within a BK-deep slice, pixel kk sits at position
-// (kk & 1) * BK/2 + kk / 2, so the 8 pixels a lane consumes over the slice's
-// 8 MFMA steps (kk = 2 s + lane / 32) are contiguous: two ds_read_b128 per
-// 32-row block and slice.  Operands are staged through registers: the
-// loads of slice t + 1 are issued before the MFMAs of slice t and written to
-// the other LDS buffer after them; one barrier per slice.  Loads are raw
-// buffer loads, so out-of-range elements (padding, ragged tiles, the end of
-// the split) read 0 without branches.  VEC: P*Q % 4 == 0, so four
-// consecutive pixels of one dy row are one aligned float4.
-// ---------------------------------------------------------------------------
-// The raw buffer-load builtins return bit patterns: reinterpret, never convert.
-__device__ __forceinline__ float buf_load(__amdgpu_buffer_rsrc_t r, uint32_t voff)
-{
-    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, voff, 0, 0));
-}
-
-__device__ __forceinline__ float4 buf_load4(__amdgpu_buffer_rsrc_t r, uint32_t voff)
-{
-    typedef float f32x4 __attribute__((ext_vector_type(4)));
-    f32x4 v = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, 0, 0));
-    return make_float4(v[0], v[1], v[2], v[3]);
-}
-
-template <int BM, int BN, int WM, int WN, bool VEC>
-__global__ __launch_bounds__(64 * WM * WN) void wgrad_gemm_kernel(const WgradArgs a)
-{
-    constexpr int BK = 16, NT = 64 * WM * WN;
-    constexpr int TM = BM / WM, TN = BN / WN, FM = TM / 32, FN = TN / 32;
-    constexpr int KP = BK + 4;                 // row stride (words), keeps b128 rows aligned
-    constexpr int G4 = BK / 4;                 // 4-pixel groups per slice
-    constexpr int RA = BM * G4 / NT, RB = BN * G4 / NT;  // 4-pixel groups per thread
-    static_assert((BM * G4) % NT == 0 && (BN * G4) % NT == 0, "loader mapping");
-
-    // 16-byte aligned: rows are written as float2 and read as float4.
-    __shared__ __attribute__((aligned(16))) float As[2][BM][KP];
-    __shared__ __attribute__((aligned(16))) float Bs[2][BN][KP];
-
-    const int tid = threadIdx.x, lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wm = wave % WM, wn = wave / WM;
-    const int mtiles = (a.M + BM - 1) / BM, ntiles = (a.Ncol + BN - 1) / BN;
-    const int tiles = mtiles * ntiles;
-    const int lin = xcd_tile(blockIdx.x, tiles * a.groups * a.nsplit);
-    const int split = lin / (tiles * a.groups);
-    const int rest = lin - split * tiles * a.groups;
-    const int g = rest / tiles, tile = rest - g * tiles;
-    const int mt = tile % mtiles, nt = tile / mtiles;
-    const int m0 = mt * BM, n0 = nt * BN;
-    const int kbeg = split * a.chunk;
-    const int kend = min(a.Kred, kbeg + a.chunk);
-
-    const __amdgpu_buffer_rsrc_t rdy = make_rsrc(a.dy, a.dy_bytes);
-    const __amdgpu_buffer_rsrc_t rx = make_rsrc(a.x, a.x_bytes);
-
-    // Loader mapping: thread -> 4-pixel group q4 (same for A and B) and rows
-    // row = tid / G4 + (NT / G4) * i.
-    const int q4 = tid % G4, row0 = tid / G4;
-    constexpr int RSTEP = NT / G4;
-    uint32_t a_row[RA];  // byte offset of dy row (g*Kg + m) within an image, masked
-#pragma unroll
-    for (int i = 0; i < RA; i++) {
-        int m = m0 + row0 + RSTEP * i;
-        a_row[i] = ((uint32_t)(g * a.M + m) * (uint32_t)a.PQ * 4u) | oob_mask(m < a.M);
-    }
-    uint32_t b_col[RB];  // byte offset of x[., g*Cg + c][r][s] within an image, masked
-    int b_r[RB], b_s[RB];
-#pragma unroll
-    for (int i = 0; i < RB; i++) {
-        int n = n0 + row0 + RSTEP * i;
-        bool ok = n < a.Ncol;
-        uint32_t nc = ok ? (uint32_t)n : 0u;
-        uint32_t c = fast_div(nc, a.n_rs);
-        uint32_t rs = nc - c * a.n_rs.d;
-        uint32_t r = fast_div(rs, a.n_s);
-        uint32_t s_ = rs - r * a.n_s.d;
-        b_r[i] = (int)r;
-        b_s[i] = (int)s_;
-        b_col[i] = ((uint32_t)(g * a.Cg + c) * (uint32_t)a.HW * 4u) | oob_mask(ok);
-    }
-
-    float ra[RA][4], rb[RB][4];
-    auto load_slice = [&](int k0) {
-        const int pix = k0 + 4 * q4;
-        // A: dy[img][g*Kg + m][pq .. pq+3]
-        if constexpr (VEC) {
-            const bool ok = pix < kend;  // the whole group shares one image row
-            const uint32_t pc = ok ? (uint32_t)pix : 0u;
-            const uint32_t img = fast_div(pc, a.pix_pq);
-            const uint32_t pq = pc - img * a.pix_pq.d;
-            const uint32_t base = (img * (uint32_t)a.dy_img_words + pq) * 4u | oob_mask(ok);
-#pragma unroll
-            for (int i = 0; i < RA; i++) {
-                float4 v = buf_load4(rdy, (base + a_row[i]) | (a_row[i] & kOob) | (base & kOob));
-                ra[i][0] = v.x;
-                ra[i][1] = v.y;
-                ra[i][2] = v.z;
-                ra[i][3] = v.w;
-            }
-        }
-        // per-pixel decode (needed by B, and by A when not vectorised)
-        int pimg[4], pp[4], pq_[4];
-        bool pok[4];
-#pragma unroll
-        for (int e = 0; e < 4; e++) {
-            const int px = pix + e;
-            pok[e] = px < kend;
-            const uint32_t pc = pok[e] ? (uint32_t)px : 0u;
-            const uint32_t img = fast_div(pc, a.pix_pq);
-            const uint32_t pq = pc - img * a.pix_pq.d;
-            const uint32_t p = fast_div(pq, a.pix_q);
-            pimg[e] = (int)img;
-            pq_[e] = (int)pq;
-            pp[e] = (int)p;
-        }
-        if constexpr (!VEC) {
-#pragma unroll
-            for (int e = 0; e < 4; e++) {
-                const uint32_t base = ((uint32_t)pimg[e] * (uint32_t)a.dy_img_words +
-                                       (uint32_t)pq_[e]) * 4u | oob_mask(pok[e]);
-#pragma unroll
-                for (int i = 0; i < RA; i++)
-                    ra[i][e] = buf_load(rdy, (base + a_row[i]) | (a_row[i] & kOob) | (base & kOob));
-            }
-        }
-        // B: x[img][g*Cg + c][p*st - pad + r][q*st - pad + s]
-#pragma unroll
-        for (int e = 0; e < 4; e++) {
-            const int q = pq_[e] - pp[e] * (int)a.pix_q.d;
-            const int h0 = pp[e] * a.stride - a.pad, w0 = q * a.stride - a.pad;
-            const uint32_t ibase = (uint32_t)pimg[e] * (uint32_t)a.x_img_words * 4u;
-#pragma unroll
-            for (int i = 0; i < RB; i++) {
-                const int h = h0 + b_r[i], w = w0 + b_s[i];
-                const bool ok = pok[e] && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
-                const uint32_t off = ibase + b_col[i] + (uint32_t)(h * a.W + w) * 4u;
-                rb[i][e] = buf_load(rx, off | oob_mask(ok) | (b_col[i] & kOob));
-            }
-        }
-    };
-    // Pixel kk = 4 q4 + e goes to position (kk & 1) * BK/2 + kk / 2: the even
-    // pixels (e = 0, 2) are adjacent, and so are the odd ones (e = 1, 3).
-    auto store_slice = [&](int buf) {
-        const int pe = 2 * q4, po = BK / 2 + 2 * q4;
-#pragma unroll
-        for (int i = 0; i < RA; i++) {
-            float *rowp = &As[buf][row0 + RSTEP * i][0];
-            *(float2 *)&rowp[pe] = make_float2(ra[i][0], ra[i][2]);
-            *(float2 *)&rowp[po] = make_float2(ra[i][1], ra[i][3]);
-        }
-#pragma unroll
-        for (int i = 0; i < RB; i++) {
-            float *rowp = &Bs[buf][row0 + RSTEP * i][0];
-            *(float2 *)&rowp[pe] = make_float2(rb[i][0], rb[i][2]);
-            *(float2 *)&rowp[po] = make_float2(rb[i][1], rb[i][3]);
-        }
-    };
-
-    f32x16 acc[FM][FN];
-#pragma unroll
-    for (int i = 0; i < FM; i++)
-#pragma unroll
-        for (int j = 0; j < FN; j++)
-#pragma unroll
-            for (int v = 0; v < 16; v++)
-                acc[i][j][v] = 0.f;
-
-    // Bias gradient: the workgroups of the first column tile also sum the dy
-    // rows they stage (thread -> row tid / TPR, BK / TPR slice positions).
-    constexpr int TPR = NT / BM;
-    const bool do_bias = a.db_part != nullptr && nt == 0;
-    const int brow = tid / TPR, bpart = tid % TPR;
-    float bsum = 0.f;
-
-    const int kr = lane >> 5, lc = lane & 31;
-    const int nslices = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
-    if (nslices > 0) {
-        load_slice(kbeg);
-        store_slice(0);
-    }
-    __syncthreads();
-    for (int t = 0; t < nslices; t++) {
-        const int buf = t & 1;
-        if (t + 1 < nslices)
-            load_slice(kbeg + (t + 1) * BK);
-        if (do_bias) {
-            const float *rowp = &As[buf][brow][bpart * (BK / TPR)];
-#pragma unroll
-            for (int u = 0; u < BK / TPR; u += 4) {
-                float4 v = *(const float4 *)&rowp[u];
-                bsum += v.x;
-                bsum += v.y;
-                bsum += v.z;
-                bsum += v.w;
-            }
-        }
-        float4 af[FM][2], bf[FN][2];
-#pragma unroll
-        for (int i = 0; i < FM; i++) {
-            const float *rowp = &As[buf][wm * TM + i * 32 + lc][kr * (BK / 2)];
-            af[i][0] = *(const float4 *)&rowp[0];
-            af[i][1] = *(const float4 *)&rowp[4];
-        }
-#pragma unroll
-        for (int j = 0; j < FN; j++) {
-            const float *rowp = &Bs[buf][wn * TN + j * 32 + lc][kr * (BK / 2)];
-            bf[j][0] = *(const float4 *)&rowp[0];
-            bf[j][1] = *(const float4 *)&rowp[4];
-        }
-#pragma unroll
-        for (int s = 0; s < BK / 2; s++) {
-#pragma unroll
-            for (int i = 0; i < FM; i++) {
-                const float4 &av = af[i][s >> 2];
-                const float aval = (s & 3) == 0 ? av.x : (s & 3) == 1 ? av.y : (s & 3) == 2 ? av.z : av.w;
-#pragma unroll
-                for (int j = 0; j < FN; j++) {
-                    const float4 &bv = bf[j][s >> 2];
-                    const float bval = (s & 3) == 0 ? bv.x : (s & 3) == 1 ? bv.y : (s & 3) == 2 ? bv.z : bv.w;
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(aval, bval, acc[i][j], 0, 0, 0);
-                }
-            }
-        }
-        if (t + 1 < nslices)
-            store_slice(buf ^ 1);
-        __syncthreads();
-    }
-
-    if (do_bias) {
-#pragma unroll
-        for (int off = 1; off < TPR; off <<= 1)
-            bsum += __shfl_xor(bsum, off, 64);
-        const int m = m0 + brow;
-        if (bpart == 0 && m < a.M)
-            a.db_part[(long long)split * a.K + g * a.M + m] = bsum;
-    }
-
-    float *outg = a.out + (long long)split * a.split_stride + (long long)g * a.M * a.Ncol;
-#pragma unroll
-    for (int i = 0; i < FM; i++)
-#pragma unroll
-        for (int v = 0; v < 16; v++) {
-            int m = m0 + wm * TM + i * 32 + acc_row(v, lane);
-            if (m >= a.M)
-                continue;
-#pragma unroll
-            for (int j = 0; j < FN; j++) {
-                int n = n0 + wn * TN + j * 32 + lc;
-                if (n < a.Ncol)
-                    outg[(long long)m * a.Ncol + n] = acc[i][j][v];
-            }
-        }
-}
-
-// ---------------------------------------------------------------------------
-// Backward-weight GEMM with tap-uniform tiles (same WgradArgs; requires the
-// columns of a tile to share one filter tap).
-//
-// dw columns are taken in (tap, channel) order: a workgroup tile owns one tap
+// Tap-uniform tiles (PACKED = false) take dw columns in (tap, channel) order:
+// a workgroup tile owns one tap
 // t = r S + s and BN consecutive channels, so its B operand is x shifted by
 // (r, s) — for a given pixel, the BN rows of B are BN channels at one
 // spatial position.  A slice of the reduction is 64 consecutive pixels; lane
@@ -670,6 +381,15 @@ __global__ __launch_bounds__(64 * WM * WN) void wgrad_gemm_kernel(const WgradArg
 // direct-to-LDS wave-load whose offset is that base plus a row stride: one
 // VALU add.  Rows past K/G or C/G read neighbouring data (or zeros) and are
 // simply not stored.
+//
+// Packed tiles (PACKED = true, for few channels per group, e.g. the 3 colour
+// channels of a first layer) own BN consecutive columns n = (c R + r) S + s
+// of dw instead.  The byte offset of x for (pixel, column) splits into a
+// per-lane part, (h0 W + w0) with h0 = p stride - pad and w0 = q stride - pad,
+// and a per-column part, c H W + r W + s, which is wave-uniform (scalar
+// registers); a row-load adds the two and checks h0 + r and w0 + s against
+// the image (skipped when pad = 0, where every tap of a valid output pixel
+// lies inside the image).
 //
 // LDS holds each row pixel-contiguous (64 words + 4 of padding, so the
 // ds_read_b128 of 16 consecutive rows hit distinct banks).  With the 32x32x2
@@ -682,8 +402,8 @@ __global__ __launch_bounds__(64 * WM * WN) void wgrad_gemm_kernel(const WgradArg
 // barrier frees the LDS, the next slice's loads are issued, and the slice's
 // MFMAs run while they land.
 // ---------------------------------------------------------------------------
-template <int BM, int BN, int WM, int WN, int MF>
-__global__ __launch_bounds__(64 * WM * WN) void wgrad_tap_kernel(const WgradArgs a)
+template <int BM, int BN, int WM, int WN, int MF, bool PACKED>
+__global__ __launch_bounds__(64 * WM * WN) void wgrad_kernel(const WgradArgs a)
 {
     typedef MfmaAcc<MF> Mf;
     constexpr int BK = 64, LDR = BK + 4;
@@ -699,14 +419,18 @@ __global__ __launch_bounds__(64 * WM * WN) void wgrad_tap_kernel(const WgradArgs
     const int wm = wave % WM, wn = wave / WM;
     const int RS = (int)a.n_rs.d;
     const int cblocks = (a.Cg + BN - 1) / BN;
-    const int mtiles = (a.M + BM - 1) / BM, ntiles = RS * cblocks;
+    const int mtiles = (a.M + BM - 1) / BM;
+    const int ntiles = PACKED ? (a.Ncol + BN - 1) / BN : RS * cblocks;
     const int tiles = mtiles * ntiles;
     const int lin = xcd_tile(blockIdx.x, tiles * a.groups * a.nsplit);
     const int split = lin / (tiles * a.groups);
     const int rest = lin - split * tiles * a.groups;
     const int g = rest / tiles, tile = rest - g * tiles;
     const int mt = tile % mtiles, nt = tile / mtiles;
-    const int tap = nt / cblocks, c0 = (nt - tap * cblocks) * BN;
+    // Tap-uniform: tap and first channel of the tile.  Packed: first column.
+    const int tap = PACKED ? 0 : nt / cblocks;
+    const int c0 = PACKED ? 0 : (nt - tap * cblocks) * BN;
+    const int n0 = PACKED ? nt * BN : 0;
     const int r = (int)fast_div((uint32_t)tap, a.n_s), s_ = tap - r * (int)a.n_s.d;
     const int m0 = mt * BM;
     const int kbeg = split * a.chunk;
@@ -726,20 +450,39 @@ __global__ __launch_bounds__(64 * WM * WN) void wgrad_tap_kernel(const WgradArgs
         const uint32_t pq = pc - img * a.pix_pq.d;
         const uint32_t p = fast_div(pq, a.pix_q);
         const int q = (int)(pq - p * a.pix_q.d);
-        const int h = (int)p * a.stride - a.pad + r, w = q * a.stride - a.pad + s_;
-        const bool xok = pok && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
         const uint32_t abase = pok ? (img * a.dy_img_words + pq) * 4u + a_row0 : kOob;
-        const uint32_t bbase =
-            xok ? (img * a.x_img_words + (uint32_t)(h * a.W + w)) * 4u + b_row0 : kOob;
 #pragma unroll
         for (int i = 0; i < BM / NW; i++) {
             const int j = wave + NW * i;
             lds_load(rdy, &L[j * LDR], abase + (uint32_t)j * a_rowstep);
         }
+        if constexpr (PACKED) {
+            const int h0 = (int)p * a.stride - a.pad, w0 = q * a.stride - a.pad;
+            const uint32_t pbase = (img * a.x_img_words + (uint32_t)(h0 * a.W + w0)) * 4u + b_row0;
 #pragma unroll
-        for (int i = 0; i < BN / NW; i++) {
-            const int j = wave + NW * i;
-            lds_load(rx, &L[(BM + j) * LDR], bbase + (uint32_t)j * b_rowstep);
+            for (int i = 0; i < BN / NW; i++) {
+                const int n = n0 + wave + NW * i;  // wave-uniform column
+                const uint32_t c = fast_div((uint32_t)n, a.n_rs);
+                const uint32_t rs = (uint32_t)n - c * a.n_rs.d;
+                const uint32_t rr = fast_div(rs, a.n_s);
+                const int ss = (int)(rs - rr * a.n_s.d);
+                bool ok = pok && n < a.Ncol;
+                if (a.pad != 0)
+                    ok = ok && (unsigned)(h0 + (int)rr) < (unsigned)a.H &&
+                         (unsigned)(w0 + ss) < (unsigned)a.W;
+                const uint32_t cofs = (c * (uint32_t)a.HW + rr * (uint32_t)a.W + (uint32_t)ss) * 4u;
+                lds_load(rx, &L[(BM + wave + NW * i) * LDR], ok ? pbase + cofs : kOob);
+            }
+        } else {
+            const int h = (int)p * a.stride - a.pad + r, w = q * a.stride - a.pad + s_;
+            const bool xok = pok && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
+            const uint32_t bbase =
+                xok ? (img * a.x_img_words + (uint32_t)(h * a.W + w)) * 4u + b_row0 : kOob;
+#pragma unroll
+            for (int i = 0; i < BN / NW; i++) {
+                const int j = wave + NW * i;
+                lds_load(rx, &L[(BM + j) * LDR], bbase + (uint32_t)j * b_rowstep);
+            }
         }
     };
 
@@ -752,10 +495,12 @@ __global__ __launch_bounds__(64 * WM * WN) void wgrad_tap_kernel(const WgradArgs
             for (int v = 0; v < Mf::NV; v++)
                 acc[i][j][v] = 0.f;
 
-    // Bias gradient: the workgroups of tap 0 and the first channel block also
-    // sum the dy rows they stage (thread -> row tid / TPR, 64 / TPR pixels).
-    constexpr int TPR = 64 * NW / BM;
-    const bool do_bias = a.db_part != nullptr && tap == 0 && c0 == 0;
+    // Bias gradient: the workgroups of the first column tile also sum the dy
+    // rows they stage (thread -> row tid / TPR, 64 / TPR pixels; TPR is the
+    // largest power of two with BM * TPR threads at most).
+    constexpr int TPR = 64 * NW / BM >= 8 ? 8 : 64 * NW / BM >= 4 ? 4 : 64 * NW / BM >= 2 ? 2 : 1;
+    static_assert(BM <= 64 * NW, "one thread per bias row at least");
+    const bool do_bias = a.db_part != nullptr && nt == 0;
     const int brow = threadIdx.x / TPR, bpart = threadIdx.x % TPR;
     float bsum = 0.f;
 
@@ -766,7 +511,7 @@ __global__ __launch_bounds__(64 * WM * WN) void wgrad_tap_kernel(const WgradArgs
     for (int t = 0; t < nslices; t++) {
         __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();  // slice t is in LDS
-        if (do_bias) {
+        if (do_bias && brow < BM) {
             const float *rowp = &L[brow * LDR + bpart * (BK / TPR)];
 #pragma unroll
             for (int u = 0; u < BK / TPR; u += 4) {
@@ -812,14 +557,16 @@ __global__ __launch_bounds__(64 * WM * WN) void wgrad_tap_kernel(const WgradArgs
         for (int off = 1; off < TPR; off <<= 1)
             bsum += __shfl_xor(bsum, off, 64);
         const int m = m0 + brow;
-        if (bpart == 0 && m < a.M)
+        if (bpart == 0 && brow < BM && m < a.M)
             a.db_part[(long long)split * a.K + g * a.M + m] = bsum;
     }
 
-    // Partial dw in tile order [split][g*Kg + m][tap][c] (coalesced along c);
-    // the reduction kernel moves it to dw[k][c][r][s].
+    // Tap-uniform: partial dw in tile order [split][g*Kg + m][tap][c]
+    // (coalesced along c); the reduction kernel moves it to dw[k][c][r][s].
+    // Packed: dw[k][n] itself, or its partial [split][k][n].
     float *outg = a.out + (long long)split * a.split_stride + (long long)g * a.M * a.Ncol +
-                  (long long)tap * a.Cg;
+                  (PACKED ? (long long)n0 : (long long)tap * a.Cg);
+    const int ncols = PACKED ? a.Ncol - n0 : a.Cg - c0;
 #pragma unroll
     for (int i = 0; i < FM; i++)
 #pragma unroll
@@ -829,9 +576,9 @@ __global__ __launch_bounds__(64 * WM * WN) void wgrad_tap_kernel(const WgradArgs
                 continue;
 #pragma unroll
             for (int j = 0; j < FN; j++) {
-                int c = c0 + wn * TN + j * MF + lc;
-                if (c < a.Cg)
-                    outg[(long long)m * a.Ncol + c] = acc[i][j][v];
+                int c = wn * TN + j * MF + lc;
+                if (c < ncols)
+                    outg[(long long)m * a.Ncol + (PACKED ? 0 : c0) + c] = acc[i][j][v];
             }
         }
 }
@@ -976,38 +723,27 @@ hipError_t launch_img_gemm(const ImgGemmArgs &a, int tile, bool fast, hipStream_
     }
 }
 
-template <int BM, int BN, int WM, int WN>
-static hipError_t wgrad_launch(const WgradArgs &a, bool vec, hipStream_t stream)
-{
-    int tiles = ((a.M + BM - 1) / BM) * ((a.Ncol + BN - 1) / BN);
-    dim3 grid(tiles * a.groups * a.nsplit);
-    if (vec)
-        hipLaunchKernelGGL((wgrad_gemm_kernel<BM, BN, WM, WN, true>), grid, dim3(64 * WM * WN),
-                           0, stream, a);
-    else
-        hipLaunchKernelGGL((wgrad_gemm_kernel<BM, BN, WM, WN, false>), grid, dim3(64 * WM * WN),
-                           0, stream, a);
-    return hipGetLastError();
-}
-
-template <int BM, int BN, int WM, int WN, int MF = 32>
-static hipError_t wgrad_tap_launch(const WgradArgs &a, hipStream_t stream)
+template <int BM, int BN, int WM, int WN, int MF, bool PACKED = false>
+static hipError_t wgrad_launch(const WgradArgs &a, hipStream_t stream)
 {
     int RS = (int)a.n_rs.d;
-    int tiles = ((a.M + BM - 1) / BM) * RS * ((a.Cg + BN - 1) / BN);
-    hipLaunchKernelGGL((wgrad_tap_kernel<BM, BN, WM, WN, MF>), dim3(tiles * a.groups * a.nsplit),
-                       dim3(64 * WM * WN), 0, stream, a);
+    int ntiles = PACKED ? (a.Ncol + BN - 1) / BN : RS * ((a.Cg + BN - 1) / BN);
+    int tiles = ((a.M + BM - 1) / BM) * ntiles;
+    hipLaunchKernelGGL((wgrad_kernel<BM, BN, WM, WN, MF, PACKED>),
+                       dim3(tiles * a.groups * a.nsplit), dim3(64 * WM * WN), 0, stream, a);
     return hipGetLastError();
 }
 
-hipError_t launch_wgrad_gemm(const WgradArgs &a, int tile, bool vec, hipStream_t stream)
+hipError_t launch_wgrad_gemm(const WgradArgs &a, int tile, hipStream_t stream)
 {
     switch (tile) {
-    case WG_128x128: return wgrad_launch<128, 128, 2, 2>(a, vec, stream);
-    case WG_TAP_64x32: return wgrad_tap_launch<64, 32, 2, 2, 16>(a, stream);
-    case WG_TAP_64x48: return wgrad_tap_launch<64, 48, 4, 1, 16>(a, stream);
-    case WG_TAP_64x16: return wgrad_tap_launch<64, 16, 4, 1, 16>(a, stream);
-    default: return wgrad_launch<64, 64, 2, 2>(a, vec, stream);
+    case WG_TAP_64x32: return wgrad_launch<64, 32, 2, 2, 16>(a, stream);
+    case WG_TAP_64x48: return wgrad_launch<64, 48, 4, 1, 16>(a, stream);
+    case WG_TAP_64x16: return wgrad_launch<64, 16, 4, 1, 16>(a, stream);
+    case WG_PIX_96x64: return wgrad_launch<96, 64, 2, 2, 16, true>(a, stream);
+    case WG_PIX_64x64: return wgrad_launch<64, 64, 4, 1, 16, true>(a, stream);
+    case WG_PIX_64x32: return wgrad_launch<64, 32, 2, 2, 16, true>(a, stream);
+    default: return hipErrorInvalidValue;
     }
 }
 

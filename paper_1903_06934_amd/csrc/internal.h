@@ -98,13 +98,13 @@ enum ImgTile {
     IMG_64x64 = 0, IMG_128x64, IMG_16x128, IMG_32x64, IMG_48x64, IMG_48x128, IMG_96x64,
     IMG_96x128
 };
-// Backward-weight kernels: packed (c, r, s) columns, or tap-uniform tiles
-// (BM rows of K/G x BN channels of one tap).
-// Every tap-uniform shape follows WG_TAP_64x32.
-enum WgradTile { WG_128x128 = 0, WG_64x64, WG_TAP_64x32, WG_TAP_64x48, WG_TAP_64x16 };
+// Backward-weight tiles of the one-pixel-per-lane kernel: tap-uniform
+// (BM rows of K/G x BN channels of one tap) or packed (BM rows x BN
+// consecutive (c, r, s) columns).
+enum WgradTile { WG_TAP_64x32 = 0, WG_TAP_64x48, WG_TAP_64x16, WG_PIX_96x64, WG_PIX_64x64, WG_PIX_64x32 };
 
 hipError_t launch_img_gemm(const ImgGemmArgs &a, int tile, bool fast, hipStream_t stream);
-hipError_t launch_wgrad_gemm(const WgradArgs &a, int tile, bool vec, hipStream_t stream);
+hipError_t launch_wgrad_gemm(const WgradArgs &a, int tile, hipStream_t stream);
 
 // wp[g][kk][k] = w[g*Kg + k][c][r][s] with kk = (r*S + s)*Cg + c, or, if
 // cblock (Cg % 16 == 0), kk = ((c / 16) * R*S + r*S + s) * 16 + c % 16.
