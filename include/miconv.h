@@ -54,8 +54,9 @@ typedef enum miconv_status {
     MICONV_ERR_SHAPE = -1,     /* a dim < 1, pad < 0, stride < 1, C or K not divisible by
                                   group, P or Q < 1, a tensor above 2^31 - 1 elements, one
                                   image (C*H*W or K*P*Q) or the filter bank above 2^29 - 1
-                                  elements, H, W, R, S or pad above 32767, or group above
-                                  65535 */
+                                  elements (also counted as K rows of (C/G)*R*S and as C
+                                  rows of (K/G)*R*S, each rounded up to a multiple of 16),
+                                  H, W, R, S or pad above 32767, or group above 65535 */
     MICONV_ERR_NULL = -2,      /* a required pointer is NULL */
     MICONV_ERR_WORKSPACE = -3, /* ws_bytes below conv_workspace_size(), or ws NULL when
                                   a workspace is needed */

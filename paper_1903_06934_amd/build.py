@@ -5,6 +5,9 @@ import os
 import subprocess
 import sys
 
+if __package__ in (None, ""):
+    sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
@@ -34,6 +37,10 @@ def build(verbose: bool = False) -> str:
         raise RuntimeError(f"hipcc failed ({res.returncode}):\n{out}")
     if out.strip() and verbose:
         print(out, file=sys.stderr)
+    # The image GEMM's untracked filter loads are only correct if the
+    # compiler kept their registers out of reach while in flight.
+    from paper_1903_06934_amd import isa_check
+    isa_check.check(HIPCC, FLAGS, os.path.join(CSRC, "conv_kernels.hip"))
     os.replace(tmp, LIBRARY)
     return LIBRARY
 

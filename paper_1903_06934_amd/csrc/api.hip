@@ -79,9 +79,12 @@ int make_geom(int N, int C, int H, int W, int K, int R, int S, int stride, int p
         return MICONV_ERR_SHAPE;
     // Kernels address the images of one launch, and the packed filter bank,
     // with byte offsets below 2^31: one image and the filters must each stay
-    // below 2^29 elements.
+    // below 2^29 elements, the filters also as packed (each filter's
+    // (C/G) R S, and each input channel's (K/G) R S, rounded up to 16).
+    long long pw_fwd = (long long)K * (((long long)(C / group) * R * S + 15) / 16 * 16);
+    long long pw_bwd = (long long)C * (((long long)(K / group) * R * S + 15) / 16 * 16);
     if ((long long)C * H * W > kMaxChunkElems || (long long)K * P * Q > kMaxChunkElems ||
-        nw > kMaxChunkElems)
+        nw > kMaxChunkElems || pw_fwd > kMaxChunkElems || pw_bwd > kMaxChunkElems)
         return MICONV_ERR_SHAPE;
     *g = Geom{N, C, H, W, K, R, S, stride, pad, group, P, Q, C / group, K / group};
     return MICONV_OK;
@@ -257,7 +260,7 @@ ImgPlan img_plan(int M, long long Ncol, int Kred, int G, bool allow_split)
 // ------------------------------------------------------------ fwd plan
 size_t fwd_pack_bytes(const Geom &g)
 {
-    return align_up((size_t)g.K * g.Cg * g.R * g.S * sizeof(float));
+    return align_up((size_t)g.K * pad16(g.Cg * g.R * g.S) * sizeof(float));
 }
 
 ImgPlan fwd_plan(const Geom &g)
@@ -302,7 +305,7 @@ size_t bwd_data_pack_bytes(const Geom &g)
         for (int pw = 0; pw < g.st; pw++) {
             Axis ah = phase_axis(g.H, g.R, g.st, g.pad, ph);
             Axis aw = phase_axis(g.W, g.S, g.st, g.pad, pw);
-            total += align_up((size_t)g.K * g.Cg * ah.nt * aw.nt * sizeof(float));
+            total += align_up((size_t)g.C * pad16(g.Kg * ah.nt * aw.nt) * sizeof(float));
         }
     return total;
 }
@@ -492,7 +495,13 @@ int conv_fwd(int N, int C, int H, int W, int K, int R, int S, int stride, int pa
     (void)hipGetLastError();
 
     float *wp = (float *)ws;
-    if (launch_pack_fwd(w, wp, K, g.Cg, R, S, group, g.Cg % kBK == 0, stream) != hipSuccess)
+    const int a_ld = pad16(g.Cg * R * S);
+    const ImgPlan plan = fwd_plan(g);
+    // The filter layout follows the tile; every launch of the call uses a
+    // tile of the same kind (the kind depends on M only).
+    const bool kmajor = img_tile_shares_a(plan.tile);
+    if (launch_pack_fwd(w, wp, K, g.Cg, R, S, group, g.Cg % kBK == 0, a_ld, kmajor, stream) !=
+        hipSuccess)
         return MICONV_ERR_LAUNCH;
 
     const int nb = images_per_launch(g);
@@ -502,7 +511,8 @@ int conv_fwd(int N, int C, int H, int W, int K, int R, int S, int stride, int pa
     a.Kred = g.Cg * R * S;
     a.groups = group;
     a.A = wp;
-    a.a_bytes = (uint32_t)((size_t)K * a.Kred * fb);
+    a.a_ld = a_ld;
+    a.a_bytes = (uint32_t)((size_t)K * a_ld * fb);
     a.cin = g.Cg;
     a.src_h = H;
     a.src_w = W;
@@ -525,7 +535,6 @@ int conv_fwd(int N, int C, int H, int W, int K, int R, int S, int stride, int pa
     a.ooff_h = 0;
     a.ooff_w = 0;
     const bool fast = g.Cg % kBK == 0;
-    const ImgPlan plan = fwd_plan(g);
     float *part = (float *)((char *)ws + fwd_pack_bytes(g));
     if (mark(tl_events.before, stream) != hipSuccess)
         return MICONV_ERR_LAUNCH;
@@ -539,6 +548,8 @@ int conv_fwd(int N, int C, int H, int W, int K, int R, int S, int stride, int pa
         a.kchunk = plan.kchunk;
         a.split_stride = (long long)N * yi;
         int tile = n == N ? plan.tile : pick_img_tile(a.M, a.Ncol, a.Kred, group);
+        if (img_tile_shares_a(tile) != kmajor)
+            tile = plan.tile;
         if ((st = launch_status(launch_img_gemm(a, tile, fast, stream))) != MICONV_OK)
             return st;
     }
@@ -581,20 +592,28 @@ int conv_bwd_data(int N, int C, int H, int W, int K, int R, int S, int stride, i
         for (int pw = 0; pw < stride; pw++) {
             Axis ah = phase_axis(H, R, stride, pad, ph);
             Axis aw = phase_axis(W, S, stride, pad, pw);
-            size_t bytes = align_up((size_t)K * g.Cg * ah.nt * aw.nt * fb);
+            const int a_ld = pad16(g.Kg * ah.nt * aw.nt);
+            size_t bytes = align_up((size_t)C * a_ld * fb);
             float *wr = (float *)wsp;
             wsp += bytes;
             if (ah.n == 0 || aw.n == 0)
                 continue;
+            const int kred = ah.nt * aw.nt * g.Kg;
+            const int tile0 = stride == 1 ? plan.tile
+                                          : pick_img_tile(g.Cg, (long long)(N < nb ? N : nb) *
+                                                                    ah.n * aw.n, kred, group);
+            const bool kmajor = img_tile_shares_a(tile0);
             if (launch_pack_bwd_phase(w, wr, K, g.Cg, R, S, group, ah.t0, aw.t0, ah.nt, aw.nt,
-                                      stride, g.Kg % kBK == 0, stream) != hipSuccess)
+                                      stride, g.Kg % kBK == 0, a_ld, kmajor, stream) !=
+                hipSuccess)
                 return MICONV_ERR_LAUNCH;
             ImgGemmArgs a;
             a.M = g.Cg;
-            a.Kred = ah.nt * aw.nt * g.Kg;
+            a.Kred = kred;
             a.groups = group;
             a.A = wr;
-            a.a_bytes = (uint32_t)((size_t)C * a.Kred * fb);
+            a.a_ld = a_ld;
+            a.a_bytes = (uint32_t)((size_t)C * a_ld * fb);
             a.cin = g.Kg;
             a.src_h = g.P;
             a.src_w = g.Q;
@@ -629,7 +648,10 @@ int conv_bwd_data(int N, int C, int H, int W, int K, int R, int S, int stride, i
                 a.nsplit = plan.nsplit;
                 a.kchunk = plan.nsplit > 1 ? plan.kchunk : a.Kred;
                 a.split_stride = (long long)N * xi;
-                int tile = stride == 1 && n == N ? plan.tile : pick_img_tile(a.M, a.Ncol, a.Kred, group);
+                int tile = stride == 1 && n == N ? plan.tile
+                                                 : pick_img_tile(a.M, a.Ncol, a.Kred, group);
+                if (img_tile_shares_a(tile) != kmajor)
+                    tile = tile0;
                 if ((st = launch_status(launch_img_gemm(a, tile, fast, stream))) != MICONV_OK)
                     return st;
             }

@@ -80,6 +80,35 @@ __device__ __forceinline__ void lds_load(__amdgpu_buffer_rsrc_t r, float *lds_ro
     __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (LDS_AS void *)lds_row, 4, voff, 0, 0, 0);
 }
 
+// The same raw buffer descriptor as four dwords, for inline assembly.
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ i32x4 rsrc_words(const void *p, uint32_t bytes)
+{
+    const uint64_t a = (uint64_t)p;
+    i32x4 r;
+    r[0] = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+    r[1] = __builtin_amdgcn_readfirstlane((int)(uint32_t)(a >> 32));
+    r[2] = __builtin_amdgcn_readfirstlane((int)bytes);
+    r[3] = 0x00020000;
+    return r;
+}
+
+// buffer_load_dwordx4 into registers, issued as inline assembly so that the
+// compiler does not track it as a pending memory operation: its own waits
+// (which it places conservatively across the rotating register stages,
+// draining the pipeline) are then not generated.  The caller owns the wait
+// (s_waitcnt vmcnt) before the result is read, and the result must reach its
+// only consumers (MFMAs after that wait) without compiler-made copies:
+// paper_1903_06934_amd/isa_check.py verifies both on the built code.
+__device__ __forceinline__ f32x4 load4_untracked(i32x4 rsrc, uint32_t voff)
+{
+    f32x4 v;
+    // Early-clobber output: the destination never doubles as the address
+    // register, so only these loads write the destination registers.
+    asm volatile("buffer_load_dwordx4 %0, %1, %2, 0 offen" : "=&v"(v) : "v"(voff), "s"(rsrc));
+    return v;
+}
+
 // Out-of-range bit for a lane whose element is absent.
 __device__ __forceinline__ uint32_t oob_mask(bool ok) { return ok ? 0u : kOob; }
 
@@ -96,47 +125,50 @@ __device__ __forceinline__ int xcd_tile(int hw, int total)
 // ---------------------------------------------------------------------------
 // Forward / backward-data implicit GEMM (see ImgGemmArgs).
 //
-// Workgroup = WM x WN waves computing a BM x BN tile; each wave owns a
-// (BM/WM) x (BN/WN) block of 32x32 MFMA accumulators.  Slices of BK rows of
-// the reduction are staged through a double-buffered LDS tile shared by the
-// workgroup (rows optionally padded by PAD words; measured: no padding is
-// best, the extra LDS costs more occupancy than the rare bank conflict).  Per slice a wave first reads
-// all its MFMA operands from LDS into registers, then issues its share of the
-// loads of the next slice into the other buffer, then runs its MFMAs, so the
-// loads overlap the MFMAs; one barrier per slice.
+// Workgroup = WM x WN waves computing a BM x BN tile on the 16x16x4 MFMA; each
+// wave owns a (BM/WM) x (BN/WN) block of 16x16 accumulators.  The reduction is
+// walked in 16-row slices; MFMA lane group kr (lanes 16 kr .. 16 kr + 15) takes
+// reduction rows 4 kr .. 4 kr + 3 of a slice, one per MFMA step.
 //
-// A wave-load fills one LDS row segment of 64 words: for A, 64 consecutive
-// output rows m of one reduction row k (the packed filter is k-major, so the
-// load is coalesced); for B, 64 consecutive output columns (pixels) of one
-// reduction row k (coalesced along the pixel row).  k is the same for the
-// whole wave, so the (tap, channel) decode of k is scalar work.
-// FAST: cin % BK == 0, so a slice lies inside one filter tap; the spatial
+// A (the packed filter) goes straight into registers when the waves split
+// the tile's rows (WM > 1): packed m-major with each filter's reduction rows
+// contiguous, a lane's A[m][4 kr .. 4 kr + 3] is one aligned
+// buffer_load_dwordx4.  With one wave row (WM == 1, tiles of 16 or 48 rows)
+// every wave needs the same A rows, so A is packed k-major and shared through
+// LDS like B (one wave-load = 64 consecutive rows m of one reduction row).  B (the
+// gathered image) is shared by the waves of the workgroup through LDS: a
+// wave-load (buffer_load_dword ... lds) fills one LDS row of 64 pixels of one
+// reduction row, coalesced along the pixel row; rows are padded to BN + 4
+// words so that the four lane groups of a ds_read_b32, which read rows 4
+// apart, hit distinct banks.  k is the same for the whole wave, so the
+// (tap, channel) decode of k is scalar work.
+// FAST: cin % 16 == 0, so a slice lies inside one filter tap; the spatial
 // bounds test and offset are then computed once per slice and column.
+//
+// Pipeline: three stages (LDS buffers for B, and for A or register sets for
+// A); slices t + 1 and t + 2 are in flight while slice t computes.
 // ---------------------------------------------------------------------------
 template <int BM, int BN, int BK, int WM, int WN, int PAD, bool FAST, int NST, int MF>
 __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArgs a)
 {
-    // MF: MFMA shape, 32 (v_mfma_f32_32x32x2f32) or 16 (v_mfma_f32_16x16x4f32,
-    // for tiles of 16 or 48 rows).  A wave-load always fills 64 words, so a
-    // tile narrower than 64 rows stages a 64-wide A row and uses BM of it.
-    typedef MfmaAcc<MF> Mf;
+    typedef MfmaAcc<16> Mf;
     constexpr int NW = WM * WN;
     constexpr int TM = BM / WM, TN = BN / WN;
-    constexpr int FM = TM / MF, FN = TN / MF;
-    constexpr int KS = 64 / MF;                        // reduction rows per MFMA
-    constexpr int HA = (BM + 63) / 64, HB = BN / 64;   // 64-wide segments per row
-    constexpr int LA = BK * HA / NW, LB = BK * HB / NW;  // wave-loads per slice
+    constexpr int FM = TM / 16, FN = TN / 16;
+    constexpr bool ASH = WM == 1;          // A shared through LDS
+    constexpr int HA = ASH ? (BM + 63) / 64 : 1, HB = BN / 64;  // 64-wide row segments
+    constexpr int LA = ASH ? BK * HA / NW : FM;  // A loads per wave and slice
+    constexpr int LB = BK * HB / NW;       // B wave-loads per slice
     constexpr int LDA = 64 * HA + PAD, LDB = BN + PAD;
-    static_assert(BN % 64 == 0 && TM % MF == 0 && TN % MF == 0 && BK % KS == 0, "tile");
+    static_assert(MF == 16 && BK == 16 && NST == 3, "16x16x4 MFMA, 16-row slices, 3 stages");
+    static_assert(BN % 64 == 0 && TM % 16 == 0 && TN % 16 == 0, "tile");
     static_assert(BK % NW == 0, "reduction rows per wave");
-    static_assert(!FAST || BK == 16, "the FAST reduction order packs 16-channel blocks");
-    static_assert(NST == 2 || NST == 3, "pipeline depth");
 
     // One distinct array per pipeline stage, so that the compiler's alias
     // analysis can tell an in-flight direct-to-LDS load from a read of
     // another stage's buffer (it would otherwise wait for every load).
-    __shared__ float As0[BK][LDA], As1[BK][LDA], As2[NST == 3 ? BK : 1][LDA];
-    __shared__ float Bs0[BK][LDB], Bs1[BK][LDB], Bs2[NST == 3 ? BK : 1][LDB];
+    __shared__ float As0[ASH ? BK : 1][LDA], As1[ASH ? BK : 1][LDA], As2[ASH ? BK : 1][LDA];
+    __shared__ float Bs0[BK][LDB], Bs1[BK][LDB], Bs2[BK][LDB];
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -152,18 +184,32 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
     const int m0 = mt * BM, n0 = nt * BN;
     const int kbeg = split * a.kchunk;
     const int kend = min(a.Kred, kbeg + a.kchunk);
+    const int kr = lane >> 4, lc = lane & 15;
 
+    const i32x4 rAw = rsrc_words(a.A, a.a_bytes);
     const __amdgpu_buffer_rsrc_t rA = make_rsrc(a.A, a.a_bytes);
     const __amdgpu_buffer_rsrc_t rB = make_rsrc(a.src, a.src_bytes);
 
-    // Per-lane A offsets (byte offset of row m within a packed row), masked.
-    uint32_t a_off[HA];
+    // Per-lane A byte offsets; rows past M read zero (and are not stored).
+    // Registers (m-major): row m of the packed filter, reduction rows 4 kr ..;
+    // the reduction rows of a filter are zero-padded to a multiple of 16
+    // (a.a_ld), so a slice never reads another filter's rows.  LDS (k-major):
+    // row m within a packed reduction row of M floats.
+    constexpr int NAO = ASH ? HA : FM;
+    uint32_t a_off[NAO], a_msk[NAO];
 #pragma unroll
-    for (int h = 0; h < HA; h++) {
-        int m = m0 + 64 * h + lane;
-        a_off[h] = (uint32_t)(m * 4) | oob_mask(m < a.M);
+    for (int i = 0; i < NAO; i++) {
+        if constexpr (ASH) {
+            const int m = m0 + 64 * i + lane;
+            a_off[i] = (uint32_t)(m * 4);
+            a_msk[i] = oob_mask(m < a.M);
+        } else {
+            const int m = m0 + wm * TM + i * 16 + lc;
+            a_off[i] = ((uint32_t)(g * a.M + (m < a.M ? m : 0)) * (uint32_t)a.a_ld + 4u * kr) * 4u;
+            a_msk[i] = oob_mask(m < a.M);
+        }
     }
-    const uint32_t a_gbase = (uint32_t)g * (uint32_t)a.Kred * (uint32_t)a.M * 4u;
+    const uint32_t a_gbase = (uint32_t)g * (uint32_t)a.a_ld * (uint32_t)a.M * 4u;
 
     // Per-lane B column data: image base offset, base coordinates, validity.
     uint32_t b_base[HB];
@@ -183,15 +229,21 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
         b_base[h] = (img * a.src_img_words + (uint32_t)g * a.cin * a.src_hw) * 4u;
     }
 
-    auto issue = [&](int k0, float (*Ad)[LDA], float (*Bd)[LDB]) {
-        // Wave-load j: LDS row kk = wave + NW * (j / HA), 64-wide segment h = j % HA
-        // (h is a compile-time index, so the per-lane arrays stay in registers).
+    // Loads of the slice starting at reduction row k0: A into registers ar
+    // or into the LDS buffer Ad, B into the LDS buffer Bd (wave-load j fills
+    // LDS row kk = wave + NW * (j / H), 64-wide segment h = j % H).
+    auto issue = [&](int k0, float (*Ad)[LDA], float (*Bd)[LDB], f32x4 (&ar)[FM]) {
+        if constexpr (ASH) {
 #pragma unroll
-        for (int j = 0; j < LA; j++) {
-            const int kk = wave + NW * (j / HA), h = j % HA;
-            const int k = k0 + kk;
-            const uint32_t row = a_gbase + (uint32_t)k * (uint32_t)a.M * 4u;
-            lds_load(rA, &Ad[kk][64 * h], (row + a_off[h]) | oob_mask(k < kend));
+            for (int j = 0; j < LA; j++) {
+                const int kk = wave + NW * (j / HA), h = j % HA;
+                const uint32_t row = a_gbase + (uint32_t)(k0 + kk) * (uint32_t)a.M * 4u;
+                lds_load(rA, &Ad[kk][64 * h], (row + a_off[h]) | a_msk[h]);
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < FM; i++)
+                ar[i] = load4_untracked(rAw, (a_off[i] + (uint32_t)k0 * 4u) | a_msk[i]);
         }
         if constexpr (FAST) {
             // Slice k0 / 16 = cb * taps + tap covers channels 16 cb .. 16 cb + 15.
@@ -247,88 +299,76 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
             for (int v = 0; v < Mf::NV; v++)
                 acc[i][j][v] = 0.f;
 
-    const int kr = lane / MF, lc = lane % MF;
     const int nslices = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
 
-    // Operands of one slice -> registers, then MFMAs.  MFMA step s takes
-    // reduction row kr * (BK / KS) + s in lane group kr: with rows of
-    // 64 + 4 words, the KS groups of one ds_read then hit distinct banks.
-    auto compute = [&](float (*Ac)[LDA], float (*Bc)[LDB], auto &&between) {
-        float af[BK / KS][FM], bf[BK / KS][FN];
+    // Operands of one slice -> registers, then MFMAs.
+    auto compute = [&](float (*Ac)[LDA], float (*Bc)[LDB], const f32x4 (&ar)[FM],
+                       auto &&between) {
+        float bf[4][FN];
 #pragma unroll
-        for (int s = 0; s < BK / KS; s++) {
-#pragma unroll
-            for (int i = 0; i < FM; i++)
-                af[s][i] = Ac[kr * (BK / KS) + s][wm * TM + i * MF + lc];
+        for (int s = 0; s < 4; s++)
 #pragma unroll
             for (int j = 0; j < FN; j++)
-                bf[s][j] = Bc[kr * (BK / KS) + s][wn * TN + j * MF + lc];
+                bf[s][j] = Bc[4 * kr + s][wn * TN + j * 16 + lc];
+        f32x4 af[FM];
+#pragma unroll
+        for (int i = 0; i < FM; i++) {
+            if constexpr (ASH) {
+#pragma unroll
+                for (int s = 0; s < 4; s++)
+                    af[i][s] = Ac[4 * kr + s][i * 16 + lc];
+            } else {
+                // The untracked load's value may only be used after the
+                // stage's wait: route it through an empty asm statement that
+                // is ordered after that wait, so no use can move above it.
+                af[i] = ar[i];
+            }
         }
         between();  // issue later slices' loads once this slice's reads are out
 #pragma unroll
-        for (int s = 0; s < BK / KS; s++)
+        for (int s = 0; s < 4; s++)
 #pragma unroll
             for (int i = 0; i < FM; i++)
 #pragma unroll
                 for (int j = 0; j < FN; j++)
-                    acc[i][j] = Mf::mma(af[s][i], bf[s][j], acc[i][j]);
+                    acc[i][j] = Mf::mma(af[i][s], bf[s][j], acc[i][j]);
     };
 
-    if constexpr (NST == 2) {
-        // Two stages: slice t + 1 loads while slice t computes; one barrier
-        // per slice (every wave's loads of slice t landed, and every wave is
-        // done reading the buffer about to be refilled).
-        auto stage = [&](int t, float (*Ac)[LDA], float (*Bc)[LDB], float (*An)[LDA],
-                         float (*Bn)[LDB]) {
+    // Before the barrier of slice t a wave waits only until its own loads of
+    // slice t are done (vmcnt counts down in issue order, and the FM + LB
+    // loads of slice t + 1 may stay outstanding).  This wait is also the one
+    // that makes the A registers of slice t valid: their loads are untracked
+    // by the compiler.  A raw s_barrier (no fence, which would wait for every
+    // load) then publishes the B slice, and the compiler barriers keep LDS
+    // accesses on their side.
+    constexpr int LPS = LA + LB;
+    constexpr int WAIT_NEXT = (LPS & 15) | (((LPS >> 4) & 3) << 14) | (7 << 4) | (15 << 8);
+    static_assert(LPS < 64, "vmcnt range");
+    f32x4 ar0[FM], ar1[FM], ar2[FM];
+    auto stage = [&](int t, float (*Ac)[LDA], float (*Bc)[LDB], const f32x4 (&ac)[FM],
+                     float (*An)[LDA], float (*Bn)[LDB], f32x4 (&an)[FM]) {
+        if (t + 1 < nslices)
+            __builtin_amdgcn_s_waitcnt(WAIT_NEXT);
+        else
             __builtin_amdgcn_s_waitcnt(0);
-            __syncthreads();
-            compute(Ac, Bc, [&] {
-                if (t + 1 < nslices)
-                    issue(kbeg + (t + 1) * BK, An, Bn);
-            });
-        };
-        if (nslices > 0)
-            issue(kbeg, As0, Bs0);
-        for (int t = 0; t < nslices; t += 2) {
-            stage(t, As0, Bs0, As1, Bs1);
-            if (t + 1 < nslices)
-                stage(t + 1, As1, Bs1, As0, Bs0);
-        }
-    } else {
-        // Three stages: slices t + 1 and t + 2 are in flight while slice t
-        // computes.  Before the barrier a wave waits only until its own loads
-        // of slice t are done (vmcnt counts down in issue order, and the
-        // LA + LB loads of slice t + 1 may stay outstanding); a raw s_barrier
-        // (no fence, which would wait for every load) then publishes the
-        // slice, and the compiler barriers keep LDS accesses on their side.
-        constexpr int LPS = LA + LB;
-        constexpr int WAIT_NEXT = (LPS & 15) | (((LPS >> 4) & 3) << 14) | (7 << 4) | (15 << 8);
-        static_assert(LPS < 64, "vmcnt range");
-        auto stage = [&](int t, float (*Ac)[LDA], float (*Bc)[LDB], float (*An)[LDA],
-                         float (*Bn)[LDB]) {
-            if (t + 1 < nslices)
-                __builtin_amdgcn_s_waitcnt(WAIT_NEXT);
-            else
-                __builtin_amdgcn_s_waitcnt(0);
-            __asm__ volatile("" ::: "memory");
-            __builtin_amdgcn_s_barrier();
-            __asm__ volatile("" ::: "memory");
-            compute(Ac, Bc, [&] {
-                if (t + 2 < nslices)
-                    issue(kbeg + (t + 2) * BK, An, Bn);
-            });
-        };
-        if (nslices > 0)
-            issue(kbeg, As0, Bs0);
-        if (nslices > 1)
-            issue(kbeg + BK, As1, Bs1);
-        for (int t = 0; t < nslices; t += 3) {
-            stage(t, As0, Bs0, As2, Bs2);
-            if (t + 1 < nslices)
-                stage(t + 1, As1, Bs1, As0, Bs0);
+        __asm__ volatile("" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        __asm__ volatile("" ::: "memory");
+        compute(Ac, Bc, ac, [&] {
             if (t + 2 < nslices)
-                stage(t + 2, As2, Bs2, As1, Bs1);
-        }
+                issue(kbeg + (t + 2) * BK, An, Bn, an);
+        });
+    };
+    if (nslices > 0)
+        issue(kbeg, As0, Bs0, ar0);
+    if (nslices > 1)
+        issue(kbeg + BK, As1, Bs1, ar1);
+    for (int t = 0; t < nslices; t += 3) {
+        stage(t, As0, Bs0, ar0, As2, Bs2, ar2);
+        if (t + 1 < nslices)
+            stage(t + 1, As1, Bs1, ar1, As0, Bs0, ar0);
+        if (t + 2 < nslices)
+            stage(t + 2, As2, Bs2, ar2, As1, Bs1, ar1);
     }
 
     // Epilogue: + bias, scatter columns back to image coordinates (a split
@@ -587,16 +627,30 @@ __global__ __launch_bounds__(64 * WM * WN) void wgrad_kernel(const WgradArgs a)
 // Filter packing.
 // ---------------------------------------------------------------------------
 __global__ void pack_fwd_kernel(const float *__restrict__ w, float *__restrict__ wp, int Kg,
-                                int Cg, int R, int S, int cblock, long long total)
+                                int Cg, int R, int S, int cblock, int a_ld, int kmajor,
+                                long long total)
 {
     long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= total)
         return;
-    // i = (g * R*S*Cg + kk) * Kg + k
-    int k = (int)(i % Kg);
-    long long t = i / Kg;
-    int kk = (int)(t % ((long long)R * S * Cg));
-    int g = (int)(t / ((long long)R * S * Cg));
+    // m-major: i = (g * Kg + k) * a_ld + kk; k-major: i = (g * a_ld + kk) * Kg + k;
+    // zero for kk >= R*S*Cg
+    int kk, k, g;
+    if (kmajor) {
+        k = (int)(i % Kg);
+        long long t = i / Kg;
+        kk = (int)(t % a_ld);
+        g = (int)(t / a_ld);
+    } else {
+        kk = (int)(i % a_ld);
+        long long t = i / a_ld;
+        k = (int)(t % Kg);
+        g = (int)(t / Kg);
+    }
+    if (kk >= R * S * Cg) {
+        wp[i] = 0.f;
+        return;
+    }
     int c, rs;
     if (cblock) {  // kk = (cb * RS + rs) * 16 + ci
         int ci = kk % 16, sl = kk / 16;
@@ -612,17 +666,31 @@ __global__ void pack_fwd_kernel(const float *__restrict__ w, float *__restrict__
 
 __global__ void pack_bwd_phase_kernel(const float *__restrict__ w, float *__restrict__ wr,
                                       int Kg, int Cg, int R, int S, int r0, int s0, int nr,
-                                      int ns, int stride, int cblock, long long total)
+                                      int ns, int stride, int cblock, int a_ld, int kmajor,
+                                      long long total)
 {
     long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= total)
         return;
-    // i = (g * nr*ns*Kg + kk) * Cg + c
-    int c = (int)(i % Cg);
-    long long t = i / Cg;
+    // m-major: i = (g * Cg + c) * a_ld + kk; k-major: i = (g * a_ld + kk) * Cg + c;
+    // zero for kk >= nr*ns*Kg
+    int kk, c, g;
+    if (kmajor) {
+        c = (int)(i % Cg);
+        long long t = i / Cg;
+        kk = (int)(t % a_ld);
+        g = (int)(t / a_ld);
+    } else {
+        kk = (int)(i % a_ld);
+        long long t = i / a_ld;
+        c = (int)(t % Cg);
+        g = (int)(t / Cg);
+    }
     int ntap = nr * ns;
-    int kk = (int)(t % ((long long)ntap * Kg));
-    int g = (int)(t / ((long long)ntap * Kg));
+    if (kk >= ntap * Kg) {
+        wr[i] = 0.f;
+        return;
+    }
     int k, tap;
     if (cblock) {  // kk = (kb * ntap + tap) * 16 + ki
         int ki = kk % 16, sl = kk / 16;
@@ -681,14 +749,11 @@ __global__ __launch_bounds__(RED_E * RED_J) void splitk_reduce_kernel(
 // ---------------------------------------------------------------------------
 // Launchers.
 // ---------------------------------------------------------------------------
-#ifndef MICONV_IMG_NST
-#define MICONV_IMG_NST 3
-#endif
 
 template <int BM, int BN, int BK, int WM, int WN, int PAD, int MF = 32>
 static hipError_t img_launch(const ImgGemmArgs &a, bool fast, hipStream_t stream)
 {
-    constexpr int NST = MICONV_IMG_NST;
+    constexpr int NST = 3;
     int tiles = ((a.M + BM - 1) / BM) * ((a.Ncol + BN - 1) / BN);
     dim3 grid(tiles * a.groups * a.nsplit);
     if (fast)
@@ -753,24 +818,24 @@ static unsigned blocks_for(long long total, int nt)
 }
 
 hipError_t launch_pack_fwd(const float *w, float *wp, int K, int Cg, int R, int S, int G,
-                           bool cblock, hipStream_t stream)
+                           bool cblock, int a_ld, bool kmajor, hipStream_t stream)
 {
-    long long total = (long long)K * Cg * R * S;
+    long long total = (long long)K * a_ld;
     hipLaunchKernelGGL(pack_fwd_kernel, dim3(blocks_for(total, 256)), dim3(256), 0, stream, w,
-                       wp, K / G, Cg, R, S, cblock ? 1 : 0, total);
+                       wp, K / G, Cg, R, S, cblock ? 1 : 0, a_ld, kmajor ? 1 : 0, total);
     return hipGetLastError();
 }
 
 hipError_t launch_pack_bwd_phase(const float *w, float *wr, int K, int Cg, int R, int S,
                                  int G, int r0, int s0, int nr, int ns, int stride, bool cblock,
-                                 hipStream_t stream)
+                                 int a_ld, bool kmajor, hipStream_t stream)
 {
-    long long total = (long long)K * Cg * nr * ns;
+    long long total = (long long)G * Cg * a_ld;
     if (total == 0)
         return hipSuccess;
     hipLaunchKernelGGL(pack_bwd_phase_kernel, dim3(blocks_for(total, 256)), dim3(256), 0,
                        stream, w, wr, K / G, Cg, R, S, r0, s0, nr, ns, stride, cblock ? 1 : 0,
-                       total);
+                       a_ld, kmajor ? 1 : 0, total);
     return hipGetLastError();
 }
 

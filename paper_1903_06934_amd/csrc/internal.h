@@ -32,7 +32,10 @@ FastDiv make_fastdiv(uint32_t d);
 // one phase, taps = the filter taps of that phase).
 //
 // Per group g (grid z):  out[g] (M x Ncol) = A[g] (M x Kred) * B[g] (Kred x Ncol)
-//   A[g][m][k]  = Ap[g * Kred * M + k * M + m]          (packed, k-major)
+//   A[g][m][k]  = Ap[(g * M + m) * a_ld + k]            (packed m-major), or, for
+//                 the tiles of one wave row (img_tile_shares_a), Ap[(g * a_ld + k) * M + m]
+//                 (k-major); a_ld = Kred rounded up to a multiple of 16, rows past
+//                 Kred zero
 //   k           = tap * cin + ch (general), or, when cin % 16 == 0 (FAST),
 //                 (cb * taps + tap) * 16 + ci with ch = 16 cb + ci: the taps of a
 //                 16-channel block are consecutive, so the source rows a
@@ -47,7 +50,8 @@ FastDiv make_fastdiv(uint32_t d);
 struct ImgGemmArgs {
     int M, Ncol, Kred, groups;
     const float *A;
-    uint32_t a_bytes;     // groups * Kred * M * 4 (< 2^31)
+    int a_ld;             // packed row length: Kred rounded up to a multiple of 16
+    uint32_t a_bytes;     // groups * M * a_ld * 4 (< 2^31)
     const float *src;
     uint32_t src_bytes;   // bytes of the source images this launch reads (< 2^31)
     int cin;              // source channels per group
@@ -98,6 +102,12 @@ enum ImgTile {
     IMG_64x64 = 0, IMG_128x64, IMG_16x128, IMG_32x64, IMG_48x64, IMG_48x128, IMG_96x64,
     IMG_96x128
 };
+// Tiles with one wave row (WM == 1 in launch_img_gemm): every wave needs the
+// same filter rows, which the kernel then shares through LDS, packed k-major.
+inline bool img_tile_shares_a(int tile)
+{
+    return tile == IMG_16x128 || tile == IMG_48x64 || tile == IMG_48x128;
+}
 // Backward-weight tiles of the one-pixel-per-lane kernel: tap-uniform
 // (BM rows of K/G x BN channels of one tap) or packed (BM rows x BN
 // consecutive (c, r, s) columns).
@@ -106,16 +116,20 @@ enum WgradTile { WG_TAP_64x32 = 0, WG_TAP_64x48, WG_TAP_64x16, WG_PIX_96x64, WG_
 hipError_t launch_img_gemm(const ImgGemmArgs &a, int tile, bool fast, hipStream_t stream);
 hipError_t launch_wgrad_gemm(const WgradArgs &a, int tile, hipStream_t stream);
 
-// wp[g][kk][k] = w[g*Kg + k][c][r][s] with kk = (r*S + s)*Cg + c, or, if
-// cblock (Cg % 16 == 0), kk = ((c / 16) * R*S + r*S + s) * 16 + c % 16.
+// wp[(g*Kg + k) * a_ld + kk] (or, if kmajor, wp[(g*a_ld + kk) * Kg + k]) =
+// w[g*Kg + k][c][r][s] with kk = (r*S + s)*Cg + c, or, if cblock (Cg % 16 == 0),
+// kk = ((c / 16) * R*S + r*S + s) * 16 + c % 16; zero for kk >= Cg*R*S.
 hipError_t launch_pack_fwd(const float *w, float *wp, int K, int Cg, int R, int S, int G,
-                           bool cblock, hipStream_t stream);
-// One stride phase of the backward-data filter: wr[g][kk][c] =
-// w[g*Kg + k][c][r0 + st*rr][s0 + st*ss] with tap = rr*ns + ss and kk = tap*Kg + k,
-// or, if cblock (Kg % 16 == 0), kk = ((k / 16) * nr*ns + tap) * 16 + k % 16.
+                           bool cblock, int a_ld, bool kmajor, hipStream_t stream);
+// One stride phase of the backward-data filter: wr[(g*Cg + c) * a_ld + kk] (or, if
+// kmajor, wr[(g*a_ld + kk) * Cg + c]) = w[g*Kg + k][c][r0 + st*rr][s0 + st*ss] with
+// tap = rr*ns + ss and kk = tap*Kg + k, or, if cblock (Kg % 16 == 0),
+// kk = ((k / 16) * nr*ns + tap) * 16 + k % 16; zero for kk >= nr*ns*Kg.
 hipError_t launch_pack_bwd_phase(const float *w, float *wr, int K, int Cg, int R, int S,
                                  int G, int r0, int s0, int nr, int ns, int stride,
-                                 bool cblock, hipStream_t stream);
+                                 bool cblock, int a_ld, bool kmajor, hipStream_t stream);
+// Packed reduction-row length of the image GEMM's filter operand.
+inline int pad16(int k) { return (k + 15) & ~15; }
 // out[dst(i)] = sum over s < nsplit of part[s * stride + i] for i < count, in a
 // fixed order; dst = identity, or (tap_cg > 0) [k][tap][c] -> [k][c][tap].
 hipError_t launch_splitk_reduce(const float *part, int nsplit, long long stride, int count,
