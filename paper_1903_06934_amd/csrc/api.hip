@@ -170,8 +170,8 @@ double cu_balance(long long tiles)
 // Tile choice for the image GEMM, from measured sweeps on MI355X across the
 // layers of the five benchmark stacks.  The 64x64 tile (small accumulators,
 // six workgroups per CU) is the default.  Row counts that would leave a
-// 64-row tile partly empty take 16-, 32-, 48- or 96-row tiles (128 columns
-// wide when that still gives 4 tiles per CU).  The 128x64 tile halves the
+// 64-row tile partly empty take 16-, 32-, 48- (three waves) or 96-row tiles
+// (96 rows: 128 columns wide when that still gives 4 tiles per CU).  The 128x64 tile halves the
 // gathered-operand loads per MFMA and runs about 5 % faster per tile when it
 // leaves no row empty and the reduction is not trivially short; it is taken
 // when it gives every CU a workgroup and does not leave noticeably more CU
@@ -187,7 +187,7 @@ int pick_img_tile(int M, long long Ncol, int Kred, int G)
     if (M <= 32)
         return IMG_32x64;
     if (M <= 48)
-        return tiles(48, 128) >= 4 * kNumCUs ? IMG_48x128 : IMG_48x64;
+        return IMG_48x64;
     if (M > 64 && M <= 96)
         return tiles(96, 128) >= 4 * kNumCUs ? IMG_96x128 : IMG_96x64;
     if (M % 128 == 0 && Kred >= 256 && tiles(128, 64) >= kNumCUs &&
@@ -199,7 +199,7 @@ int pick_img_tile(int M, long long Ncol, int Kred, int G)
 void img_tile_dims(int tile, int &bm, int &bn)
 {
     static const int dims[][2] = {{64, 64}, {128, 64}, {16, 128}, {32, 64},
-                                  {48, 64}, {48, 128}, {96, 64},  {96, 128}};
+                                  {48, 64}, {96, 64},  {96, 128}};
     bm = dims[tile][0];
     bn = dims[tile][1];
 }

@@ -133,7 +133,7 @@ __device__ __forceinline__ int xcd_tile(int hw, int total)
 // A (the packed filter) goes straight into registers when the waves split
 // the tile's rows (WM > 1): packed m-major with each filter's reduction rows
 // contiguous, a lane's A[m][4 kr .. 4 kr + 3] is one aligned
-// buffer_load_dwordx4.  With one wave row (WM == 1, tiles of 16 or 48 rows)
+// buffer_load_dwordx4.  With one wave row (WM == 1, the 16-row tile)
 // every wave needs the same A rows, so A is packed k-major and shared through
 // LDS like B (one wave-load = 64 consecutive rows m of one reduction row).  B (the
 // gathered image) is shared by the waves of the workgroup through LDS: a
@@ -158,17 +158,23 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
     constexpr bool ASH = WM == 1;          // A shared through LDS
     constexpr int HA = ASH ? (BM + 63) / 64 : 1, HB = BN / 64;  // 64-wide row segments
     constexpr int LA = ASH ? BK * HA / NW : FM;  // A loads per wave and slice
-    constexpr int LB = BK * HB / NW;       // B wave-loads per slice
+    // B wave-loads per slice and wave; when the waves do not divide the BK
+    // rows (3-wave tiles, one 64-wide segment), the waves with a row fewer
+    // issue one more load into a spare LDS row (out-of-range offset: it
+    // reads zero and touches no memory), so every wave issues LB loads.
+    constexpr int LB = (BK * HB + NW - 1) / NW;
+    constexpr int BROWS = BK + ((BK * HB) % NW ? 1 : 0);
     constexpr int LDA = 64 * HA + PAD, LDB = BN + PAD;
     static_assert(MF == 16 && BK == 16 && NST == 3, "16x16x4 MFMA, 16-row slices, 3 stages");
     static_assert(BN % 64 == 0 && TM % 16 == 0 && TN % 16 == 0, "tile");
-    static_assert(BK % NW == 0, "reduction rows per wave");
+    static_assert(BK % NW == 0 || HB == 1, "uneven B rows need one segment per row");
+    static_assert(!ASH || (BK * HA) % NW == 0, "A rows per wave");
 
     // One distinct array per pipeline stage, so that the compiler's alias
     // analysis can tell an in-flight direct-to-LDS load from a read of
     // another stage's buffer (it would otherwise wait for every load).
     __shared__ float As0[ASH ? BK : 1][LDA], As1[ASH ? BK : 1][LDA], As2[ASH ? BK : 1][LDA];
-    __shared__ float Bs0[BK][LDB], Bs1[BK][LDB], Bs2[BK][LDB];
+    __shared__ float Bs0[BROWS][LDB], Bs1[BROWS][LDB], Bs2[BROWS][LDB];
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -266,15 +272,18 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
 #pragma unroll
             for (int j = 0; j < LB; j++) {
                 const int kk = wave + NW * (j / HB), h = j % HB;
-                lds_load(rB, &Bd[kk][64 * h],
-                         (sp[h] + (uint32_t)kk * (uint32_t)a.src_hw * 4u) | msk[h]);
+                const bool live = kk < BK;
+                lds_load(rB, &Bd[live ? kk : BK][64 * h],
+                         (sp[h] + (uint32_t)kk * (uint32_t)a.src_hw * 4u) | msk[h] |
+                             oob_mask(live));
             }
         } else {
 #pragma unroll
             for (int j = 0; j < LB; j++) {
                 const int kk = wave + NW * (j / HB), h = j % HB;
+                const bool live = kk < BK;
                 const int k = k0 + kk;
-                const bool kok = k < kend;
+                const bool kok = live && k < kend;
                 const uint32_t kc = kok ? (uint32_t)k : 0u;
                 const uint32_t tap = fast_div(kc, a.k_cin);
                 const int ch = (int)(kc - tap * a.k_cin.d);
@@ -285,7 +294,7 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
                           (unsigned)wx < (unsigned)a.src_w;
                 uint32_t off = b_base[h] + ((uint32_t)ch * (uint32_t)a.src_hw +
                                             (uint32_t)(hy * a.src_w + wx)) * 4u;
-                lds_load(rB, &Bd[kk][64 * h], off | oob_mask(ok));
+                lds_load(rB, &Bd[live ? kk : BK][64 * h], off | oob_mask(ok));
             }
         }
     };
@@ -775,13 +784,12 @@ hipError_t launch_img_gemm(const ImgGemmArgs &a, int tile, bool fast, hipStream_
     switch (tile) {
     // Every shape runs on the 16x16x4 MFMA with LDS rows padded by 4 words,
     // so that its four 16-lane groups, which read rows 4 apart, hit distinct
-    // banks.  Waves: 4 x 1 (each wave a 16- or 32-row band across the tile),
-    // 2 x 2, or 1 x 4 (each wave a column band).
+    // banks.  Waves: 4 x 1 or 3 x 1 (each wave a 16- or 32-row band across
+    // the tile), 2 x 2, or 1 x 4 (each wave a column band, 16 rows).
     case IMG_128x64: return img_launch<128, 64, K, 4, 1, 4, 16>(a, fast, stream);
     case IMG_16x128: return img_launch<16, 128, K, 1, 4, 4, 16>(a, fast, stream);
     case IMG_32x64: return img_launch<32, 64, K, 2, 2, 4, 16>(a, fast, stream);
-    case IMG_48x64: return img_launch<48, 64, K, 1, 4, 4, 16>(a, fast, stream);
-    case IMG_48x128: return img_launch<48, 128, K, 1, 4, 4, 16>(a, fast, stream);
+    case IMG_48x64: return img_launch<48, 64, K, 3, 1, 4, 16>(a, fast, stream);
     case IMG_96x64: return img_launch<96, 64, K, 2, 2, 4, 16>(a, fast, stream);
     case IMG_96x128: return img_launch<96, 128, K, 2, 2, 4, 16>(a, fast, stream);
     default: return img_launch<64, 64, K, 4, 1, 4, 16>(a, fast, stream);

@@ -97,17 +97,11 @@ struct WgradArgs {
     float *db_part;          // [split][K] partial bias gradients, or null
 };
 
-// Image-GEMM tile shapes (BM x BN; every shape runs 4 waves).
-enum ImgTile {
-    IMG_64x64 = 0, IMG_128x64, IMG_16x128, IMG_32x64, IMG_48x64, IMG_48x128, IMG_96x64,
-    IMG_96x128
-};
+// Image-GEMM tile shapes (BM x BN; 4 waves, 3 for 48x64).
+enum ImgTile { IMG_64x64 = 0, IMG_128x64, IMG_16x128, IMG_32x64, IMG_48x64, IMG_96x64, IMG_96x128 };
 // Tiles with one wave row (WM == 1 in launch_img_gemm): every wave needs the
 // same filter rows, which the kernel then shares through LDS, packed k-major.
-inline bool img_tile_shares_a(int tile)
-{
-    return tile == IMG_16x128 || tile == IMG_48x64 || tile == IMG_48x128;
-}
+inline bool img_tile_shares_a(int tile) { return tile == IMG_16x128; }
 // Backward-weight tiles of the one-pixel-per-lane kernel: tap-uniform
 // (BM rows of K/G x BN channels of one tap) or packed (BM rows x BN
 // consecutive (c, r, s) columns).

@@ -77,15 +77,15 @@ def test_edge_shapes(shape):
     full_parity(shape)
 
 
-# Shapes for each image-GEMM tile: 128x64, 48x128 and 96x128 need at least
-# 1024 tiles (128x64 also 128-row multiples); the others cover ragged rows
-# and columns.
+# Shapes for each image-GEMM tile: 128x64 and 96x128 need at least 1024
+# tiles (128x64 also 128-row multiples); the others cover ragged rows and
+# columns.
 TILE_SHAPES = [
     (16, 32, 65, 63, 128, 3, 3, 1, 1, 1),  # fwd 128x64, ragged columns
     (16, 128, 63, 65, 16, 3, 3, 1, 1, 1),  # bwd-data 128x64, ragged columns
     (8, 32, 64, 64, 200, 3, 3, 1, 1, 1),   # fwd 64x64, channel-aligned, ragged M
     (8, 3, 128, 128, 96, 3, 3, 1, 1, 1),   # fwd 96x128, per-element tap decode
-    (33, 48, 64, 63, 16, 3, 3, 1, 1, 1),   # bwd-data 48x128, ragged columns
+    (33, 48, 64, 63, 16, 3, 3, 1, 1, 1),   # bwd-data 48x64 (three waves), ragged columns
     # Narrow-row tiles (16, 32, 48 and 96 rows), with ragged rows and columns.
     (4, 64, 20, 20, 80, 3, 3, 1, 1, 1),    # fwd M = 80 (96x64)
     (4, 80, 21, 21, 40, 3, 3, 1, 1, 1),    # fwd M = 40 (48), bwd-data M = 80, tap decode
