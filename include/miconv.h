@@ -131,8 +131,9 @@ int conv_bwd_weight(int N, int C, int H, int W, int K, int R, int S, int stride,
  * pass's first implicit-GEMM kernel and `after` immediately after its last
  * one, so hipEventElapsedTime(before, after) is the GEMM kernels' device
  * time without the filter packing, split-K reduction and bias-gradient
- * kernels around them (for a strided conv_bwd_data it spans every stride
- * phase, packing in between included).  Pass two NULLs to stop.  The events
+ * kernels around them (for a conv_bwd_data computed phase by phase it spans
+ * every stride phase, packing in between included; one with few input
+ * channels per group runs a single blocked GEMM instead).  Pass two NULLs to stop.  The events
  * are created and owned by the caller.  Returns MICONV_OK, or
  * MICONV_ERR_NULL if exactly one of the two is NULL.
  */

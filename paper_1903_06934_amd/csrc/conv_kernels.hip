@@ -383,6 +383,41 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
     // Epilogue: + bias, scatter columns back to image coordinates (a split
     // writes its partial sums, without bias, to its own output-shaped slab).
     float *const out = a.nsplit > 1 ? a.out + (long long)split * a.split_stride : a.out;
+    if (a.mblock > 1) {
+        // Blocked backward-data: row m is channel c, block offset (ph, pw).
+        const int b = a.mblock, bb = b * b, cg = a.M / bb;
+        int oh[FN], ow[FN];
+        long long cbase[FN];
+#pragma unroll
+        for (int j = 0; j < FN; j++) {
+            int n = n0 + wn * TN + j * MF + lc;
+            bool ok = n < a.Ncol;
+            uint32_t c = ok ? (uint32_t)n : 0u;
+            uint32_t img = fast_div(c, a.col_hw);
+            uint32_t rem = c - img * a.col_hw.d;
+            uint32_t ci = fast_div(rem, a.col_w);
+            uint32_t cj = rem - ci * a.col_w.d;
+            oh[j] = ok ? (int)ci * a.ostep + a.ooff_h : -b;  // -b: no row is inside
+            ow[j] = (int)cj * a.ostep + a.ooff_w;
+            cbase[j] = (long long)img * a.out_img_stride + (long long)oh[j] * a.out_w + ow[j];
+        }
+#pragma unroll
+        for (int i = 0; i < FM; i++)
+#pragma unroll
+            for (int v = 0; v < Mf::NV; v++) {
+                int m = m0 + wm * TM + i * MF + acc_row_mf<MF>(v, lane);
+                if (m >= a.M)
+                    continue;
+                const int c = m / bb, rem = m - c * bb, ph = rem / b, pw = rem - ph * b;
+                const long long roff = (long long)(g * cg + c) * a.out_hw + ph * a.out_w + pw;
+#pragma unroll
+                for (int j = 0; j < FN; j++)
+                    if ((unsigned)(oh[j] + ph) < (unsigned)a.out_h &&
+                        (unsigned)(ow[j] + pw) < (unsigned)a.out_w)
+                        out[cbase[j] + roff] = acc[i][j][v];
+            }
+        return;
+    }
     const float *const bias = a.nsplit > 1 ? nullptr : a.bias;
     long long obase[FN];
     bool nok[FN];
@@ -713,6 +748,52 @@ __global__ void pack_bwd_phase_kernel(const float *__restrict__ w, float *__rest
     wr[i] = w[(((long long)(g * Kg + k) * Cg + c) * R + r) * S + s];
 }
 
+// Blocked backward-data filter.  Input pixel h with h + pad = b hb + ph
+// (b = stride * f) receives dy rows p = f hb + u through filter row
+// r = ph - stride u, for u = f - 1 - tu, tu < ntr; the taps of all b phases
+// share these ntr dy rows, and a (phase, tap) pair whose r falls outside the
+// filter gets a zero weight.  Likewise for columns.
+__global__ void pack_bwd_block_kernel(const float *__restrict__ w, float *__restrict__ wp, int Kg,
+                                      int Cg, int R, int S, int st, int f, int ntr, int nts,
+                                      int cblock, int a_ld, int kmajor, long long total)
+{
+    long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= total)
+        return;
+    const int b = st * f, M = Cg * b * b;
+    int kk, m, g;
+    if (kmajor) {
+        m = (int)(i % M);
+        long long t = i / M;
+        kk = (int)(t % a_ld);
+        g = (int)(t / a_ld);
+    } else {
+        kk = (int)(i % a_ld);
+        long long t = i / a_ld;
+        m = (int)(t % M);
+        g = (int)(t / M);
+    }
+    const int ntap = ntr * nts;
+    if (kk >= ntap * Kg) {
+        wp[i] = 0.f;
+        return;
+    }
+    int k, tap;
+    if (cblock) {  // kk = (kb * ntap + tap) * 16 + ki
+        int ki = kk % 16, sl = kk / 16;
+        tap = sl % ntap;
+        k = (sl / ntap) * 16 + ki;
+    } else {       // kk = tap * Kg + k
+        k = kk % Kg;
+        tap = kk / Kg;
+    }
+    const int c = m / (b * b), ph = (m / b) % b, pw = m % b;
+    const int r = ph - st * (f - 1 - tap / nts), s = pw - st * (f - 1 - tap % nts);
+    wp[i] = (r >= 0 && r < R && s >= 0 && s < S)
+                ? w[(((long long)(g * Kg + k) * Cg + c) * R + r) * S + s]
+                : 0.f;
+}
+
 // ---------------------------------------------------------------------------
 // Deterministic split-K reduction.  out[dst(i)] = sum over s < nsplit of
 // part[s * stride + i].  A block handles 32 consecutive elements with 8
@@ -844,6 +925,18 @@ hipError_t launch_pack_bwd_phase(const float *w, float *wr, int K, int Cg, int R
     hipLaunchKernelGGL(pack_bwd_phase_kernel, dim3(blocks_for(total, 256)), dim3(256), 0,
                        stream, w, wr, K / G, Cg, R, S, r0, s0, nr, ns, stride, cblock ? 1 : 0,
                        a_ld, kmajor ? 1 : 0, total);
+    return hipGetLastError();
+}
+
+hipError_t launch_pack_bwd_block(const float *w, float *wp, int K, int Cg, int R, int S, int G,
+                                 int stride, int f, int ntr, int nts, bool cblock, int a_ld,
+                                 bool kmajor, hipStream_t stream)
+{
+    const int b = stride * f;
+    long long total = (long long)G * Cg * b * b * a_ld;
+    hipLaunchKernelGGL(pack_bwd_block_kernel, dim3(blocks_for(total, 256)), dim3(256), 0, stream,
+                       w, wp, K / G, Cg, R, S, stride, f, ntr, nts, cblock ? 1 : 0, a_ld,
+                       kmajor ? 1 : 0, total);
     return hipGetLastError();
 }
 

@@ -66,6 +66,11 @@ struct ImgGemmArgs {
     long long out_img_stride;
     int out_hw, out_w;
     int ostep, ooff_h, ooff_w;
+    // Blocked backward-data (mblock = b > 1): row m = (c * b + ph) * b + pw is
+    // input channel g * (M / b^2) + c at offset (ph, pw) of column (ci, cj)'s
+    // b x b block: out[img][.][ci * ostep + ooff_h + ph][cj * ostep + ooff_w + pw],
+    // stored only inside out_h x out_w.  mblock = 0: the row is channel g * M + m.
+    int mblock, out_h;
     // Split-K: split s covers reduction rows [s * kchunk, min((s+1) * kchunk, Kred))
     // and, when nsplit > 1, writes its partial sums (no bias) to out + s * split_stride.
     int nsplit, kchunk;
@@ -122,6 +127,15 @@ hipError_t launch_pack_fwd(const float *w, float *wp, int K, int Cg, int R, int 
 hipError_t launch_pack_bwd_phase(const float *w, float *wr, int K, int Cg, int R, int S,
                                  int G, int r0, int s0, int nr, int ns, int stride,
                                  bool cblock, int a_ld, bool kmajor, hipStream_t stream);
+// Blocked backward-data filter (b = stride * f, taps ntr x nts per block):
+// wp[(g*M + m) * a_ld + kk] (or, if kmajor, wp[(g*a_ld + kk) * M + m]) with
+// M = Cg b^2, m = (c*b + ph)*b + pw, tap = tu*nts + tv and kk = tap*Kg + k, or,
+// if cblock (Kg % 16 == 0), kk = ((k / 16) * ntr*nts + tap) * 16 + k % 16:
+// w[g*Kg + k][c][ph - stride*(f-1-tu)][pw - stride*(f-1-tv)], zero where that
+// tap lies outside the filter and for kk >= ntr*nts*Kg.
+hipError_t launch_pack_bwd_block(const float *w, float *wp, int K, int Cg, int R, int S, int G,
+                                 int stride, int f, int ntr, int nts, bool cblock, int a_ld,
+                                 bool kmajor, hipStream_t stream);
 // Packed reduction-row length of the image GEMM's filter operand.
 inline int pad16(int k) { return (k + 15) & ~15; }
 // out[dst(i)] = sum over s < nsplit of part[s * stride + i] for i < count, in a

@@ -94,6 +94,34 @@ def test_workspace_sizes(L):
     assert m.workspace_size(1, (2, 4, 9, 9, 8, 3, 3, 2, 1, 1)) >= 8 * 4 * 9 * 4
 
 
+def _align(n):
+    return (n + 255) // 256 * 256
+
+
+@pytest.mark.parametrize("shape,b,taps", [
+    # AlexNet conv1: 4 x 4 blocks (48 rows), 3 x 3 dy taps per block
+    ((128, 3, 227, 227, 96, 11, 11, 4, 0, 1), 4, 9),
+    # ResNet stem: 4 x 4 blocks (f = 2), 5 x 5 taps
+    ((64, 3, 224, 224, 64, 7, 7, 2, 3, 1), 4, 25),
+    # VGG conv1_1 (stride 1): 2 x 2 blocks, 4 x 4 taps
+    ((32, 3, 224, 224, 64, 3, 3, 1, 1, 1), 2, 16),
+])
+def test_bwd_data_blocked_plan_for_first_layers(L, shape, b, taps):
+    """Few input channels: backward-data stacks the b x b pixels of a block
+    into the GEMM rows, and its workspace is that one packed filter bank of
+    C b^2 rows by (K/G) x taps reduction rows (padded to 16)."""
+    N, C, H, W, K, R, S, st, pad, G = shape
+    rows = C * b * b
+    red = (K // G * taps + 15) // 16 * 16
+    assert m.workspace_size(1, shape) == _align(rows * red * 4)
+
+
+def test_bwd_data_phase_plan_for_wide_layers(L):
+    """Channel-aligned layers keep one GEMM per stride phase (AlexNet conv2)."""
+    shape = (128, 96, 27, 27, 256, 5, 5, 1, 2, 2)
+    assert m.workspace_size(1, shape) == _align(96 * 128 * 25 * 4)
+
+
 @pytest.mark.parametrize("shape", BAD_SHAPES)
 def test_bad_shapes(L, shape):
     assert L.conv_fwd(*shape, X, W_, None, Y, WSP, 1 << 30, None) == SHAPE

@@ -100,6 +100,25 @@ def test_large_tile_paths(shape):
     full_parity(shape)
 
 
+# Backward-data with few input channels: the blocked plan (b x b input pixels
+# of a block as GEMM rows, b = stride * f).  Many edge shapes above take it
+# too; these add each row-tile class and several column tiles.
+BLOCK_SHAPES = [
+    (3, 4, 37, 35, 32, 8, 8, 4, 2, 1),     # b = 4, 64 rows, channel-aligned reduction
+    (2, 6, 33, 30, 24, 5, 5, 2, 2, 2),     # groups, 12 rows, K/G = 12 (tap decode)
+    (4, 3, 67, 61, 32, 5, 5, 2, 1, 1),     # 12 rows (shared-A tile), many column tiles
+    (2, 3, 45, 43, 48, 3, 3, 1, 1, 1),     # stride 1 in 2 x 2 blocks
+    (2, 5, 30, 29, 20, 6, 4, 3, 7, 1),     # 45 rows, pad > b, R != S, tap decode
+]
+
+
+@pytest.mark.parametrize("shape", BLOCK_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_bwd_data_blocked(shape):
+    d = _inputs(shape, (7, 1))
+    dx_ref, adx = oracle.conv_bwd_data(shape, d["dy"], d["w"])
+    assert_within(gpu_bwd_data(shape, d["dy"], d["w"]), dx_ref, adx, f"bwd_data {shape}")
+
+
 def _all_layers():
     out = []
     for cfg in (1, 2, 3, 4):
