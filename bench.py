@@ -14,7 +14,11 @@ whole library call), the roofline fraction of the dominant kernel, and the
 CPU oracle timed on a bounded sample of the same workload.
 
 All inputs are resident in device memory before the timed region; the timed
-region contains only the library's calls on torch's current stream.
+region contains only the library's calls on torch's current stream.  Before
+the warm-up, every layer pass is tuned (conv_tune: each candidate plan is
+timed on the layer's tensors and the fastest kept, as the paper's framework
+picks its convolution strategy over the first training iterations);
+--tune 0 keeps the library's built-in rule instead.
 """
 from __future__ import annotations
 
@@ -53,10 +57,16 @@ def parse():
     ap.add_argument("--reps", type=int, default=20, help="timed repeats per layer and pass")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle sample (0 disables it)")
+    ap.add_argument("--tune", type=int, default=3, metavar="REPS",
+                    help="before the warm-up, time every candidate plan of every layer pass "
+                         "with REPS runs and keep the fastest (0: the built-in rule)")
     ap.add_argument("--flush", action="store_true",
                     help="write a 512 MiB buffer between per-layer repeats (cold caches)")
     ap.add_argument("--profile-pass", default=None, metavar="CFG:LAYER:PASS",
                     help="only run one layer pass --reps times (for rocprofv3), print nothing else")
+    ap.add_argument("--plan", type=int, default=None, metavar="INDEX",
+                    help="with --profile-pass: run candidate plan INDEX (conv_plan_set) "
+                         "instead of tuning")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only copy 1 GiB device-to-device 3 times (HBM counter calibration)")
     return ap.parse_args()
@@ -109,7 +119,7 @@ class HipEvents:
 class LayerRun:
     """Device buffers and prepared library calls of one layer."""
 
-    def __init__(self, cfg, li, L, stream):
+    def __init__(self, cfg, li, L, stream, tune_reps=0):
         import numpy as np
         import torch
         import workloads
@@ -129,6 +139,8 @@ class LayerRun:
         for pid in (0, 1, 2):
             n = m.workspace_size(pid, shape)
             self.ws[pid] = torch.empty(max(n, 256), dtype=torch.uint8, device=dev)
+        if tune_reps > 0:
+            self.tune(tune_reps)
         lib = m.lib()
         ws = lambda pid: (self.ws[pid].data_ptr(), self.ws[pid].numel())
         self.calls = {
@@ -140,6 +152,28 @@ class LayerRun:
                                                          self.dw.data_ptr(), self.db.data_ptr())
                            + ws(2) + (stream,)),
         }
+
+    def tune(self, reps):
+        """conv_tune every pass on this layer's tensors, with a workspace that
+        fits every candidate; the library keeps the fastest plan per shape."""
+        import torch
+        import paper_1903_06934_amd as m
+        shape, t = self.L.shape, self.t
+        args = {0: (t["x"], t["w"], t["b"], self.y, None),
+                1: (t["dy"], t["w"], None, self.dx, None),
+                2: (t["x"], t["dy"], None, self.dw, self.db)}
+        for pid in (0, 1, 2):
+            n = m.plan_count(pid, shape)
+            need = max(m.plan_workspace_size(pid, shape, i) for i in range(n))
+            ws = torch.empty(max(need, 256), dtype=torch.uint8, device="cuda")
+            m.conv_tune(pid, shape, *args[pid], ws, reps=reps)
+            self.ws[pid] = ws
+
+    def plan(self, p):
+        import paper_1903_06934_amd as m
+        pid = PASSES.index(p)
+        i = m.plan_get(pid, self.L.shape)
+        return f"{i}: {m.plan_name(pid, self.L.shape, i)}"
 
     def run(self, p):
         fn, args = self.calls[p]
@@ -202,10 +236,11 @@ TRAFFIC_DIR = os.path.join(ROOT, "profiles")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_1903_06934_amd", "csrc", "conv_kernels.hip")
 
 
-def measured_traffic(cfg, layer, p):
+def measured_traffic(cfg, layer, p, plan):
     """HBM bytes per launch of the (cfg, layer, pass) GEMM from a committed
     rocprofv3 counter summary (profiles/traffic_*.txt), if one exists for
-    exactly this workload and the kernel source has not changed since."""
+    exactly this workload and plan and the kernel source has not changed
+    since."""
     import glob
     import hashlib
     sha = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
@@ -216,7 +251,7 @@ def measured_traffic(cfg, layer, p):
                 k, v = line.split(":", 1)
                 kv[k.strip()] = v.strip()
         if (kv.get("workload") == f"{cfg}:{layer}:{p}" and kv.get("kernel_source_sha256") == sha
-                and "traffic_bytes_per_launch" in kv):
+                and kv.get("plan") == plan and "traffic_bytes_per_launch" in kv):
             return float(kv["traffic_bytes_per_launch"])
     return None
 
@@ -260,7 +295,7 @@ def bench_config(cfg, args, with_cpu):
 
     name, layers = workloads.config(cfg)
     stream = torch.cuda.current_stream().cuda_stream
-    runs = [LayerRun(cfg, li, L, stream) for li, L in enumerate(layers)]
+    runs = [LayerRun(cfg, li, L, stream, args.tune) for li, L in enumerate(layers)]
     torch.cuda.synchronize()
     N = layers[0].N
 
@@ -289,7 +324,7 @@ def bench_config(cfg, args, with_cpu):
             per.append({"layer": L.name, "pass": p, "count": L.count, "in_stack": in_stack,
                         "ms": round(med, 4), "ms_min": round(mn, 4),
                         "tflops": round(F / med / 1e9, 2), "gbs": round(B / med / 1e6, 1),
-                        "roof_frac": round(t_roof / med, 3)})
+                        "roof_frac": round(t_roof / med, 3), "plan": r.plan(p)})
             if in_stack:
                 tot[p][0] += F * L.count
                 tot[p][1] += med * L.count
@@ -311,8 +346,8 @@ def bench_config(cfg, args, with_cpu):
         ach = bytes_of(drun.L, dom["pass"]) / k_ms / 1e6
         roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_GBS,
                 "unit": "GB/s", "frac": round(ach / PEAK_GBS, 4), "traffic": None}
-    roof["traffic"] = measured_traffic(cfg, dom["layer"], dom["pass"])
-    roof.update({"kernel": f"{dom['pass']} GEMM of {dom['layer']}",
+    roof["traffic"] = measured_traffic(cfg, dom["layer"], dom["pass"], dom["plan"])
+    roof.update({"kernel": f"{dom['pass']} GEMM of {dom['layer']} ({dom['plan']})",
                  "kernel_ms": round(k_ms, 4), "flops_per_launch": F,
                  "bytes_per_launch": bytes_of(drun.L, dom["pass"])})
 
@@ -366,11 +401,14 @@ def main():
         cfg = int(cfg)
         layers = workloads.config(cfg)[1]
         li = [L.name for L in layers].index(lname)
-        run = LayerRun(cfg, li, layers[li], torch.cuda.current_stream().cuda_stream)
+        if args.plan is not None:
+            m.plan_set(PASSES.index(p), layers[li].shape, args.plan)
+        run = LayerRun(cfg, li, layers[li], torch.cuda.current_stream().cuda_stream,
+                       0 if args.plan is not None else args.tune)
         for _ in range(args.reps):
             run.run(p)
         torch.cuda.synchronize()
-        print(f"ran {args.profile_pass} x{args.reps}", flush=True)
+        print(f"ran {args.profile_pass} x{args.reps} with plan: {run.plan(p)}", flush=True)
         return
     cfgs = [0, 1, 2, 3, 4] if args.config == "all" else [int(args.config)]
     for cfg in cfgs:

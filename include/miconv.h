@@ -30,8 +30,10 @@
  *   - kernels are enqueued on `stream` (NULL = the null stream) and the
  *     calls return without synchronising; the library keeps no pointer
  *     after returning and allocates no device memory;
- *   - results are bitwise reproducible for the same shape, inputs and
- *     device (every reduction runs in a fixed order, no float atomics);
+ *   - results are bitwise reproducible for the same shape, inputs, device
+ *     and plan (every reduction runs in a fixed order, no float atomics);
+ *     the plan is the built-in rule unless one was set or tuned for the
+ *     shape (conv_plan_set, conv_tune below);
  *   - the calls clear the calling thread's pending HIP error before
  *     launching; a fault inside a kernel surfaces at the caller's next
  *     synchronisation.
@@ -64,10 +66,11 @@ typedef enum miconv_status {
     MICONV_ERR_ALIGN = -5,     /* a tensor or workspace pointer is not 16-byte aligned */
     MICONV_ERR_DEVICE = -6,    /* no current HIP device, or it is not gfx950 */
     MICONV_ERR_LAUNCH = -7,    /* a kernel launch reported an error */
-    MICONV_ERR_PASS = -8       /* conv_workspace_size: unknown pass id */
+    MICONV_ERR_PASS = -8,      /* unknown pass id */
+    MICONV_ERR_PLAN = -9       /* plan index outside [0, conv_plan_count()) */
 } miconv_status;
 
-/* Pass ids for conv_workspace_size. */
+/* Pass ids for conv_workspace_size and the plan calls. */
 #define MICONV_PASS_FWD 0
 #define MICONV_PASS_BWD_DATA 1
 #define MICONV_PASS_BWD_WEIGHT 2
@@ -85,8 +88,9 @@ int conv_output_size(int H, int W, int R, int S, int stride, int pad, int *P, in
 
 /*
  * Bytes of device workspace that pass `pass` (MICONV_PASS_*) needs for this
- * shape; 0 if it needs none or if the shape or pass id is invalid (the pass
- * itself then reports the error).  Host-only; touches no device.
+ * shape with the plan its calls use now; 0 if it needs none or if the shape
+ * or pass id is invalid (the pass itself then reports the error).  Host-only
+ * (once a plan has been stored it reads the current device id).
  */
 size_t conv_workspace_size(int pass, int N, int C, int H, int W, int K, int R, int S,
                            int stride, int pad, int group);
@@ -138,6 +142,62 @@ int conv_bwd_weight(int N, int C, int H, int W, int K, int R, int S, int stride,
  * MICONV_ERR_NULL if exactly one of the two is NULL.
  */
 int conv_set_timing_events(hipEvent_t before, hipEvent_t after);
+
+/*
+ * Plan selection (Sec. IV-B: a mixed strategy of convolution plans, chosen
+ * per layer; Sec. VI-A: the framework times its strategies over the first
+ * training iterations and keeps the fastest).  Every pass of a shape has a
+ * list of candidate plans (kernel tile, split of the reduction, and for
+ * backward-data stride phases or pixel blocks); candidate 0 is the built-in
+ * rule.  All candidates compute the same result up to fp32 rounding order.
+ * The choice is kept per (device, pass, shape) in a process-wide table that
+ * the conv_* calls consult; the table is thread-safe.  Arguments after
+ * `pass` are those of the pass.
+ *
+ * conv_plan_count:  number of candidates (>= 1), or a negative status
+ *                   (MICONV_ERR_SHAPE, MICONV_ERR_PASS).  Host-only.
+ * conv_plan_get:    candidate the calls use now on the current device
+ *                   (0 when none is stored).
+ * conv_plan_set:    use candidate `index` from now on (0 restores the rule);
+ *                   MICONV_ERR_PLAN if index is out of range.
+ * conv_plan_clear:  forget every stored choice.
+ * conv_plan_name:   NUL-terminated description of candidate `index` into
+ *                   buf (truncated to len bytes); MICONV_ERR_NULL if buf is
+ *                   NULL or len is 0.
+ * conv_plan_workspace_size: workspace bytes of candidate `index` (0 if the
+ *                   shape, pass or index is invalid, or it needs none).
+ */
+int conv_plan_count(int pass, int N, int C, int H, int W, int K, int R, int S, int stride,
+                    int pad, int group);
+int conv_plan_get(int pass, int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+                  int group);
+int conv_plan_set(int pass, int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+                  int group, int index);
+int conv_plan_clear(void);
+int conv_plan_name(int pass, int N, int C, int H, int W, int K, int R, int S, int stride,
+                   int pad, int group, int index, char *buf, size_t len);
+size_t conv_plan_workspace_size(int pass, int N, int C, int H, int W, int K, int R, int S,
+                                int stride, int pad, int group, int index);
+
+/*
+ * Times every candidate of `pass` whose workspace fits ws_bytes on the
+ * caller's tensors (one untimed run, then `reps` timed runs back to back on
+ * `stream`, HIP events around them; reps < 1 counts as 1), stores the
+ * fastest for this shape as with conv_plan_set, writes its index to *chosen
+ * (if not NULL), and runs it once more so the outputs hold its result.
+ * Blocks the host until the timed runs finish.  Tensors:
+ *   MICONV_PASS_FWD:         in0 = x, in1 = w, in2 = b (may be NULL), out0 = y
+ *   MICONV_PASS_BWD_DATA:    in0 = dy, in1 = w, out0 = dx (in2, out1 ignored)
+ *   MICONV_PASS_BWD_WEIGHT:  in0 = x, in1 = dy, out0 = dw, out1 = db (may be
+ *                            NULL; in2 ignored)
+ * Returns the statuses of the pass (checked on the first candidate run),
+ * MICONV_ERR_WORKSPACE if no candidate fits ws_bytes, or MICONV_ERR_LAUNCH
+ * if an event call fails; on an error nothing is stored.  The events of
+ * conv_set_timing_events are not recorded by the runs inside.
+ */
+int conv_tune(int pass, int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+              int group, const float *in0, const float *in1, const float *in2, float *out0,
+              float *out1, void *ws, size_t ws_bytes, int reps, hipStream_t stream, int *chosen);
 
 /* Static, NUL-terminated description of a status code (never NULL). */
 const char *conv_error_string(int status);

@@ -1,10 +1,15 @@
 // C ABI of the convolution library (declared in include/miconv.h): argument
 // validation, output geometry, workspace layout, kernel selection and
 // launches on the caller's stream.
+#include <algorithm>
 #include <atomic>
+#include <map>
+#include <mutex>
 #include <stddef.h>
 #include <stdint.h>
+#include <stdio.h>
 #include <string.h>
+#include <vector>
 
 #include "miconv.h"
 #include "internal.h"
@@ -36,7 +41,9 @@ constexpr int kTargetWorkgroups = 1024;         // 4 per CU on 256 CUs
 // three rounds of them measured best, as long as a split keeps at least
 // kTapMinSlices slices (shorter splits cost more in partial sums than they
 // gain in balance) -- unless that would leave fewer than kTargetWorkgroups
-// workgroups (small layers), where splits go down to 8 slices.
+// workgroups (small layers), where splits go down to 8 slices.  (Timed plan
+// selection also tries half and twice the splits of this rule; halving the
+// target itself measured slower, as the caps then bind differently.)
 constexpr int kTapTargetWorkgroups = 4096;
 constexpr int kTapMinSlices = 24;
 
@@ -215,6 +222,39 @@ int images_per_launch(const Geom &g)
     return (int)(n < g.N ? n : g.N);
 }
 
+
+// ------------------------------------------------------------ plans
+// Every pass has a built-in rule (measured on MI355X, below) and a list of
+// candidate plans whose first entry is that rule.  A per-shape cache, filled
+// by conv_plan_set or by conv_tune (which times the candidates, as the
+// paper's framework times its convolution strategies over the first training
+// iterations before keeping the fastest), overrides the rule.
+
+constexpr int kNumImgTiles = 7;
+constexpr int kNumWgradTiles = 6;
+
+const char *img_tile_name(int tile)
+{
+    static const char *names[] = {"64x64", "128x64", "16x128", "32x64", "48x64", "96x64", "96x128"};
+    return tile >= 0 && tile < kNumImgTiles ? names[tile] : "?";
+}
+
+// A tile whose rows are more than twice the problem's (rounded to 16) only
+// multiplies zeros: not a candidate.
+bool tile_fits(int tile, int M)
+{
+    int bm, bn;
+    img_tile_dims(tile, bm, bn);
+    return bm <= 2 * pad16(M);
+}
+
+long long tile_count(int tile, int M, long long Ncol, int G)
+{
+    int bm, bn;
+    img_tile_dims(tile, bm, bn);
+    return (long long)((M + bm - 1) / bm) * ((Ncol + bn - 1) / bn) * G;
+}
+
 // Split-K for the image GEMM.  With fewer than 640 tiles (2.5 per CU) the
 // MFMA pipes starve for latency hiding; a deep reduction (>= kSplitMinRows)
 // is then cut into splits of at least kSplitRows rows so that ~8 workgroups
@@ -228,56 +268,112 @@ constexpr int kSplitMinRows = 3072;
 constexpr int kSplitRows = 768;
 
 struct ImgPlan {
-    int tile, nsplit, kchunk;
+    int tile, nsplit, kchunk;  // tile -1: (backward-data phases) each phase by the rule
 };
 
-ImgPlan img_plan(int M, long long Ncol, int Kred, int G, bool allow_split)
+// Splits for `tiles` workgroups over Kred rows: about 8 workgroups per CU,
+// each split at least kSplitRows rows and 8 slices; 1 if that is under two.
+int split_count(long long tiles, int Kred)
 {
-    ImgPlan p;
-    p.tile = pick_img_tile(M, Ncol, Kred, G);
-    p.nsplit = 1;
-    p.kchunk = Kred;
-    if (!allow_split || Kred < kSplitMinRows)
-        return p;
-    int bm, bn;
-    img_tile_dims(p.tile, bm, bn);
-    long long tiles = (long long)((M + bm - 1) / bm) * ((Ncol + bn - 1) / bn) * G;
     long long slices = (Kred + kBK - 1) / kBK;
-    if (tiles >= 640)
-        return p;
     long long ns = (8 * kNumCUs + tiles - 1) / tiles;
     if (ns > slices / 8)
         ns = slices / 8;
     if (ns > Kred / kSplitRows)
         ns = Kred / kSplitRows;
-    if (ns < 2)
-        return p;
-    p.kchunk = (int)((slices + ns - 1) / ns) * kBK;
-    p.nsplit = (Kred + p.kchunk - 1) / p.kchunk;
+    return ns < 2 ? 1 : (int)ns;
+}
+
+ImgPlan with_split(int tile, int Kred, int ns)
+{
+    ImgPlan p{tile, 1, Kred};
+    if (ns >= 2) {
+        long long slices = (Kred + kBK - 1) / kBK;
+        p.kchunk = (int)((slices + ns - 1) / ns) * kBK;
+        p.nsplit = (Kred + p.kchunk - 1) / p.kchunk;
+    }
     return p;
 }
 
-// ------------------------------------------------------------ fwd plan
+ImgPlan img_rule(int M, long long Ncol, int Kred, int G, bool allow_split)
+{
+    const int tile = pick_img_tile(M, Ncol, Kred, G);
+    if (!allow_split || Kred < kSplitMinRows)
+        return with_split(tile, Kred, 1);
+    const long long tiles = tile_count(tile, M, Ncol, G);
+    return with_split(tile, Kred, tiles >= 640 ? 1 : split_count(tiles, Kred));
+}
+
+bool same_img(const ImgPlan &a, const ImgPlan &b)
+{
+    return a.tile == b.tile && a.nsplit == b.nsplit;
+}
+
+bool same_plan(const ImgPlan &a, const ImgPlan &b) { return same_img(a, b); }
+struct BwdPlan;
+bool same_plan(const BwdPlan &a, const BwdPlan &b);
+
+// Every fitting tile, unsplit and (when allowed) split by split_count.
+template <class P, class Make>
+void img_variants(int M, long long Ncol, int Kred, int G, bool allow_split, Make make,
+                  std::vector<P> &out)
+{
+    for (int t = 0; t < kNumImgTiles; t++) {
+        if (!tile_fits(t, M))
+            continue;
+        ImgPlan cands[2] = {with_split(t, Kred, 1),
+                            with_split(t, Kred,
+                                       allow_split ? split_count(tile_count(t, M, Ncol, G), Kred)
+                                                   : 1)};
+        for (int i = 0; i < (cands[1].nsplit > 1 ? 2 : 1); i++) {
+            P p = make(cands[i]);
+            bool dup = false;
+            for (const P &q : out)
+                dup = dup || same_plan(p, q);
+            if (!dup)
+                out.push_back(p);
+        }
+    }
+}
+
+// ------------------------------------------------------------ forward
 size_t fwd_pack_bytes(const Geom &g)
 {
     return align_up((size_t)g.K * pad16(g.Cg * g.R * g.S) * sizeof(float));
 }
 
-ImgPlan fwd_plan(const Geom &g)
+ImgPlan fwd_rule(const Geom &g)
 {
-    return img_plan(g.Kg, (long long)g.N * g.P * g.Q, g.Cg * g.R * g.S, g.G,
-                    images_per_launch(g) >= g.N);
+    const int nb = images_per_launch(g);
+    return img_rule(g.Kg, (long long)(g.N < nb ? g.N : nb) * g.P * g.Q, g.Cg * g.R * g.S, g.G,
+                    nb >= g.N);
 }
 
-size_t fwd_ws(const Geom &g)
+void fwd_candidates(const Geom &g, std::vector<ImgPlan> &out)
 {
-    ImgPlan p = fwd_plan(g);
+    out.clear();
+    out.push_back(fwd_rule(g));
+    const int nb = images_per_launch(g);
+    img_variants<ImgPlan>(g.Kg, (long long)(g.N < nb ? g.N : nb) * g.P * g.Q, g.Cg * g.R * g.S,
+                          g.G, nb >= g.N, [](const ImgPlan &p) { return p; }, out);
+}
+
+size_t fwd_ws(const Geom &g, const ImgPlan &p)
+{
     size_t part = p.nsplit > 1 ? align_up((size_t)p.nsplit * g.N * g.K * g.P * g.Q * sizeof(float))
                                : 0;
     return fwd_pack_bytes(g) + part;
 }
 
-// ------------------------------------------------------------ bwd-data plan
+void fwd_name(const ImgPlan &p, char *buf, size_t len)
+{
+    if (p.nsplit > 1)
+        snprintf(buf, len, "image GEMM %s, %d splits", img_tile_name(p.tile), p.nsplit);
+    else
+        snprintf(buf, len, "image GEMM %s", img_tile_name(p.tile));
+}
+
+// ------------------------------------------------------------ backward-data
 // Stride phase (ph, pw): input pixels h = ph + st*i, w = pw + st*j; the taps
 // that reach them are r = r0 + st*rr (rr < nr), s = s0 + st*ss (ss < ns),
 // with r0 = (ph + pad) mod st, and p = i + dh - rr where dh = (ph + pad - r0) / st.
@@ -305,11 +401,11 @@ Axis phase_axis(int in, int filt, int st, int pad, int ph)
 // h + pad = b hb + ph takes dy rows f hb + u, u = f - 1 - tu for tu < ntr with
 // ntr = f + (R - 1) / stride, through filter row r = ph - stride u (a zero
 // weight where r is outside the filter); columns alike.  Blocks hb cover
-// [hb0, hb0 + nh) with hb0 = pad / b.  It is taken when its MFMA work, with M
-// rounded up to the tile and the reduction to the slice, is below 3/4 of the
-// phase plan's.  Work on 16-row tiles counts 5/4: measured on the ResNet stem
-// (7x7, stride 2), 4 x 4 blocks of 48 rows ran 18 % faster than 2 x 2 blocks
-// of 12 rows, despite 19 % more work.
+// [hb0, hb0 + nh) with hb0 = pad / b.  The rule takes it when its MFMA work,
+// with M rounded up to the tile and the reduction to the slice, is below 3/4
+// of the phase plan's.  Work on 16-row tiles counts 5/4: measured on the
+// ResNet stem (7x7, stride 2), 4 x 4 blocks of 48 rows ran 18 % faster than
+// 2 x 2 blocks of 12 rows, despite 19 % more work.
 struct BlockPlan {
     int f, b, ntr, nts, hb0, wb0, nh, nw, M, a_ld;
 };
@@ -329,7 +425,26 @@ double tile_rows(int M)
     return (M + 63) / 64 * 64.0;
 }
 
-bool bwd_block_plan(const Geom &g, BlockPlan *out)
+// Geometry of the blocked plan with factor f; false where it does not apply
+// (block wider than 8, more than 256 rows, or a filter bank past the limit).
+bool block_geometry(const Geom &g, int f, BlockPlan *p)
+{
+    if (f < (g.st == 1 ? 2 : 1) || g.st * f > 8)
+        return false;
+    p->f = f;
+    p->b = g.st * f;
+    p->M = g.Cg * p->b * p->b;
+    p->ntr = f + (g.R - 1) / g.st;
+    p->nts = f + (g.S - 1) / g.st;
+    p->hb0 = g.pad / p->b;
+    p->wb0 = g.pad / p->b;
+    p->nh = (g.H - 1 + g.pad) / p->b + 1 - p->hb0;
+    p->nw = (g.W - 1 + g.pad) / p->b + 1 - p->wb0;
+    p->a_ld = pad16(g.Kg * p->ntr * p->nts);
+    return p->M <= 256 && (long long)g.G * p->M * p->a_ld <= kMaxChunkElems;
+}
+
+bool block_rule(const Geom &g, BlockPlan *out)
 {
     double phase_work = 0;
     for (int ph = 0; ph < g.st; ph++)
@@ -340,23 +455,11 @@ bool bwd_block_plan(const Geom &g, BlockPlan *out)
         }
     double best = 0.75 * phase_work;
     bool found = false;
-    for (int f = g.st == 1 ? 2 : 1; g.st * f <= 8; f++) {
+    for (int f = 1; f <= 8; f++) {
         BlockPlan p;
-        p.f = f;
-        p.b = g.st * f;
-        p.M = g.Cg * p.b * p.b;
-        if (p.M > 256)
-            break;
-        p.ntr = f + (g.R - 1) / g.st;
-        p.nts = f + (g.S - 1) / g.st;
-        p.hb0 = g.pad / p.b;
-        p.wb0 = g.pad / p.b;
-        p.nh = (g.H - 1 + g.pad) / p.b + 1 - p.hb0;
-        p.nw = (g.W - 1 + g.pad) / p.b + 1 - p.wb0;
-        p.a_ld = pad16(g.Kg * p.ntr * p.nts);
-        if ((long long)g.G * p.M * p.a_ld > kMaxChunkElems)
+        if (!block_geometry(g, f, &p))
             continue;
-        double work = (double)tile_rows(p.M) * p.a_ld * p.nh * p.nw;
+        double work = tile_rows(p.M) * p.a_ld * p.nh * p.nw;
         if (work < best) {
             best = work;
             *out = p;
@@ -366,11 +469,62 @@ bool bwd_block_plan(const Geom &g, BlockPlan *out)
     return found;
 }
 
-size_t bwd_data_pack_bytes(const Geom &g)
+struct BwdPlan {
+    bool blocked;
+    BlockPlan bp;  // blocked only
+    ImgPlan img;   // blocked: the GEMM's tile; phases: tile (-1: per phase by the rule) and
+                   // split-K (stride 1 only)
+};
+
+bool same_plan(const BwdPlan &a, const BwdPlan &b)
 {
-    BlockPlan bp;
-    if (bwd_block_plan(g, &bp))
-        return align_up((size_t)g.G * bp.M * bp.a_ld * sizeof(float));
+    return a.blocked == b.blocked && (!a.blocked || a.bp.f == b.bp.f) && same_img(a.img, b.img);
+}
+
+BwdPlan bwd_rule(const Geom &g)
+{
+    BwdPlan p{};
+    const int nb = images_per_launch(g), n0 = g.N < nb ? g.N : nb;
+    if (block_rule(g, &p.bp)) {
+        p.blocked = true;
+        const int kred = g.Kg * p.bp.ntr * p.bp.nts;
+        p.img = with_split(pick_img_tile(p.bp.M, (long long)n0 * p.bp.nh * p.bp.nw, kred, g.G),
+                           kred, 1);
+    } else if (g.st == 1) {
+        // Split-K only for stride 1 (one phase covering all of dx).
+        p.img = img_rule(g.Cg, (long long)n0 * g.H * g.W, g.Kg * g.R * g.S, g.G, nb >= g.N);
+    } else {
+        p.img = ImgPlan{-1, 1, 0};
+    }
+    return p;
+}
+
+void bwd_candidates(const Geom &g, std::vector<BwdPlan> &out)
+{
+    out.clear();
+    out.push_back(bwd_rule(g));
+    const int nb = images_per_launch(g), n0 = g.N < nb ? g.N : nb;
+    // Phases, one tile for all of them.
+    const int kred_max = g.Kg * ((g.R + g.st - 1) / g.st) * ((g.S + g.st - 1) / g.st);
+    img_variants<BwdPlan>(g.Cg, (long long)n0 * g.H * g.W / (g.st * g.st), kred_max, g.G,
+                          g.st == 1 && nb >= g.N,
+                          [](const ImgPlan &i) { return BwdPlan{false, BlockPlan{}, i}; }, out);
+    // Blocked, for few channels per group.
+    if (g.Cg <= 16)
+        for (int f = 1; f <= 8; f++) {
+            BlockPlan bp;
+            if (!block_geometry(g, f, &bp))
+                continue;
+            const int kred = g.Kg * bp.ntr * bp.nts;
+            img_variants<BwdPlan>(bp.M, (long long)n0 * bp.nh * bp.nw, kred, g.G, false,
+                                  [&](const ImgPlan &i) { return BwdPlan{true, bp, i}; }, out);
+        }
+}
+
+size_t bwd_ws(const Geom &g, const BwdPlan &p)
+{
+    if (p.blocked)
+        return align_up((size_t)g.G * p.bp.M * p.bp.a_ld * sizeof(float));
     size_t total = 0;
     for (int ph = 0; ph < g.st; ph++)
         for (int pw = 0; pw < g.st; pw++) {
@@ -378,30 +532,30 @@ size_t bwd_data_pack_bytes(const Geom &g)
             Axis aw = phase_axis(g.W, g.S, g.st, g.pad, pw);
             total += align_up((size_t)g.C * pad16(g.Kg * ah.nt * aw.nt) * sizeof(float));
         }
+    if (p.img.nsplit > 1)
+        total += align_up((size_t)p.img.nsplit * g.N * g.C * g.H * g.W * sizeof(float));
     return total;
 }
 
-// Split-K only for stride 1 (one phase covering all of dx) and the phase plan.
-ImgPlan bwd_data_plan(const Geom &g)
+void bwd_name(const BwdPlan &p, char *buf, size_t len)
 {
-    BlockPlan bp;
-    return img_plan(g.Cg, (long long)g.N * g.H * g.W, g.Kg * g.R * g.S, g.G,
-                    g.st == 1 && images_per_launch(g) >= g.N && !bwd_block_plan(g, &bp));
+    if (p.blocked)
+        snprintf(buf, len, "blocked %dx%d pixels (f=%d), image GEMM %s", p.bp.b, p.bp.b, p.bp.f,
+                 img_tile_name(p.img.tile));
+    else if (p.img.tile < 0)
+        snprintf(buf, len, "stride phases, tiles by rule");
+    else if (p.img.nsplit > 1)
+        snprintf(buf, len, "stride phases, image GEMM %s, %d splits", img_tile_name(p.img.tile),
+                 p.img.nsplit);
+    else
+        snprintf(buf, len, "stride phases, image GEMM %s", img_tile_name(p.img.tile));
 }
 
-size_t bwd_data_ws(const Geom &g)
-{
-    ImgPlan p = bwd_data_plan(g);
-    size_t part = p.nsplit > 1 ? align_up((size_t)p.nsplit * g.N * g.C * g.H * g.W * sizeof(float))
-                               : 0;
-    return bwd_data_pack_bytes(g) + part;
-}
-
-// ------------------------------------------------------------ bwd-weight plan
+// ------------------------------------------------------------ backward-weight
 // The reduction over N*P*Q pixels is cut into fixed-length splits (a
-// multiple of the slice) so that about kTargetWorkgroups (packed tiles) or
-// kTapTargetWorkgroups (tap-uniform tiles) workgroups run; each split writes its own partial dw, summed afterwards in
-// split order.  Launches never straddle a batch chunk (images_per_launch).
+// multiple of the slice) so that about kTapTargetWorkgroups workgroups run;
+// each split writes its own partial dw, summed afterwards in split order.
+// Launches never straddle a batch chunk (images_per_launch).
 struct WgradPlan {
     int tile, slice, chunk, nsplit, nb;
     bool via_part;
@@ -410,42 +564,63 @@ struct WgradPlan {
 
 bool is_tap_tile(int tile) { return tile <= WG_TAP_64x16; }
 
-WgradPlan wgrad_plan(const Geom &g)
+void wgrad_tile_dims(int tile, int &bm, int &bn)
+{
+    static const int dims[][2] = {{64, 32}, {64, 48}, {64, 16}, {96, 64}, {64, 64}, {64, 32}};
+    bm = dims[tile][0];
+    bn = dims[tile][1];
+}
+
+const char *wgrad_tile_name(int tile)
+{
+    static const char *names[] = {"tap 64x32", "tap 64x48", "tap 64x16",
+                                  "pixel 96x64", "pixel 64x64", "pixel 64x32"};
+    return names[tile];
+}
+
+// tile -1: the rule's tile.  scale: the rule's split count times 2^scale.
+WgradPlan wgrad_plan(const Geom &g, int tile = -1, int scale = 0)
 {
     WgradPlan p;
     int M = g.Kg, Ncol = g.Cg * g.R * g.S;
     long long PQ = (long long)g.P * g.Q, Kred = (long long)g.N * PQ;
-    long long tiles, target = kTargetWorkgroups, min_slices = 8;
-    if (g.Cg >= 32 || g.Cg == 16) {
-        // Tap-uniform tiles of 64 rows of K/G by 32 channels of one tap, by
-        // 48 channels when C/G is a multiple of 48 but not of 64, or by 16 for
-        // 16 channels, so that no column stays idle.  Small tiles measured
-        // fastest on every layer of the five stacks: six fit on a CU.
-        const int bm = 64;
-        const int bn = g.Cg == 16 ? 16 : (g.Cg % 64 != 0 && g.Cg % 48 == 0) ? 48 : 32;
-        p.tile = bn == 16 ? WG_TAP_64x16 : bn == 48 ? WG_TAP_64x48 : WG_TAP_64x32;
-        tiles = (long long)((M + bm - 1) / bm) * g.R * g.S * ((g.Cg + bn - 1) / bn) * g.G;
-        target = kTapTargetWorkgroups;
-        min_slices = kTapMinSlices;
-        p.slice = 64;
-    } else {
-        // Few channels per group: the same one-pixel-per-lane kernel with
-        // (c, r, s) packed into the columns, 96 rows for 65-96 filters.
-        const int bm = (M > 64 && M <= 96) ? 96 : 64, bn = Ncol <= 32 ? 32 : 64;
-        p.tile = bm == 96 ? WG_PIX_96x64 : bn == 32 ? WG_PIX_64x32 : WG_PIX_64x64;
-        tiles = (long long)gemm_tiles(M, Ncol, bm, bn) * g.G;
-        target = kTapTargetWorkgroups;
-        min_slices = kTapMinSlices;
-        p.slice = 64;
+    if (tile < 0) {
+        if (g.Cg >= 32 || g.Cg == 16) {
+            // Tap-uniform tiles of 64 rows of K/G by 32 channels of one tap, by
+            // 48 channels when C/G is a multiple of 48 but not of 64, or by 16
+            // for 16 channels, so that no column stays idle.  Small tiles
+            // measured fastest on every layer of the five stacks: six fit on a CU.
+            const int bn = g.Cg == 16 ? 16 : (g.Cg % 64 != 0 && g.Cg % 48 == 0) ? 48 : 32;
+            tile = bn == 16 ? WG_TAP_64x16 : bn == 48 ? WG_TAP_64x48 : WG_TAP_64x32;
+        } else {
+            // Few channels per group: the same one-pixel-per-lane kernel with
+            // (c, r, s) packed into the columns, 96 rows for 65-96 filters.
+            const int bm = (M > 64 && M <= 96) ? 96 : 64, bn = Ncol <= 32 ? 32 : 64;
+            tile = bm == 96 ? WG_PIX_96x64 : bn == 32 ? WG_PIX_64x32 : WG_PIX_64x64;
+        }
     }
-    long long ns = (target + tiles - 1) / tiles;
-    long long long_ns = Kred / (p.slice * min_slices);
+    p.tile = tile;
+    p.slice = 64;
+    int bm, bn;
+    wgrad_tile_dims(tile, bm, bn);
+    const long long tiles =
+        is_tap_tile(tile)
+            ? (long long)((M + bm - 1) / bm) * g.R * g.S * ((g.Cg + bn - 1) / bn) * g.G
+            : (long long)gemm_tiles(M, Ncol, bm, bn) * g.G;
+    long long ns = (kTapTargetWorkgroups + tiles - 1) / tiles;
+    long long long_ns = Kred / (p.slice * kTapMinSlices);
     long long fill_ns = (kTargetWorkgroups + tiles - 1) / tiles;
     long long max_ns = long_ns > fill_ns ? long_ns : fill_ns;
     if (max_ns > Kred / (p.slice * 8))
         max_ns = Kred / (p.slice * 8);
     if (ns > max_ns)
         ns = max_ns;
+    if (scale > 0)
+        ns <<= scale;
+    else if (scale < 0)
+        ns >>= -scale;
+    if (ns > Kred / p.slice)
+        ns = Kred / p.slice;
     if (ns < 1)
         ns = 1;
     long long chunk = (Kred + ns - 1) / ns;
@@ -466,6 +641,125 @@ WgradPlan wgrad_plan(const Geom &g)
     return p;
 }
 
+void wgrad_candidates(const Geom &g, std::vector<WgradPlan> &out)
+{
+    out.clear();
+    out.push_back(wgrad_plan(g));
+    for (int t = 0; t < kNumWgradTiles; t++)
+        for (int scale : {0, 1, -1}) {
+            WgradPlan p = wgrad_plan(g, t, scale);
+            bool dup = false;
+            for (const WgradPlan &q : out)
+                dup = dup || (q.tile == p.tile && q.chunk == p.chunk);
+            if (!dup)
+                out.push_back(p);
+        }
+}
+
+size_t wgrad_ws(const WgradPlan &p) { return p.part_bytes + p.bias_bytes; }
+
+void wgrad_name(const WgradPlan &p, char *buf, size_t len)
+{
+    snprintf(buf, len, "%s, %d splits of %d pixels", wgrad_tile_name(p.tile), p.nsplit, p.chunk);
+}
+
+// ------------------------------------------------------------ plan cache
+struct PlanKey {
+    int v[12];
+    bool operator<(const PlanKey &o) const
+    {
+        return std::lexicographical_compare(v, v + 12, o.v, o.v + 12);
+    }
+};
+
+// A stored choice keeps its candidate index and the plan itself, so that a
+// call with a stored plan costs one table lookup.
+struct StoredPlan {
+    int index;
+    ImgPlan fwd;
+    BwdPlan bwd;
+    WgradPlan wgrad;
+};
+
+std::mutex g_plan_mu;
+std::map<PlanKey, StoredPlan> g_plans;
+std::atomic<int> g_plan_entries{0};
+
+PlanKey plan_key(int pass, const Geom &g)
+{
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess)
+        dev = -1;
+    return PlanKey{{dev, pass, g.N, g.C, g.H, g.W, g.K, g.R, g.S, g.st, g.pad, g.G}};
+}
+
+// The stored choice for this shape on the current device, if any.
+bool stored_plan(int pass, const Geom &g, StoredPlan *out)
+{
+    if (g_plan_entries.load(std::memory_order_acquire) == 0)
+        return false;
+    PlanKey k = plan_key(pass, g);
+    std::lock_guard<std::mutex> lock(g_plan_mu);
+    auto it = g_plans.find(k);
+    if (it == g_plans.end())
+        return false;
+    *out = it->second;
+    return true;
+}
+
+// Candidate index the calls use for this shape on the current device.
+int plan_index(int pass, const Geom &g)
+{
+    StoredPlan sp;
+    return stored_plan(pass, g, &sp) ? sp.index : 0;
+}
+
+template <class P>
+P pick(const P &rule, int index, void (*cands)(const Geom &, std::vector<P> &), const Geom &g)
+{
+    if (index <= 0)
+        return rule;
+    std::vector<P> c;
+    cands(g, c);
+    return index < (int)c.size() ? c[index] : rule;
+}
+
+void plan_store(int pass, const Geom &g, int index)
+{
+    PlanKey k = plan_key(pass, g);
+    StoredPlan sp{};
+    sp.index = index;
+    if (pass == MICONV_PASS_FWD)
+        sp.fwd = pick(fwd_rule(g), index, fwd_candidates, g);
+    else if (pass == MICONV_PASS_BWD_DATA)
+        sp.bwd = pick(bwd_rule(g), index, bwd_candidates, g);
+    else
+        sp.wgrad = pick(wgrad_plan(g), index, wgrad_candidates, g);
+    std::lock_guard<std::mutex> lock(g_plan_mu);
+    if (index <= 0)
+        g_plans.erase(k);
+    else
+        g_plans[k] = sp;
+    g_plan_entries.store((int)g_plans.size(), std::memory_order_release);
+}
+
+ImgPlan fwd_current(const Geom &g)
+{
+    StoredPlan sp;
+    return stored_plan(MICONV_PASS_FWD, g, &sp) ? sp.fwd : fwd_rule(g);
+}
+BwdPlan bwd_current(const Geom &g)
+{
+    StoredPlan sp;
+    return stored_plan(MICONV_PASS_BWD_DATA, g, &sp) ? sp.bwd : bwd_rule(g);
+}
+WgradPlan wgrad_current(const Geom &g)
+{
+    StoredPlan sp;
+    return stored_plan(MICONV_PASS_BWD_WEIGHT, g, &sp) ? sp.wgrad : wgrad_plan(g);
+}
+
+// ------------------------------------------------------------ execution
 int launch_status(hipError_t e) { return e == hipSuccess ? MICONV_OK : MICONV_ERR_LAUNCH; }
 
 // Caller-owned timing events of conv_set_timing_events, per calling thread.
@@ -479,18 +773,93 @@ hipError_t mark(hipEvent_t ev, hipStream_t stream)
     return ev ? hipEventRecord(ev, stream) : hipSuccess;
 }
 
+int fwd_exec(const Geom &g, const ImgPlan &plan, const float *x, const float *w, const float *b,
+             float *y, void *ws, size_t ws_bytes, hipStream_t stream)
+{
+    const int N = g.N, C = g.C, H = g.H, W = g.W, K = g.K, R = g.R, S = g.S;
+    const size_t fb = sizeof(float);
+    Range r[4] = {{x, (size_t)N * C * H * W * fb, false},
+                  {w, (size_t)K * g.Cg * R * S * fb, false},
+                  {b, (size_t)K * fb, false},
+                  {y, (size_t)N * K * g.P * g.Q * fb, true}};
+    bool req[4] = {true, true, false, true};
+    int st = check_buffers(r, 4, req, ws, ws_bytes, fwd_ws(g, plan));
+    if (st != MICONV_OK || (st = check_device()) != MICONV_OK)
+        return st;
+    (void)hipGetLastError();
+
+    float *wp = (float *)ws;
+    const int a_ld = pad16(g.Cg * R * S);
+    // The filter layout follows the tile, which every launch of the call shares.
+    const bool kmajor = img_tile_shares_a(plan.tile);
+    if (launch_pack_fwd(w, wp, K, g.Cg, R, S, g.G, g.Cg % kBK == 0, a_ld, kmajor, stream) !=
+        hipSuccess)
+        return MICONV_ERR_LAUNCH;
+
+    const int nb = images_per_launch(g);
+    const long long xi = (long long)C * H * W, yi = (long long)K * g.P * g.Q;
+    ImgGemmArgs a{};
+    a.M = g.Kg;
+    a.Kred = g.Cg * R * S;
+    a.groups = g.G;
+    a.A = wp;
+    a.a_ld = a_ld;
+    a.a_bytes = (uint32_t)((size_t)K * a_ld * fb);
+    a.cin = g.Cg;
+    a.src_h = H;
+    a.src_w = W;
+    a.src_hw = H * W;
+    a.src_img_words = (uint32_t)xi;
+    a.col_hw = make_fastdiv(g.P * g.Q);
+    a.col_w = make_fastdiv(g.Q);
+    a.cstep = g.st;
+    a.coff_h = -g.pad;
+    a.coff_w = -g.pad;
+    a.tsign = 1;
+    a.k_cin = make_fastdiv(g.Cg);
+    a.k_tw = make_fastdiv(S);
+    a.k_taps = make_fastdiv(R * S);
+    a.bias = b;
+    a.out_img_stride = yi;
+    a.out_hw = g.P * g.Q;
+    a.out_w = g.Q;
+    a.ostep = 1;
+    const bool fast = g.Cg % kBK == 0;
+    float *part = (float *)((char *)ws + fwd_pack_bytes(g));
+    if (mark(tl_events.before, stream) != hipSuccess)
+        return MICONV_ERR_LAUNCH;
+    for (int n0 = 0; n0 < N; n0 += nb) {
+        const int n = N - n0 < nb ? N - n0 : nb;
+        a.Ncol = n * g.P * g.Q;
+        a.src = x + n0 * xi;
+        a.src_bytes = (uint32_t)(n * xi * (long long)fb);
+        a.out = plan.nsplit > 1 ? part : y + n0 * yi;
+        a.nsplit = plan.nsplit;
+        a.kchunk = plan.kchunk;
+        a.split_stride = (long long)N * yi;
+        if ((st = launch_status(launch_img_gemm(a, plan.tile, fast, stream))) != MICONV_OK)
+            return st;
+    }
+    if (mark(tl_events.after, stream) != hipSuccess)
+        return MICONV_ERR_LAUNCH;
+    if (plan.nsplit > 1)
+        return launch_status(launch_splitk_bias_reduce(part, plan.nsplit, (long long)N * yi,
+                                                       (int)(N * yi), b, g.P * g.Q, K, y,
+                                                       stream));
+    return MICONV_OK;
+}
+
 // Backward-data by the blocked plan: one GEMM per batch chunk over columns
 // (image, block row, block column), rows (channel, ph, pw).
-int bwd_data_blocked(const Geom &g, const BlockPlan &bp, const float *dy, const float *w,
-                     float *dx, void *ws, hipStream_t stream)
+int bwd_blocked(const Geom &g, const BwdPlan &plan, const float *dy, const float *w, float *dx,
+                void *ws, hipStream_t stream)
 {
+    const BlockPlan &bp = plan.bp;
     const size_t fb = sizeof(float);
     const int nb = images_per_launch(g);
     const long long xi = (long long)g.C * g.H * g.W, yi = (long long)g.K * g.P * g.Q;
     const int kred = g.Kg * bp.ntr * bp.nts;
-    const int tile0 = pick_img_tile(bp.M, (long long)(g.N < nb ? g.N : nb) * bp.nh * bp.nw, kred,
-                                    g.G);
-    const bool kmajor = img_tile_shares_a(tile0);
+    const bool kmajor = img_tile_shares_a(plan.img.tile);
     float *wp = (float *)ws;
     if (launch_pack_bwd_block(w, wp, g.K, g.Cg, g.R, g.S, g.G, g.st, bp.f, bp.ntr, bp.nts,
                               g.Kg % kBK == 0, bp.a_ld, kmajor, stream) != hipSuccess)
@@ -538,205 +907,39 @@ int bwd_data_blocked(const Geom &g, const BlockPlan &bp, const float *dy, const 
         a.src = dy + n0 * yi;
         a.src_bytes = (uint32_t)(n * yi * (long long)fb);
         a.out = dx + n0 * xi;
-        int tile = pick_img_tile(a.M, a.Ncol, a.Kred, g.G);
-        if (img_tile_shares_a(tile) != kmajor)
-            tile = tile0;
-        int st = launch_status(launch_img_gemm(a, tile, fast, stream));
+        int st = launch_status(launch_img_gemm(a, plan.img.tile, fast, stream));
         if (st != MICONV_OK)
             return st;
     }
     return mark(tl_events.after, stream) == hipSuccess ? MICONV_OK : MICONV_ERR_LAUNCH;
 }
 
-}  // namespace
-}  // namespace miconv
-
-using namespace miconv;
-
-extern "C" {
-
-int conv_output_size(int H, int W, int R, int S, int stride, int pad, int *P, int *Q)
+int bwd_exec(const Geom &g, const BwdPlan &plan, const float *dy, const float *w, float *dx,
+             void *ws, size_t ws_bytes, hipStream_t stream)
 {
-    if (!P || !Q)
-        return MICONV_ERR_NULL;
-    if (H < 1 || W < 1 || R < 1 || S < 1 || stride < 1 || pad < 0)
-        return MICONV_ERR_SHAPE;
-    int p = out_extent(H, R, stride, pad), q = out_extent(W, S, stride, pad);
-    if (p < 1 || q < 1)
-        return MICONV_ERR_SHAPE;
-    *P = p;
-    *Q = q;
-    return MICONV_OK;
-}
-
-size_t conv_workspace_size(int pass, int N, int C, int H, int W, int K, int R, int S,
-                           int stride, int pad, int group)
-{
-    Geom g;
-    if (make_geom(N, C, H, W, K, R, S, stride, pad, group, &g) != MICONV_OK)
-        return 0;
-    switch (pass) {
-    case MICONV_PASS_FWD:
-        return fwd_ws(g);
-    case MICONV_PASS_BWD_DATA:
-        return bwd_data_ws(g);
-    case MICONV_PASS_BWD_WEIGHT: {
-        WgradPlan p = wgrad_plan(g);
-        return p.part_bytes + p.bias_bytes;
-    }
-    default:
-        return 0;
-    }
-}
-
-int conv_set_timing_events(hipEvent_t before, hipEvent_t after)
-{
-    if ((before == nullptr) != (after == nullptr))
-        return MICONV_ERR_NULL;
-    tl_events.before = before;
-    tl_events.after = after;
-    return MICONV_OK;
-}
-
-const char *conv_error_string(int status)
-{
-    switch (status) {
-    case MICONV_OK: return "success";
-    case MICONV_ERR_SHAPE: return "invalid shape, stride, padding or group";
-    case MICONV_ERR_NULL: return "a required pointer is NULL";
-    case MICONV_ERR_WORKSPACE: return "workspace missing or smaller than conv_workspace_size()";
-    case MICONV_ERR_ALIAS: return "an output overlaps an input, another output or the workspace";
-    case MICONV_ERR_ALIGN: return "a tensor or workspace pointer is not 16-byte aligned";
-    case MICONV_ERR_DEVICE: return "no current HIP device, or it is not gfx950";
-    case MICONV_ERR_LAUNCH: return "kernel launch failed";
-    case MICONV_ERR_PASS: return "unknown pass id";
-    default: return "unknown status";
-    }
-}
-
-int conv_fwd(int N, int C, int H, int W, int K, int R, int S, int stride, int pad, int group,
-             const float *x, const float *w, const float *b, float *y, void *ws, size_t ws_bytes,
-             hipStream_t stream)
-{
-    Geom g;
-    int st = make_geom(N, C, H, W, K, R, S, stride, pad, group, &g);
-    if (st != MICONV_OK)
-        return st;
-    const size_t fb = sizeof(float);
-    Range r[4] = {{x, (size_t)N * C * H * W * fb, false},
-                  {w, (size_t)K * g.Cg * R * S * fb, false},
-                  {b, (size_t)K * fb, false},
-                  {y, (size_t)N * K * g.P * g.Q * fb, true}};
-    bool req[4] = {true, true, false, true};
-    size_t need = fwd_ws(g);
-    if ((st = check_buffers(r, 4, req, ws, ws_bytes, need)) != MICONV_OK)
-        return st;
-    if ((st = check_device()) != MICONV_OK)
-        return st;
-    (void)hipGetLastError();
-
-    float *wp = (float *)ws;
-    const int a_ld = pad16(g.Cg * R * S);
-    const ImgPlan plan = fwd_plan(g);
-    // The filter layout follows the tile; every launch of the call uses a
-    // tile of the same kind (the kind depends on M only).
-    const bool kmajor = img_tile_shares_a(plan.tile);
-    if (launch_pack_fwd(w, wp, K, g.Cg, R, S, group, g.Cg % kBK == 0, a_ld, kmajor, stream) !=
-        hipSuccess)
-        return MICONV_ERR_LAUNCH;
-
-    const int nb = images_per_launch(g);
-    const long long xi = (long long)C * H * W, yi = (long long)K * g.P * g.Q;
-    ImgGemmArgs a{};
-    a.M = g.Kg;
-    a.Kred = g.Cg * R * S;
-    a.groups = group;
-    a.A = wp;
-    a.a_ld = a_ld;
-    a.a_bytes = (uint32_t)((size_t)K * a_ld * fb);
-    a.cin = g.Cg;
-    a.src_h = H;
-    a.src_w = W;
-    a.src_hw = H * W;
-    a.src_img_words = (uint32_t)xi;
-    a.col_hw = make_fastdiv(g.P * g.Q);
-    a.col_w = make_fastdiv(g.Q);
-    a.cstep = stride;
-    a.coff_h = -pad;
-    a.coff_w = -pad;
-    a.tsign = 1;
-    a.k_cin = make_fastdiv(g.Cg);
-    a.k_tw = make_fastdiv(S);
-    a.k_taps = make_fastdiv(R * S);
-    a.bias = b;
-    a.out_img_stride = yi;
-    a.out_hw = g.P * g.Q;
-    a.out_w = g.Q;
-    a.ostep = 1;
-    a.ooff_h = 0;
-    a.ooff_w = 0;
-    const bool fast = g.Cg % kBK == 0;
-    float *part = (float *)((char *)ws + fwd_pack_bytes(g));
-    if (mark(tl_events.before, stream) != hipSuccess)
-        return MICONV_ERR_LAUNCH;
-    for (int n0 = 0; n0 < N; n0 += nb) {
-        const int n = N - n0 < nb ? N - n0 : nb;
-        a.Ncol = n * g.P * g.Q;
-        a.src = x + n0 * xi;
-        a.src_bytes = (uint32_t)(n * xi * (long long)fb);
-        a.out = plan.nsplit > 1 ? part : y + n0 * yi;
-        a.nsplit = plan.nsplit;
-        a.kchunk = plan.kchunk;
-        a.split_stride = (long long)N * yi;
-        int tile = n == N ? plan.tile : pick_img_tile(a.M, a.Ncol, a.Kred, group);
-        if (img_tile_shares_a(tile) != kmajor)
-            tile = plan.tile;
-        if ((st = launch_status(launch_img_gemm(a, tile, fast, stream))) != MICONV_OK)
-            return st;
-    }
-    if (mark(tl_events.after, stream) != hipSuccess)
-        return MICONV_ERR_LAUNCH;
-    if (plan.nsplit > 1)
-        return launch_status(launch_splitk_bias_reduce(part, plan.nsplit, (long long)N * yi,
-                                                       (int)(N * yi), b, g.P * g.Q, K, y,
-                                                       stream));
-    return MICONV_OK;
-}
-
-int conv_bwd_data(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
-                  int group, const float *dy, const float *w, float *dx, void *ws,
-                  size_t ws_bytes, hipStream_t stream)
-{
-    Geom g;
-    int st = make_geom(N, C, H, W, K, R, S, stride, pad, group, &g);
-    if (st != MICONV_OK)
-        return st;
+    const int N = g.N, C = g.C, H = g.H, W = g.W, K = g.K, R = g.R, S = g.S;
+    const int stride = g.st, group = g.G;
     const size_t fb = sizeof(float);
     Range r[3] = {{dy, (size_t)N * K * g.P * g.Q * fb, false},
                   {w, (size_t)K * g.Cg * R * S * fb, false},
                   {dx, (size_t)N * C * H * W * fb, true}};
     bool req[3] = {true, true, true};
-    size_t need = bwd_data_ws(g);
-    if ((st = check_buffers(r, 3, req, ws, ws_bytes, need)) != MICONV_OK)
-        return st;
-    if ((st = check_device()) != MICONV_OK)
+    int st = check_buffers(r, 3, req, ws, ws_bytes, bwd_ws(g, plan));
+    if (st != MICONV_OK || (st = check_device()) != MICONV_OK)
         return st;
     (void)hipGetLastError();
-
-    BlockPlan bp;
-    if (bwd_block_plan(g, &bp))
-        return bwd_data_blocked(g, bp, dy, w, dx, ws, stream);
+    if (plan.blocked)
+        return bwd_blocked(g, plan, dy, w, dx, ws, stream);
 
     const int nb = images_per_launch(g);
     const long long xi = (long long)C * H * W, yi = (long long)K * g.P * g.Q;
-    const ImgPlan plan = bwd_data_plan(g);  // nsplit > 1 only for stride 1
-    float *part = (float *)((char *)ws + bwd_data_pack_bytes(g));
+    const bool split = plan.img.nsplit > 1;  // stride 1 only
     char *wsp = (char *)ws;
     bool marked = false;
     for (int ph = 0; ph < stride; ph++)
         for (int pw = 0; pw < stride; pw++) {
-            Axis ah = phase_axis(H, R, stride, pad, ph);
-            Axis aw = phase_axis(W, S, stride, pad, pw);
+            Axis ah = phase_axis(H, R, stride, g.pad, ph);
+            Axis aw = phase_axis(W, S, stride, g.pad, pw);
             const int a_ld = pad16(g.Kg * ah.nt * aw.nt);
             size_t bytes = align_up((size_t)C * a_ld * fb);
             float *wr = (float *)wsp;
@@ -744,10 +947,11 @@ int conv_bwd_data(int N, int C, int H, int W, int K, int R, int S, int stride, i
             if (ah.n == 0 || aw.n == 0)
                 continue;
             const int kred = ah.nt * aw.nt * g.Kg;
-            const int tile0 = stride == 1 ? plan.tile
-                                          : pick_img_tile(g.Cg, (long long)(N < nb ? N : nb) *
-                                                                    ah.n * aw.n, kred, group);
-            const bool kmajor = img_tile_shares_a(tile0);
+            const int tile = plan.img.tile >= 0
+                                 ? plan.img.tile
+                                 : pick_img_tile(g.Cg, (long long)(N < nb ? N : nb) * ah.n * aw.n,
+                                                 kred, group);
+            const bool kmajor = img_tile_shares_a(tile);
             if (launch_pack_bwd_phase(w, wr, K, g.Cg, R, S, group, ah.t0, aw.t0, ah.nt, aw.nt,
                                       stride, g.Kg % kBK == 0, a_ld, kmajor, stream) !=
                 hipSuccess)
@@ -789,46 +993,35 @@ int conv_bwd_data(int N, int C, int H, int W, int K, int R, int S, int stride, i
                 a.Ncol = n * ah.n * aw.n;
                 a.src = dy + n0 * yi;
                 a.src_bytes = (uint32_t)(n * yi * (long long)fb);
-                a.out = plan.nsplit > 1 ? part : dx + n0 * xi;
-                a.nsplit = plan.nsplit;
-                a.kchunk = plan.nsplit > 1 ? plan.kchunk : a.Kred;
+                a.out = split ? (float *)wsp : dx + n0 * xi;
+                a.nsplit = plan.img.nsplit;
+                a.kchunk = split ? plan.img.kchunk : a.Kred;
                 a.split_stride = (long long)N * xi;
-                int tile = stride == 1 && n == N ? plan.tile
-                                                 : pick_img_tile(a.M, a.Ncol, a.Kred, group);
-                if (img_tile_shares_a(tile) != kmajor)
-                    tile = tile0;
                 if ((st = launch_status(launch_img_gemm(a, tile, fast, stream))) != MICONV_OK)
                     return st;
             }
         }
     if (mark(tl_events.after, stream) != hipSuccess)
         return MICONV_ERR_LAUNCH;
-    if (plan.nsplit > 1)
-        return launch_status(launch_splitk_bias_reduce(part, plan.nsplit, (long long)N * xi,
-                                                       (int)(N * xi), nullptr, 1, 1, dx,
-                                                       stream));
+    if (split)
+        return launch_status(launch_splitk_bias_reduce((float *)wsp, plan.img.nsplit,
+                                                       (long long)N * xi, (int)(N * xi),
+                                                       nullptr, 1, 1, dx, stream));
     return MICONV_OK;
 }
 
-int conv_bwd_weight(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
-                    int group, const float *x, const float *dy, float *dw, float *db, void *ws,
-                    size_t ws_bytes, hipStream_t stream)
+int wgrad_exec(const Geom &g, const WgradPlan &p, const float *x, const float *dy, float *dw,
+               float *db, void *ws, size_t ws_bytes, hipStream_t stream)
 {
-    Geom g;
-    int st = make_geom(N, C, H, W, K, R, S, stride, pad, group, &g);
-    if (st != MICONV_OK)
-        return st;
+    const int N = g.N, C = g.C, H = g.H, W = g.W, K = g.K, R = g.R, S = g.S;
     const size_t fb = sizeof(float);
     Range r[4] = {{x, (size_t)N * C * H * W * fb, false},
                   {dy, (size_t)N * K * g.P * g.Q * fb, false},
                   {dw, (size_t)K * g.Cg * R * S * fb, true},
                   {db, (size_t)K * fb, true}};
     bool req[4] = {true, true, true, false};
-    WgradPlan p = wgrad_plan(g);
-    size_t need = p.part_bytes + p.bias_bytes;
-    if ((st = check_buffers(r, 4, req, ws, ws_bytes, need)) != MICONV_OK)
-        return st;
-    if ((st = check_device()) != MICONV_OK)
+    int st = check_buffers(r, 4, req, ws, ws_bytes, wgrad_ws(p));
+    if (st != MICONV_OK || (st = check_device()) != MICONV_OK)
         return st;
     (void)hipGetLastError();
 
@@ -836,7 +1029,7 @@ int conv_bwd_weight(int N, int C, int H, int W, int K, int R, int S, int stride,
     WgradArgs a;
     a.M = g.Kg;
     a.Ncol = g.Cg * R * S;
-    a.groups = group;
+    a.groups = g.G;
     a.dy_img_words = (uint32_t)yi;
     a.x_img_words = (uint32_t)xi;
     a.Cg = g.Cg;
@@ -844,8 +1037,8 @@ int conv_bwd_weight(int N, int C, int H, int W, int K, int R, int S, int stride,
     a.W = W;
     a.HW = H * W;
     a.PQ = g.P * g.Q;
-    a.stride = stride;
-    a.pad = pad;
+    a.stride = g.st;
+    a.pad = g.pad;
     a.pix_pq = make_fastdiv(g.P * g.Q);
     a.pix_q = make_fastdiv(g.Q);
     a.n_rs = make_fastdiv(R * S);
@@ -886,6 +1079,323 @@ int conv_bwd_weight(int N, int C, int H, int W, int K, int R, int S, int stride,
                                                        stream))) != MICONV_OK)
         return st;
     return MICONV_OK;
+}
+
+// Number, workspace, name and execution of candidate `index` of a pass.
+int candidate_count(int pass, const Geom &g)
+{
+    switch (pass) {
+    case MICONV_PASS_FWD: {
+        std::vector<ImgPlan> c;
+        fwd_candidates(g, c);
+        return (int)c.size();
+    }
+    case MICONV_PASS_BWD_DATA: {
+        std::vector<BwdPlan> c;
+        bwd_candidates(g, c);
+        return (int)c.size();
+    }
+    case MICONV_PASS_BWD_WEIGHT: {
+        std::vector<WgradPlan> c;
+        wgrad_candidates(g, c);
+        return (int)c.size();
+    }
+    default:
+        return MICONV_ERR_PASS;
+    }
+}
+
+size_t candidate_ws(int pass, const Geom &g, int index)
+{
+    switch (pass) {
+    case MICONV_PASS_FWD:
+        return fwd_ws(g, pick(fwd_rule(g), index, fwd_candidates, g));
+    case MICONV_PASS_BWD_DATA:
+        return bwd_ws(g, pick(bwd_rule(g), index, bwd_candidates, g));
+    case MICONV_PASS_BWD_WEIGHT:
+        return wgrad_ws(pick(wgrad_plan(g), index, wgrad_candidates, g));
+    default:
+        return 0;
+    }
+}
+
+// Tensors of conv_tune: fwd (x, w, b | y), bwd-data (dy, w, - | dx),
+// bwd-weight (x, dy, - | dw, db).
+struct TuneBuffers {
+    const float *in0, *in1, *in2;
+    float *out0, *out1;
+};
+
+int candidate_run(int pass, const Geom &g, int index, const TuneBuffers &t, void *ws,
+                  size_t ws_bytes, hipStream_t stream)
+{
+    switch (pass) {
+    case MICONV_PASS_FWD:
+        return fwd_exec(g, pick(fwd_rule(g), index, fwd_candidates, g), t.in0, t.in1, t.in2,
+                        t.out0, ws, ws_bytes, stream);
+    case MICONV_PASS_BWD_DATA:
+        return bwd_exec(g, pick(bwd_rule(g), index, bwd_candidates, g), t.in0, t.in1, t.out0, ws,
+                        ws_bytes, stream);
+    case MICONV_PASS_BWD_WEIGHT:
+        return wgrad_exec(g, pick(wgrad_plan(g), index, wgrad_candidates, g), t.in0, t.in1,
+                          t.out0, t.out1, ws, ws_bytes, stream);
+    default:
+        return MICONV_ERR_PASS;
+    }
+}
+
+}  // namespace
+}  // namespace miconv
+
+using namespace miconv;
+
+extern "C" {
+
+int conv_output_size(int H, int W, int R, int S, int stride, int pad, int *P, int *Q)
+{
+    if (!P || !Q)
+        return MICONV_ERR_NULL;
+    if (H < 1 || W < 1 || R < 1 || S < 1 || stride < 1 || pad < 0)
+        return MICONV_ERR_SHAPE;
+    int p = out_extent(H, R, stride, pad), q = out_extent(W, S, stride, pad);
+    if (p < 1 || q < 1)
+        return MICONV_ERR_SHAPE;
+    *P = p;
+    *Q = q;
+    return MICONV_OK;
+}
+
+size_t conv_workspace_size(int pass, int N, int C, int H, int W, int K, int R, int S,
+                           int stride, int pad, int group)
+{
+    Geom g;
+    if (make_geom(N, C, H, W, K, R, S, stride, pad, group, &g) != MICONV_OK)
+        return 0;
+    if (pass < MICONV_PASS_FWD || pass > MICONV_PASS_BWD_WEIGHT)
+        return 0;
+    return candidate_ws(pass, g, plan_index(pass, g));
+}
+
+int conv_set_timing_events(hipEvent_t before, hipEvent_t after)
+{
+    if ((before == nullptr) != (after == nullptr))
+        return MICONV_ERR_NULL;
+    tl_events.before = before;
+    tl_events.after = after;
+    return MICONV_OK;
+}
+
+const char *conv_error_string(int status)
+{
+    switch (status) {
+    case MICONV_OK: return "success";
+    case MICONV_ERR_SHAPE: return "invalid shape, stride, padding or group";
+    case MICONV_ERR_NULL: return "a required pointer is NULL";
+    case MICONV_ERR_WORKSPACE: return "workspace missing or smaller than conv_workspace_size()";
+    case MICONV_ERR_ALIAS: return "an output overlaps an input, another output or the workspace";
+    case MICONV_ERR_ALIGN: return "a tensor or workspace pointer is not 16-byte aligned";
+    case MICONV_ERR_DEVICE: return "no current HIP device, or it is not gfx950";
+    case MICONV_ERR_LAUNCH: return "kernel launch failed";
+    case MICONV_ERR_PASS: return "unknown pass id";
+    case MICONV_ERR_PLAN: return "plan index out of range";
+    default: return "unknown status";
+    }
+}
+
+int conv_fwd(int N, int C, int H, int W, int K, int R, int S, int stride, int pad, int group,
+             const float *x, const float *w, const float *b, float *y, void *ws, size_t ws_bytes,
+             hipStream_t stream)
+{
+    Geom g;
+    int st = make_geom(N, C, H, W, K, R, S, stride, pad, group, &g);
+    if (st != MICONV_OK)
+        return st;
+    return fwd_exec(g, fwd_current(g), x, w, b, y, ws, ws_bytes, stream);
+}
+
+int conv_bwd_data(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+                  int group, const float *dy, const float *w, float *dx, void *ws,
+                  size_t ws_bytes, hipStream_t stream)
+{
+    Geom g;
+    int st = make_geom(N, C, H, W, K, R, S, stride, pad, group, &g);
+    if (st != MICONV_OK)
+        return st;
+    return bwd_exec(g, bwd_current(g), dy, w, dx, ws, ws_bytes, stream);
+}
+
+int conv_bwd_weight(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+                    int group, const float *x, const float *dy, float *dw, float *db, void *ws,
+                    size_t ws_bytes, hipStream_t stream)
+{
+    Geom g;
+    int st = make_geom(N, C, H, W, K, R, S, stride, pad, group, &g);
+    if (st != MICONV_OK)
+        return st;
+    return wgrad_exec(g, wgrad_current(g), x, dy, dw, db, ws, ws_bytes, stream);
+}
+
+int conv_plan_count(int pass, int N, int C, int H, int W, int K, int R, int S, int stride,
+                    int pad, int group)
+{
+    Geom g;
+    int st = make_geom(N, C, H, W, K, R, S, stride, pad, group, &g);
+    return st != MICONV_OK ? st : candidate_count(pass, g);
+}
+
+int conv_plan_get(int pass, int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+                  int group)
+{
+    Geom g;
+    int st = make_geom(N, C, H, W, K, R, S, stride, pad, group, &g);
+    if (st != MICONV_OK)
+        return st;
+    if (pass < MICONV_PASS_FWD || pass > MICONV_PASS_BWD_WEIGHT)
+        return MICONV_ERR_PASS;
+    return plan_index(pass, g);
+}
+
+int conv_plan_set(int pass, int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+                  int group, int index)
+{
+    Geom g;
+    int st = make_geom(N, C, H, W, K, R, S, stride, pad, group, &g);
+    if (st != MICONV_OK)
+        return st;
+    const int n = candidate_count(pass, g);
+    if (n < 0)
+        return n;
+    if (index < 0 || index >= n)
+        return MICONV_ERR_PLAN;
+    plan_store(pass, g, index);
+    return MICONV_OK;
+}
+
+int conv_plan_clear(void)
+{
+    std::lock_guard<std::mutex> lock(g_plan_mu);
+    g_plans.clear();
+    g_plan_entries.store(0, std::memory_order_release);
+    return MICONV_OK;
+}
+
+int conv_plan_name(int pass, int N, int C, int H, int W, int K, int R, int S, int stride,
+                   int pad, int group, int index, char *buf, size_t len)
+{
+    Geom g;
+    int st = make_geom(N, C, H, W, K, R, S, stride, pad, group, &g);
+    if (st != MICONV_OK)
+        return st;
+    if (!buf || len == 0)
+        return MICONV_ERR_NULL;
+    const int n = candidate_count(pass, g);
+    if (n < 0)
+        return n;
+    if (index < 0 || index >= n)
+        return MICONV_ERR_PLAN;
+    switch (pass) {
+    case MICONV_PASS_FWD:
+        fwd_name(pick(fwd_rule(g), index, fwd_candidates, g), buf, len);
+        break;
+    case MICONV_PASS_BWD_DATA:
+        bwd_name(pick(bwd_rule(g), index, bwd_candidates, g), buf, len);
+        break;
+    default:
+        wgrad_name(pick(wgrad_plan(g), index, wgrad_candidates, g), buf, len);
+        break;
+    }
+    return MICONV_OK;
+}
+
+size_t conv_plan_workspace_size(int pass, int N, int C, int H, int W, int K, int R, int S,
+                                int stride, int pad, int group, int index)
+{
+    Geom g;
+    if (make_geom(N, C, H, W, K, R, S, stride, pad, group, &g) != MICONV_OK)
+        return 0;
+    const int n = candidate_count(pass, g);
+    if (n < 0 || index < 0 || index >= n)
+        return 0;
+    return candidate_ws(pass, g, index);
+}
+
+int conv_tune(int pass, int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
+              int group, const float *in0, const float *in1, const float *in2, float *out0,
+              float *out1, void *ws, size_t ws_bytes, int reps, hipStream_t stream,
+              int *chosen)
+{
+    Geom g;
+    int st = make_geom(N, C, H, W, K, R, S, stride, pad, group, &g);
+    if (st != MICONV_OK)
+        return st;
+    const int n = candidate_count(pass, g);
+    if (n < 0)
+        return n;
+    if (reps < 1)
+        reps = 1;
+    const TuneBuffers t{in0, in1, pass == MICONV_PASS_FWD ? in2 : nullptr, out0,
+                        pass == MICONV_PASS_BWD_WEIGHT ? out1 : nullptr};
+    // The pass's own timing events stay quiet while candidates run.
+    const TimingEvents saved = tl_events;
+    tl_events = TimingEvents{};
+    std::vector<int> fit;
+    for (int i = 0; i < n; i++)
+        if (candidate_ws(pass, g, i) <= ws_bytes)
+            fit.push_back(i);
+    std::vector<hipEvent_t> ev(2 * reps, nullptr);
+    for (auto &e : ev)
+        if (st == MICONV_OK && hipEventCreate(&e) != hipSuccess)
+            st = MICONV_ERR_LAUNCH;
+    // Every candidate runs once untimed (this also brings the clocks up),
+    // then two rounds in turn time each candidate's runs one by one; its
+    // score is the smaller of its two median times, so that neither the
+    // order of the candidates nor a stray slow run decides.
+    std::vector<float> score(n, 0.f);
+    for (int round = -1; round < 2 && st == MICONV_OK; round++)
+        for (int i : fit) {
+            if (round < 0) {
+                if ((st = candidate_run(pass, g, i, t, ws, ws_bytes, stream)) != MICONV_OK)
+                    break;
+                continue;
+            }
+            for (int r = 0; r < reps && st == MICONV_OK; r++) {
+                if (hipEventRecord(ev[2 * r], stream) != hipSuccess)
+                    st = MICONV_ERR_LAUNCH;
+                else if ((st = candidate_run(pass, g, i, t, ws, ws_bytes, stream)) == MICONV_OK &&
+                         hipEventRecord(ev[2 * r + 1], stream) != hipSuccess)
+                    st = MICONV_ERR_LAUNCH;
+            }
+            std::vector<float> ms(reps, 0.f);
+            for (int r = 0; r < reps && st == MICONV_OK; r++)
+                if (hipEventSynchronize(ev[2 * r + 1]) != hipSuccess ||
+                    hipEventElapsedTime(&ms[r], ev[2 * r], ev[2 * r + 1]) != hipSuccess)
+                    st = MICONV_ERR_LAUNCH;
+            if (st != MICONV_OK)
+                break;
+            std::sort(ms.begin(), ms.end());
+            const float med = ms[reps / 2];
+            score[i] = round == 0 ? med : std::min(score[i], med);
+        }
+    for (auto &e : ev)
+        if (e)
+            (void)hipEventDestroy(e);
+    tl_events = saved;
+    if (st != MICONV_OK)
+        return st;
+    if (fit.empty())
+        return MICONV_ERR_WORKSPACE;
+    int best = fit[0];
+    for (int i : fit)
+        if (score[i] < score[best])
+            best = i;
+    plan_store(pass, g, best);
+    if (chosen)
+        *chosen = best;
+    // Leave the chosen plan's results in the outputs.
+    tl_events = TimingEvents{};
+    st = candidate_run(pass, g, best, t, ws, ws_bytes, stream);
+    tl_events = saved;
+    return st;
 }
 
 }  // extern "C"

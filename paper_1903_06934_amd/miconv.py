@@ -18,6 +18,7 @@ STATUS = {
     0: "MICONV_OK", -1: "MICONV_ERR_SHAPE", -2: "MICONV_ERR_NULL",
     -3: "MICONV_ERR_WORKSPACE", -4: "MICONV_ERR_ALIAS", -5: "MICONV_ERR_ALIGN",
     -6: "MICONV_ERR_DEVICE", -7: "MICONV_ERR_LAUNCH", -8: "MICONV_ERR_PASS",
+    -9: "MICONV_ERR_PLAN",
 }
 PASS_FWD, PASS_BWD_DATA, PASS_BWD_WEIGHT = 0, 1, 2
 
@@ -41,6 +42,10 @@ def lib():
         return _lib
     if not os.path.exists(LIBRARY):
         raise RuntimeError(f"{LIBRARY} is not built; run paper_1903_06934_amd.build.build()")
+    # torch first: its HIP runtime (soname libamdhip64.so.7) then also serves
+    # the library's dependency.  Loaded the other way round, torch would load
+    # a second runtime of its own next to it.
+    import torch  # noqa: F401
     L = ctypes.CDLL(LIBRARY)
     geo = [_I] * 10
     L.conv_output_size.argtypes = [_I] * 6 + [ctypes.POINTER(_I), ctypes.POINTER(_I)]
@@ -57,6 +62,21 @@ def lib():
     L.conv_set_timing_events.restype = _I
     L.conv_error_string.argtypes = [_I]
     L.conv_error_string.restype = ctypes.c_char_p
+    L.conv_plan_count.argtypes = [_I] + geo
+    L.conv_plan_count.restype = _I
+    L.conv_plan_get.argtypes = [_I] + geo
+    L.conv_plan_get.restype = _I
+    L.conv_plan_set.argtypes = [_I] + geo + [_I]
+    L.conv_plan_set.restype = _I
+    L.conv_plan_clear.argtypes = []
+    L.conv_plan_clear.restype = _I
+    L.conv_plan_name.argtypes = [_I] + geo + [_I, ctypes.c_char_p, _Z]
+    L.conv_plan_name.restype = _I
+    L.conv_plan_workspace_size.argtypes = [_I] + geo + [_I]
+    L.conv_plan_workspace_size.restype = _Z
+    L.conv_tune.argtypes = [_I] + geo + [_P, _P, _P, _P, _P, _P, _Z, _I, _P,
+                                         ctypes.POINTER(_I)]
+    L.conv_tune.restype = _I
     _lib = L
     return L
 
@@ -159,3 +179,52 @@ def conv_bwd_weight(x, dy, filter_rs, stride=1, pad=0, group=1, with_bias=True,
     _call(lib().conv_bwd_weight, "conv_bwd_weight", *shape, _ptr(x), _ptr(dy), _ptr(dw),
           _ptr(db), _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(), _stream())
     return dw, db
+
+
+# ---------------------------------------------------------------- plans
+def _shape(shape):
+    return [int(v) for v in shape]
+
+
+def plan_count(pass_id, shape):
+    n = lib().conv_plan_count(pass_id, *_shape(shape))
+    if n < 0:
+        raise MiconvError(n, "conv_plan_count")
+    return n
+
+
+def plan_get(pass_id, shape):
+    i = lib().conv_plan_get(pass_id, *_shape(shape))
+    if i < 0:
+        raise MiconvError(i, "conv_plan_get")
+    return i
+
+
+def plan_set(pass_id, shape, index):
+    _call(lib().conv_plan_set, "conv_plan_set", pass_id, *_shape(shape), int(index))
+
+
+def plan_clear():
+    _call(lib().conv_plan_clear, "conv_plan_clear")
+
+
+def plan_name(pass_id, shape, index):
+    buf = ctypes.create_string_buffer(256)
+    _call(lib().conv_plan_name, "conv_plan_name", pass_id, *_shape(shape), int(index), buf,
+          len(buf))
+    return buf.value.decode()
+
+
+def plan_workspace_size(pass_id, shape, index):
+    return int(lib().conv_plan_workspace_size(pass_id, *_shape(shape), int(index)))
+
+
+def conv_tune(pass_id, shape, in0, in1, in2, out0, out1, ws, reps=3):
+    """Time the candidate plans of one pass on these tensors (see conv_tune in
+    miconv.h for which tensor is which) and keep the fastest; returns its index."""
+    chosen = _I(-1)
+    _call(lib().conv_tune, "conv_tune", pass_id, *_shape(shape), _ptr(in0), _ptr(in1),
+          _ptr(in2), _ptr(out0), _ptr(out1), _ptr(ws),
+          0 if ws is None else ws.numel() * ws.element_size(), int(reps), _stream(),
+          ctypes.byref(chosen))
+    return chosen.value

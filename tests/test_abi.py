@@ -35,7 +35,9 @@ def test_exports_every_declared_function(L):
     names = declared_functions()
     assert set(names) == {"conv_output_size", "conv_workspace_size", "conv_fwd",
                           "conv_bwd_data", "conv_bwd_weight", "conv_error_string",
-                          "conv_set_timing_events"}
+                          "conv_set_timing_events", "conv_plan_count", "conv_plan_get",
+                          "conv_plan_set", "conv_plan_clear", "conv_plan_name",
+                          "conv_plan_workspace_size", "conv_tune"}
     for n in names:
         assert hasattr(L, n), n
 
@@ -67,7 +69,7 @@ def test_timing_events_arguments(L):
 
 
 def test_error_strings(L):
-    for s in range(-8, 1):
+    for s in range(-9, 1):
         assert L.conv_error_string(s)
     assert L.conv_error_string(12345) == b"unknown status"
 

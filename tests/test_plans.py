@@ -1,0 +1,92 @@
+"""Plan selection on the host (no GPU): candidate lists, names, the rule as
+candidate 0, storing and clearing a choice, per-candidate workspace sizes and
+argument errors."""
+import pytest
+
+import paper_1903_06934_amd as m
+import workloads
+
+PASSES = (m.PASS_FWD, m.PASS_BWD_DATA, m.PASS_BWD_WEIGHT)
+SHAPE_ERR, NULL_ERR, PASS_ERR, PLAN_ERR = -1, -2, -8, -9
+
+
+def _layers():
+    out = []
+    for cfg in (0, 1, 2, 3, 4):
+        name, layers = workloads.config(cfg)
+        out += [pytest.param(L.shape, id=f"{name}-{L.name}") for L in layers]
+    return out
+
+
+@pytest.fixture(autouse=True)
+def _clean():
+    m.plan_clear()
+    yield
+    m.plan_clear()
+
+
+@pytest.mark.parametrize("shape", _layers())
+def test_candidates_are_distinct_and_rule_first(shape):
+    for p in PASSES:
+        n = m.plan_count(p, shape)
+        assert n >= 1
+        names = [m.plan_name(p, shape, i) for i in range(n)]
+        assert len(set(names)) == n, names
+        assert m.plan_get(p, shape) == 0
+        assert m.plan_workspace_size(p, shape, 0) == m.workspace_size(p, shape)
+
+
+def test_rule_names_for_alexnet():
+    """The built-in rule on the AlexNet-shaped stack (batch 128)."""
+    _, layers = workloads.config(1)
+    by = {L.name: L.shape for L in layers}
+    assert m.plan_name(m.PASS_BWD_DATA, by["conv1"], 0) == \
+        "blocked 4x4 pixels (f=1), image GEMM 48x64"
+    assert m.plan_name(m.PASS_BWD_DATA, by["conv2"], 0) == "stride phases, image GEMM 48x64"
+    assert m.plan_name(m.PASS_FWD, by["conv1"], 0) == "image GEMM 96x128"
+    assert m.plan_name(m.PASS_BWD_WEIGHT, by["conv2"], 0).startswith("tap 64x48, ")
+    assert m.plan_name(m.PASS_BWD_WEIGHT, by["conv1"], 0).startswith("pixel 96x64, ")
+
+
+def test_set_get_clear_and_workspace():
+    shape = (8, 3, 67, 67, 32, 11, 11, 4, 2, 1)
+    n = m.plan_count(m.PASS_BWD_DATA, shape)
+    assert n > 2
+    m.plan_set(m.PASS_BWD_DATA, shape, n - 1)
+    assert m.plan_get(m.PASS_BWD_DATA, shape) == n - 1
+    assert m.plan_get(m.PASS_FWD, shape) == 0  # per pass
+    assert m.workspace_size(m.PASS_BWD_DATA, shape) == \
+        m.plan_workspace_size(m.PASS_BWD_DATA, shape, n - 1)
+    m.plan_set(m.PASS_BWD_DATA, shape, 0)
+    assert m.plan_get(m.PASS_BWD_DATA, shape) == 0
+    m.plan_set(m.PASS_BWD_DATA, shape, 1)
+    m.plan_clear()
+    assert m.plan_get(m.PASS_BWD_DATA, shape) == 0
+
+
+def test_split_candidates_grow_the_workspace():
+    """A split plan's partial sums are in the workspace; the rule here does
+    not split (the grid is large), a split candidate does."""
+    shape = (2, 64, 12, 12, 32, 5, 5, 1, 2, 1)
+    n = m.plan_count(m.PASS_FWD, shape)
+    names = [m.plan_name(m.PASS_FWD, shape, i) for i in range(n)]
+    split = [i for i, s in enumerate(names) if "splits" in s]
+    assert split, names
+    for i in split:
+        assert m.plan_workspace_size(m.PASS_FWD, shape, i) > m.workspace_size(m.PASS_FWD, shape)
+
+
+def test_plan_errors():
+    good = (2, 16, 32, 32, 32, 3, 3, 1, 1, 1)
+    bad = (2, 15, 32, 32, 32, 3, 3, 1, 1, 2)
+    L = m.lib()
+    assert L.conv_plan_count(7, *good) == PASS_ERR
+    assert L.conv_plan_count(0, *bad) == SHAPE_ERR
+    assert L.conv_plan_get(3, *good) == PASS_ERR
+    n = m.plan_count(0, good)
+    assert L.conv_plan_set(0, *good, n) == PLAN_ERR
+    assert L.conv_plan_set(0, *good, -1) == PLAN_ERR
+    assert L.conv_plan_name(0, *good, 0, None, 16) == NULL_ERR
+    assert L.conv_plan_name(0, *good, n, b"x" * 8, 8) == PLAN_ERR
+    assert L.conv_plan_workspace_size(0, *good, n) == 0
+    assert m.plan_get(0, good) == 0
