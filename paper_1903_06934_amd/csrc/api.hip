@@ -269,6 +269,7 @@ constexpr int kSplitRows = 768;
 
 struct ImgPlan {
     int tile, nsplit, kchunk;  // tile -1: (backward-data phases) each phase by the rule
+    int xnb = 0;               // forward: explicit plan, images per column chunk (0: implicit)
 };
 
 // Splits for `tiles` workgroups over Kred rows: about 8 workgroups per CU,
@@ -306,7 +307,50 @@ ImgPlan img_rule(int M, long long Ncol, int Kred, int G, bool allow_split)
 
 bool same_img(const ImgPlan &a, const ImgPlan &b)
 {
-    return a.tile == b.tile && a.nsplit == b.nsplit;
+    return a.tile == b.tile && a.nsplit == b.nsplit && a.xnb == b.xnb;
+}
+
+// ------------------------------------------------------------ explicit plan
+// The paper's explicit strategy (Sec. IV-B): im2col (forward, backward-weight)
+// or col2im (backward-data) through HBM around a plain GEMM -- here the 1x1
+// stride-1 convolution over the column tensor, run by the same kernels.  The
+// column tensor is built for chunks of images within kExplicitColElems.
+constexpr long long kExplicitColElems = 64LL << 20;  // 256 MB of fp32
+
+// The 1x1 stride-1 problem over the column tensor of n images: channels
+// c' = (c R + r) S + s (C R S of them, grouped as the input's), map P x Q.
+Geom one_by_one(const Geom &g, int n)
+{
+    const int crs = g.Cg * g.R * g.S;
+    return Geom{n, g.G * crs, g.P, g.Q, g.K, 1, 1, 1, 0, g.G, g.P, g.Q, crs, g.Kg};
+}
+
+long long col_elems_per_image(const Geom &g) { return (long long)g.C * g.R * g.S * g.P * g.Q; }
+
+// Images per column chunk, or 0 where the explicit plan does not apply: a 1x1
+// stride-1 layer without padding (its columns are its input), or one image's
+// columns (or the packed filters of the transposed GEMM) beyond the limits.
+int explicit_images(const Geom &g)
+{
+    if (g.R == 1 && g.S == 1 && g.st == 1 && g.pad == 0)
+        return 0;
+    const long long col1 = col_elems_per_image(g);
+    if (col1 > kExplicitColElems || (long long)g.C * g.R * g.S * pad16(g.Kg) > kMaxChunkElems)
+        return 0;
+    long long n = kExplicitColElems / col1;
+    const long long x1 = (long long)g.C * g.H * g.W, y1 = (long long)g.K * g.P * g.Q;
+    if (n * x1 > kMaxChunkElems)
+        n = kMaxChunkElems / x1;
+    if (n * y1 > kMaxChunkElems)
+        n = kMaxChunkElems / y1;
+    if (n > g.N)
+        n = g.N;
+    return (int)n;
+}
+
+size_t col_bytes(const Geom &g, int xnb)
+{
+    return align_up((size_t)xnb * col_elems_per_image(g) * sizeof(float));
 }
 
 bool same_plan(const ImgPlan &a, const ImgPlan &b) { return same_img(a, b); }
@@ -356,10 +400,19 @@ void fwd_candidates(const Geom &g, std::vector<ImgPlan> &out)
     const int nb = images_per_launch(g);
     img_variants<ImgPlan>(g.Kg, (long long)(g.N < nb ? g.N : nb) * g.P * g.Q, g.Cg * g.R * g.S,
                           g.G, nb >= g.N, [](const ImgPlan &p) { return p; }, out);
+    // Explicit: im2col, then the 1x1 GEMM with its own rule's tile.
+    if (const int xnb = explicit_images(g)) {
+        const int kred = g.Cg * g.R * g.S;
+        ImgPlan e = with_split(pick_img_tile(g.Kg, (long long)xnb * g.P * g.Q, kred, g.G), kred, 1);
+        e.xnb = xnb;
+        out.push_back(e);
+    }
 }
 
 size_t fwd_ws(const Geom &g, const ImgPlan &p)
 {
+    if (p.xnb > 0)
+        return fwd_pack_bytes(g) + col_bytes(g, p.xnb);
     size_t part = p.nsplit > 1 ? align_up((size_t)p.nsplit * g.N * g.K * g.P * g.Q * sizeof(float))
                                : 0;
     return fwd_pack_bytes(g) + part;
@@ -367,7 +420,10 @@ size_t fwd_ws(const Geom &g, const ImgPlan &p)
 
 void fwd_name(const ImgPlan &p, char *buf, size_t len)
 {
-    if (p.nsplit > 1)
+    if (p.xnb > 0)
+        snprintf(buf, len, "explicit im2col (%d images a chunk), image GEMM %s", p.xnb,
+                 img_tile_name(p.tile));
+    else if (p.nsplit > 1)
         snprintf(buf, len, "image GEMM %s, %d splits", img_tile_name(p.tile), p.nsplit);
     else
         snprintf(buf, len, "image GEMM %s", img_tile_name(p.tile));
@@ -472,13 +528,15 @@ bool block_rule(const Geom &g, BlockPlan *out)
 struct BwdPlan {
     bool blocked;
     BlockPlan bp;  // blocked only
-    ImgPlan img;   // blocked: the GEMM's tile; phases: tile (-1: per phase by the rule) and
-                   // split-K (stride 1 only)
+    ImgPlan img;   // blocked, explicit: the GEMM's tile; phases: tile (-1: per phase by the
+                   // rule) and split-K (stride 1 only)
+    int xnb;       // explicit plan: images per column chunk (0: not explicit)
 };
 
 bool same_plan(const BwdPlan &a, const BwdPlan &b)
 {
-    return a.blocked == b.blocked && (!a.blocked || a.bp.f == b.bp.f) && same_img(a.img, b.img);
+    return a.blocked == b.blocked && (!a.blocked || a.bp.f == b.bp.f) && a.xnb == b.xnb &&
+           same_img(a.img, b.img);
 }
 
 BwdPlan bwd_rule(const Geom &g)
@@ -508,7 +566,7 @@ void bwd_candidates(const Geom &g, std::vector<BwdPlan> &out)
     const int kred_max = g.Kg * ((g.R + g.st - 1) / g.st) * ((g.S + g.st - 1) / g.st);
     img_variants<BwdPlan>(g.Cg, (long long)n0 * g.H * g.W / (g.st * g.st), kred_max, g.G,
                           g.st == 1 && nb >= g.N,
-                          [](const ImgPlan &i) { return BwdPlan{false, BlockPlan{}, i}; }, out);
+                          [](const ImgPlan &i) { return BwdPlan{false, BlockPlan{}, i, 0}; }, out);
     // Blocked, for few channels per group.
     if (g.Cg <= 16)
         for (int f = 1; f <= 8; f++) {
@@ -517,12 +575,23 @@ void bwd_candidates(const Geom &g, std::vector<BwdPlan> &out)
                 continue;
             const int kred = g.Kg * bp.ntr * bp.nts;
             img_variants<BwdPlan>(bp.M, (long long)n0 * bp.nh * bp.nw, kred, g.G, false,
-                                  [&](const ImgPlan &i) { return BwdPlan{true, bp, i}; }, out);
+                                  [&](const ImgPlan &i) { return BwdPlan{true, bp, i, 0}; }, out);
         }
+    // Explicit: the transposed 1x1 GEMM into the column tensor, then col2im.
+    if (const int xnb = explicit_images(g)) {
+        const int crs = g.Cg * g.R * g.S;
+        BwdPlan e{};
+        e.xnb = xnb;
+        e.img = with_split(pick_img_tile(crs, (long long)xnb * g.P * g.Q, g.Kg, g.G), g.Kg, 1);
+        out.push_back(e);
+    }
 }
 
 size_t bwd_ws(const Geom &g, const BwdPlan &p)
 {
+    if (p.xnb > 0)
+        return align_up((size_t)g.C * g.R * g.S * pad16(g.Kg) * sizeof(float)) +
+               col_bytes(g, p.xnb);
     if (p.blocked)
         return align_up((size_t)g.G * p.bp.M * p.bp.a_ld * sizeof(float));
     size_t total = 0;
@@ -539,7 +608,10 @@ size_t bwd_ws(const Geom &g, const BwdPlan &p)
 
 void bwd_name(const BwdPlan &p, char *buf, size_t len)
 {
-    if (p.blocked)
+    if (p.xnb > 0)
+        snprintf(buf, len, "explicit GEMM + col2im (%d images a chunk), image GEMM %s", p.xnb,
+                 img_tile_name(p.img.tile));
+    else if (p.blocked)
         snprintf(buf, len, "blocked %dx%d pixels (f=%d), image GEMM %s", p.bp.b, p.bp.b, p.bp.f,
                  img_tile_name(p.img.tile));
     else if (p.img.tile < 0)
@@ -560,6 +632,7 @@ struct WgradPlan {
     int tile, slice, chunk, nsplit, nb;
     bool via_part;
     size_t part_bytes, bias_bytes;
+    int xnb;  // explicit plan: images per column chunk (0: implicit); nb = xnb then
 };
 
 bool is_tap_tile(int tile) { return tile <= WG_TAP_64x16; }
@@ -579,9 +652,10 @@ const char *wgrad_tile_name(int tile)
 }
 
 // tile -1: the rule's tile.  scale: the rule's split count times 2^scale.
-WgradPlan wgrad_plan(const Geom &g, int tile = -1, int scale = 0)
+// nb > 0: launches of nb images (else images_per_launch).
+WgradPlan wgrad_plan(const Geom &g, int tile = -1, int scale = 0, int nb = 0)
 {
-    WgradPlan p;
+    WgradPlan p{};
     int M = g.Kg, Ncol = g.Cg * g.R * g.S;
     long long PQ = (long long)g.P * g.Q, Kred = (long long)g.N * PQ;
     if (tile < 0) {
@@ -626,7 +700,7 @@ WgradPlan wgrad_plan(const Geom &g, int tile = -1, int scale = 0)
     long long chunk = (Kred + ns - 1) / ns;
     chunk = (chunk + p.slice - 1) / p.slice * p.slice;
     p.chunk = (int)chunk;
-    p.nb = images_per_launch(g);
+    p.nb = nb > 0 ? nb : images_per_launch(g);
     long long total = 0;
     for (int n0 = 0; n0 < g.N; n0 += p.nb) {
         long long n = g.N - n0 < p.nb ? g.N - n0 : p.nb;
@@ -650,17 +724,31 @@ void wgrad_candidates(const Geom &g, std::vector<WgradPlan> &out)
             WgradPlan p = wgrad_plan(g, t, scale);
             bool dup = false;
             for (const WgradPlan &q : out)
-                dup = dup || (q.tile == p.tile && q.chunk == p.chunk);
+                dup = dup || (q.tile == p.tile && q.chunk == p.chunk && q.xnb == 0);
             if (!dup)
                 out.push_back(p);
         }
+    // Explicit: im2col, then the 1x1 problem over the columns by its own rule.
+    if (const int xnb = explicit_images(g)) {
+        WgradPlan e = wgrad_plan(one_by_one(g, g.N), -1, 0, xnb);
+        e.xnb = xnb;
+        out.push_back(e);
+    }
 }
 
-size_t wgrad_ws(const WgradPlan &p) { return p.part_bytes + p.bias_bytes; }
+size_t wgrad_ws(const Geom &g, const WgradPlan &p)
+{
+    return p.part_bytes + p.bias_bytes + (p.xnb > 0 ? col_bytes(g, p.xnb) : 0);
+}
 
 void wgrad_name(const WgradPlan &p, char *buf, size_t len)
 {
-    snprintf(buf, len, "%s, %d splits of %d pixels", wgrad_tile_name(p.tile), p.nsplit, p.chunk);
+    if (p.xnb > 0)
+        snprintf(buf, len, "explicit im2col (%d images a chunk), %s, %d splits of %d pixels",
+                 p.xnb, wgrad_tile_name(p.tile), p.nsplit, p.chunk);
+    else
+        snprintf(buf, len, "%s, %d splits of %d pixels", wgrad_tile_name(p.tile), p.nsplit,
+                 p.chunk);
 }
 
 // ------------------------------------------------------------ plan cache
@@ -773,6 +861,59 @@ hipError_t mark(hipEvent_t ev, hipStream_t stream)
     return ev ? hipEventRecord(ev, stream) : hipSuccess;
 }
 
+// Forward GEMM launches over n images of geometry g (images from src, outputs
+// to y), at most images_per_launch(g) images a launch; wp is the packed
+// filter bank, part the split-K slabs (plan.nsplit > 1: n must be all of g's).
+int fwd_gemms(const Geom &g, const ImgPlan &plan, const float *wp, const float *src,
+              const float *b, float *y, float *part, int n_images, hipStream_t stream)
+{
+    const size_t fb = sizeof(float);
+    const int a_ld = pad16(g.Cg * g.R * g.S);
+    const int nb = images_per_launch(g);
+    const long long xi = (long long)g.C * g.H * g.W, yi = (long long)g.K * g.P * g.Q;
+    ImgGemmArgs a{};
+    a.M = g.Kg;
+    a.Kred = g.Cg * g.R * g.S;
+    a.groups = g.G;
+    a.A = wp;
+    a.a_ld = a_ld;
+    a.a_bytes = (uint32_t)((size_t)g.K * a_ld * fb);
+    a.cin = g.Cg;
+    a.src_h = g.H;
+    a.src_w = g.W;
+    a.src_hw = g.H * g.W;
+    a.src_img_words = (uint32_t)xi;
+    a.col_hw = make_fastdiv(g.P * g.Q);
+    a.col_w = make_fastdiv(g.Q);
+    a.cstep = g.st;
+    a.coff_h = -g.pad;
+    a.coff_w = -g.pad;
+    a.tsign = 1;
+    a.k_cin = make_fastdiv(g.Cg);
+    a.k_tw = make_fastdiv(g.S);
+    a.k_taps = make_fastdiv(g.R * g.S);
+    a.bias = b;
+    a.out_img_stride = yi;
+    a.out_hw = g.P * g.Q;
+    a.out_w = g.Q;
+    a.ostep = 1;
+    const bool fast = g.Cg % kBK == 0;
+    for (int n0 = 0; n0 < n_images; n0 += nb) {
+        const int n = n_images - n0 < nb ? n_images - n0 : nb;
+        a.Ncol = n * g.P * g.Q;
+        a.src = src + n0 * xi;
+        a.src_bytes = (uint32_t)(n * xi * (long long)fb);
+        a.out = plan.nsplit > 1 ? part : y + n0 * yi;
+        a.nsplit = plan.nsplit;
+        a.kchunk = plan.kchunk;
+        a.split_stride = (long long)n_images * yi;
+        int st = launch_status(launch_img_gemm(a, plan.tile, fast, stream));
+        if (st != MICONV_OK)
+            return st;
+    }
+    return MICONV_OK;
+}
+
 int fwd_exec(const Geom &g, const ImgPlan &plan, const float *x, const float *w, const float *b,
              float *y, void *ws, size_t ws_bytes, hipStream_t stream)
 {
@@ -788,64 +929,41 @@ int fwd_exec(const Geom &g, const ImgPlan &plan, const float *x, const float *w,
         return st;
     (void)hipGetLastError();
 
+    // The filter bank, packed in the layout the tile reads.  The explicit
+    // plan's 1x1 GEMM reads the same matrix: its reduction index is the
+    // column tensor's channel (c R + r) S + s, the filter's own order.
     float *wp = (float *)ws;
-    const int a_ld = pad16(g.Cg * R * S);
-    // The filter layout follows the tile, which every launch of the call shares.
-    const bool kmajor = img_tile_shares_a(plan.tile);
-    if (launch_pack_fwd(w, wp, K, g.Cg, R, S, g.G, g.Cg % kBK == 0, a_ld, kmajor, stream) !=
-        hipSuccess)
+    const Geom g1 = one_by_one(g, N);
+    const Geom &gp = plan.xnb > 0 ? g1 : g;
+    if (launch_pack_fwd(w, wp, K, gp.Cg, gp.R, gp.S, g.G, gp.Cg % kBK == 0,
+                        pad16(g.Cg * R * S), img_tile_shares_a(plan.tile), stream) != hipSuccess)
         return MICONV_ERR_LAUNCH;
-
-    const int nb = images_per_launch(g);
-    const long long xi = (long long)C * H * W, yi = (long long)K * g.P * g.Q;
-    ImgGemmArgs a{};
-    a.M = g.Kg;
-    a.Kred = g.Cg * R * S;
-    a.groups = g.G;
-    a.A = wp;
-    a.a_ld = a_ld;
-    a.a_bytes = (uint32_t)((size_t)K * a_ld * fb);
-    a.cin = g.Cg;
-    a.src_h = H;
-    a.src_w = W;
-    a.src_hw = H * W;
-    a.src_img_words = (uint32_t)xi;
-    a.col_hw = make_fastdiv(g.P * g.Q);
-    a.col_w = make_fastdiv(g.Q);
-    a.cstep = g.st;
-    a.coff_h = -g.pad;
-    a.coff_w = -g.pad;
-    a.tsign = 1;
-    a.k_cin = make_fastdiv(g.Cg);
-    a.k_tw = make_fastdiv(S);
-    a.k_taps = make_fastdiv(R * S);
-    a.bias = b;
-    a.out_img_stride = yi;
-    a.out_hw = g.P * g.Q;
-    a.out_w = g.Q;
-    a.ostep = 1;
-    const bool fast = g.Cg % kBK == 0;
-    float *part = (float *)((char *)ws + fwd_pack_bytes(g));
+    float *tail = (float *)((char *)ws + fwd_pack_bytes(g));
     if (mark(tl_events.before, stream) != hipSuccess)
         return MICONV_ERR_LAUNCH;
-    for (int n0 = 0; n0 < N; n0 += nb) {
-        const int n = N - n0 < nb ? N - n0 : nb;
-        a.Ncol = n * g.P * g.Q;
-        a.src = x + n0 * xi;
-        a.src_bytes = (uint32_t)(n * xi * (long long)fb);
-        a.out = plan.nsplit > 1 ? part : y + n0 * yi;
-        a.nsplit = plan.nsplit;
-        a.kchunk = plan.kchunk;
-        a.split_stride = (long long)N * yi;
-        if ((st = launch_status(launch_img_gemm(a, plan.tile, fast, stream))) != MICONV_OK)
-            return st;
+    if (plan.xnb > 0) {
+        // Explicit: im2col of a chunk of images, then the 1x1 GEMM over it.
+        const long long xi = (long long)C * H * W, yi = (long long)K * g.P * g.Q;
+        for (int n0 = 0; n0 < N; n0 += plan.xnb) {
+            const int n = N - n0 < plan.xnb ? N - n0 : plan.xnb;
+            if (launch_im2col(x + n0 * xi, tail, n, C, H, W, R, S, g.st, g.pad, g.P, g.Q,
+                              stream) != hipSuccess)
+                return MICONV_ERR_LAUNCH;
+            if ((st = fwd_gemms(one_by_one(g, n), plan, wp, tail, b, y + n0 * yi, nullptr, n,
+                                stream)) != MICONV_OK)
+                return st;
+        }
+    } else if ((st = fwd_gemms(g, plan, wp, x, b, y, tail, N, stream)) != MICONV_OK) {
+        return st;
     }
     if (mark(tl_events.after, stream) != hipSuccess)
         return MICONV_ERR_LAUNCH;
-    if (plan.nsplit > 1)
-        return launch_status(launch_splitk_bias_reduce(part, plan.nsplit, (long long)N * yi,
+    if (plan.nsplit > 1) {
+        const long long yi = (long long)K * g.P * g.Q;
+        return launch_status(launch_splitk_bias_reduce(tail, plan.nsplit, (long long)N * yi,
                                                        (int)(N * yi), b, g.P * g.Q, K, y,
                                                        stream));
+    }
     return MICONV_OK;
 }
 
@@ -914,43 +1032,45 @@ int bwd_blocked(const Geom &g, const BwdPlan &plan, const float *dy, const float
     return mark(tl_events.after, stream) == hipSuccess ? MICONV_OK : MICONV_ERR_LAUNCH;
 }
 
-int bwd_exec(const Geom &g, const BwdPlan &plan, const float *dy, const float *w, float *dx,
-             void *ws, size_t ws_bytes, hipStream_t stream)
+// Backward-data by stride phases over n images of geometry g (dy from dy,
+// dx to dx): each phase packs its filter taps into wsp (advancing it past
+// every phase's bank) and runs its GEMM; with split-K (stride 1, all images)
+// the slabs follow the banks and the caller reduces them.  *marked tells
+// whether the first GEMM's timing event has been recorded.
+int phase_gemms(const Geom &g, const BwdPlan &plan, const float *w, char *&wsp, const float *dy,
+                float *dx, int n_images, bool *marked, hipStream_t stream)
 {
-    const int N = g.N, C = g.C, H = g.H, W = g.W, K = g.K, R = g.R, S = g.S;
-    const int stride = g.st, group = g.G;
+    const int H = g.H, W = g.W, K = g.K, R = g.R, S = g.S, stride = g.st, group = g.G;
     const size_t fb = sizeof(float);
-    Range r[3] = {{dy, (size_t)N * K * g.P * g.Q * fb, false},
-                  {w, (size_t)K * g.Cg * R * S * fb, false},
-                  {dx, (size_t)N * C * H * W * fb, true}};
-    bool req[3] = {true, true, true};
-    int st = check_buffers(r, 3, req, ws, ws_bytes, bwd_ws(g, plan));
-    if (st != MICONV_OK || (st = check_device()) != MICONV_OK)
-        return st;
-    (void)hipGetLastError();
-    if (plan.blocked)
-        return bwd_blocked(g, plan, dy, w, dx, ws, stream);
-
     const int nb = images_per_launch(g);
-    const long long xi = (long long)C * H * W, yi = (long long)K * g.P * g.Q;
-    const bool split = plan.img.nsplit > 1;  // stride 1 only
-    char *wsp = (char *)ws;
-    bool marked = false;
+    const long long xi = (long long)g.C * H * W, yi = (long long)K * g.P * g.Q;
+    const bool split = plan.img.nsplit > 1;
+    char *banks = wsp;
+    size_t bank_bytes = 0;
+    for (int ph = 0; ph < stride; ph++)
+        for (int pw = 0; pw < stride; pw++) {
+            Axis ah = phase_axis(H, R, stride, g.pad, ph);
+            Axis aw = phase_axis(W, S, stride, g.pad, pw);
+            bank_bytes += align_up((size_t)g.C * pad16(g.Kg * ah.nt * aw.nt) * fb);
+        }
+    float *part = (float *)(banks + bank_bytes);
+    wsp = banks + bank_bytes;
+    char *bank = banks;
     for (int ph = 0; ph < stride; ph++)
         for (int pw = 0; pw < stride; pw++) {
             Axis ah = phase_axis(H, R, stride, g.pad, ph);
             Axis aw = phase_axis(W, S, stride, g.pad, pw);
             const int a_ld = pad16(g.Kg * ah.nt * aw.nt);
-            size_t bytes = align_up((size_t)C * a_ld * fb);
-            float *wr = (float *)wsp;
-            wsp += bytes;
+            float *wr = (float *)bank;
+            bank += align_up((size_t)g.C * a_ld * fb);
             if (ah.n == 0 || aw.n == 0)
                 continue;
             const int kred = ah.nt * aw.nt * g.Kg;
-            const int tile = plan.img.tile >= 0
-                                 ? plan.img.tile
-                                 : pick_img_tile(g.Cg, (long long)(N < nb ? N : nb) * ah.n * aw.n,
-                                                 kred, group);
+            const int tile =
+                plan.img.tile >= 0
+                    ? plan.img.tile
+                    : pick_img_tile(g.Cg, (long long)(n_images < nb ? n_images : nb) * ah.n * aw.n,
+                                    kred, group);
             const bool kmajor = img_tile_shares_a(tile);
             if (launch_pack_bwd_phase(w, wr, K, g.Cg, R, S, group, ah.t0, aw.t0, ah.nt, aw.nt,
                                       stride, g.Kg % kBK == 0, a_ld, kmajor, stream) !=
@@ -962,7 +1082,7 @@ int bwd_exec(const Geom &g, const BwdPlan &plan, const float *dy, const float *w
             a.groups = group;
             a.A = wr;
             a.a_ld = a_ld;
-            a.a_bytes = (uint32_t)((size_t)C * a_ld * fb);
+            a.a_bytes = (uint32_t)((size_t)g.C * a_ld * fb);
             a.cin = g.Kg;
             a.src_h = g.P;
             a.src_w = g.Q;
@@ -985,28 +1105,116 @@ int bwd_exec(const Geom &g, const BwdPlan &plan, const float *dy, const float *w
             a.ooff_h = ph;
             a.ooff_w = pw;
             const bool fast = g.Kg % kBK == 0;
-            if (!marked && mark(tl_events.before, stream) != hipSuccess)
+            if (!*marked && mark(tl_events.before, stream) != hipSuccess)
                 return MICONV_ERR_LAUNCH;
-            marked = true;
-            for (int n0 = 0; n0 < N; n0 += nb) {
-                const int n = N - n0 < nb ? N - n0 : nb;
+            *marked = true;
+            for (int n0 = 0; n0 < n_images; n0 += nb) {
+                const int n = n_images - n0 < nb ? n_images - n0 : nb;
                 a.Ncol = n * ah.n * aw.n;
                 a.src = dy + n0 * yi;
                 a.src_bytes = (uint32_t)(n * yi * (long long)fb);
-                a.out = split ? (float *)wsp : dx + n0 * xi;
+                a.out = split ? part : dx + n0 * xi;
                 a.nsplit = plan.img.nsplit;
                 a.kchunk = split ? plan.img.kchunk : a.Kred;
-                a.split_stride = (long long)N * xi;
-                if ((st = launch_status(launch_img_gemm(a, tile, fast, stream))) != MICONV_OK)
+                a.split_stride = (long long)n_images * xi;
+                int st = launch_status(launch_img_gemm(a, tile, fast, stream));
+                if (st != MICONV_OK)
                     return st;
             }
         }
+    return MICONV_OK;
+}
+
+int bwd_exec(const Geom &g, const BwdPlan &plan, const float *dy, const float *w, float *dx,
+             void *ws, size_t ws_bytes, hipStream_t stream)
+{
+    const int N = g.N, C = g.C, H = g.H, W = g.W, K = g.K, R = g.R, S = g.S;
+    const size_t fb = sizeof(float);
+    Range r[3] = {{dy, (size_t)N * K * g.P * g.Q * fb, false},
+                  {w, (size_t)K * g.Cg * R * S * fb, false},
+                  {dx, (size_t)N * C * H * W * fb, true}};
+    bool req[3] = {true, true, true};
+    int st = check_buffers(r, 3, req, ws, ws_bytes, bwd_ws(g, plan));
+    if (st != MICONV_OK || (st = check_device()) != MICONV_OK)
+        return st;
+    (void)hipGetLastError();
+    if (plan.blocked)
+        return bwd_blocked(g, plan, dy, w, dx, ws, stream);
+
+    const long long xi = (long long)C * H * W, yi = (long long)K * g.P * g.Q;
+    bool marked = false;
+    if (plan.xnb > 0) {
+        // Explicit: per chunk of images, the transposed 1x1 GEMM writes the
+        // column tensor (the backward-data of the 1x1 problem), then col2im.
+        float *col = (float *)((char *)ws + align_up((size_t)C * R * S * pad16(g.Kg) * fb));
+        for (int n0 = 0; n0 < N; n0 += plan.xnb) {
+            const int n = N - n0 < plan.xnb ? N - n0 : plan.xnb;
+            char *wsp = (char *)ws;
+            if ((st = phase_gemms(one_by_one(g, n), plan, w, wsp, dy + n0 * yi, col, n, &marked,
+                                  stream)) != MICONV_OK)
+                return st;
+            if (launch_col2im(col, dx + n0 * xi, n, C, H, W, R, S, g.st, g.pad, g.P, g.Q,
+                              stream) != hipSuccess)
+                return MICONV_ERR_LAUNCH;
+        }
+        return mark(tl_events.after, stream) == hipSuccess ? MICONV_OK : MICONV_ERR_LAUNCH;
+    }
+    char *wsp = (char *)ws;
+    if ((st = phase_gemms(g, plan, w, wsp, dy, dx, N, &marked, stream)) != MICONV_OK)
+        return st;
     if (mark(tl_events.after, stream) != hipSuccess)
         return MICONV_ERR_LAUNCH;
-    if (split)
+    if (plan.img.nsplit > 1)  // stride 1 only
         return launch_status(launch_splitk_bias_reduce((float *)wsp, plan.img.nsplit,
                                                        (long long)N * xi, (int)(N * xi),
                                                        nullptr, 1, 1, dx, stream));
+    return MICONV_OK;
+}
+
+// Backward-weight launches over n images of geometry g (x from x, dy from
+// dy), writing splits [split0, ...) of the partial sums; returns the status
+// and advances split0.
+int wgrad_launches(const Geom &g, const WgradPlan &p, const float *x, const float *dy, float *dw,
+                   bool with_db, float *part, float *db_part, int n_images, int &split0,
+                   hipStream_t stream)
+{
+    const size_t fb = sizeof(float);
+    const long long xi = (long long)g.C * g.H * g.W, yi = (long long)g.K * g.P * g.Q;
+    WgradArgs a;
+    a.M = g.Kg;
+    a.Ncol = g.Cg * g.R * g.S;
+    a.groups = g.G;
+    a.dy_img_words = (uint32_t)yi;
+    a.x_img_words = (uint32_t)xi;
+    a.Cg = g.Cg;
+    a.H = g.H;
+    a.W = g.W;
+    a.HW = g.H * g.W;
+    a.PQ = g.P * g.Q;
+    a.stride = g.st;
+    a.pad = g.pad;
+    a.pix_pq = make_fastdiv(g.P * g.Q);
+    a.pix_q = make_fastdiv(g.Q);
+    a.n_rs = make_fastdiv(g.R * g.S);
+    a.n_s = make_fastdiv(g.S);
+    a.chunk = p.chunk;
+    a.split_stride = (long long)g.K * a.Ncol;
+    a.K = g.K;
+    for (int n0 = 0; n0 < n_images; n0 += p.nb) {
+        const int n = n_images - n0 < p.nb ? n_images - n0 : p.nb;
+        a.Kred = n * a.PQ;
+        a.nsplit = (a.Kred + p.chunk - 1) / p.chunk;
+        a.dy = dy + n0 * yi;
+        a.x = x + n0 * xi;
+        a.dy_bytes = (uint32_t)(n * yi * (long long)fb);
+        a.x_bytes = (uint32_t)(n * xi * (long long)fb);
+        a.out = p.via_part ? part + (long long)split0 * a.split_stride : dw;
+        a.db_part = with_db ? db_part + (long long)split0 * g.K : nullptr;
+        int st = launch_status(launch_wgrad_gemm(a, p.tile, stream));
+        if (st != MICONV_OK)
+            return st;
+        split0 += a.nsplit;
+    }
     return MICONV_OK;
 }
 
@@ -1020,60 +1228,45 @@ int wgrad_exec(const Geom &g, const WgradPlan &p, const float *x, const float *d
                   {dw, (size_t)K * g.Cg * R * S * fb, true},
                   {db, (size_t)K * fb, true}};
     bool req[4] = {true, true, true, false};
-    int st = check_buffers(r, 4, req, ws, ws_bytes, wgrad_ws(p));
+    int st = check_buffers(r, 4, req, ws, ws_bytes, wgrad_ws(g, p));
     if (st != MICONV_OK || (st = check_device()) != MICONV_OK)
         return st;
     (void)hipGetLastError();
 
-    const long long xi = (long long)C * H * W, yi = (long long)K * g.P * g.Q;
-    WgradArgs a;
-    a.M = g.Kg;
-    a.Ncol = g.Cg * R * S;
-    a.groups = g.G;
-    a.dy_img_words = (uint32_t)yi;
-    a.x_img_words = (uint32_t)xi;
-    a.Cg = g.Cg;
-    a.H = H;
-    a.W = W;
-    a.HW = H * W;
-    a.PQ = g.P * g.Q;
-    a.stride = g.st;
-    a.pad = g.pad;
-    a.pix_pq = make_fastdiv(g.P * g.Q);
-    a.pix_q = make_fastdiv(g.Q);
-    a.n_rs = make_fastdiv(R * S);
-    a.n_s = make_fastdiv(S);
-    a.chunk = p.chunk;
-    a.split_stride = (long long)K * a.Ncol;
-    a.K = K;
     float *part = (float *)ws;
     float *db_part = (float *)((char *)ws + p.part_bytes);
-    a.db_part = db ? db_part : nullptr;
+    int split0 = 0;
     if (mark(tl_events.before, stream) != hipSuccess)
         return MICONV_ERR_LAUNCH;
-    int split0 = 0;
-    for (int n0 = 0; n0 < N; n0 += p.nb) {
-        const int n = N - n0 < p.nb ? N - n0 : p.nb;
-        a.Kred = n * a.PQ;
-        a.nsplit = (a.Kred + p.chunk - 1) / p.chunk;
-        a.dy = dy + n0 * yi;
-        a.x = x + n0 * xi;
-        a.dy_bytes = (uint32_t)(n * yi * (long long)fb);
-        a.x_bytes = (uint32_t)(n * xi * (long long)fb);
-        a.out = p.via_part ? part + (long long)split0 * a.split_stride : dw;
-        if (db)
-            a.db_part = db_part + (long long)split0 * K;
-        if ((st = launch_status(launch_wgrad_gemm(a, p.tile, stream))) != MICONV_OK)
-            return st;
-        split0 += a.nsplit;
+    if (p.xnb > 0) {
+        // Explicit: im2col of a chunk of images, then the 1x1 problem over the
+        // columns, whose dw[k][c'] is dw[k][c][r][s].
+        float *col = (float *)((char *)ws + p.part_bytes + p.bias_bytes);
+        const long long xi = (long long)C * H * W, yi = (long long)K * g.P * g.Q;
+        for (int n0 = 0; n0 < N; n0 += p.xnb) {
+            const int n = N - n0 < p.xnb ? N - n0 : p.xnb;
+            if (launch_im2col(x + n0 * xi, col, n, C, H, W, R, S, g.st, g.pad, g.P, g.Q,
+                              stream) != hipSuccess)
+                return MICONV_ERR_LAUNCH;
+            if ((st = wgrad_launches(one_by_one(g, n), p, col, dy + n0 * yi, dw, db != nullptr,
+                                     part, db_part, n, split0, stream)) != MICONV_OK)
+                return st;
+        }
+    } else if ((st = wgrad_launches(g, p, x, dy, dw, db != nullptr, part, db_part, N, split0,
+                                    stream)) != MICONV_OK) {
+        return st;
     }
     if (mark(tl_events.after, stream) != hipSuccess)
         return MICONV_ERR_LAUNCH;
+    // Tap-ordered partials go back to dw's [k][c][r][s] (a 1x1 problem has one tap).
+    const int taps = p.xnb > 0 ? 1 : R * S;
+    const int ncol = g.Cg * R * S;
     const bool tap_order = is_tap_tile(p.tile);
     if (p.via_part &&
-        (st = launch_status(launch_splitk_reduce(part, p.nsplit, a.split_stride, K * a.Ncol, dw,
-                                                 tap_order ? R * S : 0, tap_order ? g.Cg : 0,
-                                                 stream))) != MICONV_OK)
+        (st = launch_status(launch_splitk_reduce(part, p.nsplit, (long long)K * ncol, K * ncol,
+                                                 dw, tap_order ? taps : 0,
+                                                 tap_order ? ncol / taps : 0, stream))) !=
+            MICONV_OK)
         return st;
     if (db && (st = launch_status(launch_splitk_reduce(db_part, p.nsplit, K, K, db, 0, 0,
                                                        stream))) != MICONV_OK)
@@ -1113,7 +1306,7 @@ size_t candidate_ws(int pass, const Geom &g, int index)
     case MICONV_PASS_BWD_DATA:
         return bwd_ws(g, pick(bwd_rule(g), index, bwd_candidates, g));
     case MICONV_PASS_BWD_WEIGHT:
-        return wgrad_ws(pick(wgrad_plan(g), index, wgrad_candidates, g));
+        return wgrad_ws(g, pick(wgrad_plan(g), index, wgrad_candidates, g));
     default:
         return 0;
     }

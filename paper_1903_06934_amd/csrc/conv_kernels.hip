@@ -795,6 +795,66 @@ __global__ void pack_bwd_block_kernel(const float *__restrict__ w, float *__rest
 }
 
 // ---------------------------------------------------------------------------
+// Explicit plan: im2col and col2im (memory-bound; one thread per written
+// element, the index decoded with constant-divisor division).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void im2col_kernel(const float *__restrict__ x,
+                                                     float *__restrict__ col, FastDiv pq,
+                                                     FastDiv q_, FastDiv rs, FastDiv s_,
+                                                     int H, int W, int stride, int pad,
+                                                     long long total)
+{
+    for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+         i += (long long)gridDim.x * blockDim.x) {
+        // i = row * PQ + pix, row = (n * C + c) * RS + tap; total < 2^31
+        const uint32_t row = fast_div((uint32_t)i, pq);
+        const uint32_t pix = (uint32_t)i - row * pq.d;
+        const uint32_t p = fast_div(pix, q_), q = pix - p * q_.d;
+        const uint32_t nc = fast_div(row, rs), tap = row - nc * rs.d;
+        const uint32_t r = fast_div(tap, s_), sx = tap - r * s_.d;
+        const int h = (int)(p * stride + r) - pad, w = (int)(q * stride + sx) - pad;
+        float v = 0.f;
+        if ((unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W)
+            v = x[((long long)nc * H + h) * W + w];
+        col[i] = v;
+    }
+}
+
+__global__ __launch_bounds__(256) void col2im_kernel(const float *__restrict__ col,
+                                                     float *__restrict__ dx, FastDiv hw,
+                                                     FastDiv w_, int R, int S, int stride,
+                                                     int pad, int P, int Q, long long total)
+{
+    for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+         i += (long long)gridDim.x * blockDim.x) {
+        // i = nc * HW + h * W + w; total < 2^31
+        const uint32_t nc = fast_div((uint32_t)i, hw);
+        const uint32_t pix = (uint32_t)i - nc * hw.d;
+        const uint32_t h = fast_div(pix, w_), w = pix - h * w_.d;
+        const long long base = (long long)nc * R * S * P * Q;
+        float acc = 0.f;
+        for (int r = 0; r < R; r++) {
+            const int hp = (int)h + pad - r;
+            if (hp < 0 || hp % stride)
+                continue;
+            const int p = hp / stride;
+            if (p >= P)
+                continue;
+            for (int s = 0; s < S; s++) {
+                const int wp = (int)w + pad - s;
+                if (wp < 0 || wp % stride)
+                    continue;
+                const int q = wp / stride;
+                if (q >= Q)
+                    continue;
+                acc += col[base + ((long long)(r * S + s) * P + p) * Q + q];
+            }
+        }
+        dx[i] = acc;
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Deterministic split-K reduction.  out[dst(i)] = sum over s < nsplit of
 // part[s * stride + i].  A block handles 32 consecutive elements with 8
 // threads each: thread j sums splits j, j + 8, j + 16, ... in order, and the
@@ -937,6 +997,31 @@ hipError_t launch_pack_bwd_block(const float *w, float *wp, int K, int Cg, int R
     hipLaunchKernelGGL(pack_bwd_block_kernel, dim3(blocks_for(total, 256)), dim3(256), 0, stream,
                        w, wp, K / G, Cg, R, S, stride, f, ntr, nts, cblock ? 1 : 0, a_ld,
                        kmajor ? 1 : 0, total);
+    return hipGetLastError();
+}
+
+static unsigned grid_for(long long total)
+{
+    long long b = (total + 255) / 256;
+    return (unsigned)(b < 65536 ? b : 65536);
+}
+
+hipError_t launch_im2col(const float *x, float *col, int n, int C, int H, int W, int R, int S,
+                         int stride, int pad, int P, int Q, hipStream_t stream)
+{
+    const long long total = (long long)n * C * R * S * P * Q;
+    hipLaunchKernelGGL(im2col_kernel, dim3(grid_for(total)), dim3(256), 0, stream, x, col,
+                       make_fastdiv(P * Q), make_fastdiv(Q), make_fastdiv(R * S),
+                       make_fastdiv(S), H, W, stride, pad, total);
+    return hipGetLastError();
+}
+
+hipError_t launch_col2im(const float *col, float *dx, int n, int C, int H, int W, int R, int S,
+                         int stride, int pad, int P, int Q, hipStream_t stream)
+{
+    const long long total = (long long)n * C * H * W;
+    hipLaunchKernelGGL(col2im_kernel, dim3(grid_for(total)), dim3(256), 0, stream, col, dx,
+                       make_fastdiv(H * W), make_fastdiv(W), R, S, stride, pad, P, Q, total);
     return hipGetLastError();
 }
 

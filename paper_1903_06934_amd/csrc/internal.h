@@ -136,6 +136,17 @@ hipError_t launch_pack_bwd_phase(const float *w, float *wr, int K, int Cg, int R
 hipError_t launch_pack_bwd_block(const float *w, float *wp, int K, int Cg, int R, int S, int G,
                                  int stride, int f, int ntr, int nts, bool cblock, int a_ld,
                                  bool kmajor, hipStream_t stream);
+// Explicit plan (im2col / col2im around a 1x1 GEMM).  The column tensor of n
+// images is col[n][c'][p][q], c' = (c_all * R + r) * S + s over all C channels
+// (group g owns c' in [g (C/G) R S, (g+1) (C/G) R S)), p < P, q < Q:
+//   im2col:  col[n][c'][p][q] = x[n][c_all][p st - pad + r][q st - pad + s] (0 outside)
+//   col2im:  dx[n][c_all][h][w] = sum over (r, s) in order of col[n][c'][p][q] with
+//            h + pad - r = p st, w + pad - s = q st, 0 <= p < P, 0 <= q < Q (0 if none)
+// Both need fewer than 2^31 written elements.
+hipError_t launch_im2col(const float *x, float *col, int n, int C, int H, int W, int R, int S,
+                         int stride, int pad, int P, int Q, hipStream_t stream);
+hipError_t launch_col2im(const float *col, float *dx, int n, int C, int H, int W, int R, int S,
+                         int stride, int pad, int P, int Q, hipStream_t stream);
 // Packed reduction-row length of the image GEMM's filter operand.
 inline int pad16(int k) { return (k + 15) & ~15; }
 // out[dst(i)] = sum over s < nsplit of part[s * stride + i] for i < count, in a

@@ -90,3 +90,22 @@ def test_plan_errors():
     assert L.conv_plan_name(0, *good, n, b"x" * 8, 8) == PLAN_ERR
     assert L.conv_plan_workspace_size(0, *good, n) == 0
     assert m.plan_get(0, good) == 0
+
+
+def test_explicit_candidates():
+    """The explicit plan (im2col / col2im around the 1x1 GEMM) is a candidate
+    of every pass where its columns differ from the input, with a column
+    chunk of at most 256 MB in its workspace; not for a 1x1 stride-1 layer."""
+    conv1 = (128, 3, 227, 227, 96, 11, 11, 4, 0, 1)
+    for p in PASSES:
+        n = m.plan_count(p, conv1)
+        names = [m.plan_name(p, conv1, i) for i in range(n)]
+        ex = [i for i, s in enumerate(names) if s.startswith("explicit")]
+        assert len(ex) == 1, names
+        col_chunk = int(names[ex[0]].split("(")[1].split()[0])   # images a chunk
+        assert col_chunk * 3 * 121 * 55 * 55 * 4 <= 256 << 20
+        assert m.plan_workspace_size(p, conv1, ex[0]) >= col_chunk * 3 * 121 * 55 * 55 * 4
+    one = (64, 256, 56, 56, 64, 1, 1, 1, 0, 1)
+    for p in PASSES:
+        n = m.plan_count(p, one)
+        assert not any(m.plan_name(p, one, i).startswith("explicit") for i in range(n))
