@@ -1,4 +1,5 @@
-"""Plain CPU oracle for the three passes of a convolution layer.
+"""Plain CPU oracle for the three passes of a convolution layer, and for a
+pooling layer's forward and backward passes.
 
 TEST INFRASTRUCTURE ONLY: the test suite, the smoke check and the benchmark's
 CPU-baseline leg are the only callers.  The product library never imports,
@@ -71,11 +72,15 @@ class Oracle:
             "oracle_conv_bwd_data_at": _GEO + [_D, _D, _L, ctypes.c_int64, _D, _D],
             "oracle_conv_bwd_weight_at": _GEO + [_D, _D, _L, ctypes.c_int64, _D, _D],
             "oracle_bias_grad": [_I, _I, _I, _I, _D, _D, _D],
+            "oracle_pool_fwd": [_I] * 9 + [_D, _D, _D, _L],
+            "oracle_pool_bwd": [_I] * 9 + [_D, _L, _D, _D],
         }
         for name, args in sigs.items():
             fn = getattr(lib, name)
             fn.argtypes = args
             fn.restype = None
+        lib.oracle_pool_out_size.argtypes = [_I, _I, _I, _I]
+        lib.oracle_pool_out_size.restype = _I
         self.lib = lib
 
     def out_size(self, n_in: int, filt: int, stride: int, pad: int) -> int:
@@ -143,6 +148,40 @@ class Oracle:
         """dw at flat indices into [K,C/G,R,S] (gather form)."""
         return self._at("oracle_conv_bwd_weight_at", shape, [_f64(x), _f64(dy)], idx)
 
+    # Pooling (Sec. IV-D).  pshape = (N, C, H, W, R, S, stride, pad); mode
+    # "max" or "avg".
+    def pool_out_size(self, n_in: int, filt: int, stride: int, pad: int) -> int:
+        return int(self.lib.oracle_pool_out_size(n_in, filt, stride, pad))
+
+    def pool_fwd(self, mode, pshape, x):
+        """(y, ay, mask): y [N,C,P,Q] float64, its abs-sum scale (|y| for max,
+        sum|x| / area for avg), and for max the argmax h*W+w within the plane
+        (int64; -1 for avg)."""
+        N, C, H, W, R, S, st, pad = (int(v) for v in pshape)
+        P, Q = self.pool_out_size(H, R, st, pad), self.pool_out_size(W, S, st, pad)
+        x = _f64(x)
+        y = np.empty((N, C, P, Q))
+        ay = np.empty_like(y)
+        mask = np.full((N, C, P, Q), -1, dtype=np.int64)
+        self.lib.oracle_pool_fwd(_pool_mode(mode), N, C, H, W, R, S, st, pad, _ptr(x), _ptr(y),
+                                 _ptr(ay), mask.ctypes.data_as(_L))
+        return y, ay, mask
+
+    def pool_bwd(self, mode, pshape, dy, mask=None):
+        """(dx, adx) [N,C,H,W] float64 (scatter form); max needs the mask."""
+        N, C, H, W, R, S, st, pad = (int(v) for v in pshape)
+        dy = _f64(dy)
+        m = None
+        if _pool_mode(mode) == 0:
+            m = np.ascontiguousarray(np.asarray(mask, dtype=np.int64))
+            assert m.shape == dy.shape
+        dx = np.empty((N, C, H, W))
+        adx = np.empty_like(dx)
+        self.lib.oracle_pool_bwd(_pool_mode(mode), N, C, H, W, R, S, st, pad, _ptr(dy),
+                                 None if m is None else m.ctypes.data_as(_L), _ptr(dx),
+                                 _ptr(adx))
+        return dx, adx
+
     def bias_grad(self, dy):
         """db and its abs-sum from dy [N,K,P,Q]."""
         dy = _f64(dy)
@@ -151,6 +190,10 @@ class Oracle:
         adb = np.empty(K)
         self.lib.oracle_bias_grad(N, K, P, Q, _ptr(dy), _ptr(db), _ptr(adb))
         return db, adb
+
+
+def _pool_mode(mode):
+    return {"max": 0, "avg": 1}[mode]
 
 
 _default = None
@@ -200,3 +243,15 @@ def conv_bwd_weight_at(shape, x, dy, idx):
 
 def bias_grad(dy):
     return default().bias_grad(dy)
+
+
+def pool_out_size(n_in, filt, stride, pad):
+    return default().pool_out_size(n_in, filt, stride, pad)
+
+
+def pool_fwd(mode, pshape, x):
+    return default().pool_fwd(mode, pshape, x)
+
+
+def pool_bwd(mode, pshape, dy, mask=None):
+    return default().pool_bwd(mode, pshape, dy, mask)

@@ -1,5 +1,6 @@
 /*
- * Plain CPU oracle for the three training passes of a convolution layer.
+ * Plain CPU oracle for the three training passes of a convolution layer,
+ * and for the forward and backward passes of a pooling layer (at the end).
  *
  * TEST INFRASTRUCTURE ONLY.  Nothing on the product path may call, link or
  * load this file; only the test suite, the smoke check and the benchmark's
@@ -341,5 +342,133 @@ void oracle_bias_grad(int N, int K, int P, int Q, const double *dy,
             }
         db[k] = acc;
         adb[k] = aacc;
+    }
+}
+
+/* ------------------------------------------------------------------ */
+/* Pooling (Sec. IV-D): each output is the maximum or the average of   */
+/* one window of its input plane.  The paper's layer tiles the image   */
+/* into non-overlapping K x K windows; the general Caffe form below    */
+/* (window R x S, stride, zero padding) contains that case             */
+/* (R = S = stride, pad = 0).  Readings (Caffe's pooling layer):       */
+/*   - output size ceil((H + 2 pad - R) / stride) + 1, less one when    */
+/*     pad > 0 and the last window would start at or past H + pad;      */
+/*   - max: over the window's elements inside the image (padding never  */
+/*     wins); the argmax is the first maximum in row-major order, kept  */
+/*     as the index h * W + w within the plane;                         */
+/*   - avg: the sum over the window's elements inside the image divided */
+/*     by the window's area clipped to the padded image [-pad, H + pad) */
+/*     (padding counts as zeros, the overhang past it does not).        */
+/* The backward pass routes dy back along the same definition, in the   */
+/* scatter form: max adds dy to its argmax, avg adds dy / area to every */
+/* element of its window inside the image.                              */
+/* ------------------------------------------------------------------ */
+int oracle_pool_out_size(int in, int filt, int stride, int pad)
+{
+    i64 span = (i64)in + 2 * (i64)pad - (i64)filt;
+    if (stride < 1 || span < 0)
+        return 0;
+    i64 out = (span + stride - 1) / stride + 1;
+    if (pad > 0 && (out - 1) * stride >= (i64)in + pad)
+        out--;
+    return (int)out;
+}
+
+/* Window of output index p along an axis: [lo, hi) inside the image and
+ * the clipped padded area's extent. */
+static void pool_window(int p, int stride, int pad, int filt, int in, i64 *lo, i64 *hi,
+                        i64 *ext)
+{
+    i64 start = (i64)p * stride - pad;
+    i64 end = start + filt;
+    if (end > (i64)in + pad)
+        end = (i64)in + pad;
+    *ext = end - start;
+    *lo = start < 0 ? 0 : start;
+    *hi = end > in ? in : end;
+}
+
+void oracle_pool_fwd(int mode, int N, int C, int H, int W, int R, int S, int stride, int pad,
+                     const double *x, double *y, double *ay, i64 *mask)
+{
+    int P = oracle_pool_out_size(H, R, stride, pad);
+    int Q = oracle_pool_out_size(W, S, stride, pad);
+    i64 nc;
+#pragma omp parallel for schedule(static)
+    for (nc = 0; nc < (i64)N * C; nc++) {
+        const double *xp = x + nc * H * W;
+        for (int p = 0; p < P; p++)
+            for (int q = 0; q < Q; q++) {
+                i64 h0, h1, eh, w0, w1, ew;
+                pool_window(p, stride, pad, R, H, &h0, &h1, &eh);
+                pool_window(q, stride, pad, S, W, &w0, &w1, &ew);
+                i64 o = (nc * P + p) * Q + q;
+                if (mode == 0) {
+                    double best = -INFINITY;
+                    i64 arg = -1;
+                    for (i64 h = h0; h < h1; h++)
+                        for (i64 w = w0; w < w1; w++)
+                            if (xp[h * W + w] > best) {
+                                best = xp[h * W + w];
+                                arg = h * W + w;
+                            }
+                    y[o] = best;
+                    if (ay)
+                        ay[o] = fabs(best);
+                    if (mask)
+                        mask[o] = arg;
+                } else {
+                    double sum = 0.0, asum = 0.0;
+                    for (i64 h = h0; h < h1; h++)
+                        for (i64 w = w0; w < w1; w++) {
+                            sum += xp[h * W + w];
+                            asum += fabs(xp[h * W + w]);
+                        }
+                    double area = (double)(eh * ew);
+                    y[o] = sum / area;
+                    if (ay)
+                        ay[o] = asum / area;
+                }
+            }
+    }
+}
+
+void oracle_pool_bwd(int mode, int N, int C, int H, int W, int R, int S, int stride, int pad,
+                     const double *dy, const i64 *mask, double *dx, double *adx)
+{
+    int P = oracle_pool_out_size(H, R, stride, pad);
+    int Q = oracle_pool_out_size(W, S, stride, pad);
+    i64 nc;
+#pragma omp parallel for schedule(static)
+    for (nc = 0; nc < (i64)N * C; nc++) {
+        double *dxp = dx + nc * H * W;
+        double *adxp = adx ? adx + nc * H * W : NULL;
+        for (i64 i = 0; i < (i64)H * W; i++) {
+            dxp[i] = 0.0;
+            if (adxp)
+                adxp[i] = 0.0;
+        }
+        for (int p = 0; p < P; p++)
+            for (int q = 0; q < Q; q++) {
+                i64 o = (nc * P + p) * Q + q;
+                double g = dy[o];
+                if (mode == 0) {
+                    i64 arg = mask[o];
+                    dxp[arg] += g;
+                    if (adxp)
+                        adxp[arg] += fabs(g);
+                    continue;
+                }
+                i64 h0, h1, eh, w0, w1, ew;
+                pool_window(p, stride, pad, R, H, &h0, &h1, &eh);
+                pool_window(q, stride, pad, S, W, &w0, &w1, &ew);
+                double share = g / (double)(eh * ew);
+                for (i64 h = h0; h < h1; h++)
+                    for (i64 w = w0; w < w1; w++) {
+                        dxp[h * W + w] += share;
+                        if (adxp)
+                            adxp[h * W + w] += fabs(share);
+                    }
+            }
     }
 }
