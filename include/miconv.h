@@ -67,7 +67,8 @@ typedef enum miconv_status {
     MICONV_ERR_DEVICE = -6,    /* no current HIP device, or it is not gfx950 */
     MICONV_ERR_LAUNCH = -7,    /* a kernel launch reported an error */
     MICONV_ERR_PASS = -8,      /* unknown pass id */
-    MICONV_ERR_PLAN = -9       /* plan index outside [0, conv_plan_count()) */
+    MICONV_ERR_PLAN = -9,      /* plan index outside [0, conv_plan_count()) */
+    MICONV_ERR_MODE = -10      /* pooling mode other than MICONV_POOL_MAX / _AVG */
 } miconv_status;
 
 /* Pass ids for conv_workspace_size and the plan calls. */
@@ -198,6 +199,35 @@ size_t conv_plan_workspace_size(int pass, int N, int C, int H, int W, int K, int
 int conv_tune(int pass, int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
               int group, const float *in0, const float *in1, const float *in2, float *out0,
               float *out1, void *ws, size_t ws_bytes, int reps, hipStream_t stream, int *chosen);
+
+/*
+ * Pooling layer (Sec. IV-D: each output is the maximum or the average of a
+ * window of its input plane; the paper tiles the plane into non-overlapping
+ * K x K windows, i.e. R = S = stride, pad = 0 below).  Caffe's general form:
+ * window R x S, stride, zero padding pad < min(R, S), on x [N][C][H][W]
+ * giving y [N][C][P][Q] with P = ceil((H + 2 pad - R) / stride) + 1, less one
+ * when pad > 0 and the last window would start at or past H + pad (Q alike).
+ *   MICONV_POOL_MAX: y = maximum over the window's elements inside the
+ *     image; mask (may be NULL in pool_fwd) receives the first maximum's
+ *     index h * W + w within its plane, in row-major order.
+ *   MICONV_POOL_AVG: y = sum over the window's elements inside the image,
+ *     divided by the window's area clipped to the padded image (padding
+ *     counts, the overhang past it does not); mask is not used.
+ * pool_bwd writes every element of dx: the sum, over the windows that cover
+ * the element (in window order), of their dy (max: only windows whose mask
+ * names the element; avg: dy / area).  mask is required for max.
+ * Buffers are caller-owned device memory, 16-byte aligned, outputs not
+ * overlapping inputs; no workspace.  Statuses as for the convolution calls,
+ * plus MICONV_ERR_MODE; MICONV_ERR_SHAPE also when pad >= R or pad >= S or
+ * N*C*H*W or N*C*P*Q is above 2^31 - 1.  pool_output_size is host-only.
+ */
+#define MICONV_POOL_MAX 0
+#define MICONV_POOL_AVG 1
+int pool_output_size(int H, int W, int R, int S, int stride, int pad, int *P, int *Q);
+int pool_fwd(int mode, int N, int C, int H, int W, int R, int S, int stride, int pad,
+             const float *x, float *y, int *mask, hipStream_t stream);
+int pool_bwd(int mode, int N, int C, int H, int W, int R, int S, int stride, int pad,
+             const float *dy, const int *mask, float *dx, hipStream_t stream);
 
 /* Static, NUL-terminated description of a status code (never NULL). */
 const char *conv_error_string(int status);

@@ -1337,6 +1337,42 @@ int candidate_run(int pass, const Geom &g, int index, const TuneBuffers &t, void
     }
 }
 
+// ------------------------------------------------------------ pooling
+// Output extent of a pooling window along one axis (Caffe's rule: ceil,
+// less one when pad > 0 and the last window would start at or past
+// in + pad); 0 when the window does not fit.
+int pool_extent(int in, int filt, int stride, int pad)
+{
+    long long span = (long long)in + 2LL * pad - filt;
+    if (span < 0)
+        return 0;
+    long long out = (span + stride - 1) / stride + 1;
+    if (pad > 0 && (out - 1) * stride >= (long long)in + pad)
+        out--;
+    return (int)out;
+}
+
+struct PoolGeom {
+    int N, C, H, W, R, S, st, pad, P, Q;
+};
+
+int make_pool(int mode, int N, int C, int H, int W, int R, int S, int stride, int pad,
+              PoolGeom *g)
+{
+    if (mode != MICONV_POOL_MAX && mode != MICONV_POOL_AVG)
+        return MICONV_ERR_MODE;
+    if (N < 1 || C < 1 || H < 1 || W < 1 || R < 1 || S < 1 || stride < 1 || pad < 0 ||
+        pad >= R || pad >= S || H > 32767 || W > 32767 || R > 32767 || S > 32767)
+        return MICONV_ERR_SHAPE;
+    const int P = pool_extent(H, R, stride, pad), Q = pool_extent(W, S, stride, pad);
+    if (P < 1 || Q < 1)
+        return MICONV_ERR_SHAPE;
+    if ((long long)N * C * H * W > kMaxElems || (long long)N * C * P * Q > kMaxElems)
+        return MICONV_ERR_SHAPE;
+    *g = PoolGeom{N, C, H, W, R, S, stride, pad, P, Q};
+    return MICONV_OK;
+}
+
 }  // namespace
 }  // namespace miconv
 
@@ -1391,6 +1427,7 @@ const char *conv_error_string(int status)
     case MICONV_ERR_LAUNCH: return "kernel launch failed";
     case MICONV_ERR_PASS: return "unknown pass id";
     case MICONV_ERR_PLAN: return "plan index out of range";
+    case MICONV_ERR_MODE: return "unknown pooling mode";
     default: return "unknown status";
     }
 }
@@ -1589,6 +1626,71 @@ int conv_tune(int pass, int N, int C, int H, int W, int K, int R, int S, int str
     st = candidate_run(pass, g, best, t, ws, ws_bytes, stream);
     tl_events = saved;
     return st;
+}
+
+int pool_output_size(int H, int W, int R, int S, int stride, int pad, int *P, int *Q)
+{
+    if (!P || !Q)
+        return MICONV_ERR_NULL;
+    PoolGeom g;
+    int st = make_pool(MICONV_POOL_MAX, 1, 1, H, W, R, S, stride, pad, &g);
+    if (st != MICONV_OK)
+        return st;
+    *P = g.P;
+    *Q = g.Q;
+    return MICONV_OK;
+}
+
+int pool_fwd(int mode, int N, int C, int H, int W, int R, int S, int stride, int pad,
+             const float *x, float *y, int *mask, hipStream_t stream)
+{
+    PoolGeom g;
+    int st = make_pool(mode, N, C, H, W, R, S, stride, pad, &g);
+    if (st != MICONV_OK)
+        return st;
+    const bool max_mode = mode == MICONV_POOL_MAX;
+    const size_t in = (size_t)N * C * H * W * sizeof(float);
+    const size_t out = (size_t)N * C * g.P * g.Q * sizeof(float);
+    Range r[3] = {{x, in, false}, {y, out, true}, {max_mode ? mask : nullptr, out, true}};
+    bool req[3] = {true, true, false};
+    if ((st = check_buffers(r, 3, req, nullptr, 0, 0)) != MICONV_OK)
+        return st;
+    if ((st = check_device()) != MICONV_OK)
+        return st;
+    (void)hipGetLastError();
+    if (mark(tl_events.before, stream) != hipSuccess)
+        return MICONV_ERR_LAUNCH;
+    if ((st = launch_status(launch_pool_fwd(max_mode, x, y, max_mode ? mask : nullptr, N, C, H,
+                                            W, R, S, stride, pad, g.P, g.Q, stream))) !=
+        MICONV_OK)
+        return st;
+    return mark(tl_events.after, stream) == hipSuccess ? MICONV_OK : MICONV_ERR_LAUNCH;
+}
+
+int pool_bwd(int mode, int N, int C, int H, int W, int R, int S, int stride, int pad,
+             const float *dy, const int *mask, float *dx, hipStream_t stream)
+{
+    PoolGeom g;
+    int st = make_pool(mode, N, C, H, W, R, S, stride, pad, &g);
+    if (st != MICONV_OK)
+        return st;
+    const bool max_mode = mode == MICONV_POOL_MAX;
+    const size_t in = (size_t)N * C * H * W * sizeof(float);
+    const size_t out = (size_t)N * C * g.P * g.Q * sizeof(float);
+    Range r[3] = {{dy, out, false}, {max_mode ? mask : nullptr, out, false}, {dx, in, true}};
+    bool req[3] = {true, max_mode, true};
+    if ((st = check_buffers(r, 3, req, nullptr, 0, 0)) != MICONV_OK)
+        return st;
+    if ((st = check_device()) != MICONV_OK)
+        return st;
+    (void)hipGetLastError();
+    if (mark(tl_events.before, stream) != hipSuccess)
+        return MICONV_ERR_LAUNCH;
+    if ((st = launch_status(launch_pool_bwd(max_mode, dy, max_mode ? mask : nullptr, dx, N, C,
+                                            H, W, R, S, stride, pad, g.P, g.Q, stream))) !=
+        MICONV_OK)
+        return st;
+    return mark(tl_events.after, stream) == hipSuccess ? MICONV_OK : MICONV_ERR_LAUNCH;
 }
 
 }  // extern "C"

@@ -147,6 +147,15 @@ hipError_t launch_im2col(const float *x, float *col, int n, int C, int H, int W,
                          int stride, int pad, int P, int Q, hipStream_t stream);
 hipError_t launch_col2im(const float *col, float *dx, int n, int C, int H, int W, int R, int S,
                          int stride, int pad, int P, int Q, hipStream_t stream);
+// Pooling (max with argmax mask h * W + w within the plane, or average over
+// the window clipped to the padded image), forward over N*C*P*Q outputs and
+// backward over N*C*H*W inputs (both < 2^31); pad < window.
+hipError_t launch_pool_fwd(bool max_mode, const float *x, float *y, int *mask, int N, int C, int H,
+                           int W, int R, int S, int stride, int pad, int P, int Q,
+                           hipStream_t stream);
+hipError_t launch_pool_bwd(bool max_mode, const float *dy, const int *mask, float *dx, int N,
+                           int C, int H, int W, int R, int S, int stride, int pad, int P, int Q,
+                           hipStream_t stream);
 // Packed reduction-row length of the image GEMM's filter operand.
 inline int pad16(int k) { return (k + 15) & ~15; }
 // out[dst(i)] = sum over s < nsplit of part[s * stride + i] for i < count, in a

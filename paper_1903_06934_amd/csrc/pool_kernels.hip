@@ -1,0 +1,139 @@
+// Pooling layer (forward and backward), max with argmax mask or average.
+// Memory-bound: one thread per written element, index decoded with
+// constant-divisor division, windows read through the caches.
+#include "internal.h"
+
+namespace miconv {
+
+namespace {
+
+// Window of output index p along an axis: inside the image [lo, hi), and
+// the extent of the window clipped to the padded image (the average's
+// divisor counts padding but not the overhang past it).
+struct Win {
+    int lo, hi, ext;
+};
+
+__device__ __forceinline__ Win window(int p, int stride, int pad, int filt, int in)
+{
+    const int start = p * stride - pad;
+    const int end = min(start + filt, in + pad);
+    return Win{max(start, 0), min(end, in), end - start};
+}
+
+template <bool MAX>
+__global__ __launch_bounds__(256) void pool_fwd_kernel(const float *__restrict__ x,
+                                                       float *__restrict__ y,
+                                                       int *__restrict__ mask, int H, int W,
+                                                       int R, int S, int stride, int pad,
+                                                       FastDiv pq, FastDiv q_, uint32_t total)
+{
+    for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < total;
+         i += gridDim.x * blockDim.x) {
+        const uint32_t nc = fast_div(i, pq), pix = i - nc * pq.d;
+        const uint32_t p = fast_div(pix, q_), q = pix - p * q_.d;
+        const Win wh = window((int)p, stride, pad, R, H), ww = window((int)q, stride, pad, S, W);
+        const float *xp = x + (size_t)nc * H * W;
+        if constexpr (MAX) {
+            // First maximum in row-major order; the window always holds an
+            // image element (pad < window), so arg is set.
+            float best = -__builtin_inff();
+            int arg = -1;
+            for (int h = wh.lo; h < wh.hi; h++)
+                for (int w = ww.lo; w < ww.hi; w++) {
+                    const float v = xp[h * W + w];
+                    if (v > best) {
+                        best = v;
+                        arg = h * W + w;
+                    }
+                }
+            y[i] = best;
+            if (mask)
+                mask[i] = arg;
+        } else {
+            float sum = 0.f;
+            for (int h = wh.lo; h < wh.hi; h++)
+                for (int w = ww.lo; w < ww.hi; w++)
+                    sum += xp[h * W + w];
+            y[i] = sum / (float)(wh.ext * ww.ext);
+        }
+    }
+}
+
+// dx[h][w] gathers, in the order of the windows (p, then q), the dy of every
+// window that covers it: all of it for max when the window's argmax is this
+// element, dy / area for the average.  No atomics: each thread writes one dx.
+template <bool MAX>
+__global__ __launch_bounds__(256) void pool_bwd_kernel(const float *__restrict__ dy,
+                                                       const int *__restrict__ mask,
+                                                       float *__restrict__ dx, int H, int W,
+                                                       int P, int Q, int R, int S, int stride,
+                                                       int pad, FastDiv hw, FastDiv w_,
+                                                       uint32_t total)
+{
+    for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < total;
+         i += gridDim.x * blockDim.x) {
+        const uint32_t nc = fast_div(i, hw), pix = i - nc * hw.d;
+        const int h = (int)fast_div(pix, w_), w = (int)(pix - (uint32_t)h * w_.d);
+        // windows p with p stride - pad <= h < p stride - pad + R
+        const int hp = h + pad, wp = w + pad;
+        const int p0 = hp < R ? 0 : (hp - R) / stride + 1, p1 = min(hp / stride, P - 1);
+        const int q0 = wp < S ? 0 : (wp - S) / stride + 1, q1 = min(wp / stride, Q - 1);
+        const size_t base = (size_t)nc * P * Q;
+        float acc = 0.f;
+        for (int p = p0; p <= p1; p++)
+            for (int q = q0; q <= q1; q++) {
+                const size_t o = base + (size_t)p * Q + q;
+                if constexpr (MAX) {
+                    if (mask[o] == (int)pix)
+                        acc += dy[o];
+                } else {
+                    const Win wh = window(p, stride, pad, R, H), ww = window(q, stride, pad, S, W);
+                    acc += dy[o] / (float)(wh.ext * ww.ext);
+                }
+            }
+        dx[i] = acc;
+    }
+}
+
+unsigned pool_grid(uint32_t total)
+{
+    uint32_t b = (total + 255) / 256;
+    return b < 65536u ? b : 65536u;
+}
+
+}  // namespace
+
+hipError_t launch_pool_fwd(bool max_mode, const float *x, float *y, int *mask, int N, int C, int H,
+                           int W, int R, int S, int stride, int pad, int P, int Q,
+                           hipStream_t stream)
+{
+    const uint32_t total = (uint32_t)((long long)N * C * P * Q);
+    if (max_mode)
+        hipLaunchKernelGGL(pool_fwd_kernel<true>, dim3(pool_grid(total)), dim3(256), 0, stream, x,
+                           y, mask, H, W, R, S, stride, pad, make_fastdiv(P * Q),
+                           make_fastdiv(Q), total);
+    else
+        hipLaunchKernelGGL(pool_fwd_kernel<false>, dim3(pool_grid(total)), dim3(256), 0, stream,
+                           x, y, nullptr, H, W, R, S, stride, pad, make_fastdiv(P * Q),
+                           make_fastdiv(Q), total);
+    return hipGetLastError();
+}
+
+hipError_t launch_pool_bwd(bool max_mode, const float *dy, const int *mask, float *dx, int N,
+                           int C, int H, int W, int R, int S, int stride, int pad, int P, int Q,
+                           hipStream_t stream)
+{
+    const uint32_t total = (uint32_t)((long long)N * C * H * W);
+    if (max_mode)
+        hipLaunchKernelGGL(pool_bwd_kernel<true>, dim3(pool_grid(total)), dim3(256), 0, stream,
+                           dy, mask, dx, H, W, P, Q, R, S, stride, pad, make_fastdiv(H * W),
+                           make_fastdiv(W), total);
+    else
+        hipLaunchKernelGGL(pool_bwd_kernel<false>, dim3(pool_grid(total)), dim3(256), 0, stream,
+                           dy, nullptr, dx, H, W, P, Q, R, S, stride, pad, make_fastdiv(H * W),
+                           make_fastdiv(W), total);
+    return hipGetLastError();
+}
+
+}  // namespace miconv

@@ -18,8 +18,9 @@ STATUS = {
     0: "MICONV_OK", -1: "MICONV_ERR_SHAPE", -2: "MICONV_ERR_NULL",
     -3: "MICONV_ERR_WORKSPACE", -4: "MICONV_ERR_ALIAS", -5: "MICONV_ERR_ALIGN",
     -6: "MICONV_ERR_DEVICE", -7: "MICONV_ERR_LAUNCH", -8: "MICONV_ERR_PASS",
-    -9: "MICONV_ERR_PLAN",
+    -9: "MICONV_ERR_PLAN", -10: "MICONV_ERR_MODE",
 }
+POOL_MODES = {"max": 0, "avg": 1}
 PASS_FWD, PASS_BWD_DATA, PASS_BWD_WEIGHT = 0, 1, 2
 
 _lib = None
@@ -77,6 +78,12 @@ def lib():
     L.conv_tune.argtypes = [_I] + geo + [_P, _P, _P, _P, _P, _P, _Z, _I, _P,
                                          ctypes.POINTER(_I)]
     L.conv_tune.restype = _I
+    L.pool_output_size.argtypes = [_I] * 6 + [ctypes.POINTER(_I), ctypes.POINTER(_I)]
+    L.pool_output_size.restype = _I
+    L.pool_fwd.argtypes = [_I] * 9 + [_P, _P, _P, _P]
+    L.pool_fwd.restype = _I
+    L.pool_bwd.argtypes = [_I] * 9 + [_P, _P, _P, _P]
+    L.pool_bwd.restype = _I
     _lib = L
     return L
 
@@ -228,3 +235,43 @@ def conv_tune(pass_id, shape, in0, in1, in2, out0, out1, ws, reps=3):
           0 if ws is None else ws.numel() * ws.element_size(), int(reps), _stream(),
           ctypes.byref(chosen))
     return chosen.value
+
+
+# ---------------------------------------------------------------- pooling
+def pool_output_size(H, W, R, S, stride, pad):
+    P, Q = _I(), _I()
+    st = lib().pool_output_size(H, W, R, S, stride, pad, ctypes.byref(P), ctypes.byref(Q))
+    if st != OK:
+        raise MiconvError(st, "pool_output_size")
+    return P.value, Q.value
+
+
+def pool_fwd(x, window, stride, pad=0, mode="max", y=None, mask=None):
+    """(y [N,C,P,Q], mask [N,C,P,Q] int32 for max, else None) from x [N,C,H,W];
+    window = (R, S)."""
+    import torch
+    N, C, H, W = x.shape
+    R, S = window
+    _check(x, "x")
+    P, Q = pool_output_size(H, W, R, S, stride, pad)
+    if y is None:
+        y = torch.empty((N, C, P, Q), dtype=torch.float32, device=x.device)
+    if mode == "max" and mask is None:
+        mask = torch.empty((N, C, P, Q), dtype=torch.int32, device=x.device)
+    _call(lib().pool_fwd, "pool_fwd", POOL_MODES[mode], N, C, H, W, R, S, stride, pad,
+          _ptr(x), _ptr(y), _ptr(mask) if mode == "max" else None, _stream())
+    return y, (mask if mode == "max" else None)
+
+
+def pool_bwd(dy, input_hw, window, stride, pad=0, mode="max", mask=None, dx=None):
+    """dx [N,C,H,W] from dy [N,C,P,Q] (and, for max, the forward's mask)."""
+    import torch
+    N, C, _, _ = dy.shape
+    H, W = input_hw
+    R, S = window
+    _check(dy, "dy")
+    if dx is None:
+        dx = torch.empty((N, C, H, W), dtype=torch.float32, device=dy.device)
+    _call(lib().pool_bwd, "pool_bwd", POOL_MODES[mode], N, C, H, W, R, S, stride, pad,
+          _ptr(dy), _ptr(mask) if mode == "max" else None, _ptr(dx), _stream())
+    return dx

@@ -37,7 +37,8 @@ def test_exports_every_declared_function(L):
                           "conv_bwd_data", "conv_bwd_weight", "conv_error_string",
                           "conv_set_timing_events", "conv_plan_count", "conv_plan_get",
                           "conv_plan_set", "conv_plan_clear", "conv_plan_name",
-                          "conv_plan_workspace_size", "conv_tune"}
+                          "conv_plan_workspace_size", "conv_tune", "pool_output_size",
+                          "pool_fwd", "pool_bwd"}
     for n in names:
         assert hasattr(L, n), n
 
@@ -69,7 +70,7 @@ def test_timing_events_arguments(L):
 
 
 def test_error_strings(L):
-    for s in range(-9, 1):
+    for s in range(-10, 1):
         assert L.conv_error_string(s)
     assert L.conv_error_string(12345) == b"unknown status"
 
@@ -174,3 +175,22 @@ def test_device_check_without_gpu(L):
         pytest.skip("a GPU is present")
     ws = m.workspace_size(0, GOOD)
     assert L.conv_fwd(*GOOD, X, W_, B, Y, WSP, ws, None) == DEVICE
+
+
+@pytest.mark.parametrize("args,want", [
+    ((55, 55, 3, 3, 2, 0), (27, 27)), ((224, 224, 2, 2, 2, 0), (112, 112)),
+    ((6, 5, 3, 3, 2, 0), (3, 2)), ((3, 3, 2, 2, 2, 1), (2, 2))])
+def test_pool_output_size(L, args, want):
+    assert m.pool_output_size(*args) == want
+
+
+def test_pool_rejects(L):
+    X, Y, M = 0x10000000, 0x20000000, 0x30000000
+    MODE = -10
+    assert L.pool_fwd(2, 1, 1, 8, 8, 2, 2, 2, 0, X, Y, M, None) == MODE
+    assert L.pool_fwd(0, 1, 1, 8, 8, 2, 2, 2, 2, X, Y, M, None) == SHAPE   # pad >= window
+    assert L.pool_fwd(0, 1, 1, 2, 2, 5, 5, 1, 0, X, Y, M, None) == SHAPE   # window > image
+    assert L.pool_fwd(0, 1, 1, 8, 8, 2, 2, 2, 0, None, Y, M, None) == NULL
+    assert L.pool_bwd(0, 1, 1, 8, 8, 2, 2, 2, 0, Y, None, X, None) == NULL   # max needs mask
+    assert L.pool_fwd(1, 1, 1, 8, 8, 2, 2, 2, 0, X + 4, Y, None, None) == ALIGN
+    assert L.pool_fwd(1, 1, 1, 8, 8, 2, 2, 2, 0, X, X + 64, None, None) == ALIAS
