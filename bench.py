@@ -45,6 +45,8 @@ WORKLOAD_NAMES = {
     2: "VGG-16-shaped conv stack fwd+bwd, batch 32, input 3x224x224 (13 conv layers)",
     3: "ResNet-50-shaped bottleneck conv set fwd+bwd, batch 64 (stem, 4 stages, projections)",
     4: "GoogLeNet-inception-shaped conv set fwd+bwd, batch 64 (3 modules on 28x28/14x14)",
+    5: "AlexNet-shaped network step fwd+bwd, batch 128: 5 conv, 3 max-pool (3x3/2), "
+       "3 inner-product layers (no element-wise layers)",
 }
 
 
@@ -53,7 +55,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", default="1", help="0-4, or 'all' (one JSON line each)")
+    ap.add_argument("--config", default="1", help="0-5, or 'all' (one JSON line each)")
     ap.add_argument("--reps", type=int, default=20, help="timed repeats per layer and pass")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle sample (0 disables it)")
@@ -73,11 +75,17 @@ def parse():
 
 
 def flops_of(L):
+    if not hasattr(L, "K"):
+        return 0.0  # pooling
     return 2.0 * L.N * L.K * L.P * L.Q * (L.C // L.group) * L.R * L.S
 
 
 def bytes_of(L, p):
-    """Compulsory HBM bytes of one pass (each tensor read or written once)."""
+    """Compulsory HBM bytes of one pass (each tensor read or written once;
+    pooling: x, y and the int32 mask forward, dy, mask and dx backward)."""
+    if not hasattr(L, "K"):
+        x, y = L.N * L.C * L.H * L.W, L.N * L.C * L.P * L.Q
+        return 4.0 * (x + 2 * y)
     x = L.N * L.C * L.H * L.W
     y = L.N * L.K * L.P * L.Q
     w = L.K * (L.C // L.group) * L.R * L.S
@@ -183,13 +191,55 @@ class LayerRun:
             raise m.MiconvError(st, f"{p} {self.L.name}")
 
 
+class PoolRun:
+    """Device buffers and prepared library calls of one pooling layer; its
+    passes are "fwd" and "bwd_data" (the input gradient)."""
+
+    passes = ("fwd", "bwd_data")
+
+    def __init__(self, cfg, li, L, stream):
+        import numpy as np
+        import torch
+        import workloads
+        import paper_1903_06934_amd as m
+
+        self.L = L
+        d = workloads.pool_inputs(cfg, li, L)
+        dev = torch.device("cuda")
+        self.x = torch.from_numpy(np.ascontiguousarray(d["x"])).to(dev)
+        self.dy = torch.from_numpy(np.ascontiguousarray(d["dy"])).to(dev)
+        self.y = torch.empty((L.N, L.C, L.P, L.Q), dtype=torch.float32, device=dev)
+        self.mask = torch.empty((L.N, L.C, L.P, L.Q), dtype=torch.int32, device=dev)
+        self.dx = torch.empty_like(self.x)
+        lib = m.lib()
+        mode = m.miconv.POOL_MODES[L.mode]
+        geo = (mode,) + L.pshape
+        self.calls = {
+            "fwd": (lib.pool_fwd, geo + (self.x.data_ptr(), self.y.data_ptr(),
+                                         self.mask.data_ptr(), stream)),
+            "bwd_data": (lib.pool_bwd, geo + (self.dy.data_ptr(), self.mask.data_ptr(),
+                                              self.dx.data_ptr(), stream)),
+        }
+
+    def plan(self, p):
+        return f"{self.L.mode} pooling"
+
+    def run(self, p):
+        fn, args = self.calls[p]
+        st = fn(*args)
+        if st != 0:
+            import paper_1903_06934_amd as m
+            raise m.MiconvError(st, f"{p} {self.L.name}")
+
+
 def stack_step(runs):
     for r in runs:
         for _ in range(r.L.count):
             r.run("fwd")
     for r in reversed(runs):
         for _ in range(r.L.count):
-            r.run("bwd_weight")
+            if not isinstance(r, PoolRun):
+                r.run("bwd_weight")
             if not r.L.first:
                 r.run("bwd_data")
 
@@ -295,7 +345,8 @@ def bench_config(cfg, args, with_cpu):
 
     name, layers = workloads.config(cfg)
     stream = torch.cuda.current_stream().cuda_stream
-    runs = [LayerRun(cfg, li, L, stream, args.tune) for li, L in enumerate(layers)]
+    runs = [PoolRun(cfg, li, L, stream) if isinstance(L, workloads.PoolLayer)
+            else LayerRun(cfg, li, L, stream, args.tune) for li, L in enumerate(layers)]
     torch.cuda.synchronize()
     N = layers[0].N
 
@@ -315,7 +366,7 @@ def bench_config(cfg, args, with_cpu):
     tot = {p: [0.0, 0.0] for p in PASSES}
     for r in runs:
         L = r.L
-        for p in PASSES:
+        for p in getattr(r, "passes", PASSES):
             med, mn = time_call(lambda: r.run(p), args.reps, flush)
             F = flops_of(L)
             B = bytes_of(L, p)
@@ -325,13 +376,14 @@ def bench_config(cfg, args, with_cpu):
                         "ms": round(med, 4), "ms_min": round(mn, 4),
                         "tflops": round(F / med / 1e9, 2), "gbs": round(B / med / 1e6, 1),
                         "roof_frac": round(t_roof / med, 3), "plan": r.plan(p)})
-            if in_stack:
+            if in_stack and F > 0:
                 tot[p][0] += F * L.count
                 tot[p][1] += med * L.count
 
     # Dominant kernel: the GEMM of the (layer, pass) with the largest share
     # of the step.
-    dom = max((x for x in per if x["in_stack"]), key=lambda x: x["ms"] * x["count"])
+    dom = max((x for x in per if x["in_stack"] and x["tflops"] > 0),
+              key=lambda x: x["ms"] * x["count"])
     hev = HipEvents()
     drun = next(r for r in runs if r.L.name == dom["layer"])
     k_ms = kernel_time(drun, dom["pass"], args.reps, hev)
@@ -410,7 +462,7 @@ def main():
         torch.cuda.synchronize()
         print(f"ran {args.profile_pass} x{args.reps} with plan: {run.plan(p)}", flush=True)
         return
-    cfgs = [0, 1, 2, 3, 4] if args.config == "all" else [int(args.config)]
+    cfgs = [0, 1, 2, 3, 4, 5] if args.config == "all" else [int(args.config)]
     for cfg in cfgs:
         line = bench_config(cfg, args, with_cpu=args.cpu_seconds > 0 and cfg == cfgs[0])
         print(json.dumps(line), flush=True)

@@ -270,6 +270,7 @@ constexpr int kSplitRows = 768;
 struct ImgPlan {
     int tile, nsplit, kchunk;  // tile -1: (backward-data phases) each phase by the rule
     int xnb = 0;               // forward: explicit plan, images per column chunk (0: implicit)
+    bool bt = false;           // inner product: batch-transposed plan
 };
 
 // Splits for `tiles` workgroups over Kred rows: about 8 workgroups per CU,
@@ -307,7 +308,38 @@ ImgPlan img_rule(int M, long long Ncol, int Kred, int G, bool allow_split)
 
 bool same_img(const ImgPlan &a, const ImgPlan &b)
 {
-    return a.tile == b.tile && a.nsplit == b.nsplit && a.xnb == b.xnb;
+    return a.tile == b.tile && a.nsplit == b.nsplit && a.xnb == b.xnb && a.bt == b.bt;
+}
+
+// ------------------------------------------------------------ inner product
+// A layer of 1 x 1 images and 1 x 1 filters is an inner-product layer
+// (Sec. IV-A): y[n][k] = b[k] + sum_c w[k][c] x[n][c].  Its GEMMs have the
+// batch as columns, C (or K) floats apart in x (or dy), so the gathered
+// operand would be read one float per cache line.  The batch-transposed plan
+// keeps every gathered row contiguous instead: forward transposes x once into
+// [C][N] and runs the GEMM over one image of 1 x N pixels with w itself as the
+// filter operand (its rows are the packed layout when C % 16 == 0);
+// backward-data takes the batch as rows (dy as the row operand, padded to a
+// multiple of 16 only when K is not one) and w as one image of 1 x C pixels;
+// backward-weight transposes x and dy into [C][N] and [K][N] and runs the
+// one-pixel-per-lane kernel over one image of N pixels.  The epilogues write
+// y [N][K] and dx [N][C] directly.
+bool is_inner_product(const Geom &g)
+{
+    return g.H == 1 && g.W == 1 && g.R == 1 && g.S == 1 && g.P == 1 && g.Q == 1 && g.G == 1 &&
+           g.N <= 65535 * 32 && (long long)g.C * g.N <= kMaxChunkElems &&
+           (long long)g.K * g.N <= kMaxChunkElems;
+}
+
+// Whether the inner product's forward must pack w: its rows are already the
+// packed m-major layout when C is a multiple of 16 (tiles with a k-major
+// filter operand need the copy).
+bool ip_packs_w(const Geom &g, int tile) { return g.C % kBK != 0 || img_tile_shares_a(tile); }
+
+// The problem over the transposed batch: one image of 1 x N pixels.
+Geom batch_columns(const Geom &g)
+{
+    return Geom{1, g.C, 1, g.N, g.K, 1, 1, 1, 0, 1, 1, g.N, g.C, g.K};
 }
 
 // ------------------------------------------------------------ explicit plan
@@ -388,6 +420,11 @@ size_t fwd_pack_bytes(const Geom &g)
 
 ImgPlan fwd_rule(const Geom &g)
 {
+    if (is_inner_product(g)) {
+        ImgPlan p = img_rule(g.K, g.N, g.C, 1, true);
+        p.bt = true;
+        return p;
+    }
     const int nb = images_per_launch(g);
     return img_rule(g.Kg, (long long)(g.N < nb ? g.N : nb) * g.P * g.Q, g.Cg * g.R * g.S, g.G,
                     nb >= g.N);
@@ -397,6 +434,14 @@ void fwd_candidates(const Geom &g, std::vector<ImgPlan> &out)
 {
     out.clear();
     out.push_back(fwd_rule(g));
+    if (is_inner_product(g))
+        img_variants<ImgPlan>(g.K, g.N, g.C, 1, true,
+                              [](const ImgPlan &p) {
+                                  ImgPlan q = p;
+                                  q.bt = true;
+                                  return q;
+                              },
+                              out);
     const int nb = images_per_launch(g);
     img_variants<ImgPlan>(g.Kg, (long long)(g.N < nb ? g.N : nb) * g.P * g.Q, g.Cg * g.R * g.S,
                           g.G, nb >= g.N, [](const ImgPlan &p) { return p; }, out);
@@ -411,6 +456,10 @@ void fwd_candidates(const Geom &g, std::vector<ImgPlan> &out)
 
 size_t fwd_ws(const Geom &g, const ImgPlan &p)
 {
+    if (p.bt)
+        return (ip_packs_w(g, p.tile) ? fwd_pack_bytes(g) : 0) +
+               align_up((size_t)g.C * g.N * sizeof(float)) +
+               (p.nsplit > 1 ? align_up((size_t)p.nsplit * g.N * g.K * sizeof(float)) : 0);
     if (p.xnb > 0)
         return fwd_pack_bytes(g) + col_bytes(g, p.xnb);
     size_t part = p.nsplit > 1 ? align_up((size_t)p.nsplit * g.N * g.K * g.P * g.Q * sizeof(float))
@@ -420,13 +469,14 @@ size_t fwd_ws(const Geom &g, const ImgPlan &p)
 
 void fwd_name(const ImgPlan &p, char *buf, size_t len)
 {
+    const char *pre = p.bt ? "batch-transposed, " : "";
     if (p.xnb > 0)
         snprintf(buf, len, "explicit im2col (%d images a chunk), image GEMM %s", p.xnb,
                  img_tile_name(p.tile));
     else if (p.nsplit > 1)
-        snprintf(buf, len, "image GEMM %s, %d splits", img_tile_name(p.tile), p.nsplit);
+        snprintf(buf, len, "%simage GEMM %s, %d splits", pre, img_tile_name(p.tile), p.nsplit);
     else
-        snprintf(buf, len, "image GEMM %s", img_tile_name(p.tile));
+        snprintf(buf, len, "%simage GEMM %s", pre, img_tile_name(p.tile));
 }
 
 // ------------------------------------------------------------ backward-data
@@ -531,19 +581,23 @@ struct BwdPlan {
     ImgPlan img;   // blocked, explicit: the GEMM's tile; phases: tile (-1: per phase by the
                    // rule) and split-K (stride 1 only)
     int xnb;       // explicit plan: images per column chunk (0: not explicit)
+    bool bt;       // inner product: batch-transposed plan
 };
 
 bool same_plan(const BwdPlan &a, const BwdPlan &b)
 {
     return a.blocked == b.blocked && (!a.blocked || a.bp.f == b.bp.f) && a.xnb == b.xnb &&
-           same_img(a.img, b.img);
+           a.bt == b.bt && same_img(a.img, b.img);
 }
 
 BwdPlan bwd_rule(const Geom &g)
 {
     BwdPlan p{};
     const int nb = images_per_launch(g), n0 = g.N < nb ? g.N : nb;
-    if (block_rule(g, &p.bp)) {
+    if (is_inner_product(g)) {
+        p.bt = true;
+        p.img = img_rule(g.N, g.C, g.K, 1, true);  // rows: the batch
+    } else if (block_rule(g, &p.bp)) {
         p.blocked = true;
         const int kred = g.Kg * p.bp.ntr * p.bp.nts;
         p.img = with_split(pick_img_tile(p.bp.M, (long long)n0 * p.bp.nh * p.bp.nw, kred, g.G),
@@ -561,6 +615,15 @@ void bwd_candidates(const Geom &g, std::vector<BwdPlan> &out)
 {
     out.clear();
     out.push_back(bwd_rule(g));
+    if (is_inner_product(g))
+        img_variants<BwdPlan>(g.N, g.C, g.K, 1, true,
+                              [](const ImgPlan &i) {
+                                  BwdPlan b{};
+                                  b.img = i;
+                                  b.bt = true;
+                                  return b;
+                              },
+                              out);
     const int nb = images_per_launch(g), n0 = g.N < nb ? g.N : nb;
     // Phases, one tile for all of them.
     const int kred_max = g.Kg * ((g.R + g.st - 1) / g.st) * ((g.S + g.st - 1) / g.st);
@@ -589,6 +652,12 @@ void bwd_candidates(const Geom &g, std::vector<BwdPlan> &out)
 
 size_t bwd_ws(const Geom &g, const BwdPlan &p)
 {
+    if (p.bt)  // dy padded to 16 columns (unless K already is), then split slabs
+        return (g.K % kBK || img_tile_shares_a(p.img.tile)
+                    ? align_up((size_t)g.N * pad16(g.K) * sizeof(float))
+                    : 0) +
+               (p.img.nsplit > 1 ? align_up((size_t)p.img.nsplit * g.N * g.C * sizeof(float))
+                                 : 0);
     if (p.xnb > 0)
         return align_up((size_t)g.C * g.R * g.S * pad16(g.Kg) * sizeof(float)) +
                col_bytes(g, p.xnb);
@@ -608,7 +677,12 @@ size_t bwd_ws(const Geom &g, const BwdPlan &p)
 
 void bwd_name(const BwdPlan &p, char *buf, size_t len)
 {
-    if (p.xnb > 0)
+    if (p.bt && p.img.nsplit > 1)
+        snprintf(buf, len, "batch-transposed, image GEMM %s, %d splits", img_tile_name(p.img.tile),
+                 p.img.nsplit);
+    else if (p.bt)
+        snprintf(buf, len, "batch-transposed, image GEMM %s", img_tile_name(p.img.tile));
+    else if (p.xnb > 0)
         snprintf(buf, len, "explicit GEMM + col2im (%d images a chunk), image GEMM %s", p.xnb,
                  img_tile_name(p.img.tile));
     else if (p.blocked)
@@ -633,6 +707,7 @@ struct WgradPlan {
     bool via_part;
     size_t part_bytes, bias_bytes;
     int xnb;  // explicit plan: images per column chunk (0: implicit); nb = xnb then
+    bool bt;  // inner product: batch-transposed plan (the problem of batch_columns)
 };
 
 bool is_tap_tile(int tile) { return tile <= WG_TAP_64x16; }
@@ -715,16 +790,38 @@ WgradPlan wgrad_plan(const Geom &g, int tile = -1, int scale = 0, int nb = 0)
     return p;
 }
 
+WgradPlan wgrad_rule(const Geom &g)
+{
+    if (!is_inner_product(g))
+        return wgrad_plan(g);
+    // Packed-column tiles write dw directly when unsplit (the reduction over a
+    // batch is short); tap-uniform tiles would add a partial buffer of dw's size.
+    WgradPlan p = wgrad_plan(batch_columns(g), g.K > 64 && g.K <= 96 ? WG_PIX_96x64 : WG_PIX_64x64);
+    p.bt = true;
+    return p;
+}
+
 void wgrad_candidates(const Geom &g, std::vector<WgradPlan> &out)
 {
     out.clear();
-    out.push_back(wgrad_plan(g));
+    out.push_back(wgrad_rule(g));
+    if (is_inner_product(g))
+        for (int t = 0; t < kNumWgradTiles; t++)
+            for (int scale : {0, 1, -1}) {
+                WgradPlan p = wgrad_plan(batch_columns(g), t, scale);
+                p.bt = true;
+                bool dup = false;
+                for (const WgradPlan &q : out)
+                    dup = dup || (q.bt && q.tile == p.tile && q.chunk == p.chunk);
+                if (!dup)
+                    out.push_back(p);
+            }
     for (int t = 0; t < kNumWgradTiles; t++)
         for (int scale : {0, 1, -1}) {
             WgradPlan p = wgrad_plan(g, t, scale);
             bool dup = false;
             for (const WgradPlan &q : out)
-                dup = dup || (q.tile == p.tile && q.chunk == p.chunk && q.xnb == 0);
+                dup = dup || (q.tile == p.tile && q.chunk == p.chunk && q.xnb == 0 && !q.bt);
             if (!dup)
                 out.push_back(p);
         }
@@ -738,7 +835,10 @@ void wgrad_candidates(const Geom &g, std::vector<WgradPlan> &out)
 
 size_t wgrad_ws(const Geom &g, const WgradPlan &p)
 {
-    return p.part_bytes + p.bias_bytes + (p.xnb > 0 ? col_bytes(g, p.xnb) : 0);
+    const size_t bt = p.bt ? align_up((size_t)g.C * g.N * sizeof(float)) +
+                                 align_up((size_t)g.K * g.N * sizeof(float))
+                           : 0;
+    return p.part_bytes + p.bias_bytes + (p.xnb > 0 ? col_bytes(g, p.xnb) : 0) + bt;
 }
 
 void wgrad_name(const WgradPlan &p, char *buf, size_t len)
@@ -747,8 +847,8 @@ void wgrad_name(const WgradPlan &p, char *buf, size_t len)
         snprintf(buf, len, "explicit im2col (%d images a chunk), %s, %d splits of %d pixels",
                  p.xnb, wgrad_tile_name(p.tile), p.nsplit, p.chunk);
     else
-        snprintf(buf, len, "%s, %d splits of %d pixels", wgrad_tile_name(p.tile), p.nsplit,
-                 p.chunk);
+        snprintf(buf, len, "%s%s, %d splits of %d pixels", p.bt ? "batch-transposed, " : "",
+                 wgrad_tile_name(p.tile), p.nsplit, p.chunk);
 }
 
 // ------------------------------------------------------------ plan cache
@@ -822,7 +922,7 @@ void plan_store(int pass, const Geom &g, int index)
     else if (pass == MICONV_PASS_BWD_DATA)
         sp.bwd = pick(bwd_rule(g), index, bwd_candidates, g);
     else
-        sp.wgrad = pick(wgrad_plan(g), index, wgrad_candidates, g);
+        sp.wgrad = pick(wgrad_rule(g), index, wgrad_candidates, g);
     std::lock_guard<std::mutex> lock(g_plan_mu);
     if (index <= 0)
         g_plans.erase(k);
@@ -844,7 +944,7 @@ BwdPlan bwd_current(const Geom &g)
 WgradPlan wgrad_current(const Geom &g)
 {
     StoredPlan sp;
-    return stored_plan(MICONV_PASS_BWD_WEIGHT, g, &sp) ? sp.wgrad : wgrad_plan(g);
+    return stored_plan(MICONV_PASS_BWD_WEIGHT, g, &sp) ? sp.wgrad : wgrad_rule(g);
 }
 
 // ------------------------------------------------------------ execution
@@ -914,6 +1014,134 @@ int fwd_gemms(const Geom &g, const ImgPlan &plan, const float *wp, const float *
     return MICONV_OK;
 }
 
+// Inner product by the batch-transposed plan (see is_inner_product).
+int ip_fwd(const Geom &g, const ImgPlan &plan, const float *x, const float *w, const float *b,
+           float *y, void *ws, hipStream_t stream)
+{
+    const int N = g.N, C = g.C, K = g.K;
+    const size_t fb = sizeof(float);
+    const int a_ld = pad16(C);
+    const float *A = w;
+    char *tail = (char *)ws;
+    if (ip_packs_w(g, plan.tile)) {
+        float *wp = (float *)ws;
+        if (launch_pack_fwd(w, wp, K, C, 1, 1, 1, C % kBK == 0, a_ld,
+                            img_tile_shares_a(plan.tile), stream) != hipSuccess)
+            return MICONV_ERR_LAUNCH;
+        A = wp;
+        tail += fwd_pack_bytes(g);
+    }
+    float *xt = (float *)tail;
+    float *part = (float *)(tail + align_up((size_t)C * N * fb));
+    if (launch_transpose(x, xt, N, C, stream) != hipSuccess)
+        return MICONV_ERR_LAUNCH;
+    // Rows: the K filters; columns: the N images, one image of 1 x N pixels
+    // of [C][N]; y[n][k] at n * K + k.
+    ImgGemmArgs a{};
+    a.M = K;
+    a.Ncol = N;
+    a.Kred = C;
+    a.groups = 1;
+    a.A = A;
+    a.a_ld = a_ld;
+    a.a_bytes = (uint32_t)((size_t)K * a_ld * fb);
+    a.src = xt;
+    a.src_bytes = (uint32_t)((size_t)C * N * fb);
+    a.cin = C;
+    a.src_h = 1;
+    a.src_w = N;
+    a.src_hw = N;
+    a.src_img_words = (uint32_t)((size_t)C * N);
+    a.col_hw = make_fastdiv(N);
+    a.col_w = make_fastdiv(N);
+    a.cstep = 1;
+    a.tsign = 1;
+    a.k_cin = make_fastdiv(C);
+    a.k_tw = make_fastdiv(1);
+    a.k_taps = make_fastdiv(1);
+    a.bias = b;
+    a.out = plan.nsplit > 1 ? part : y;
+    a.out_hw = 1;
+    a.out_w = 1;
+    a.ostep = K;
+    a.nsplit = plan.nsplit;
+    a.kchunk = plan.kchunk;
+    a.split_stride = (long long)N * K;
+    if (mark(tl_events.before, stream) != hipSuccess)
+        return MICONV_ERR_LAUNCH;
+    int st = launch_status(launch_img_gemm(a, plan.tile, C % kBK == 0, stream));
+    if (st != MICONV_OK)
+        return st;
+    if (mark(tl_events.after, stream) != hipSuccess)
+        return MICONV_ERR_LAUNCH;
+    if (plan.nsplit > 1)
+        return launch_status(launch_splitk_bias_reduce(part, plan.nsplit, (long long)N * K, N * K,
+                                                       b, 1, K, y, stream));
+    return MICONV_OK;
+}
+
+int ip_bwd_data(const Geom &g, const BwdPlan &plan, const float *dy, const float *w, float *dx,
+                void *ws, hipStream_t stream)
+{
+    const int N = g.N, C = g.C, K = g.K;
+    const size_t fb = sizeof(float);
+    const int a_ld = pad16(K);
+    const float *A = dy;
+    char *tail = (char *)ws;
+    if (K % kBK || img_tile_shares_a(plan.img.tile)) {
+        // dy rows padded to a multiple of 16 (the rows of 1 x 1 "filters").
+        float *dp = (float *)ws;
+        if (launch_pack_fwd(dy, dp, N, K, 1, 1, 1, K % kBK == 0, a_ld,
+                            img_tile_shares_a(plan.img.tile), stream) != hipSuccess)
+            return MICONV_ERR_LAUNCH;
+        A = dp;
+        tail += align_up((size_t)N * a_ld * fb);
+    }
+    float *part = (float *)tail;
+    // Rows: the N images; columns: the C inputs, one image of 1 x C pixels
+    // of w [K][C]; dx[n][c] at n * C + c.
+    ImgGemmArgs a{};
+    a.M = N;
+    a.Ncol = C;
+    a.Kred = K;
+    a.groups = 1;
+    a.A = A;
+    a.a_ld = a_ld;
+    a.a_bytes = (uint32_t)((size_t)N * a_ld * fb);
+    a.src = w;
+    a.src_bytes = (uint32_t)((size_t)K * C * fb);
+    a.cin = K;
+    a.src_h = 1;
+    a.src_w = C;
+    a.src_hw = C;
+    a.src_img_words = (uint32_t)((size_t)K * C);
+    a.col_hw = make_fastdiv(C);
+    a.col_w = make_fastdiv(C);
+    a.cstep = 1;
+    a.tsign = 1;
+    a.k_cin = make_fastdiv(K);
+    a.k_tw = make_fastdiv(1);
+    a.k_taps = make_fastdiv(1);
+    a.out = plan.img.nsplit > 1 ? part : dx;
+    a.out_hw = C;
+    a.out_w = C;
+    a.ostep = 1;
+    a.nsplit = plan.img.nsplit;
+    a.kchunk = plan.img.nsplit > 1 ? plan.img.kchunk : K;
+    a.split_stride = (long long)N * C;
+    if (mark(tl_events.before, stream) != hipSuccess)
+        return MICONV_ERR_LAUNCH;
+    int st = launch_status(launch_img_gemm(a, plan.img.tile, K % kBK == 0, stream));
+    if (st != MICONV_OK)
+        return st;
+    if (mark(tl_events.after, stream) != hipSuccess)
+        return MICONV_ERR_LAUNCH;
+    if (plan.img.nsplit > 1)
+        return launch_status(launch_splitk_bias_reduce(part, plan.img.nsplit, (long long)N * C,
+                                                       N * C, nullptr, 1, 1, dx, stream));
+    return MICONV_OK;
+}
+
 int fwd_exec(const Geom &g, const ImgPlan &plan, const float *x, const float *w, const float *b,
              float *y, void *ws, size_t ws_bytes, hipStream_t stream)
 {
@@ -928,6 +1156,8 @@ int fwd_exec(const Geom &g, const ImgPlan &plan, const float *x, const float *w,
     if (st != MICONV_OK || (st = check_device()) != MICONV_OK)
         return st;
     (void)hipGetLastError();
+    if (plan.bt)
+        return ip_fwd(g, plan, x, w, b, y, ws, stream);
 
     // The filter bank, packed in the layout the tile reads.  The explicit
     // plan's 1x1 GEMM reads the same matrix: its reduction index is the
@@ -1140,6 +1370,8 @@ int bwd_exec(const Geom &g, const BwdPlan &plan, const float *dy, const float *w
     (void)hipGetLastError();
     if (plan.blocked)
         return bwd_blocked(g, plan, dy, w, dx, ws, stream);
+    if (plan.bt)
+        return ip_bwd_data(g, plan, dy, w, dx, ws, stream);
 
     const long long xi = (long long)C * H * W, yi = (long long)K * g.P * g.Q;
     bool marked = false;
@@ -1235,31 +1467,44 @@ int wgrad_exec(const Geom &g, const WgradPlan &p, const float *x, const float *d
 
     float *part = (float *)ws;
     float *db_part = (float *)((char *)ws + p.part_bytes);
+    float *tail = (float *)((char *)ws + p.part_bytes + p.bias_bytes);
     int split0 = 0;
-    if (mark(tl_events.before, stream) != hipSuccess)
-        return MICONV_ERR_LAUNCH;
-    if (p.xnb > 0) {
+    if (p.bt) {
+        // Inner product: both operands transposed to [C][N] and [K][N], one image.
+        float *dyt = (float *)((char *)tail + align_up((size_t)C * N * fb));
+        if (launch_transpose(x, tail, N, C, stream) != hipSuccess ||
+            launch_transpose(dy, dyt, N, K, stream) != hipSuccess ||
+            mark(tl_events.before, stream) != hipSuccess)
+            return MICONV_ERR_LAUNCH;
+        if ((st = wgrad_launches(batch_columns(g), p, tail, dyt, dw, db != nullptr, part, db_part,
+                                 1, split0, stream)) != MICONV_OK)
+            return st;
+    } else if (p.xnb > 0) {
         // Explicit: im2col of a chunk of images, then the 1x1 problem over the
         // columns, whose dw[k][c'] is dw[k][c][r][s].
-        float *col = (float *)((char *)ws + p.part_bytes + p.bias_bytes);
+        if (mark(tl_events.before, stream) != hipSuccess)
+            return MICONV_ERR_LAUNCH;
         const long long xi = (long long)C * H * W, yi = (long long)K * g.P * g.Q;
         for (int n0 = 0; n0 < N; n0 += p.xnb) {
             const int n = N - n0 < p.xnb ? N - n0 : p.xnb;
-            if (launch_im2col(x + n0 * xi, col, n, C, H, W, R, S, g.st, g.pad, g.P, g.Q,
+            if (launch_im2col(x + n0 * xi, tail, n, C, H, W, R, S, g.st, g.pad, g.P, g.Q,
                               stream) != hipSuccess)
                 return MICONV_ERR_LAUNCH;
-            if ((st = wgrad_launches(one_by_one(g, n), p, col, dy + n0 * yi, dw, db != nullptr,
+            if ((st = wgrad_launches(one_by_one(g, n), p, tail, dy + n0 * yi, dw, db != nullptr,
                                      part, db_part, n, split0, stream)) != MICONV_OK)
                 return st;
         }
-    } else if ((st = wgrad_launches(g, p, x, dy, dw, db != nullptr, part, db_part, N, split0,
-                                    stream)) != MICONV_OK) {
-        return st;
+    } else {
+        if (mark(tl_events.before, stream) != hipSuccess)
+            return MICONV_ERR_LAUNCH;
+        if ((st = wgrad_launches(g, p, x, dy, dw, db != nullptr, part, db_part, N, split0,
+                                 stream)) != MICONV_OK)
+            return st;
     }
     if (mark(tl_events.after, stream) != hipSuccess)
         return MICONV_ERR_LAUNCH;
     // Tap-ordered partials go back to dw's [k][c][r][s] (a 1x1 problem has one tap).
-    const int taps = p.xnb > 0 ? 1 : R * S;
+    const int taps = p.xnb > 0 || p.bt ? 1 : R * S;
     const int ncol = g.Cg * R * S;
     const bool tap_order = is_tap_tile(p.tile);
     if (p.via_part &&
@@ -1306,7 +1551,7 @@ size_t candidate_ws(int pass, const Geom &g, int index)
     case MICONV_PASS_BWD_DATA:
         return bwd_ws(g, pick(bwd_rule(g), index, bwd_candidates, g));
     case MICONV_PASS_BWD_WEIGHT:
-        return wgrad_ws(g, pick(wgrad_plan(g), index, wgrad_candidates, g));
+        return wgrad_ws(g, pick(wgrad_rule(g), index, wgrad_candidates, g));
     default:
         return 0;
     }
@@ -1330,7 +1575,7 @@ int candidate_run(int pass, const Geom &g, int index, const TuneBuffers &t, void
         return bwd_exec(g, pick(bwd_rule(g), index, bwd_candidates, g), t.in0, t.in1, t.out0, ws,
                         ws_bytes, stream);
     case MICONV_PASS_BWD_WEIGHT:
-        return wgrad_exec(g, pick(wgrad_plan(g), index, wgrad_candidates, g), t.in0, t.in1,
+        return wgrad_exec(g, pick(wgrad_rule(g), index, wgrad_candidates, g), t.in0, t.in1,
                           t.out0, t.out1, ws, ws_bytes, stream);
     default:
         return MICONV_ERR_PASS;
@@ -1531,7 +1776,7 @@ int conv_plan_name(int pass, int N, int C, int H, int W, int K, int R, int S, in
         bwd_name(pick(bwd_rule(g), index, bwd_candidates, g), buf, len);
         break;
     default:
-        wgrad_name(pick(wgrad_plan(g), index, wgrad_candidates, g), buf, len);
+        wgrad_name(pick(wgrad_rule(g), index, wgrad_candidates, g), buf, len);
         break;
     }
     return MICONV_OK;

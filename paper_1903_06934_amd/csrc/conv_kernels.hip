@@ -854,6 +854,28 @@ __global__ __launch_bounds__(256) void col2im_kernel(const float *__restrict__ c
     }
 }
 
+// out[c][r] = in[r][c] for a rows x cols row-major matrix: 32 x 32 tiles
+// through LDS (rows padded to 33 words), coalesced on both sides.
+__global__ __launch_bounds__(256) void transpose_kernel(const float *__restrict__ in,
+                                                        float *__restrict__ out, int rows,
+                                                        int cols)
+{
+    __shared__ float t[32][33];
+    const int c0 = blockIdx.x * 32, r0 = blockIdx.y * 32;
+    const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+    for (int j = ty; j < 32; j += 8) {
+        const int r = r0 + j, c = c0 + tx;
+        if (r < rows && c < cols)
+            t[j][tx] = in[(size_t)r * cols + c];
+    }
+    __syncthreads();
+    for (int j = ty; j < 32; j += 8) {
+        const int c = c0 + j, r = r0 + tx;
+        if (c < cols && r < rows)
+            out[(size_t)c * rows + r] = t[tx][j];
+    }
+}
+
 // ---------------------------------------------------------------------------
 // Deterministic split-K reduction.  out[dst(i)] = sum over s < nsplit of
 // part[s * stride + i].  A block handles 32 consecutive elements with 8
@@ -1022,6 +1044,13 @@ hipError_t launch_col2im(const float *col, float *dx, int n, int C, int H, int W
     const long long total = (long long)n * C * H * W;
     hipLaunchKernelGGL(col2im_kernel, dim3(grid_for(total)), dim3(256), 0, stream, col, dx,
                        make_fastdiv(H * W), make_fastdiv(W), R, S, stride, pad, P, Q, total);
+    return hipGetLastError();
+}
+
+hipError_t launch_transpose(const float *in, float *out, int rows, int cols, hipStream_t stream)
+{
+    dim3 grid((cols + 31) / 32, (rows + 31) / 32);
+    hipLaunchKernelGGL(transpose_kernel, grid, dim3(256), 0, stream, in, out, rows, cols);
     return hipGetLastError();
 }
 

@@ -156,6 +156,8 @@ hipError_t launch_pool_fwd(bool max_mode, const float *x, float *y, int *mask, i
 hipError_t launch_pool_bwd(bool max_mode, const float *dy, const int *mask, float *dx, int N,
                            int C, int H, int W, int R, int S, int stride, int pad, int P, int Q,
                            hipStream_t stream);
+// out[c][r] = in[r][c] for a rows x cols row-major matrix; rows < 65536 * 32.
+hipError_t launch_transpose(const float *in, float *out, int rows, int cols, hipStream_t stream);
 // Packed reduction-row length of the image GEMM's filter operand.
 inline int pad16(int k) { return (k + 15) & ~15; }
 // out[dst(i)] = sum over s < nsplit of part[s * stride + i] for i < count, in a

@@ -69,16 +69,18 @@ __global__ __launch_bounds__(256) void pool_bwd_kernel(const float *__restrict__
                                                        float *__restrict__ dx, int H, int W,
                                                        int P, int Q, int R, int S, int stride,
                                                        int pad, FastDiv hw, FastDiv w_,
-                                                       uint32_t total)
+                                                       FastDiv st_, uint32_t total)
 {
     for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < total;
          i += gridDim.x * blockDim.x) {
         const uint32_t nc = fast_div(i, hw), pix = i - nc * hw.d;
         const int h = (int)fast_div(pix, w_), w = (int)(pix - (uint32_t)h * w_.d);
         // windows p with p stride - pad <= h < p stride - pad + R
-        const int hp = h + pad, wp = w + pad;
-        const int p0 = hp < R ? 0 : (hp - R) / stride + 1, p1 = min(hp / stride, P - 1);
-        const int q0 = wp < S ? 0 : (wp - S) / stride + 1, q1 = min(wp / stride, Q - 1);
+        const int hp = h + pad, wp = w + pad;  // >= 0
+        const int p0 = hp < R ? 0 : (int)fast_div((uint32_t)(hp - R), st_) + 1;
+        const int p1 = min((int)fast_div((uint32_t)hp, st_), P - 1);
+        const int q0 = wp < S ? 0 : (int)fast_div((uint32_t)(wp - S), st_) + 1;
+        const int q1 = min((int)fast_div((uint32_t)wp, st_), Q - 1);
         const size_t base = (size_t)nc * P * Q;
         float acc = 0.f;
         for (int p = p0; p <= p1; p++)
@@ -128,11 +130,11 @@ hipError_t launch_pool_bwd(bool max_mode, const float *dy, const int *mask, floa
     if (max_mode)
         hipLaunchKernelGGL(pool_bwd_kernel<true>, dim3(pool_grid(total)), dim3(256), 0, stream,
                            dy, mask, dx, H, W, P, Q, R, S, stride, pad, make_fastdiv(H * W),
-                           make_fastdiv(W), total);
+                           make_fastdiv(W), make_fastdiv(stride), total);
     else
         hipLaunchKernelGGL(pool_bwd_kernel<false>, dim3(pool_grid(total)), dim3(256), 0, stream,
                            dy, nullptr, dx, H, W, P, Q, R, S, stride, pad, make_fastdiv(H * W),
-                           make_fastdiv(W), total);
+                           make_fastdiv(W), make_fastdiv(stride), total);
     return hipGetLastError();
 }
 

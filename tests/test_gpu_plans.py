@@ -20,6 +20,8 @@ PLAN_SHAPES = [
     (2, 3, 35, 33, 24, 11, 11, 4, 2, 1),   # blocked backward-data, f = 1 and 2
     (2, 6, 17, 16, 16, 3, 3, 1, 1, 2),     # groups, stride 1 blocks, tap decode
     (3, 48, 11, 11, 40, 3, 3, 2, 1, 2),    # stride phases with groups
+    (4, 64, 1, 1, 48, 1, 1, 1, 0, 1),      # inner product, channel-aligned (w read in place)
+    (5, 300, 1, 1, 70, 1, 1, 1, 0, 1),     # inner product, ragged (w and dy padded copies)
 ]
 
 

@@ -128,12 +128,58 @@ def _googlenet(N=64):
     return out
 
 
+@dataclass(frozen=True)
+class PoolLayer:
+    """A pooling layer (max or average over R x S windows)."""
+    name: str
+    N: int
+    C: int
+    H: int
+    W: int
+    R: int
+    S: int
+    stride: int
+    pad: int
+    mode: str       # "max" | "avg"
+    P: int          # stated output extent (configuration data)
+    Q: int
+    count: int = 1
+    first: bool = False
+
+    @property
+    def pshape(self):
+        return (self.N, self.C, self.H, self.W, self.R, self.S, self.stride, self.pad)
+
+    def with_batch(self, n: int) -> "PoolLayer":
+        return replace(self, N=n)
+
+
+def _alexnet_net(N=128):
+    # The AlexNet-shaped stack with its three overlapping 3x3 / 2 max-pools and
+    # its three inner-product layers (each the convolution of 1 x 1 images
+    # with 1 x 1 filters): the layers of a whole network step minus the
+    # element-wise ones (activations, normalisation, dropout, loss).
+    c = _alexnet(N)
+    x = "xavier"
+
+    def pool(name, C, HW, PQ):
+        return PoolLayer(name, N, C, HW, HW, 3, 3, 2, 0, "max", PQ, PQ)
+
+    def fc(name, cin, cout):
+        return _sq(name, N, cin, 1, cout, 1, 1, 0, 1, 1, x)
+
+    return [c[0], pool("pool1", 96, 55, 27), c[1], pool("pool2", 256, 27, 13), c[2], c[3],
+            c[4], pool("pool5", 256, 13, 6), fc("fc6", 256 * 6 * 6, 4096),
+            fc("fc7", 4096, 4096), fc("fc8", 4096, 1000)]
+
+
 CONFIGS = {
     0: ("tiny", _tiny()),
     1: ("alexnet", _alexnet()),
     2: ("vgg16", _vgg16()),
     3: ("resnet50", _resnet50()),
     4: ("googlenet", _googlenet()),
+    5: ("alexnet_net", _alexnet_net()),
 }
 
 
@@ -198,6 +244,13 @@ def make_inputs(shape, P, Q, seed=(0, 0), init="he", tensors=("x", "w", "b", "dy
     if "dy" in tensors:
         out["dy"] = _normal((cfg, li, 3), (N, K, P, Q))
     return out
+
+
+def pool_inputs(cfg: int, li: int, layer: PoolLayer):
+    """x [N,C,H,W] and dy [N,C,P,Q] of pooling layer ``li`` of ``cfg``, drawn
+    like a convolution layer's x and dy (t = 0 and 3)."""
+    return {"x": _normal((cfg, li, 0), (layer.N, layer.C, layer.H, layer.W)),
+            "dy": _normal((cfg, li, 3), (layer.N, layer.C, layer.P, layer.Q))}
 
 
 def layer_inputs(cfg: int, li: int, layer: Layer | None = None, tensors=("x", "w", "b", "dy")):
