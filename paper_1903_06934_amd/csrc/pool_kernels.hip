@@ -87,8 +87,9 @@ __global__ __launch_bounds__(256) void pool_bwd_kernel(const float *__restrict__
             for (int q = q0; q <= q1; q++) {
                 const size_t o = base + (size_t)p * Q + q;
                 if constexpr (MAX) {
-                    if (mask[o] == (int)pix)
-                        acc += dy[o];
+                    // Both loads issued together; the select keeps the sum's order.
+                    const float g = dy[o];
+                    acc += mask[o] == (int)pix ? g : 0.f;
                 } else {
                     const Win wh = window(p, stride, pad, R, H), ww = window(q, stride, pad, S, W);
                     acc += dy[o] / (float)(wh.ext * ww.ext);
