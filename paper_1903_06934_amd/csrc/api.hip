@@ -231,7 +231,7 @@ int images_per_launch(const Geom &g)
 // iterations before keeping the fastest), overrides the rule.
 
 constexpr int kNumImgTiles = 7;
-constexpr int kNumWgradTiles = 6;
+constexpr int kNumWgradTiles = 9;
 
 const char *img_tile_name(int tile)
 {
@@ -710,19 +710,21 @@ struct WgradPlan {
     bool bt;  // inner product: batch-transposed plan (the problem of batch_columns)
 };
 
-bool is_tap_tile(int tile) { return tile <= WG_TAP_64x16; }
+bool is_tap_tile(int tile) { return wgrad_tile_is_tap(tile); }
 
 void wgrad_tile_dims(int tile, int &bm, int &bn)
 {
-    static const int dims[][2] = {{64, 32}, {64, 48}, {64, 16}, {96, 64}, {64, 64}, {64, 32}};
+    static const int dims[][2] = {{64, 32}, {64, 48}, {64, 16}, {96, 64}, {64, 64},
+                                  {64, 32}, {128, 32}, {64, 64}, {128, 64}};
     bm = dims[tile][0];
     bn = dims[tile][1];
 }
 
 const char *wgrad_tile_name(int tile)
 {
-    static const char *names[] = {"tap 64x32", "tap 64x48", "tap 64x16",
-                                  "pixel 96x64", "pixel 64x64", "pixel 64x32"};
+    static const char *names[] = {"tap 64x32", "tap 64x48",  "tap 64x16",
+                                  "pixel 96x64", "pixel 64x64", "pixel 64x32",
+                                  "tap 128x32", "tap 64x64",  "tap 128x64"};
     return names[tile];
 }
 
@@ -735,12 +737,16 @@ WgradPlan wgrad_plan(const Geom &g, int tile = -1, int scale = 0, int nb = 0)
     long long PQ = (long long)g.P * g.Q, Kred = (long long)g.N * PQ;
     if (tile < 0) {
         if (g.Cg >= 32 || g.Cg == 16) {
-            // Tap-uniform tiles of 64 rows of K/G by 32 channels of one tap, by
-            // 48 channels when C/G is a multiple of 48 but not of 64, or by 16
-            // for 16 channels, so that no column stays idle.  Small tiles
-            // measured fastest on every layer of the five stacks: six fit on a CU.
-            const int bn = g.Cg == 16 ? 16 : (g.Cg % 64 != 0 && g.Cg % 48 == 0) ? 48 : 32;
-            tile = bn == 16 ? WG_TAP_64x16 : bn == 48 ? WG_TAP_64x48 : WG_TAP_64x32;
+            // Tap-uniform tiles of 64 rows of K/G by 64 channels of one tap when
+            // C/G is a multiple of 64 (3-13 % over 64 x 32 on the VGG-16 and
+            // ResNet 1x1 layers, up to 5 % behind it on ResNet's 3x3 ones), by 48
+            // when it is a multiple of 48, by 16 for 16 channels, else by 32, so
+            // that no column stays idle.
+            const int bn = g.Cg == 16 ? 16 : g.Cg % 64 == 0 ? 64 : g.Cg % 48 == 0 ? 48 : 32;
+            tile = bn == 16   ? WG_TAP_64x16
+                   : bn == 64 ? WG_TAP_64x64
+                   : bn == 48 ? WG_TAP_64x48
+                              : WG_TAP_64x32;
         } else {
             // Few channels per group: the same one-pixel-per-lane kernel with
             // (c, r, s) packed into the columns, 96 rows for 65-96 filters.

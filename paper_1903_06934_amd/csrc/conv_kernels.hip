@@ -976,6 +976,9 @@ hipError_t launch_wgrad_gemm(const WgradArgs &a, int tile, hipStream_t stream)
     case WG_TAP_64x32: return wgrad_launch<64, 32, 2, 2, 16>(a, stream);
     case WG_TAP_64x48: return wgrad_launch<64, 48, 4, 1, 16>(a, stream);
     case WG_TAP_64x16: return wgrad_launch<64, 16, 4, 1, 16>(a, stream);
+    case WG_TAP_128x32: return wgrad_launch<128, 32, 4, 1, 16>(a, stream);
+    case WG_TAP_64x64: return wgrad_launch<64, 64, 2, 2, 16>(a, stream);
+    case WG_TAP_128x64: return wgrad_launch<128, 64, 2, 2, 16>(a, stream);
     case WG_PIX_96x64: return wgrad_launch<96, 64, 2, 2, 16, true>(a, stream);
     case WG_PIX_64x64: return wgrad_launch<64, 64, 4, 1, 16, true>(a, stream);
     case WG_PIX_64x32: return wgrad_launch<64, 32, 2, 2, 16, true>(a, stream);

@@ -110,7 +110,11 @@ inline bool img_tile_shares_a(int tile) { return tile == IMG_16x128; }
 // Backward-weight tiles of the one-pixel-per-lane kernel: tap-uniform
 // (BM rows of K/G x BN channels of one tap) or packed (BM rows x BN
 // consecutive (c, r, s) columns).
-enum WgradTile { WG_TAP_64x32 = 0, WG_TAP_64x48, WG_TAP_64x16, WG_PIX_96x64, WG_PIX_64x64, WG_PIX_64x32 };
+enum WgradTile {
+    WG_TAP_64x32 = 0, WG_TAP_64x48, WG_TAP_64x16, WG_PIX_96x64, WG_PIX_64x64, WG_PIX_64x32,
+    WG_TAP_128x32, WG_TAP_64x64, WG_TAP_128x64
+};
+inline bool wgrad_tile_is_tap(int tile) { return tile <= WG_TAP_64x16 || tile >= WG_TAP_128x32; }
 
 hipError_t launch_img_gemm(const ImgGemmArgs &a, int tile, bool fast, hipStream_t stream);
 hipError_t launch_wgrad_gemm(const WgradArgs &a, int tile, hipStream_t stream);
