@@ -29,7 +29,10 @@
  *     conv_workspace_size(...) bytes; its contents are undefined afterwards;
  *   - kernels are enqueued on `stream` (NULL = the null stream) and the
  *     calls return without synchronising; the library keeps no pointer
- *     after returning and allocates no device memory;
+ *     after returning and allocates no device memory; as the passes only
+ *     launch kernels (no memset, copy or synchronisation), they can be
+ *     captured into a HIP graph and replayed (conv_tune, which times and
+ *     synchronises, cannot);
  *   - results are bitwise reproducible for the same shape, inputs, device
  *     and plan (every reduction runs in a fixed order, no float atomics);
  *     the plan is the built-in rule unless one was set or tuned for the
