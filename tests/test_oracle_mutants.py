@@ -9,6 +9,7 @@ import pytest
 
 import oracle
 from oracle_pins import ALL_CHECKS
+from test_oracle_pool import POOL_CHECKS
 
 # (name, text in oracle.c, replacement, which occurrence (0-based))
 MUTANTS = [
@@ -31,6 +32,23 @@ MUTANTS = [
     ("gather_dx_phase_check_dropped", "ph < 0 || qw < 0 || ph % stride || qw % stride",
      "ph < 0 || qw < 0 || qw % stride", 0),
     ("gather_dw_group_dropped", "x_at(x, C, H, W, n, g * Cg + c,", "x_at(x, C, H, W, n, c,", 2),
+]
+
+# Pooling (checked against the pooling pins).
+POOL_MUTANTS = [
+    ("pool_size_floor", "i64 out = (span + stride - 1) / stride + 1;",
+     "i64 out = span / stride + 1;", 0),
+    ("pool_size_no_last_window_rule", "if (pad > 0 && (out - 1) * stride >= (i64)in + pad)",
+     "if (0)", 0),
+    ("pool_window_ignores_pad", "i64 start = (i64)p * stride - pad;",
+     "i64 start = (i64)p * stride;", 0),
+    ("pool_avg_divisor_without_padding", "*ext = end - start;",
+     "*ext = (end > in ? in : end) - (start < 0 ? 0 : start);", 0),
+    ("pool_avg_overhang_counted", "end = (i64)in + pad;", "end = end + 0;", 0),
+    ("pool_max_last_maximum", "if (xp[h * W + w] > best) {", "if (xp[h * W + w] >= best) {", 0),
+    ("pool_bwd_avg_share_undivided", "double share = g / (double)(eh * ew);",
+     "double share = g;", 0),
+    ("pool_bwd_max_wrong_element", "dxp[arg] += g;", "dxp[arg > 0 ? arg - 1 : 0] += g;", 0),
 ]
 
 
@@ -56,3 +74,19 @@ def test_mutant_is_caught(tmp_path, name, old, new, nth):
         except Exception:  # any pin that fails or cannot even run catches it
             failed.append(check.__name__)
     assert failed, f"mutant {name} passed every pin"
+
+
+@pytest.mark.parametrize("name,old,new,nth", POOL_MUTANTS, ids=[m[0] for m in POOL_MUTANTS])
+def test_pool_mutant_is_caught(tmp_path, name, old, new, nth):
+    src = open(oracle.SOURCE).read()
+    path = tmp_path / f"{name}.c"
+    path.write_text(_mutate(src, old, new, nth))
+    lib = oracle.build(str(path), str(tmp_path / f"lib{name}.so"), werror=False)
+    o = oracle.Oracle(lib)
+    failed = []
+    for check in POOL_CHECKS:
+        try:
+            check(o)
+        except Exception:
+            failed.append(check.__name__)
+    assert failed, f"mutant {name} passed every pooling pin"
