@@ -69,6 +69,9 @@ def parse():
     ap.add_argument("--plan", type=int, default=None, metavar="INDEX",
                     help="with --profile-pass: run candidate plan INDEX (conv_plan_set) "
                          "instead of tuning")
+    ap.add_argument("--graph", type=int, default=0, choices=(0, 1),
+                    help="1: capture one stack step into a HIP graph and time its replays "
+                         "(0: eager launches)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only copy 1 GiB device-to-device 3 times (HBM counter calibration)")
     return ap.parse_args()
@@ -340,6 +343,16 @@ def cpu_baseline(cfg, layers, target_s):
 
 
 def bench_config(cfg, args, with_cpu):
+    import contextlib
+    import torch
+    # A graph is captured on a side stream (the legacy stream cannot
+    # capture), so then every launch of the run goes there.
+    side = torch.cuda.Stream() if args.graph else None
+    with torch.cuda.stream(side) if side is not None else contextlib.nullcontext():
+        return _bench_config(cfg, args, with_cpu)
+
+
+def _bench_config(cfg, args, with_cpu):
     import torch
     import workloads
 
@@ -353,10 +366,18 @@ def bench_config(cfg, args, with_cpu):
     for _ in range(args.warmup):
         stack_step(runs)
     torch.cuda.synchronize()
+    step = lambda: stack_step(runs)  # noqa: E731
+    if args.graph:
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=torch.cuda.current_stream()):
+            stack_step(runs)
+        graph.replay()
+        torch.cuda.synchronize()
+        step = graph.replay
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     for _ in range(args.steps):
-        stack_step(runs)
+        step()
     e1.record()
     torch.cuda.synchronize()
     step_ms = e0.elapsed_time(e1) / args.steps
@@ -412,7 +433,8 @@ def bench_config(cfg, args, with_cpu):
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "f32", "data": "synthetic",
         "config": {"workload": WORKLOAD_NAMES[cfg], "name": name, "global_batch": N,
-                   "layers": len(layers), "parallelism": "single GPU"},
+                   "layers": len(layers), "parallelism": "single GPU",
+                   "launch": "hip graph" if args.graph else "eager"},
         "tflops_per_pass": {p: round(tot[p][0] / tot[p][1] / 1e9, 2) if tot[p][1] else None
                             for p in PASSES},
         "stack_tflops": round(sum(v[0] for v in tot.values()) / (step_ms * 1e9), 2),
