@@ -807,6 +807,17 @@ WgradPlan wgrad_rule(const Geom &g)
     return p;
 }
 
+// A tile whose columns are more than twice the problem's (channels of one
+// tap for tap-uniform tiles, packed (c, r, s) columns otherwise; rounded up
+// to 16) only multiplies zeros: not a candidate.  (Rows are not pruned: a
+// 64-row tap tile was measured fastest on a 16-filter 1x1 layer.)
+bool wgrad_tile_fits(const Geom &g, int tile)
+{
+    int bm, bn;
+    wgrad_tile_dims(tile, bm, bn);
+    return bn <= 2 * pad16(is_tap_tile(tile) ? g.Cg : g.Cg * g.R * g.S);
+}
+
 void wgrad_candidates(const Geom &g, std::vector<WgradPlan> &out)
 {
     out.clear();
@@ -814,6 +825,8 @@ void wgrad_candidates(const Geom &g, std::vector<WgradPlan> &out)
     if (is_inner_product(g))
         for (int t = 0; t < kNumWgradTiles; t++)
             for (int scale : {0, 1, -1}) {
+                if (!wgrad_tile_fits(batch_columns(g), t))
+                    continue;
                 WgradPlan p = wgrad_plan(batch_columns(g), t, scale);
                 p.bt = true;
                 bool dup = false;
@@ -824,6 +837,8 @@ void wgrad_candidates(const Geom &g, std::vector<WgradPlan> &out)
             }
     for (int t = 0; t < kNumWgradTiles; t++)
         for (int scale : {0, 1, -1}) {
+            if (!wgrad_tile_fits(g, t))
+                continue;
             WgradPlan p = wgrad_plan(g, t, scale);
             bool dup = false;
             for (const WgradPlan &q : out)
