@@ -126,3 +126,63 @@ def test_tune_respects_workspace():
     assert m.plan_workspace_size(m.PASS_FWD, shape, chosen) <= nbytes
     ref, absum = oracle.conv_fwd(shape, d["x"], d["w"], d["b"])
     assert_within(host(y), ref, absum, "tuned forward")
+
+
+def _tuned_cases():
+    out = []
+    for cfg in (1, 5):
+        name, layers = workloads.config(cfg)
+        for li, L in enumerate(layers):
+            if isinstance(L, workloads.PoolLayer) or (cfg == 5 and L.R > 1):
+                continue  # pooling has its own tests; config 5's convolutions are config 1's
+            out.append(pytest.param(cfg, li, id=f"{name}-{L.name}"))
+    return out
+
+
+@pytest.mark.parametrize("cfg,li", _tuned_cases())
+def test_tuned_plans_full_batch_sampled(cfg, li):
+    """The benchmark's launch configuration: every pass of the layer at its
+    configured batch with the plan conv_tune keeps (as bench.py does before
+    timing), then sampled elements against the oracle's gather forms."""
+    import torch
+    import paper_1903_06934_amd as m
+    from gpu_util import sample_indices
+    L = workloads.config(cfg)[1][li]
+    d = workloads.layer_inputs(cfg, li)
+    shape = L.shape
+    N, C, H, W, K, R, S, st, pad, G = shape
+    t = {k: dev(v) for k, v in d.items()}
+    outs = {0: [torch.empty((N, K, L.P, L.Q), device="cuda")],
+            1: [torch.empty((N, C, H, W), device="cuda")],
+            2: [torch.empty((K, C // G, R, S), device="cuda"), torch.empty(K, device="cuda")]}
+    ins = {0: (t["x"], t["w"], t["b"]), 1: (t["dy"], t["w"], None), 2: (t["x"], t["dy"], None)}
+    names = {}
+    for p in (m.PASS_FWD, m.PASS_BWD_DATA, m.PASS_BWD_WEIGHT):
+        n = m.plan_count(p, shape)
+        nbytes = max(m.plan_workspace_size(p, shape, i) for i in range(n))
+        ws = torch.empty(max(nbytes, 16), dtype=torch.uint8, device="cuda")
+        o = outs[p] + [None] * (2 - len(outs[p]))
+        chosen = m.conv_tune(p, shape, *ins[p], o[0], o[1], ws, reps=2)
+        names[p] = f"{chosen}: {m.plan_name(p, shape, chosen)}"
+        del ws
+    # The ordinary calls now run the stored plans.
+    rng = np.random.default_rng([cfg, li, 77])
+    y = host(m.conv_fwd(t["x"], t["w"], t["b"], st, pad, G))
+    idx = sample_indices(y.shape, rng, groups=G)
+    v, a = oracle.conv_fwd_at(shape, d["x"], d["w"], d["b"], idx)
+    assert_within(y.ravel()[idx], v, a, f"fwd with plan {names[0]}")
+    del y
+    dx = host(m.conv_bwd_data(t["dy"], t["w"], (H, W), st, pad, G))
+    idx = sample_indices(dx.shape, rng, groups=G)
+    v, a = oracle.conv_bwd_data_at(shape, d["dy"], d["w"], idx)
+    assert_within(dx.ravel()[idx], v, a, f"bwd_data with plan {names[1]}")
+    del dx
+    dw, db = m.conv_bwd_weight(t["x"], t["dy"], (R, S), st, pad, G)
+    dw, db = host(dw), host(db)
+    npq = N * L.P * L.Q
+    count = int(min(2048, max(128, 1e9 / npq)))
+    idx = sample_indices(dw.shape, rng, count=count, groups=1, channel_axis=0)
+    v, a = oracle.conv_bwd_weight_at(shape, d["x"], d["dy"], idx)
+    assert_within(dw.ravel()[idx], v, a, f"bwd_weight with plan {names[2]}")
+    v, a = oracle.bias_grad(d["dy"])
+    assert_within(db, v, a, f"bias_grad with plan {names[2]}")
