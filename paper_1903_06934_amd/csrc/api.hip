@@ -236,6 +236,7 @@ constexpr int kNumWgradTiles = 9;
 const char *img_tile_name(int tile)
 {
     static const char *names[] = {"64x64", "128x64", "16x128", "32x64", "48x64", "96x64", "96x128"};
+    static_assert(sizeof(names) / sizeof(names[0]) == kNumImgTiles, "one name per tile");
     return tile >= 0 && tile < kNumImgTiles ? names[tile] : "?";
 }
 
@@ -716,16 +717,18 @@ void wgrad_tile_dims(int tile, int &bm, int &bn)
 {
     static const int dims[][2] = {{64, 32}, {64, 48}, {64, 16}, {96, 64}, {64, 64},
                                   {64, 32}, {128, 32}, {64, 64}, {128, 64}};
+    static_assert(sizeof(dims) / sizeof(dims[0]) == kNumWgradTiles, "one shape per tile");
     bm = dims[tile][0];
     bn = dims[tile][1];
 }
 
 const char *wgrad_tile_name(int tile)
 {
-    static const char *names[] = {"tap 64x32", "tap 64x48",  "tap 64x16",
+    static const char *names[] = {"tap 64x32",  "tap 64x48",   "tap 64x16",
                                   "pixel 96x64", "pixel 64x64", "pixel 64x32",
-                                  "tap 128x32", "tap 64x64",  "tap 128x64"};
-    return names[tile];
+                                  "tap 128x32", "tap 64x64",   "tap 128x64"};
+    static_assert(sizeof(names) / sizeof(names[0]) == kNumWgradTiles, "one name per tile");
+    return tile >= 0 && tile < kNumWgradTiles ? names[tile] : "?";
 }
 
 // tile -1: the rule's tile.  scale: the rule's split count times 2^scale.
