@@ -109,3 +109,32 @@ def test_explicit_candidates():
     for p in PASSES:
         n = m.plan_count(p, one)
         assert not any(m.plan_name(p, one, i).startswith("explicit") for i in range(n))
+
+
+def test_plan_table_is_thread_safe():
+    """Threads storing and reading choices for their own shapes at the same
+    time (ctypes releases the GIL around each call) each read back exactly
+    what they stored."""
+    import threading
+    shapes = [(8 + i, 16, 20, 20, 32, 3, 3, 1, 1, 1) for i in range(8)]
+    errors = []
+
+    def work(shape):
+        try:
+            n = m.plan_count(m.PASS_FWD, shape)
+            for r in range(400):
+                idx = r % n
+                m.plan_set(m.PASS_FWD, shape, idx)
+                got = m.plan_get(m.PASS_FWD, shape)
+                if got != idx:
+                    errors.append((shape, idx, got))
+                    return
+        except Exception as e:  # noqa: BLE001 - reported below
+            errors.append(e)
+
+    threads = [threading.Thread(target=work, args=(s,)) for s in shapes]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors[:3]
