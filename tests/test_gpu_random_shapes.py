@@ -1,10 +1,11 @@
 """Parity over a fixed set of seeded random small shapes: every pass with the
-built-in rule and with up to two more candidate plans drawn from the pass's list,
-against the oracle (full tensors).  The shapes mix strides 1-4, padding up to
-the larger filter side minus one (so at times past the smaller one), 1-4 groups, square and oblong filters and images,
-and channel counts on and off multiples of 16, so that every tile, the
-blocked and phase backward-data plans and the tap-uniform and packed
-backward-weight tiles meet ragged edges they are not tuned for."""
+built-in rule and with up to two more candidate plans drawn from the pass's
+list, against the oracle (full tensors).  The shapes mix strides 1-4, padding
+up to the larger filter side minus one (so at times past the smaller one),
+1-4 groups, square and oblong filters and images, and channel counts on and
+off multiples of 16, so that every tile, the blocked and phase backward-data
+plans and the tap-uniform and packed backward-weight tiles meet ragged edges
+they are not tuned for."""
 import numpy as np
 import pytest
 
