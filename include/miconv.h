@@ -221,8 +221,11 @@ int conv_tune(int pass, int N, int C, int H, int W, int K, int R, int S, int str
  * names the element; avg: dy / area).  mask is required for max.
  * Buffers are caller-owned device memory, 16-byte aligned, outputs not
  * overlapping inputs; no workspace.  Statuses as for the convolution calls,
- * plus MICONV_ERR_MODE; MICONV_ERR_SHAPE also when pad >= R or pad >= S or
- * N*C*H*W or N*C*P*Q is above 2^31 - 1.  pool_output_size is host-only.
+ * plus MICONV_ERR_MODE; MICONV_ERR_SHAPE also when pad >= R or pad >= S,
+ * when N*C*H*W or N*C*P*Q is above 2^31 - 1, or when the last window would
+ * cover no element of the image (possible without padding when the stride
+ * exceeds the window: the rounded-up count then puts that window past the
+ * edge).  pool_output_size is host-only.
  */
 #define MICONV_POOL_MAX 0
 #define MICONV_POOL_AVG 1

@@ -159,6 +159,8 @@ class Oracle:
         (int64; -1 for avg)."""
         N, C, H, W, R, S, st, pad = (int(v) for v in pshape)
         P, Q = self.pool_out_size(H, R, st, pad), self.pool_out_size(W, S, st, pad)
+        if P < 1 or Q < 1:
+            raise ValueError(f"no pooling for {pshape}: a window would cover no input element")
         x = _f64(x)
         y = np.empty((N, C, P, Q))
         ay = np.empty_like(y)
@@ -175,6 +177,8 @@ class Oracle:
         if _pool_mode(mode) == 0:
             m = np.ascontiguousarray(np.asarray(mask, dtype=np.int64))
             assert m.shape == dy.shape
+            if m.size and (m.min() < 0 or m.max() >= H * W):
+                raise ValueError("max-pooling mask entry outside the input plane")
         dx = np.empty((N, C, H, W))
         adx = np.empty_like(dx)
         self.lib.oracle_pool_bwd(_pool_mode(mode), N, C, H, W, R, S, st, pad, _ptr(dy),

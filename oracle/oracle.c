@@ -371,6 +371,10 @@ int oracle_pool_out_size(int in, int filt, int stride, int pad)
     i64 out = (span + stride - 1) / stride + 1;
     if (pad > 0 && (out - 1) * stride >= (i64)in + pad)
         out--;
+    /* Without padding the rounded-up count can put the last window wholly
+     * past the image (stride > filt): no input element, no pooling. */
+    if ((out - 1) * stride - pad >= (i64)in)
+        return 0;
     return (int)out;
 }
 
@@ -454,6 +458,8 @@ void oracle_pool_bwd(int mode, int N, int C, int H, int W, int R, int S, int str
                 double g = dy[o];
                 if (mode == 0) {
                     i64 arg = mask[o];
+                    if (arg < 0 || arg >= (i64)H * W)
+                        continue; /* the Python side rejects such masks first */
                     dxp[arg] += g;
                     if (adxp)
                         adxp[arg] += fabs(g);

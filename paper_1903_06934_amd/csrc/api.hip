@@ -1636,6 +1636,10 @@ int make_pool(int mode, int N, int C, int H, int W, int R, int S, int stride, in
     const int P = pool_extent(H, R, stride, pad), Q = pool_extent(W, S, stride, pad);
     if (P < 1 || Q < 1)
         return MICONV_ERR_SHAPE;
+    // Without padding the rounded-up count can put the last window wholly past
+    // the image (stride > window): a window with no input element.
+    if ((long long)(P - 1) * stride - pad >= H || (long long)(Q - 1) * stride - pad >= W)
+        return MICONV_ERR_SHAPE;
     if ((long long)N * C * H * W > kMaxElems || (long long)N * C * P * Q > kMaxElems)
         return MICONV_ERR_SHAPE;
     *g = PoolGeom{N, C, H, W, R, S, stride, pad, P, Q};

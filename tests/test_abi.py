@@ -190,6 +190,8 @@ def test_pool_rejects(L):
     assert L.pool_fwd(2, 1, 1, 8, 8, 2, 2, 2, 0, X, Y, M, None) == MODE
     assert L.pool_fwd(0, 1, 1, 8, 8, 2, 2, 2, 2, X, Y, M, None) == SHAPE   # pad >= window
     assert L.pool_fwd(0, 1, 1, 2, 2, 5, 5, 1, 0, X, Y, M, None) == SHAPE   # window > image
+    assert L.pool_fwd(0, 1, 1, 10, 9, 1, 1, 2, 0, X, Y, M, None) == SHAPE  # last window past the image
+    assert L.pool_bwd(1, 1, 1, 9, 10, 1, 1, 2, 0, Y, None, X, None) == SHAPE
     assert L.pool_fwd(0, 1, 1, 8, 8, 2, 2, 2, 0, None, Y, M, None) == NULL
     assert L.pool_bwd(0, 1, 1, 8, 8, 2, 2, 2, 0, Y, None, X, None) == NULL   # max needs mask
     assert L.pool_fwd(1, 1, 1, 8, 8, 2, 2, 2, 0, X + 4, Y, None, None) == ALIGN

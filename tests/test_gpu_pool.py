@@ -60,6 +60,42 @@ def test_pool_matches_oracle(mode, pshape):
     assert np.array_equal(dx.view(np.uint32), dx2.view(np.uint32))
 
 
+def _random_pool_cases(count=60, seed=1903):
+    rng = np.random.default_rng(seed)
+    out = []
+    while len(out) < count:
+        R = int(rng.integers(1, 6))
+        S = int(rng.choice([R, int(rng.integers(1, 6))]))
+        st = int(rng.integers(1, 5))
+        pad = int(rng.integers(0, min(R, S)))
+        H = int(rng.integers(max(R, S), 21))
+        W = int(rng.integers(max(R, S), 21))
+        if oracle.pool_out_size(H, R, st, pad) < 1 or oracle.pool_out_size(W, S, st, pad) < 1:
+            continue  # a window past the image: refused (tested on the CPU)
+        out.append(("max" if len(out) % 2 == 0 else "avg",
+                    (int(rng.integers(1, 4)), int(rng.integers(1, 9)), H, W, R, S, st, pad)))
+    return out
+
+
+@pytest.mark.parametrize("mode,pshape", _random_pool_cases(), ids=lambda v: str(v))
+def test_pool_random_shapes(mode, pshape):
+    """Seeded random windows, strides, padding and plane sizes (ceil-mode
+    edges, overhangs and dropped last windows among them)."""
+    N, C, H, W, R, S, st, pad = pshape
+    rng = np.random.default_rng(list(pshape) + [7])
+    x = rng.standard_normal((N, C, H, W)).astype(np.float32)
+    y_ref, ay, mask_ref = oracle.pool_fwd(mode, pshape, x)
+    dy = rng.standard_normal(y_ref.shape).astype(np.float32)
+    y, mask, dx = _pool_gpu(mode, pshape, x, dy)
+    if mode == "max":
+        assert np.array_equal(y.astype(np.float64), y_ref)
+        assert np.array_equal(mask.astype(np.int64), mask_ref)
+    else:
+        assert_within(y, y_ref, ay, f"avg pool fwd {pshape}")
+    dx_ref, adx = oracle.pool_bwd(mode, pshape, dy, mask_ref)
+    assert_within(dx, dx_ref, adx, f"{mode} pool bwd {pshape}")
+
+
 def test_max_pool_ties_take_the_first_element():
     """A constant plane: every window's argmax is its first element inside
     the image, in row-major order."""

@@ -40,6 +40,7 @@ POOL_MUTANTS = [
      "i64 out = span / stride + 1;", 0),
     ("pool_size_no_last_window_rule", "if (pad > 0 && (out - 1) * stride >= (i64)in + pad)",
      "if (0)", 0),
+    ("pool_size_allows_empty_window", "if ((out - 1) * stride - pad >= (i64)in)", "if (0)", 0),
     ("pool_window_ignores_pad", "i64 start = (i64)p * stride - pad;",
      "i64 start = (i64)p * stride;", 0),
     ("pool_avg_divisor_without_padding", "*ext = end - start;",

@@ -38,6 +38,25 @@ def pin_pool_out_size(o):
         assert o.pool_out_size(n_in, f, st, pad) == want, (n_in, f, st, pad)
 
 
+def pin_every_window_holds_an_element(o):
+    """Every window of an accepted extent holds at least one image element
+    (brute force over small extents); without padding and with a stride
+    above the window the ceil rule can put its last window past the image,
+    and such an extent is refused (0): 10 elements, window 1, stride 2 would
+    be 6 windows, the sixth starting at 10."""
+    for n in range(1, 13):
+        for f in range(1, min(n, 5) + 1):
+            for st in range(1, 6):
+                for pad in range(f):
+                    for p in range(o.pool_out_size(n, f, st, pad)):
+                        start = p * st - pad
+                        assert min(start + f, n) > max(start, 0), (n, f, st, pad, p)
+    assert o.pool_out_size(10, 1, 2, 0) == 0
+    assert o.pool_out_size(18, 1, 4, 0) == 0
+    assert o.pool_out_size(9, 1, 2, 0) == 5     # windows at 0, 2, 4, 6, 8
+    assert o.pool_out_size(10, 3, 4, 0) == 3    # windows at 0, 4, 8 (the last one overhangs)
+
+
 def pin_max_hand_example(o):
     """Non-overlapping 2 x 2 tiles (the paper's case) of a 4 x 4 plane."""
     x = np.array([[1, 5, 2, 0],
@@ -129,7 +148,7 @@ def pin_avg_finite_differences(o):
         assert abs(fd - dx.ravel()[i]) <= 1e-9 * (1 + abs(fd))
 
 
-POOL_CHECKS = [pin_pool_out_size, pin_max_hand_example, pin_avg_constant_with_padding,
+POOL_CHECKS = [pin_pool_out_size, pin_every_window_holds_an_element, pin_max_hand_example, pin_avg_constant_with_padding,
                pin_avg_overhang_does_not_count, pin_global_pooling_is_numpy_reduction,
                pin_avg_adjoint, pin_max_mask_mass_and_finite_differences,
                pin_avg_finite_differences]
