@@ -40,7 +40,30 @@ def _shapes(count=120, seed=1903):
     return out
 
 
-SHAPES = _shapes()
+def _wide_shapes(count=60, seed=3141):
+    """Padding past the filter (windows wholly in the padding: outputs equal to
+    the bias, no contribution to dx or dw) and images smaller than the filter
+    that only the padding lets fit."""
+    rng = np.random.default_rng(seed)
+    out = []
+    while len(out) < count:
+        G = int(rng.choice([1, 1, 2, 4]))
+        Cg = int(rng.choice([1, 3, 16, 20, 32]))
+        Kg = int(rng.choice([8, 16, 24, 64]))
+        R = int(rng.integers(1, 8))
+        S = int(rng.integers(1, 8))
+        st = int(rng.integers(1, 5))
+        pad = int(rng.integers(0, max(R, S) + 4))
+        H = int(rng.integers(1, 20))
+        W = int(rng.integers(1, 20))
+        N = int(rng.integers(1, 4))
+        if oracle.out_size(H, R, st, pad) < 1 or oracle.out_size(W, S, st, pad) < 1:
+            continue
+        out.append((N, Cg * G, H, W, Kg * G, R, S, st, pad, G))
+    return out
+
+
+SHAPES = _shapes() + _wide_shapes()
 
 
 @pytest.fixture(autouse=True)
