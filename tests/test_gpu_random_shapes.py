@@ -63,7 +63,15 @@ def _wide_shapes(count=60, seed=3141):
     return out
 
 
-SHAPES = _shapes() + _wide_shapes()
+def _fc_shapes(count=24, seed=2718):
+    """Inner-product layers (1 x 1 images and filters) of ragged sizes: the
+    batch-transposed plans with padded copies of w and dy."""
+    rng = np.random.default_rng(seed)
+    return [(int(rng.integers(1, 300)), int(rng.integers(1, 600)), 1, 1, int(rng.integers(1, 300)),
+             1, 1, 1, 0, 1) for _ in range(count)]
+
+
+SHAPES = _shapes() + _wide_shapes() + _fc_shapes()
 
 
 @pytest.fixture(autouse=True)
