@@ -11,7 +11,7 @@ import pytest
 
 import oracle
 import workloads
-from gpu_util import (assert_within, gpu_bwd_data, gpu_bwd_weight, gpu_fwd,
+from gpu_util import (assert_within, dev, gpu_bwd_data, gpu_bwd_weight, gpu_fwd,
                       sample_indices)
 from oracle_pins import SMALL_SHAPES
 
@@ -234,3 +234,34 @@ def test_no_bias_and_no_db():
     dw, db = gpu_bwd_weight(shape, d["x"], d["dy"], with_bias=False)
     assert db is None
     assert_within(dw, dw_ref, adw, "bwd_weight no db")
+
+
+def test_failed_call_writes_nothing():
+    """On the device too, a call that reports an error has launched nothing:
+    outputs filled with a sentinel keep it (workspace too small, an output
+    overlapping an input, a misaligned pointer)."""
+    import torch
+    import paper_1903_06934_amd as m
+    L = m.lib()
+    shape = (2, 32, 12, 12, 48, 3, 3, 1, 1, 1)
+    N, C, H, W, K, R, S, st, pad, G = shape
+    d = _inputs(shape, (96, 0))
+    x, w, b, dy = (dev(d[k]) for k in ("x", "w", "b", "dy"))
+    y = torch.full((N, K, 12, 12), 7.0, device="cuda")
+    dx = torch.full((N, C, H, W), 7.0, device="cuda")
+    dw = torch.full((K, C, R, S), 7.0, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    need = [m.workspace_size(p, shape) for p in (0, 1, 2)]
+    ws = torch.empty(max(need) + 64, dtype=torch.uint8, device="cuda")
+    p = lambda t: t.data_ptr()  # noqa: E731
+    small = [max(n - 1, 0) for n in need]
+    if need[0]:
+        assert L.conv_fwd(*shape, p(x), p(w), p(b), p(y), p(ws), small[0], stream) == -3
+    assert L.conv_fwd(*shape, p(x), p(w), p(b), p(x), p(ws), need[0], stream) == -4
+    assert L.conv_bwd_data(*shape, p(dy), p(w), p(dx) + 4, p(ws), need[1], stream) == -5
+    if need[2]:
+        assert L.conv_bwd_weight(*shape, p(x), p(dy), p(dw), None, p(ws), small[2],
+                                 stream) == -3
+    torch.cuda.synchronize()
+    for t in (y, dx, dw):
+        assert bool((t == 7.0).all())
