@@ -18,7 +18,9 @@ region contains only the library's calls on torch's current stream.  Before
 the warm-up, every layer pass is tuned (conv_tune: each candidate plan is
 timed on the layer's tensors and the fastest kept, as the paper's framework
 picks its convolution strategy over the first training iterations);
---tune 0 keeps the library's built-in rule instead.
+--tune 0 keeps the library's built-in rule instead.  With --graph 1 the step
+is captured once into a HIP graph (on a side stream) and its replays are
+timed instead of eager calls.
 """
 from __future__ import annotations
 
