@@ -1,6 +1,13 @@
 // C ABI of the convolution library (declared in include/miconv.h): argument
 // validation, output geometry, workspace layout, kernel selection and
 // launches on the caller's stream.
+//
+// Layout of this file: geometry and limits; the image-GEMM tile and split
+// rules; per pass, its built-in rule, candidate plans, workspace size and
+// plan name (forward, backward-data with stride phases or pixel blocks,
+// backward-weight, the inner-product and explicit variants); the table of
+// stored plan choices; the executors that pack filters and launch kernels;
+// pooling; and the extern "C" entry points at the end.
 #include <algorithm>
 #include <atomic>
 #include <map>
