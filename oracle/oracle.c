@@ -352,7 +352,10 @@ void oracle_bias_grad(int N, int K, int P, int Q, const double *dy,
 /* (window R x S, stride, zero padding) contains that case             */
 /* (R = S = stride, pad = 0).  Readings (Caffe's pooling layer):       */
 /*   - output size ceil((H + 2 pad - R) / stride) + 1, less one when    */
-/*     pad > 0 and the last window would start at or past H + pad;      */
+/*     pad > 0 and the last window would start at or past H + pad; a    */
+/*     size whose last window would hold no image element (possible     */
+/*     without padding when stride > R) is refused (0): a window must   */
+/*     hold at least one element;                                       */
 /*   - max: over the window's elements inside the image (padding never  */
 /*     wins); the argmax is the first maximum in row-major order, kept  */
 /*     as the index h * W + w within the plane;                         */
