@@ -20,9 +20,10 @@ Recipe (used for every config):
     U(+-sqrt(6 / (fan_in + fan_out))), fan_in = (C/G) R S, fan_out = (K/G) R S;
   * b ~ U(-0.1, 0.1).
 
-The five configurations stand in for the paper's ImageNet networks (AlexNet,
-VGG-16, ResNet-50, GoogLeNet; Sec. VI, Tables II and III): same layer shapes,
-synthetic values, no dataset and no trained weights.
+The configurations (five convolution stacks, and the AlexNet network step
+with its pooling and inner-product layers) stand in for the paper's ImageNet
+networks (AlexNet, VGG-16, ResNet-50, GoogLeNet; Sec. VI, Tables II and III):
+same layer shapes, synthetic values, no dataset and no trained weights.
 """
 from __future__ import annotations
 
