@@ -60,7 +60,10 @@ def test_pool_matches_oracle(mode, pshape):
     assert np.array_equal(dx.view(np.uint32), dx2.view(np.uint32))
 
 
-def _random_pool_cases(count=60, seed=1903):
+def _random_pool_cases(count=60, seed=1903, lo=0, hi=21):
+    """Seeded random pooling shapes with planes of lo..hi-1 rows and columns
+    (small planes go through the per-element kernels, planes of 512 to 12288
+    elements through the whole-plane ones)."""
     rng = np.random.default_rng(seed)
     out = []
     while len(out) < count:
@@ -68,8 +71,8 @@ def _random_pool_cases(count=60, seed=1903):
         S = int(rng.choice([R, int(rng.integers(1, 6))]))
         st = int(rng.integers(1, 5))
         pad = int(rng.integers(0, min(R, S)))
-        H = int(rng.integers(max(R, S), 21))
-        W = int(rng.integers(max(R, S), 21))
+        H = int(rng.integers(max(R, S, lo), hi))
+        W = int(rng.integers(max(R, S, lo), hi))
         if oracle.pool_out_size(H, R, st, pad) < 1 or oracle.pool_out_size(W, S, st, pad) < 1:
             continue  # a window past the image: refused (tested on the CPU)
         out.append(("max" if len(out) % 2 == 0 else "avg",
@@ -77,7 +80,8 @@ def _random_pool_cases(count=60, seed=1903):
     return out
 
 
-@pytest.mark.parametrize("mode,pshape", _random_pool_cases(), ids=lambda v: str(v))
+@pytest.mark.parametrize("mode,pshape", _random_pool_cases() +
+                         _random_pool_cases(30, 2024, lo=23, hi=100), ids=lambda v: str(v))
 def test_pool_random_shapes(mode, pshape):
     """Seeded random windows, strides, padding and plane sizes (ceil-mode
     edges, overhangs and dropped last windows among them)."""
