@@ -22,6 +22,7 @@ PLAN_SHAPES = [
     (3, 48, 11, 11, 40, 3, 3, 2, 1, 2),    # stride phases with groups
     (4, 64, 1, 1, 48, 1, 1, 1, 0, 1),      # inner product, channel-aligned (w read in place)
     (5, 300, 1, 1, 70, 1, 1, 1, 0, 1),     # inner product, ragged (w and dy padded copies)
+    (32, 200, 1, 1, 72, 1, 1, 1, 0, 1),    # inner product, batch of 16s: dW as an image GEMM
 ]
 
 
