@@ -420,6 +420,30 @@ void img_variants(int M, long long Ncol, int Kred, int G, bool allow_split, Make
     }
 }
 
+// Inner products are skinny GEMMs (the batch as the short side) that fill
+// few tiles: also offer each tile with two and four times the rule's split
+// count (or 2 and 4 splits where the rule has none), down to splits of 16
+// slices.
+template <class P, class Make>
+void ip_fine_splits(int M, long long Ncol, int Kred, Make make, std::vector<P> &out)
+{
+    const long long slices = (Kred + kBK - 1) / kBK;
+    for (int t = 0; t < kNumImgTiles; t++) {
+        if (!tile_fits(t, M))
+            continue;
+        const int ns = split_count(tile_count(t, M, Ncol, 1), Kred);
+        for (int f : {2, 4})
+            if ((long long)ns * f <= slices / 16) {
+                P p = make(with_split(t, Kred, ns * f));
+                bool dup = false;
+                for (const P &q : out)
+                    dup = dup || same_plan(p, q);
+                if (!dup)
+                    out.push_back(p);
+            }
+    }
+}
+
 // ------------------------------------------------------------ forward
 size_t fwd_pack_bytes(const Geom &g)
 {
@@ -442,14 +466,15 @@ void fwd_candidates(const Geom &g, std::vector<ImgPlan> &out)
 {
     out.clear();
     out.push_back(fwd_rule(g));
-    if (is_inner_product(g))
-        img_variants<ImgPlan>(g.K, g.N, g.C, 1, true,
-                              [](const ImgPlan &p) {
-                                  ImgPlan q = p;
-                                  q.bt = true;
-                                  return q;
-                              },
-                              out);
+    if (is_inner_product(g)) {
+        auto bt = [](const ImgPlan &p) {
+            ImgPlan q = p;
+            q.bt = true;
+            return q;
+        };
+        img_variants<ImgPlan>(g.K, g.N, g.C, 1, true, bt, out);
+        ip_fine_splits<ImgPlan>(g.K, g.N, g.C, bt, out);
+    }
     const int nb = images_per_launch(g);
     img_variants<ImgPlan>(g.Kg, (long long)(g.N < nb ? g.N : nb) * g.P * g.Q, g.Cg * g.R * g.S,
                           g.G, nb >= g.N, [](const ImgPlan &p) { return p; }, out);
@@ -623,15 +648,16 @@ void bwd_candidates(const Geom &g, std::vector<BwdPlan> &out)
 {
     out.clear();
     out.push_back(bwd_rule(g));
-    if (is_inner_product(g))
-        img_variants<BwdPlan>(g.N, g.C, g.K, 1, true,
-                              [](const ImgPlan &i) {
-                                  BwdPlan b{};
-                                  b.img = i;
-                                  b.bt = true;
-                                  return b;
-                              },
-                              out);
+    if (is_inner_product(g)) {
+        auto bt = [](const ImgPlan &i) {
+            BwdPlan b{};
+            b.img = i;
+            b.bt = true;
+            return b;
+        };
+        img_variants<BwdPlan>(g.N, g.C, g.K, 1, true, bt, out);
+        ip_fine_splits<BwdPlan>(g.N, g.C, g.K, bt, out);
+    }
     const int nb = images_per_launch(g), n0 = g.N < nb ? g.N : nb;
     // Phases, one tile for all of them.
     const int kred_max = g.Kg * ((g.R + g.st - 1) / g.st) * ((g.S + g.st - 1) / g.st);

@@ -23,6 +23,8 @@ PLAN_SHAPES = [
     (4, 64, 1, 1, 48, 1, 1, 1, 0, 1),      # inner product, channel-aligned (w read in place)
     (5, 300, 1, 1, 70, 1, 1, 1, 0, 1),     # inner product, ragged (w and dy padded copies)
     (32, 200, 1, 1, 72, 1, 1, 1, 0, 1),    # inner product, batch of 16s: dW as an image GEMM
+    (8, 1024, 1, 1, 100, 1, 1, 1, 0, 1),   # inner product, forward fine splits
+    (8, 100, 1, 1, 1024, 1, 1, 1, 0, 1),   # inner product, backward-data fine splits
 ]
 
 
