@@ -163,6 +163,7 @@ __global__ __launch_bounds__(256) void pool_bwd_plane_kernel(const float *__rest
     extern __shared__ float gs[];  // dy plane, then (max) the mask plane
     int *ms = (int *)(gs + P * Q);
     const uint32_t hw = (uint32_t)H * (uint32_t)W, pq = (uint32_t)P * (uint32_t)Q;
+    const uint32_t rows = blockDim.x / (uint32_t)W;
     for (uint32_t nc = blockIdx.x; nc < planes; nc += gridDim.x) {
         for (uint32_t i = threadIdx.x; i < pq; i += blockDim.x) {
             gs[i] = dy[(size_t)nc * pq + i];
@@ -170,26 +171,33 @@ __global__ __launch_bounds__(256) void pool_bwd_plane_kernel(const float *__rest
                 ms[i] = mask[(size_t)nc * pq + i];
         }
         __syncthreads();
-        for (uint32_t pix = threadIdx.x; pix < hw; pix += blockDim.x) {
-            const int h = (int)fast_div(pix, w_), w = (int)(pix - (uint32_t)h * w_.d);
-            const int hp = h + pad, wp = w + pad;
-            const int p0 = hp < R ? 0 : (int)fast_div((uint32_t)(hp - R), st_) + 1;
-            const int p1 = min((int)fast_div((uint32_t)hp, st_), P - 1);
+        // Thread t keeps column w = t % W of rows t / W, t / W + rows, ...
+        // (rows = blockDim.x / W rows at a time, W <= blockDim.x), so the
+        // column's window range is decoded once and each row's once per row.
+        if (threadIdx.x < rows * (uint32_t)W) {
+            const int w = (int)(threadIdx.x - fast_div(threadIdx.x, w_) * w_.d);
+            const int wp = w + pad;
             const int q0 = wp < S ? 0 : (int)fast_div((uint32_t)(wp - S), st_) + 1;
             const int q1 = min((int)fast_div((uint32_t)wp, st_), Q - 1);
-            float acc = 0.f;
-            for (int p = p0; p <= p1; p++)
-                for (int q = q0; q <= q1; q++) {
-                    const int o = p * Q + q;
-                    if constexpr (MAX) {
-                        acc += ms[o] == (int)pix ? gs[o] : 0.f;
-                    } else {
-                        const Win wh = window(p, stride, pad, R, H),
-                                  ww = window(q, stride, pad, S, W);
-                        acc += gs[o] / (float)(wh.ext * ww.ext);
+            for (int h = (int)fast_div(threadIdx.x, w_); h < H; h += (int)rows) {
+                const int pix = h * W + w;
+                const int hp = h + pad;
+                const int p0 = hp < R ? 0 : (int)fast_div((uint32_t)(hp - R), st_) + 1;
+                const int p1 = min((int)fast_div((uint32_t)hp, st_), P - 1);
+                float acc = 0.f;
+                for (int p = p0; p <= p1; p++)
+                    for (int q = q0; q <= q1; q++) {
+                        const int o = p * Q + q;
+                        if constexpr (MAX) {
+                            acc += ms[o] == pix ? gs[o] : 0.f;
+                        } else {
+                            const Win wh = window(p, stride, pad, R, H),
+                                      ww = window(q, stride, pad, S, W);
+                            acc += gs[o] / (float)(wh.ext * ww.ext);
+                        }
                     }
-                }
-            dx[(size_t)nc * hw + pix] = acc;
+                dx[(size_t)nc * hw + pix] = acc;
+            }
         }
         __syncthreads();
     }
@@ -246,7 +254,7 @@ hipError_t launch_pool_bwd(bool max_mode, const float *dy, const int *mask, floa
     const uint32_t total = (uint32_t)((long long)N * C * H * W);
     const uint32_t planes = (uint32_t)((long long)N * C);
     const size_t lds = (size_t)P * Q * (max_mode ? 2 : 1) * sizeof(float);
-    if (lds <= kPlaneLds && (long long)H * W >= kPlaneMin) {
+    if (lds <= kPlaneLds && (long long)H * W >= kPlaneMin && W <= 256) {
         const dim3 grid(planes < 1048576u ? planes : 1048576u);
         if (max_mode)
             hipLaunchKernelGGL(pool_bwd_plane_kernel<true>, grid, dim3(256), lds, stream, dy, mask,
