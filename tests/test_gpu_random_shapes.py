@@ -5,7 +5,8 @@ up to the larger filter side minus one (so at times past the smaller one),
 1-4 groups, square and oblong filters and images, and channel counts on and
 off multiples of 16, so that every tile, the blocked and phase backward-data
 plans and the tap-uniform and packed backward-weight tiles meet ragged edges
-they are not tuned for."""
+they are not tuned for; inner-product shapes, some with batches that are
+multiples of 16, cover the batch-transposed plans."""
 import numpy as np
 import pytest
 
@@ -71,7 +72,16 @@ def _fc_shapes(count=24, seed=2718):
              1, 1, 1, 0, 1) for _ in range(count)]
 
 
-SHAPES = _shapes() + _wide_shapes() + _fc_shapes()
+def _fc16_shapes(count=16, seed=1618):
+    """Inner-product layers whose batch is a multiple of 16, where the
+    backward-weight rule is one image GEMM over the batch (dw = dy^T x), with
+    ragged input and output widths."""
+    rng = np.random.default_rng(seed)
+    return [(16 * int(rng.integers(1, 12)), int(rng.integers(1, 700)), 1, 1,
+             int(rng.integers(1, 400)), 1, 1, 1, 0, 1) for _ in range(count)]
+
+
+SHAPES = _shapes() + _wide_shapes() + _fc_shapes() + _fc16_shapes()
 
 
 @pytest.fixture(autouse=True)
@@ -117,3 +127,25 @@ def test_random_shape_rule_and_two_candidates(shape):
             for (ref, absum), got in zip(refs[p], outs):
                 assert_within(got, ref, absum, f"pass {p} plan {i} ({name}) {shape}")
         m.plan_set(p, shape, 0)
+
+
+@pytest.mark.parametrize("shape", _fc16_shapes(6, seed=1414), ids=lambda s: "x".join(map(str, s)))
+def test_fc_batch16_every_weight_plan(shape):
+    """Every backward-weight plan of an inner-product layer with a batch that
+    is a multiple of 16: the image-GEMM plans over the batch and the
+    batch-transposed split plans give the same dw and db as the oracle."""
+    import torch
+    import paper_1903_06934_amd as m
+    d = workloads.make_inputs(shape, 1, 1, seed=(1414, sum(shape)), init="he")
+    t = {k: dev(v) for k, v in d.items()}
+    dw_ref, adw, db_ref, adb = oracle.conv_bwd_weight(shape, d["x"], d["dy"])
+    names = []
+    for i in range(m.plan_count(2, shape)):
+        m.plan_set(2, shape, i)
+        ws = torch.empty(max(m.plan_workspace_size(2, shape, i), 16), dtype=torch.uint8, device="cuda")
+        dw, db = _run(2, shape, t, ws)
+        name = m.plan_name(2, shape, i)
+        names.append(name)
+        assert_within(host(dw), dw_ref, adw, f"dw plan {i} ({name}) {shape}")
+        assert_within(host(db), db_ref, adb, f"db plan {i} ({name}) {shape}")
+    assert any("image GEMM" in n for n in names), names
