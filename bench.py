@@ -14,7 +14,13 @@ whole library call), the roofline fraction of the dominant kernel, and the
 CPU oracle timed on a bounded sample of the same workload.
 
 All inputs are resident in device memory before the timed region; the timed
-region contains only the library's calls on torch's current stream.  Before
+region contains only the library's calls.  By default (--streams 2) each
+layer's backward-weight pass runs on a second stream beside its
+backward-data pass, ordered by events as the data dependencies of a
+training step require (a layer's dy exists once the backward-data pass of
+the layer above it has run); --streams 1 issues every pass on torch's
+current stream.  Per-pass figures and the dominant kernel are timed alone
+on the current stream.  Before
 the warm-up, every layer pass is tuned (conv_tune: each candidate plan is
 timed on the layer's tensors and the fastest kept, as the paper's framework
 picks its convolution strategy over the first training iterations);
@@ -74,6 +80,9 @@ def parse():
     ap.add_argument("--graph", type=int, default=0, choices=(0, 1),
                     help="1: capture one stack step into a HIP graph and time its replays "
                          "(0: eager launches)")
+    ap.add_argument("--streams", type=int, default=2, choices=(1, 2),
+                    help="2: each layer's backward-weight on a second stream, beside its "
+                         "backward-data (1: every pass on one stream)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only copy 1 GiB device-to-device 3 times (HBM counter calibration)")
     return ap.parse_args()
@@ -195,6 +204,19 @@ class LayerRun:
             import paper_1903_06934_amd as m
             raise m.MiconvError(st, f"{p} {self.L.name}")
 
+    def bind_side(self, stream):
+        """Also prepare the backward-weight call on a second stream (it has a
+        workspace of its own, so it may run beside the other passes)."""
+        fn, args = self.calls["bwd_weight"]
+        self.side_calls = {"bwd_weight": (fn, args[:-1] + (stream,))}
+
+    def run_side(self, p):
+        fn, args = self.side_calls[p]
+        st = fn(*args)
+        if st != 0:
+            import paper_1903_06934_amd as m
+            raise m.MiconvError(st, f"{p} {self.L.name} (side stream)")
+
 
 class PoolRun:
     """Device buffers and prepared library calls of one pooling layer; its
@@ -237,16 +259,41 @@ class PoolRun:
             raise m.MiconvError(st, f"{p} {self.L.name}")
 
 
-def stack_step(runs):
+def stack_step(runs, side=None):
+    """One training step's passes: forward over the layers, then backward in
+    reverse.  With a side stream, each layer's backward-weight runs there,
+    concurrently with its backward-data on the current stream: it starts once
+    the layer's dy exists (after the forward half for the last layer, else
+    after the backward-data of the layer above), and the step ends when both
+    streams are done (the weight update of the next step needs every dw)."""
+    import torch
     for r in runs:
         for _ in range(r.L.count):
             r.run("fwd")
+    if side is None:
+        for r in reversed(runs):
+            for _ in range(r.L.count):
+                if not isinstance(r, PoolRun):
+                    r.run("bwd_weight")
+                if not r.L.first:
+                    r.run("bwd_data")
+        return
+    main = torch.cuda.current_stream()
+
+    def handoff(src, dst):
+        ev = torch.cuda.Event()
+        ev.record(src)
+        dst.wait_event(ev)
+
+    handoff(main, side)
     for r in reversed(runs):
         for _ in range(r.L.count):
             if not isinstance(r, PoolRun):
-                r.run("bwd_weight")
+                r.run_side("bwd_weight")
             if not r.L.first:
                 r.run("bwd_data")
+                handoff(main, side)
+    handoff(side, main)
 
 
 def time_call(fn, reps, flush_buf=None):
@@ -362,17 +409,22 @@ def _bench_config(cfg, args, with_cpu):
     stream = torch.cuda.current_stream().cuda_stream
     runs = [PoolRun(cfg, li, L, stream) if isinstance(L, workloads.PoolLayer)
             else LayerRun(cfg, li, L, stream, args.tune) for li, L in enumerate(layers)]
+    side = torch.cuda.Stream() if args.streams == 2 else None
+    if side is not None:
+        for r in runs:
+            if isinstance(r, LayerRun):
+                r.bind_side(side.cuda_stream)
     torch.cuda.synchronize()
     N = layers[0].N
 
     for _ in range(args.warmup):
-        stack_step(runs)
+        stack_step(runs, side)
     torch.cuda.synchronize()
-    step = lambda: stack_step(runs)  # noqa: E731
+    step = lambda: stack_step(runs, side)  # noqa: E731
     if args.graph:
         graph = torch.cuda.CUDAGraph()
         with torch.cuda.graph(graph, stream=torch.cuda.current_stream()):
-            stack_step(runs)
+            stack_step(runs, side)
         graph.replay()
         torch.cuda.synchronize()
         step = graph.replay
@@ -436,7 +488,8 @@ def _bench_config(cfg, args, with_cpu):
         "dtype": "f32", "data": "synthetic",
         "config": {"workload": WORKLOAD_NAMES[cfg], "name": name, "global_batch": N,
                    "layers": len(layers), "parallelism": "single GPU",
-                   "launch": "hip graph" if args.graph else "eager"},
+                   "launch": ("hip graph" if args.graph else "eager") +
+                   (", backward-weight on a second stream" if args.streams == 2 else ", one stream")},
         "tflops_per_pass": {p: round(tot[p][0] / tot[p][1] / 1e9, 2) if tot[p][1] else None
                             for p in PASSES},
         "stack_tflops": round(sum(v[0] for v in tot.values()) / (step_ms * 1e9), 2),

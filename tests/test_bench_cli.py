@@ -22,5 +22,5 @@ def test_more_than_one_gpu_is_refused():
 def test_help_lists_the_options():
     r = _bench("--help")
     assert r.returncode == 0
-    for opt in ("--steps", "--warmup", "--config", "--tune", "--graph", "--cpu-seconds"):
+    for opt in ("--steps", "--warmup", "--config", "--tune", "--graph", "--streams", "--cpu-seconds"):
         assert opt in r.stdout

@@ -48,3 +48,44 @@ def test_two_streams_match_sequential():
             for a, b in zip(seq[i], outs[i]):
                 got = host(b)
                 assert np.array_equal(a.view(np.uint32), got.view(np.uint32)), (i, rep)
+
+
+def test_bench_step_on_two_streams_matches_one():
+    """The benchmark's step with backward-weight on a second stream writes
+    bit for bit what the one-stream step writes, on the AlexNet-shaped
+    network step at batch 4 (its pooling and inner-product layers included)."""
+    import torch
+    import bench
+    import workloads
+    cfg = 5
+    _, layers = workloads.config(cfg)
+    stream = torch.cuda.current_stream().cuda_stream
+    runs = []
+    for li, L in enumerate(layers):
+        L = L.with_batch(4)
+        runs.append(bench.PoolRun(cfg, li, L, stream) if isinstance(L, workloads.PoolLayer)
+                    else bench.LayerRun(cfg, li, L, stream))
+
+    def written(r):  # the first layer's dx is not computed by a step
+        return [n for n in ("y", "dx", "dw", "db") if hasattr(r, n) and not (n == "dx" and r.L.first)]
+
+    def outputs():
+        return [host(getattr(r, n)).copy() for r in runs for n in written(r)]
+
+    bench.stack_step(runs)
+    torch.cuda.synchronize()
+    ref = outputs()
+    for r in runs:
+        for n in written(r):
+            getattr(r, n).fill_(float("nan"))
+    side = torch.cuda.Stream()
+    for r in runs:
+        if isinstance(r, bench.LayerRun):
+            r.bind_side(side.cuda_stream)
+    for _ in range(2):
+        bench.stack_step(runs, side)
+    torch.cuda.synchronize()
+    got = outputs()
+    assert len(got) == len(ref) > 0
+    for a, b in zip(ref, got):
+        assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
