@@ -7,20 +7,27 @@ order, the backward-weight (+ bias) and backward-data passes (the network's
 first layer skips backward-data, whose result no layer would use).  Every
 layer occurs as many times as the stack lists it.
 
-Default workload: the AlexNet-shaped stack, batch 128, input 3x227x227.
+Default workload: the VGG-16-shaped stack, batch 32, input 3x224x224 (the
+largest configuration; the network behind the paper's per-pass Table II).
 Printed: ONE JSON line with images/s of the stack (value), TFLOP/s per pass
 (2 N K P Q (C/G) R S flops per pass, divided by the device time of the
-whole library call), the roofline fraction of the dominant kernel, and the
-CPU oracle timed on a bounded sample of the same workload.
+whole library call), the roofline fraction of the dominant kernel, the
+measured reference points of the chip (fp32 matrix-core loop, HBM copy,
+shader clock), and the CPU oracle timed on a bounded sample of the same
+workload.
 
 All inputs are resident in device memory before the timed region; the timed
-region contains only the library's calls.  By default (--streams 2) each
-layer's backward-weight pass runs on a second stream beside its
-backward-data pass, ordered by events as the data dependencies of a
-training step require (a layer's dy exists once the backward-data pass of
-the layer above it has run); --streams 1 issues every pass on torch's
-current stream.  Per-pass figures and the dominant kernel are timed alone
-on the current stream.  Before
+region contains only the library's calls.  Two schedules of the step exist:
+every pass on torch's current stream, or each layer's backward-weight pass
+on a second stream beside its backward-data pass, ordered by events as the
+data dependencies of a training step require (a layer's dy exists once the
+backward-data pass of the layer above it has run).  By default (--streams 0)
+both are timed over a few steps after the warm-up and the faster one is
+used (the event hand-offs cost more than they gain on launch-bound stacks);
+--streams 1 or 2 forces one.  Per-pass figures and the dominant kernel are
+timed alone on the current stream, from warm caches; passes whose HBM
+bytes weigh at least half as much as their flops in the roofline are also
+timed from cold caches (a 512 MiB buffer written between repeats).  Before
 the warm-up, every layer pass is tuned (conv_tune: each candidate plan is
 timed on the layer's tensors and the fastest kept, as the paper's framework
 picks its convolution strategy over the first training iterations);
@@ -63,7 +70,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", default="1", help="0-5, or 'all' (one JSON line each)")
+    ap.add_argument("--config", default="2", help="0-5, or 'all' (one JSON line each)")
     ap.add_argument("--reps", type=int, default=20, help="timed repeats per layer and pass")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle sample (0 disables it)")
@@ -71,7 +78,8 @@ def parse():
                     help="before the warm-up, time every candidate plan of every layer pass "
                          "with REPS runs and keep the fastest (0: the built-in rule)")
     ap.add_argument("--flush", action="store_true",
-                    help="write a 512 MiB buffer between per-layer repeats (cold caches)")
+                    help="time every per-layer pass from cold caches too (a 512 MiB buffer "
+                         "written between repeats), not only the memory-bound ones")
     ap.add_argument("--profile-pass", default=None, metavar="CFG:LAYER:PASS",
                     help="only run one layer pass --reps times (for rocprofv3), print nothing else")
     ap.add_argument("--plan", type=int, default=None, metavar="INDEX",
@@ -80,9 +88,13 @@ def parse():
     ap.add_argument("--graph", type=int, default=0, choices=(0, 1),
                     help="1: capture one stack step into a HIP graph and time its replays "
                          "(0: eager launches)")
-    ap.add_argument("--streams", type=int, default=2, choices=(1, 2),
+    ap.add_argument("--streams", type=int, default=0, choices=(0, 1, 2),
                     help="2: each layer's backward-weight on a second stream, beside its "
-                         "backward-data (1: every pass on one stream)")
+                         "backward-data; 1: every pass on one stream; 0: time both after "
+                         "the warm-up and keep the faster")
+    ap.add_argument("--peaks", type=int, default=1, choices=(0, 1),
+                    help="1: also measure the chip's reference points (fp32 matrix-core "
+                         "loop, HBM copy, shader clock) and report them")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only copy 1 GiB device-to-device 3 times (HBM counter calibration)")
     return ap.parse_args()
@@ -358,37 +370,74 @@ def measured_traffic(cfg, layer, p, plan):
     return None
 
 
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(cfg, layers, target_s):
     """The oracle (fp64 loop nests, all host threads) on a batch slice of
-    the same stack: images/s on the host."""
+    the same stack: images/s on the host, and GFLOP/s per layer and pass."""
     import oracle
     import workloads
     o = oracle.default()
 
     def run_stack(n):
-        secs = 0.0
+        secs, per = 0.0, []
         for li, L in enumerate(layers):
             Ls = L.with_batch(n)
             d = workloads.layer_inputs(cfg, li, Ls)
-            t0 = time.perf_counter()
-            for _ in range(L.count):
-                o.conv_fwd(Ls.shape, d["x"], d["w"], d["b"])
-                o.conv_bwd_weight(Ls.shape, d["x"], d["dy"])
-                if not L.first:
-                    o.conv_bwd_data(Ls.shape, d["dy"], d["w"])
-            secs += time.perf_counter() - t0
-        return secs
+            calls = [("fwd", lambda: o.conv_fwd(Ls.shape, d["x"], d["w"], d["b"])),
+                     ("bwd_weight", lambda: o.conv_bwd_weight(Ls.shape, d["x"], d["dy"]))]
+            if not L.first:
+                calls.append(("bwd_data", lambda: o.conv_bwd_data(Ls.shape, d["dy"], d["w"])))
+            for p, fn in calls:
+                t0 = time.perf_counter()
+                fn()
+                dt = time.perf_counter() - t0
+                secs += dt * L.count
+                per.append({"layer": L.name, "pass": p,
+                            "gflops": round(flops_of(Ls) / dt / 1e9, 3)})
+        return secs, per
 
     # Calibrate on one image, then size the sample to the target time.
-    t1 = run_stack(1)
+    t1, per = run_stack(1)
     n = max(1, min(layers[0].N, int(target_s / max(t1, 1e-6))))
-    if n == 1:
-        secs = t1
-    else:
-        secs = run_stack(n)
+    secs = t1
+    if n > 1:
+        secs, per = run_stack(n)
     return {"value": n / secs, "unit": "img/s", "cores": o.num_threads(), "kind": "oracle",
+            "cpu_model": cpu_model(),
             "sample": f"the same stack at batch {n} of {layers[0].N}, every layer and pass "
-                      f"(fp64 direct loop nests; input generation not timed), {secs:.1f} s"}
+                      f"(fp64 direct loop nests; input generation not timed), {secs:.1f} s; "
+                      "img/s is exact for the full batch since every pass is linear in it",
+            "per_layer_gflops": per}
+
+
+def measured_peaks():
+    """The chip's reference points next to the datasheet peaks: a
+    register-only fp32 matrix-core loop at 1, 2 and 4 waves per SIMD (with
+    the shader clock it ran at), and a 1 GiB device copy."""
+    import torch
+    from paper_1903_06934_amd import peaks
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    mfma = {}
+    for wps in (1, 2, 4):
+        tf, ghz = peaks.mfma_f32(wps, cus)
+        mfma[f"{wps}_waves_per_simd"] = {"tflops": round(tf, 1), "shader_ghz": round(ghz, 3)}
+    gbs, ok = peaks.copy_gbs()
+    if not ok:
+        raise RuntimeError("peak_copy produced a wrong copy")
+    return {"compute_units": cus,
+            "mfma_f32_16x16x4_loop": mfma,
+            "hbm_copy_gbs": round(gbs, 1),
+            "note": "register-only v_mfma_f32_16x16x4f32 loop with 8 independent chains per "
+                    "wave; copy of 1 GiB by a float4 kernel, read + write bytes over time"}
 
 
 def bench_config(cfg, args, with_cpu):
@@ -409,17 +458,38 @@ def _bench_config(cfg, args, with_cpu):
     stream = torch.cuda.current_stream().cuda_stream
     runs = [PoolRun(cfg, li, L, stream) if isinstance(L, workloads.PoolLayer)
             else LayerRun(cfg, li, L, stream, args.tune) for li, L in enumerate(layers)]
-    side = torch.cuda.Stream() if args.streams == 2 else None
-    if side is not None:
+    side_stream = torch.cuda.Stream() if args.streams != 1 else None
+    if side_stream is not None:
         for r in runs:
             if isinstance(r, LayerRun):
-                r.bind_side(side.cuda_stream)
+                r.bind_side(side_stream.cuda_stream)
     torch.cuda.synchronize()
     N = layers[0].N
 
+    def timed_steps(side, k):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(k):
+            stack_step(runs, side)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / k
+
+    side = side_stream if args.streams == 2 else None
     for _ in range(args.warmup):
         stack_step(runs, side)
     torch.cuda.synchronize()
+    schedule_ms = None
+    if args.streams == 0:
+        # Time both schedules (alternating, best of two rounds) and keep the
+        # faster for the timed region.
+        k = max(3, min(10, args.steps // 2))
+        one, two = [], []
+        for _ in range(2):
+            one.append(timed_steps(None, k))
+            two.append(timed_steps(side_stream, k))
+        schedule_ms = {"one_stream": round(min(one), 4), "two_streams": round(min(two), 4)}
+        side = side_stream if min(two) < min(one) else None
     step = lambda: stack_step(runs, side)  # noqa: E731
     if args.graph:
         graph = torch.cuda.CUDAGraph()
@@ -436,24 +506,32 @@ def _bench_config(cfg, args, with_cpu):
     torch.cuda.synchronize()
     step_ms = e0.elapsed_time(e1) / args.steps
 
-    flush = torch.empty(128 << 20, dtype=torch.float32, device="cuda") if args.flush else None
+    flush = torch.empty(128 << 20, dtype=torch.float32, device="cuda")
+    ridge = PEAK_TFLOPS * 1e12 / (PEAK_GBS * 1e9)
     per = []
     tot = {p: [0.0, 0.0] for p in PASSES}
     for r in runs:
         L = r.L
         for p in getattr(r, "passes", PASSES):
-            med, mn = time_call(lambda: r.run(p), args.reps, flush)
+            med, mn = time_call(lambda: r.run(p), args.reps)
             F = flops_of(L)
             B = bytes_of(L, p)
             t_roof = max(F / (PEAK_TFLOPS * 1e12), B / (PEAK_GBS * 1e9)) * 1e3
             in_stack = not (p == "bwd_data" and L.first)
-            per.append({"layer": L.name, "pass": p, "count": L.count, "in_stack": in_stack,
-                        "ms": round(med, 4), "ms_min": round(mn, 4),
-                        "tflops": round(F / med / 1e9, 2), "gbs": round(B / med / 1e6, 1),
-                        "roof_frac": round(t_roof / med, 3), "plan": r.plan(p)})
+            row = {"layer": L.name, "pass": p, "count": L.count, "in_stack": in_stack,
+                   "cache": "warm", "ms": round(med, 4), "ms_min": round(mn, 4),
+                   "tflops": round(F / med / 1e9, 2), "gbs": round(B / med / 1e6, 1),
+                   "roof_frac": round(t_roof / med, 3), "plan": r.plan(p)}
+            if args.flush or F < 2 * ridge * B:
+                # Memory-bound or near the ridge: also from cold caches.
+                cmed, _ = time_call(lambda: r.run(p), args.reps, flush)
+                row.update({"ms_cold": round(cmed, 4), "gbs_cold": round(B / cmed / 1e6, 1),
+                            "roof_frac_cold": round(t_roof / cmed, 3)})
+            per.append(row)
             if in_stack and F > 0:
                 tot[p][0] += F * L.count
                 tot[p][1] += med * L.count
+    del flush
 
     # Dominant kernel: the GEMM of the (layer, pass) with the largest share
     # of the step.
@@ -464,7 +542,6 @@ def _bench_config(cfg, args, with_cpu):
     k_ms = kernel_time(drun, dom["pass"], args.reps, hev)
     F = flops_of(drun.L)
     ai = F / bytes_of(drun.L, dom["pass"])
-    ridge = PEAK_TFLOPS * 1e12 / (PEAK_GBS * 1e9)
     if ai >= ridge:
         ach = F / k_ms / 1e9
         roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_TFLOPS,
@@ -489,13 +566,18 @@ def _bench_config(cfg, args, with_cpu):
         "config": {"workload": WORKLOAD_NAMES[cfg], "name": name, "global_batch": N,
                    "layers": len(layers), "parallelism": "single GPU",
                    "launch": ("hip graph" if args.graph else "eager") +
-                   (", backward-weight on a second stream" if args.streams == 2 else ", one stream")},
+                   (", backward-weight on a second stream" if side is not None
+                    else ", one stream")},
         "tflops_per_pass": {p: round(tot[p][0] / tot[p][1] / 1e9, 2) if tot[p][1] else None
                             for p in PASSES},
         "stack_tflops": round(sum(v[0] for v in tot.values()) / (step_ms * 1e9), 2),
         "roofline": roof,
         "per_layer": per,
     }
+    if schedule_ms is not None:
+        line["schedule_ms_per_step"] = schedule_ms
+    if args.peaks:
+        line["measured_peaks"] = measured_peaks()
     if with_cpu:
         line["cpu_baseline"] = cpu_baseline(cfg, layers, args.cpu_seconds)
     del runs

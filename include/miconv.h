@@ -63,8 +63,9 @@ typedef enum miconv_status {
                                   rows of (K/G)*R*S, each rounded up to a multiple of 16),
                                   H, W, R, S or pad above 32767, or group above 65535 */
     MICONV_ERR_NULL = -2,      /* a required pointer is NULL */
-    MICONV_ERR_WORKSPACE = -3, /* ws_bytes below conv_workspace_size(), or ws NULL when
-                                  a workspace is needed */
+    MICONV_ERR_WORKSPACE = -3, /* ws_bytes below the need of the plan the call runs (a size
+                                  from conv_workspace_size() always suffices), or ws
+                                  NULL when a workspace is needed */
     MICONV_ERR_ALIAS = -4,     /* an output range overlaps an input, another output or ws */
     MICONV_ERR_ALIGN = -5,     /* a tensor or workspace pointer is not 16-byte aligned */
     MICONV_ERR_DEVICE = -6,    /* no current HIP device, or it is not gfx950 */
@@ -92,9 +93,14 @@ int conv_output_size(int H, int W, int R, int S, int stride, int pad, int *P, in
 
 /*
  * Bytes of device workspace that pass `pass` (MICONV_PASS_*) needs for this
- * shape with the plan its calls use now; 0 if it needs none or if the shape
- * or pass id is invalid (the pass itself then reports the error).  Host-only
- * (once a plan has been stored it reads the current device id).
+ * shape: the largest need over all of the shape's candidate plans (see
+ * conv_plan_count below), so that a workspace of this size stays sufficient
+ * whatever plan is stored for the shape later, by conv_plan_set or conv_tune,
+ * from this or another thread.  conv_plan_workspace_size gives one plan's
+ * (often smaller) need.  0 if no plan needs a workspace or if the shape or
+ * pass id is invalid (the pass itself then reports the error).  Host-only
+ * (the candidate plans depend on the current device's compute-unit count,
+ * read once per device; 256 when no device can be queried).
  */
 size_t conv_workspace_size(int pass, int N, int C, int H, int W, int K, int R, int S,
                            int stride, int pad, int group);

@@ -42,16 +42,16 @@ constexpr long long kMaxElems = 2147483647LL;  // 2^31 - 1
 constexpr long long kMaxChunkElems = (1LL << 29) - 1;  // per launch, per source tensor
 constexpr size_t kAlign = 256;                  // sub-buffer alignment inside ws
 constexpr int kBK = 16;                         // reduction slice of every GEMM kernel
-constexpr int kNumCUs = 256;                    // MI355X: 8 XCDs x 32 CUs
-constexpr int kTargetWorkgroups = 1024;         // 4 per CU on 256 CUs
+// Workgroup targets are per compute unit (the rules below were measured on
+// the MI355X's 256 CUs): target_workgroups() = 4 per CU.
 // Tap-uniform backward-weight tiles: six fit on a CU at once, and about
-// three rounds of them measured best, as long as a split keeps at least
-// kTapMinSlices slices (shorter splits cost more in partial sums than they
-// gain in balance) -- unless that would leave fewer than kTargetWorkgroups
-// workgroups (small layers), where splits go down to 8 slices.  (Timed plan
-// selection also tries half and twice the splits of this rule; halving the
-// target itself measured slower, as the caps then bind differently.)
-constexpr int kTapTargetWorkgroups = 4096;
+// three rounds of them (16 per CU) measured best, as long as a split keeps
+// at least kTapMinSlices slices (shorter splits cost more in partial sums
+// than they gain in balance) -- unless that would leave fewer than
+// target_workgroups() workgroups (small layers), where splits go down to 8
+// slices.  (Timed plan selection also tries half and twice the splits of
+// this rule; halving the target itself measured slower, as the caps then
+// bind differently.)
 constexpr int kTapMinSlices = 24;
 
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
@@ -81,7 +81,8 @@ int make_geom(int N, int C, int H, int W, int K, int R, int S, int stride, int p
     // per-axis coordinates fit the kernels' 16-bit fields.
     if (H > 32767 || W > 32767 || R > 32767 || S > 32767 || pad > 32767)
         return MICONV_ERR_SHAPE;
-    // Groups index the third grid dimension.
+    // Groups are folded with the tiles and splits into the 1-D grid; keeping
+    // them below 2^16 keeps that product far from the grid limit.
     if (group > 65535)
         return MICONV_ERR_SHAPE;
     int P = out_extent(H, R, stride, pad), Q = out_extent(W, S, stride, pad);
@@ -147,6 +148,32 @@ int check_buffers(const Range *r, int n, const bool *required, const void *ws, s
     return MICONV_OK;
 }
 
+// Compute units of the current device (its multiProcessorCount, read once
+// per device), or 256, the MI355X's, when no device can be queried (the
+// host-only plan and workspace queries still work then).
+int num_cus()
+{
+    static std::atomic<int> cache[64];  // 0: not read yet
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0)
+        return 256;
+    if (dev < 64) {
+        int c = cache[dev].load(std::memory_order_relaxed);
+        if (c > 0)
+            return c;
+    }
+    hipDeviceProp_t prop;
+    int n = 256;
+    if (hipGetDeviceProperties(&prop, dev) == hipSuccess && prop.multiProcessorCount > 0)
+        n = prop.multiProcessorCount;
+    if (dev < 64)
+        cache[dev].store(n, std::memory_order_relaxed);
+    return n;
+}
+
+int target_workgroups() { return 4 * num_cus(); }
+int tap_target_workgroups() { return 16 * num_cus(); }
+
 int check_device()
 {
     static std::atomic<int> cache[64];  // 0 unknown, 1 gfx950, 2 other
@@ -177,8 +204,9 @@ int gemm_tiles(int M, int Ncol, int bm, int bn)
 // workgroups are dealt out over 256 CUs: tiles / (256 * ceil(tiles / 256)).
 double cu_balance(long long tiles)
 {
-    long long rounds = (tiles + kNumCUs - 1) / kNumCUs;
-    return rounds > 0 ? (double)tiles / (double)(rounds * kNumCUs) : 1.0;
+    const int cus = num_cus();
+    long long rounds = (tiles + cus - 1) / cus;
+    return rounds > 0 ? (double)tiles / (double)(rounds * cus) : 1.0;
 }
 
 // Tile choice for the image GEMM, from measured sweeps on MI355X across the
@@ -203,8 +231,8 @@ int pick_img_tile(int M, long long Ncol, int Kred, int G)
     if (M <= 48)
         return IMG_48x64;
     if (M > 64 && M <= 96)
-        return tiles(96, 128) >= 4 * kNumCUs ? IMG_96x128 : IMG_96x64;
-    if (M % 128 == 0 && Kred >= 256 && tiles(128, 64) >= kNumCUs &&
+        return tiles(96, 128) >= 4 * num_cus() ? IMG_96x128 : IMG_96x64;
+    if (M % 128 == 0 && Kred >= 256 && tiles(128, 64) >= num_cus() &&
         1.05 * cu_balance(tiles(128, 64)) >= cu_balance(tiles(64, 64)))
         return IMG_128x64;
     return IMG_64x64;
@@ -263,7 +291,7 @@ long long tile_count(int tile, int M, long long Ncol, int G)
     return (long long)((M + bm - 1) / bm) * ((Ncol + bn - 1) / bn) * G;
 }
 
-// Split-K for the image GEMM.  With fewer than 640 tiles (2.5 per CU) the
+// Split-K for the image GEMM.  With fewer than 2.5 tiles per CU the
 // MFMA pipes starve for latency hiding; a deep reduction (>= kSplitMinRows)
 // is then cut into splits of at least kSplitRows rows so that ~8 workgroups
 // per CU run, each split writes an output-shaped partial slab, and a
@@ -286,7 +314,7 @@ struct ImgPlan {
 int split_count(long long tiles, int Kred)
 {
     long long slices = (Kred + kBK - 1) / kBK;
-    long long ns = (8 * kNumCUs + tiles - 1) / tiles;
+    long long ns = (8LL * num_cus() + tiles - 1) / tiles;
     if (ns > slices / 8)
         ns = slices / 8;
     if (ns > Kred / kSplitRows)
@@ -311,7 +339,8 @@ ImgPlan img_rule(int M, long long Ncol, int Kred, int G, bool allow_split)
     if (!allow_split || Kred < kSplitMinRows)
         return with_split(tile, Kred, 1);
     const long long tiles = tile_count(tile, M, Ncol, G);
-    return with_split(tile, Kred, tiles >= 640 ? 1 : split_count(tiles, Kred));
+    return with_split(tile, Kred,
+                      tiles >= 5LL * num_cus() / 2 ? 1 : split_count(tiles, Kred));
 }
 
 bool same_img(const ImgPlan &a, const ImgPlan &b)
@@ -334,8 +363,11 @@ bool same_img(const ImgPlan &a, const ImgPlan &b)
 // y [N][K] and dx [N][C] directly.
 bool is_inner_product(const Geom &g)
 {
+    // With padding the lone output pixel would read only zeros (P = Q = 1 for
+    // stride > 2 pad): such shapes take the implicit plans, whose gathers
+    // zero-fill padding.
     return g.H == 1 && g.W == 1 && g.R == 1 && g.S == 1 && g.P == 1 && g.Q == 1 && g.G == 1 &&
-           g.N <= 65535 * 32 && (long long)g.C * g.N <= kMaxChunkElems &&
+           g.pad == 0 && g.N <= 65535 * 32 && (long long)g.C * g.N <= kMaxChunkElems &&
            (long long)g.K * g.N <= kMaxChunkElems;
 }
 
@@ -733,7 +765,7 @@ void bwd_name(const BwdPlan &p, char *buf, size_t len)
 
 // ------------------------------------------------------------ backward-weight
 // The reduction over N*P*Q pixels is cut into fixed-length splits (a
-// multiple of the slice) so that about kTapTargetWorkgroups workgroups run;
+// multiple of the slice) so that about tap_target_workgroups() workgroups run;
 // each split writes its own partial dw, summed afterwards in split order.
 // Launches never straddle a batch chunk (images_per_launch).
 struct WgradPlan {
@@ -799,9 +831,9 @@ WgradPlan wgrad_plan(const Geom &g, int tile = -1, int scale = 0, int nb = 0)
         is_tap_tile(tile)
             ? (long long)((M + bm - 1) / bm) * g.R * g.S * ((g.Cg + bn - 1) / bn) * g.G
             : (long long)gemm_tiles(M, Ncol, bm, bn) * g.G;
-    long long ns = (kTapTargetWorkgroups + tiles - 1) / tiles;
+    long long ns = (tap_target_workgroups() + tiles - 1) / tiles;
     long long long_ns = Kred / (p.slice * kTapMinSlices);
-    long long fill_ns = (kTargetWorkgroups + tiles - 1) / tiles;
+    long long fill_ns = (target_workgroups() + tiles - 1) / tiles;
     long long max_ns = long_ns > fill_ns ? long_ns : fill_ns;
     if (max_ns > Kred / (p.slice * 8))
         max_ns = Kred / (p.slice * 8);
@@ -1694,6 +1726,38 @@ size_t candidate_ws(int pass, const Geom &g, int index)
     }
 }
 
+// The largest workspace over the candidates of a pass.
+size_t max_candidate_ws(int pass, const Geom &g)
+{
+    size_t need = 0;
+    switch (pass) {
+    case MICONV_PASS_FWD: {
+        std::vector<ImgPlan> c;
+        fwd_candidates(g, c);
+        for (const ImgPlan &p : c)
+            need = std::max(need, fwd_ws(g, p));
+        break;
+    }
+    case MICONV_PASS_BWD_DATA: {
+        std::vector<BwdPlan> c;
+        bwd_candidates(g, c);
+        for (const BwdPlan &p : c)
+            need = std::max(need, bwd_ws(g, p));
+        break;
+    }
+    case MICONV_PASS_BWD_WEIGHT: {
+        std::vector<WgradPlan> c;
+        wgrad_candidates(g, c);
+        for (const WgradPlan &p : c)
+            need = std::max(need, wgrad_ws(g, p));
+        break;
+    }
+    default:
+        break;
+    }
+    return need;
+}
+
 // Tensors of conv_tune: fwd (x, w, b | y), bwd-data (dy, w, - | dx),
 // bwd-weight (x, dy, - | dw, db).
 struct TuneBuffers {
@@ -1788,7 +1852,10 @@ size_t conv_workspace_size(int pass, int N, int C, int H, int W, int K, int R, i
         return 0;
     if (pass < MICONV_PASS_FWD || pass > MICONV_PASS_BWD_WEIGHT)
         return 0;
-    return candidate_ws(pass, g, plan_index(pass, g));
+    // The largest need over the shape's candidate plans, so that a size taken
+    // now stays sufficient whatever plan conv_plan_set or conv_tune stores
+    // for the shape later (from this or another thread).
+    return max_candidate_ws(pass, g);
 }
 
 int conv_set_timing_events(hipEvent_t before, hipEvent_t after)

@@ -3,7 +3,7 @@
 //
 // GEMM core: a workgroup of WM x WN waves computes a BM x BN tile of C with
 // v_mfma_f32_16x16x4f32 (each wave owns a (BM/WM) x (BN/WN) sub-tile made of
-// 16x16 accumulator blocks; the 32x32x2 shape is also described below).
+// 16x16 accumulator blocks).
 // Operands go from HBM straight into LDS with buffer_load_dword ... lds (no
 // register staging); out-of-range elements read zero through the buffer
 // range check, so padding and ragged tiles need no branches.
@@ -11,45 +11,18 @@
 
 namespace miconv {
 
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-
-// v_mfma_f32_32x32x2f32 operand layout (64 lanes):
-//   A (32 x 2): lane l holds A[l % 32][l / 32];  B (2 x 32): B[l / 32][l % 32]
-//   D (32 x 32): lane l, register v holds D[8 (v / 4) + 4 (l / 32) + v % 4][l % 32]
-// v_mfma_f32_16x16x4f32: A (16 x 4): lane l holds A[l % 16][l / 16];
-// B (4 x 16): B[l / 16][l % 16]; D (16 x 16): lane l, register v holds
-// D[4 (l / 16) + v][l % 16].
+// v_mfma_f32_16x16x4f32 operand layout (64 lanes): A (16 x 4): lane l holds
+// A[l % 16][l / 16]; B (4 x 16): B[l / 16][l % 16]; D (16 x 16): lane l,
+// register v holds D[4 (l / 16) + v][l % 16].
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+constexpr int MF = 16;  // accumulator block edge
 
-template <int MF>
-__device__ __forceinline__ int acc_row_mf(int v, int lane)
+__device__ __forceinline__ int acc_row(int v, int lane) { return 4 * (lane >> 4) + v; }
+
+__device__ __forceinline__ f32x4 mfma16(float a, float b, f32x4 c)
 {
-    if constexpr (MF == 32)
-        return 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-    else
-        return 4 * (lane >> 4) + v;
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
-
-template <int MF>
-struct MfmaAcc;
-template <>
-struct MfmaAcc<32> {
-    typedef f32x16 T;
-    static constexpr int NV = 16;
-    static __device__ __forceinline__ T mma(float a, float b, T c)
-    {
-        return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
-    }
-};
-template <>
-struct MfmaAcc<16> {
-    typedef f32x4 T;
-    static constexpr int NV = 4;
-    static __device__ __forceinline__ T mma(float a, float b, T c)
-    {
-        return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
-    }
-};
 
 
 // ---------------------------------------------------------------------------
@@ -148,10 +121,9 @@ __device__ __forceinline__ int xcd_tile(int hw, int total)
 // Pipeline: three stages (LDS buffers for B, and for A or register sets for
 // A); slices t + 1 and t + 2 are in flight while slice t computes.
 // ---------------------------------------------------------------------------
-template <int BM, int BN, int BK, int WM, int WN, int PAD, bool FAST, int NST, int MF>
+template <int BM, int BN, int BK, int WM, int WN, int PAD, bool FAST, int NST>
 __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArgs a)
 {
-    typedef MfmaAcc<16> Mf;
     constexpr int NW = WM * WN;
     constexpr int TM = BM / WM, TN = BN / WN;
     constexpr int FM = TM / 16, FN = TN / 16;
@@ -165,7 +137,7 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
     constexpr int LB = (BK * HB + NW - 1) / NW;
     constexpr int BROWS = BK + ((BK * HB) % NW ? 1 : 0);
     constexpr int LDA = 64 * HA + PAD, LDB = BN + PAD;
-    static_assert(MF == 16 && BK == 16 && NST == 3, "16x16x4 MFMA, 16-row slices, 3 stages");
+    static_assert(BK == 16 && NST == 3, "16-row slices, 3 stages");
     static_assert(BN % 64 == 0 && TM % 16 == 0 && TN % 16 == 0, "tile");
     static_assert(BK % NW == 0 || HB == 1, "uneven B rows need one segment per row");
     static_assert(!ASH || (BK * HA) % NW == 0, "A rows per wave");
@@ -299,13 +271,13 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
         }
     };
 
-    typename Mf::T acc[FM][FN];
+    f32x4 acc[FM][FN];
 #pragma unroll
     for (int i = 0; i < FM; i++)
 #pragma unroll
         for (int j = 0; j < FN; j++)
 #pragma unroll
-            for (int v = 0; v < Mf::NV; v++)
+            for (int v = 0; v < 4; v++)
                 acc[i][j][v] = 0.f;
 
     const int nslices = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
@@ -327,9 +299,11 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
                 for (int s = 0; s < 4; s++)
                     af[i][s] = Ac[4 * kr + s][i * 16 + lc];
             } else {
-                // The untracked load's value may only be used after the
-                // stage's wait: route it through an empty asm statement that
-                // is ordered after that wait, so no use can move above it.
+                // The untracked load's value is only valid after the stage's
+                // wait (s_waitcnt before the barrier).  Nothing here orders
+                // this copy after that wait: the build-time check in
+                // isa_check.py verifies on the generated code that the
+                // registers are read by MFMAs only, after the second barrier.
                 af[i] = ar[i];
             }
         }
@@ -340,7 +314,7 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
             for (int i = 0; i < FM; i++)
 #pragma unroll
                 for (int j = 0; j < FN; j++)
-                    acc[i][j] = Mf::mma(af[i][s], bf[s][j], acc[i][j]);
+                    acc[i][j] = mfma16(af[i][s], bf[s][j], acc[i][j]);
     };
 
     // Before the barrier of slice t a wave waits only until its own loads of
@@ -404,8 +378,8 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
 #pragma unroll
         for (int i = 0; i < FM; i++)
 #pragma unroll
-            for (int v = 0; v < Mf::NV; v++) {
-                int m = m0 + wm * TM + i * MF + acc_row_mf<MF>(v, lane);
+            for (int v = 0; v < 4; v++) {
+                int m = m0 + wm * TM + i * MF + acc_row(v, lane);
                 if (m >= a.M)
                     continue;
                 const int c = m / bb, rem = m - c * bb, ph = rem / b, pw = rem - ph * b;
@@ -436,8 +410,8 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
 #pragma unroll
     for (int i = 0; i < FM; i++)
 #pragma unroll
-        for (int v = 0; v < Mf::NV; v++) {
-            int m = m0 + wm * TM + i * MF + acc_row_mf<MF>(v, lane);
+        for (int v = 0; v < 4; v++) {
+            int m = m0 + wm * TM + i * MF + acc_row(v, lane);
             if (m >= a.M)
                 continue;
             int oc = g * a.M + m;
@@ -476,20 +450,16 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
 // lies inside the image).
 //
 // LDS holds each row pixel-contiguous (64 words + 4 of padding, so the
-// ds_read_b128 of 16 consecutive rows hit distinct banks).  With the 32x32x2
-// MFMA, step s (0..31) takes pixel s from the first half of the slice in
-// lanes 0-31 and pixel 32 + s in lanes 32-63, so a lane's 32 operands of a
-// row are contiguous: 8 ds_read_b128.  With the 16x16x4 MFMA (MF = 16) the
-// four 16-lane groups take the four quarters of the slice, 16 contiguous
-// operands each: 4 ds_read_b128.  The tile is single-buffered: after a barrier
+// ds_read_b128 of 16 consecutive rows hit distinct banks).  The four 16-lane
+// groups of the 16x16x4 MFMA take the four quarters of the slice, 16
+// contiguous operands each: 4 ds_read_b128.  The tile is single-buffered: after a barrier
 // every wave copies its operands of the slice into registers, a second
 // barrier frees the LDS, the next slice's loads are issued, and the slice's
 // MFMAs run while they land.
 // ---------------------------------------------------------------------------
-template <int BM, int BN, int WM, int WN, int MF, bool PACKED>
+template <int BM, int BN, int WM, int WN, bool PACKED>
 __global__ __launch_bounds__(64 * WM * WN) void wgrad_kernel(const WgradArgs a)
 {
-    typedef MfmaAcc<MF> Mf;
     constexpr int BK = 64, LDR = BK + 4;
     constexpr int NW = WM * WN, TM = BM / WM, TN = BN / WN, FM = TM / MF, FN = TN / MF;
     constexpr int PB = BK * MF / 64;  // pixels of the slice per lane group
@@ -570,13 +540,13 @@ __global__ __launch_bounds__(64 * WM * WN) void wgrad_kernel(const WgradArgs a)
         }
     };
 
-    typename Mf::T acc[FM][FN];
+    f32x4 acc[FM][FN];
 #pragma unroll
     for (int i = 0; i < FM; i++)
 #pragma unroll
         for (int j = 0; j < FN; j++)
 #pragma unroll
-            for (int v = 0; v < Mf::NV; v++)
+            for (int v = 0; v < 4; v++)
                 acc[i][j][v] = 0.f;
 
     // Bias gradient: the workgroups of the first column tile also sum the dy
@@ -632,7 +602,7 @@ __global__ __launch_bounds__(64 * WM * WN) void wgrad_kernel(const WgradArgs a)
                 for (int i = 0; i < FM; i++)
 #pragma unroll
                     for (int j = 0; j < FN; j++)
-                        acc[i][j] = Mf::mma(af[i][u][e], bf[j][u][e], acc[i][j]);
+                        acc[i][j] = mfma16(af[i][u][e], bf[j][u][e], acc[i][j]);
     }
 
     if (do_bias) {
@@ -654,8 +624,8 @@ __global__ __launch_bounds__(64 * WM * WN) void wgrad_kernel(const WgradArgs a)
 #pragma unroll
     for (int i = 0; i < FM; i++)
 #pragma unroll
-        for (int v = 0; v < Mf::NV; v++) {
-            int m = m0 + wm * TM + i * MF + acc_row_mf<MF>(v, lane);
+        for (int v = 0; v < 4; v++) {
+            int m = m0 + wm * TM + i * MF + acc_row(v, lane);
             if (m >= a.M)
                 continue;
 #pragma unroll
@@ -922,17 +892,17 @@ __global__ __launch_bounds__(RED_E * RED_J) void splitk_reduce_kernel(
 // Launchers.
 // ---------------------------------------------------------------------------
 
-template <int BM, int BN, int BK, int WM, int WN, int PAD, int MF = 32>
+template <int BM, int BN, int BK, int WM, int WN, int PAD>
 static hipError_t img_launch(const ImgGemmArgs &a, bool fast, hipStream_t stream)
 {
     constexpr int NST = 3;
     int tiles = ((a.M + BM - 1) / BM) * ((a.Ncol + BN - 1) / BN);
     dim3 grid(tiles * a.groups * a.nsplit);
     if (fast)
-        hipLaunchKernelGGL((img_gemm_kernel<BM, BN, BK, WM, WN, PAD, true, NST, MF>), grid,
+        hipLaunchKernelGGL((img_gemm_kernel<BM, BN, BK, WM, WN, PAD, true, NST>), grid,
                            dim3(64 * WM * WN), 0, stream, a);
     else
-        hipLaunchKernelGGL((img_gemm_kernel<BM, BN, BK, WM, WN, PAD, false, NST, MF>), grid,
+        hipLaunchKernelGGL((img_gemm_kernel<BM, BN, BK, WM, WN, PAD, false, NST>), grid,
                            dim3(64 * WM * WN), 0, stream, a);
     return hipGetLastError();
 }
@@ -949,23 +919,23 @@ hipError_t launch_img_gemm(const ImgGemmArgs &a, int tile, bool fast, hipStream_
     // so that its four 16-lane groups, which read rows 4 apart, hit distinct
     // banks.  Waves: 4 x 1 or 3 x 1 (each wave a 16- or 32-row band across
     // the tile), 2 x 2, or 1 x 4 (each wave a column band, 16 rows).
-    case IMG_128x64: return img_launch<128, 64, K, 4, 1, 4, 16>(a, fast, stream);
-    case IMG_16x128: return img_launch<16, 128, K, 1, 4, 4, 16>(a, fast, stream);
-    case IMG_32x64: return img_launch<32, 64, K, 2, 2, 4, 16>(a, fast, stream);
-    case IMG_48x64: return img_launch<48, 64, K, 3, 1, 4, 16>(a, fast, stream);
-    case IMG_96x64: return img_launch<96, 64, K, 2, 2, 4, 16>(a, fast, stream);
-    case IMG_96x128: return img_launch<96, 128, K, 2, 2, 4, 16>(a, fast, stream);
-    default: return img_launch<64, 64, K, 4, 1, 4, 16>(a, fast, stream);
+    case IMG_128x64: return img_launch<128, 64, K, 4, 1, 4>(a, fast, stream);
+    case IMG_16x128: return img_launch<16, 128, K, 1, 4, 4>(a, fast, stream);
+    case IMG_32x64: return img_launch<32, 64, K, 2, 2, 4>(a, fast, stream);
+    case IMG_48x64: return img_launch<48, 64, K, 3, 1, 4>(a, fast, stream);
+    case IMG_96x64: return img_launch<96, 64, K, 2, 2, 4>(a, fast, stream);
+    case IMG_96x128: return img_launch<96, 128, K, 2, 2, 4>(a, fast, stream);
+    default: return img_launch<64, 64, K, 4, 1, 4>(a, fast, stream);
     }
 }
 
-template <int BM, int BN, int WM, int WN, int MF, bool PACKED = false>
+template <int BM, int BN, int WM, int WN, bool PACKED = false>
 static hipError_t wgrad_launch(const WgradArgs &a, hipStream_t stream)
 {
     int RS = (int)a.n_rs.d;
     int ntiles = PACKED ? (a.Ncol + BN - 1) / BN : RS * ((a.Cg + BN - 1) / BN);
     int tiles = ((a.M + BM - 1) / BM) * ntiles;
-    hipLaunchKernelGGL((wgrad_kernel<BM, BN, WM, WN, MF, PACKED>),
+    hipLaunchKernelGGL((wgrad_kernel<BM, BN, WM, WN, PACKED>),
                        dim3(tiles * a.groups * a.nsplit), dim3(64 * WM * WN), 0, stream, a);
     return hipGetLastError();
 }
@@ -973,15 +943,15 @@ static hipError_t wgrad_launch(const WgradArgs &a, hipStream_t stream)
 hipError_t launch_wgrad_gemm(const WgradArgs &a, int tile, hipStream_t stream)
 {
     switch (tile) {
-    case WG_TAP_64x32: return wgrad_launch<64, 32, 2, 2, 16>(a, stream);
-    case WG_TAP_64x48: return wgrad_launch<64, 48, 4, 1, 16>(a, stream);
-    case WG_TAP_64x16: return wgrad_launch<64, 16, 4, 1, 16>(a, stream);
-    case WG_TAP_128x32: return wgrad_launch<128, 32, 4, 1, 16>(a, stream);
-    case WG_TAP_64x64: return wgrad_launch<64, 64, 2, 2, 16>(a, stream);
-    case WG_TAP_128x64: return wgrad_launch<128, 64, 2, 2, 16>(a, stream);
-    case WG_PIX_96x64: return wgrad_launch<96, 64, 2, 2, 16, true>(a, stream);
-    case WG_PIX_64x64: return wgrad_launch<64, 64, 4, 1, 16, true>(a, stream);
-    case WG_PIX_64x32: return wgrad_launch<64, 32, 2, 2, 16, true>(a, stream);
+    case WG_TAP_64x32: return wgrad_launch<64, 32, 2, 2>(a, stream);
+    case WG_TAP_64x48: return wgrad_launch<64, 48, 4, 1>(a, stream);
+    case WG_TAP_64x16: return wgrad_launch<64, 16, 4, 1>(a, stream);
+    case WG_TAP_128x32: return wgrad_launch<128, 32, 4, 1>(a, stream);
+    case WG_TAP_64x64: return wgrad_launch<64, 64, 2, 2>(a, stream);
+    case WG_TAP_128x64: return wgrad_launch<128, 64, 2, 2>(a, stream);
+    case WG_PIX_96x64: return wgrad_launch<96, 64, 2, 2, true>(a, stream);
+    case WG_PIX_64x64: return wgrad_launch<64, 64, 4, 1, true>(a, stream);
+    case WG_PIX_64x32: return wgrad_launch<64, 32, 2, 2, true>(a, stream);
     default: return hipErrorInvalidValue;
     }
 }

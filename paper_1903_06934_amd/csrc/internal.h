@@ -31,7 +31,8 @@ FastDiv make_fastdiv(uint32_t d);
 // phase of the backward-data pass (source dy, columns = the input pixels of
 // one phase, taps = the filter taps of that phase).
 //
-// Per group g (grid z):  out[g] (M x Ncol) = A[g] (M x Kred) * B[g] (Kred x Ncol)
+// Per group g (folded with the tile and split index into the 1-D grid):
+//   out[g] (M x Ncol) = A[g] (M x Kred) * B[g] (Kred x Ncol)
 //   A[g][m][k]  = Ap[(g * M + m) * a_ld + k]            (packed m-major), or, for
 //                 the tiles of one wave row (img_tile_shares_a), Ap[(g * a_ld + k) * M + m]
 //                 (k-major); a_ld = Kred rounded up to a multiple of 16, rows past

@@ -85,3 +85,20 @@ def sample_indices(dims, rng, count=2048, groups=1, channel_axis=1):
         picks.append(base + np.fromiter(sorted(ring), dtype=np.int64))
     out = np.unique(np.concatenate(picks).astype(np.int64))
     return out
+
+
+# Filter gradients with at most this many elements are checked in full at
+# every batch; larger ones on sampled elements.
+FULL_DW_ELEMS = 65536
+
+
+def dw_indices(dw_shape, npq, rng):
+    """Flat dw indices to compare with the oracle's gather form: all of them
+    when dw has at most FULL_DW_ELEMS elements, else a sample (every filter's
+    first and last input channel included) sized to the reduction length npq
+    (the products per element)."""
+    size = int(np.prod(dw_shape))
+    if size <= FULL_DW_ELEMS:
+        return np.arange(size, dtype=np.int64)
+    count = int(min(2048, max(128, 1e9 / npq)))
+    return sample_indices(dw_shape, rng, count=count, groups=1, channel_axis=0)

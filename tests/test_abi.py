@@ -25,8 +25,8 @@ def L():
     return m.lib()
 
 
-def declared_functions():
-    text = open(HEADER).read()
+def declared_functions(header=HEADER):
+    text = open(header).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b([a-z_][a-z0-9_]*)\s*\(", text)) - {"sizeof", "defined"})
 
@@ -41,6 +41,25 @@ def test_exports_every_declared_function(L):
                           "pool_fwd", "pool_bwd"}
     for n in names:
         assert hasattr(L, n), n
+
+
+def test_peak_library_exports_its_header():
+    """libmipeak.so (the benchmark's measured reference points) loads and
+    exports what include/mipeak.h declares; its calls reject bad arguments
+    before launching anything."""
+    from paper_1903_06934_amd import peaks
+    if not os.path.exists(peaks.LIBRARY):
+        libbuild.build()
+    P = peaks.lib()
+    names = declared_functions(os.path.join(ROOT, "include", "mipeak.h"))
+    assert set(names) == {"peak_mfma_f32", "peak_copy"}
+    for n in names:
+        assert hasattr(P, n), n
+    assert P.peak_mfma_f32(1, 4, 10, 5, 0x1000, None, None) == -1   # chains not 4, 8, 16
+    assert P.peak_mfma_f32(1, 17, 10, 8, 0x1000, None, None) == -1  # more than 16 waves
+    assert P.peak_mfma_f32(1, 4, 10, 8, None, None, None) == -1     # no sink
+    assert P.peak_copy(0x1000, 0x2000, 24, 8, None) == -1           # not a multiple of 16
+    assert P.peak_copy(0x1004, 0x2000, 32, 8, None) == -1           # misaligned
 
 
 @pytest.mark.parametrize("n_in,f,st,pad,want", [
@@ -92,9 +111,15 @@ def test_workspace_sizes(L):
         for bad in BAD_SHAPES:
             assert m.workspace_size(p, bad) == 0
     assert m.workspace_size(3, GOOD) == 0
-    # one packed filter per pass; stride phases partition the taps
-    assert m.workspace_size(0, GOOD) == 32 * 16 * 9 * 4
-    assert m.workspace_size(1, (2, 4, 9, 9, 8, 3, 3, 2, 1, 1)) >= 8 * 4 * 9 * 4
+    # the rule (candidate 0): one packed filter per pass; stride phases
+    # partition the taps
+    assert m.plan_workspace_size(0, GOOD, 0) == 32 * 16 * 9 * 4
+    assert m.plan_workspace_size(1, (2, 4, 9, 9, 8, 3, 3, 2, 1, 1), 0) >= 8 * 4 * 9 * 4
+    # the size to allocate covers every candidate plan of the shape
+    for p in (0, 1, 2):
+        n = m.plan_count(p, GOOD)
+        assert m.workspace_size(p, GOOD) == max(m.plan_workspace_size(p, GOOD, i)
+                                                for i in range(n))
 
 
 def _align(n):
@@ -116,13 +141,13 @@ def test_bwd_data_blocked_plan_for_first_layers(L, shape, b, taps):
     N, C, H, W, K, R, S, st, pad, G = shape
     rows = C * b * b
     red = (K // G * taps + 15) // 16 * 16
-    assert m.workspace_size(1, shape) == _align(rows * red * 4)
+    assert m.plan_workspace_size(1, shape, 0) == _align(rows * red * 4)
 
 
 def test_bwd_data_phase_plan_for_wide_layers(L):
     """Channel-aligned layers keep one GEMM per stride phase (AlexNet conv2)."""
     shape = (128, 96, 27, 27, 256, 5, 5, 1, 2, 2)
-    assert m.workspace_size(1, shape) == _align(96 * 128 * 25 * 4)
+    assert m.plan_workspace_size(1, shape, 0) == _align(96 * 128 * 25 * 4)
 
 
 @pytest.mark.parametrize("shape", BAD_SHAPES)
@@ -133,7 +158,7 @@ def test_bad_shapes(L, shape):
 
 
 def test_fwd_checks(L):
-    ws = m.workspace_size(0, GOOD)
+    ws = m.plan_workspace_size(0, GOOD, 0)  # the rule's need (no plan stored)
     f = lambda *a: L.conv_fwd(*GOOD, *a, None)
     assert f(None, W_, B, Y, WSP, ws) == NULL
     assert f(X, None, B, Y, WSP, ws) == NULL
@@ -151,13 +176,13 @@ def test_fwd_checks(L):
 
 
 def test_bwd_checks(L):
-    ws = m.workspace_size(1, GOOD)
+    ws = m.plan_workspace_size(1, GOOD, 0)
     g = lambda *a: L.conv_bwd_data(*GOOD, *a, None)
     assert g(None, W_, X, WSP, ws) == NULL
     assert g(Y, W_, None, WSP, ws) == NULL
     assert g(Y, W_, X, WSP, ws - 4) == WS
     assert g(Y, W_, Y + 16, WSP, ws) == ALIAS
-    ws = m.workspace_size(2, GOOD)
+    ws = m.plan_workspace_size(2, GOOD, 0)
     h = lambda *a: L.conv_bwd_weight(*GOOD, *a, None)
     assert h(X, Y, None, B, WSP, ws) == NULL
     assert h(X, None, W_, B, WSP, ws) == NULL

@@ -11,7 +11,7 @@ import pytest
 
 import oracle
 import workloads
-from gpu_util import (assert_within, dev, gpu_bwd_data, gpu_bwd_weight, gpu_fwd,
+from gpu_util import (assert_within, dev, dw_indices, gpu_bwd_data, gpu_bwd_weight, gpu_fwd,
                       sample_indices)
 from oracle_pins import SMALL_SHAPES
 
@@ -69,6 +69,8 @@ EDGE_SHAPES = SMALL_SHAPES + [
     (2, 32, 20, 20, 32, 3, 3, 1, 1, 1),    # channel-aligned, several tiles
     (1, 1, 1, 1, 1, 1, 1, 1, 0, 1),        # smallest layer
     (2, 16, 3, 3, 16, 3, 3, 1, 2, 1),      # map smaller than the filter span
+    (2, 4, 1, 1, 3, 1, 1, 3, 1, 1),        # 1x1 image, padded: reads only padding
+    (16, 8, 1, 1, 32, 1, 1, 5, 2, 1),      # the same with a batch of 16s
 ]
 
 
@@ -164,12 +166,7 @@ def test_config_layer_full_batch_sampled(cfg, li):
     assert_within(dx.ravel()[idx], v, a, "bwd_data")
     del dx
     dw, db = gpu_bwd_weight(shape, d["x"], d["dy"])
-    npq = N * L.P * L.Q                     # products per dw element
-    if dw.size * npq <= 2e9:
-        idx = np.arange(dw.size)
-    else:
-        count = int(min(2048, max(128, 1e9 / npq)))
-        idx = sample_indices(dw.shape, rng, count=count, groups=1, channel_axis=0)
+    idx = dw_indices(dw.shape, N * L.P * L.Q, rng)  # every element when |dw| <= 64k
     v, a = oracle.conv_bwd_weight_at(shape, d["x"], d["dy"], idx)
     assert_within(dw.ravel()[idx], v, a, "bwd_weight")
     v, a = oracle.bias_grad(d["dy"])
@@ -251,7 +248,7 @@ def test_failed_call_writes_nothing():
     dx = torch.full((N, C, H, W), 7.0, device="cuda")
     dw = torch.full((K, C, R, S), 7.0, device="cuda")
     stream = torch.cuda.current_stream().cuda_stream
-    need = [m.workspace_size(p, shape) for p in (0, 1, 2)]
+    need = [m.plan_workspace_size(p, shape, m.plan_get(p, shape)) for p in (0, 1, 2)]
     ws = torch.empty(max(need) + 64, dtype=torch.uint8, device="cuda")
     p = lambda t: t.data_ptr()  # noqa: E731
     small = [max(n - 1, 0) for n in need]

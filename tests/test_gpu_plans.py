@@ -71,8 +71,8 @@ def test_every_candidate_matches_oracle(shape):
         for i in range(n):
             name = m.plan_name(p, shape, i)
             m.plan_set(p, shape, i)
-            nbytes = m.workspace_size(p, shape)
-            assert nbytes == m.plan_workspace_size(p, shape, i)
+            nbytes = m.plan_workspace_size(p, shape, i)
+            assert nbytes <= m.workspace_size(p, shape)
             ws = torch.empty(max(nbytes, 16), dtype=torch.uint8, device="cuda")
             outs = _run(p, shape, t, ws)
             for (ref, absum), got in zip(refs[p], outs):
@@ -122,7 +122,7 @@ def test_tune_respects_workspace():
     N, C, H, W, K, R, S, st, pad, G = shape
     d = _inputs(shape, (33, 0))
     t = {k: dev(v) for k, v in d.items()}
-    nbytes = m.workspace_size(m.PASS_FWD, shape)
+    nbytes = m.plan_workspace_size(m.PASS_FWD, shape, 0)
     ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
     y = torch.empty((N, K, 12, 12), device="cuda")
     chosen = m.conv_tune(m.PASS_FWD, shape, t["x"], t["w"], t["b"], y, None, ws, reps=1)
@@ -133,7 +133,7 @@ def test_tune_respects_workspace():
 
 def _tuned_cases():
     out = []
-    for cfg in (1, 5):
+    for cfg in (1, 2, 3, 4, 5):
         name, layers = workloads.config(cfg)
         for li, L in enumerate(layers):
             if isinstance(L, workloads.PoolLayer) or (cfg == 5 and L.R > 1):
@@ -146,10 +146,11 @@ def _tuned_cases():
 def test_tuned_plans_full_batch_sampled(cfg, li):
     """The benchmark's launch configuration: every pass of the layer at its
     configured batch with the plan conv_tune keeps (as bench.py does before
-    timing), then sampled elements against the oracle's gather forms."""
+    timing), then sampled elements (every dw element when dw has at most 64k)
+    against the oracle's gather forms."""
     import torch
     import paper_1903_06934_amd as m
-    from gpu_util import sample_indices
+    from gpu_util import dw_indices, sample_indices
     L = workloads.config(cfg)[1][li]
     d = workloads.layer_inputs(cfg, li)
     shape = L.shape
@@ -182,9 +183,7 @@ def test_tuned_plans_full_batch_sampled(cfg, li):
     del dx
     dw, db = m.conv_bwd_weight(t["x"], t["dy"], (R, S), st, pad, G)
     dw, db = host(dw), host(db)
-    npq = N * L.P * L.Q
-    count = int(min(2048, max(128, 1e9 / npq)))
-    idx = sample_indices(dw.shape, rng, count=count, groups=1, channel_axis=0)
+    idx = dw_indices(dw.shape, N * L.P * L.Q, rng)  # every element when |dw| <= 64k
     v, a = oracle.conv_bwd_weight_at(shape, d["x"], d["dy"], idx)
     assert_within(dw.ravel()[idx], v, a, f"bwd_weight with plan {names[2]}")
     v, a = oracle.bias_grad(d["dy"])
