@@ -72,7 +72,9 @@ typedef enum miconv_status {
     MICONV_ERR_LAUNCH = -7,    /* a kernel launch reported an error */
     MICONV_ERR_PASS = -8,      /* unknown pass id */
     MICONV_ERR_PLAN = -9,      /* plan index outside [0, conv_plan_count()) */
-    MICONV_ERR_MODE = -10      /* pooling mode other than MICONV_POOL_MAX / _AVG */
+    MICONV_ERR_MODE = -10,     /* pooling mode other than MICONV_POOL_MAX / _AVG */
+    MICONV_ERR_SCRATCH = -11   /* conv_bwd_weight_noalloc: the plan's workspace exceeds
+                                  MICONV_NOALLOC_SCRATCH_BYTES */
 } miconv_status;
 
 /* Pass ids for conv_workspace_size and the plan calls. */
@@ -137,6 +139,27 @@ int conv_bwd_data(int N, int C, int H, int W, int K, int R, int S, int stride, i
 int conv_bwd_weight(int N, int C, int H, int W, int K, int R, int S, int stride, int pad,
                     int group, const float *x, const float *dy, float *dw, float *db,
                     void *ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * conv_bwd_weight without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): the same pass, plan and kernels as
+ * conv_bwd_weight (same results, bit for bit), with the workspace taken from
+ * a fixed device array inside the library of MICONV_NOALLOC_SCRATCH_BYTES
+ * (96 MiB), one per GPU, held from the library's first use on that GPU until
+ * the process ends.  The call allocates nothing (no hipMalloc, no allocating
+ * library routine); the first call on a device looks up that device's array.
+ * Returns the statuses of conv_bwd_weight (but never MICONV_ERR_WORKSPACE),
+ * or MICONV_ERR_SCRATCH, before any launch, when the plan the call would run
+ * needs more than the array holds (conv_plan_workspace_size of the current
+ * plan tells).  Every call on a GPU shares that GPU's array: calls that
+ * overlap in time on one GPU (other threads, other streams without ordering)
+ * race and must not be issued.  Nothing in the array needs to start at zero.
+ */
+#define MICONV_NOALLOC_SCRATCH_BYTES (96u << 20)
+int conv_bwd_weight_noalloc(int N, int C, int H, int W, int K, int R, int S, int stride,
+                            int pad, int group, const float *x, const float *dy, float *dw,
+                            float *db, hipStream_t stream);
 
 /*
  * Benchmark instrumentation; not needed to compute anything.  After this

@@ -1823,6 +1823,36 @@ int make_pool(int mode, int N, int C, int H, int W, int R, int S, int stride, in
     return MICONV_OK;
 }
 
+// ------------------------------------------------------------ fixed scratch
+// Workspace of conv_bwd_weight_noalloc: a file-scope device array, one copy
+// per GPU (each device holds it from module load until the process ends).
+// In host code `scratch` is only a host-side stand-in for the symbol; its
+// device address is read per device with hipGetSymbolAddress, and that
+// address is what the kernels receive.
+constexpr size_t kScratchBytes = (size_t)MICONV_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+std::mutex g_scratch_mu;
+void *g_scratch_dev[64];  // device address of `scratch`, per device id
+
+// Device address of this device's scratch array (looked up on the first call
+// on each device, with that device current).
+int scratch_address(void **out)
+{
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64)
+        return MICONV_ERR_DEVICE;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_dev[dev]) {
+        void *ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr)
+            return MICONV_ERR_LAUNCH;
+        g_scratch_dev[dev] = ptr;
+    }
+    *out = g_scratch_dev[dev];
+    return MICONV_OK;
+}
+
 }  // namespace
 }  // namespace miconv
 
@@ -1881,6 +1911,8 @@ const char *conv_error_string(int status)
     case MICONV_ERR_PASS: return "unknown pass id";
     case MICONV_ERR_PLAN: return "plan index out of range";
     case MICONV_ERR_MODE: return "unknown pooling mode";
+    case MICONV_ERR_SCRATCH:
+        return "the plan needs more workspace than the library's fixed device scratch holds";
     default: return "unknown status";
     }
 }
@@ -1916,6 +1948,28 @@ int conv_bwd_weight(int N, int C, int H, int W, int K, int R, int S, int stride,
     if (st != MICONV_OK)
         return st;
     return wgrad_exec(g, wgrad_current(g), x, dy, dw, db, ws, ws_bytes, stream);
+}
+
+int conv_bwd_weight_noalloc(int N, int C, int H, int W, int K, int R, int S, int stride,
+                            int pad, int group, const float *x, const float *dy, float *dw,
+                            float *db, hipStream_t stream)
+{
+    Geom g;
+    int st = make_geom(N, C, H, W, K, R, S, stride, pad, group, &g);
+    if (st != MICONV_OK)
+        return st;
+    const WgradPlan p = wgrad_current(g);
+    if (wgrad_ws(g, p) > kScratchBytes)
+        return MICONV_ERR_SCRATCH;
+    if ((st = check_device()) != MICONV_OK)
+        return st;
+    void *ws = nullptr;
+    if ((st = scratch_address(&ws)) != MICONV_OK)
+        return st;
+    // Every word of the scratch that the plan's kernels read (split
+    // partials, bias partials, transposed operands) is written earlier in the
+    // same call, so nothing needs clearing between calls.
+    return wgrad_exec(g, p, x, dy, dw, db, ws, kScratchBytes, stream);
 }
 
 int conv_plan_count(int pass, int N, int C, int H, int W, int K, int R, int S, int stride,

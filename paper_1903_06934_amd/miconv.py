@@ -18,7 +18,7 @@ STATUS = {
     0: "MICONV_OK", -1: "MICONV_ERR_SHAPE", -2: "MICONV_ERR_NULL",
     -3: "MICONV_ERR_WORKSPACE", -4: "MICONV_ERR_ALIAS", -5: "MICONV_ERR_ALIGN",
     -6: "MICONV_ERR_DEVICE", -7: "MICONV_ERR_LAUNCH", -8: "MICONV_ERR_PASS",
-    -9: "MICONV_ERR_PLAN", -10: "MICONV_ERR_MODE",
+    -9: "MICONV_ERR_PLAN", -10: "MICONV_ERR_MODE", -11: "MICONV_ERR_SCRATCH",
 }
 POOL_MODES = {"max": 0, "avg": 1}
 PASS_FWD, PASS_BWD_DATA, PASS_BWD_WEIGHT = 0, 1, 2
@@ -59,6 +59,8 @@ def lib():
     L.conv_bwd_data.restype = _I
     L.conv_bwd_weight.argtypes = geo + [_P, _P, _P, _P, _P, _Z, _P]
     L.conv_bwd_weight.restype = _I
+    L.conv_bwd_weight_noalloc.argtypes = geo + [_P, _P, _P, _P, _P]
+    L.conv_bwd_weight_noalloc.restype = _I
     L.conv_set_timing_events.argtypes = [_P, _P]
     L.conv_set_timing_events.restype = _I
     L.conv_error_string.argtypes = [_I]

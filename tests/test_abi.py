@@ -38,7 +38,7 @@ def test_exports_every_declared_function(L):
                           "conv_set_timing_events", "conv_plan_count", "conv_plan_get",
                           "conv_plan_set", "conv_plan_clear", "conv_plan_name",
                           "conv_plan_workspace_size", "conv_tune", "pool_output_size",
-                          "pool_fwd", "pool_bwd"}
+                          "pool_fwd", "pool_bwd", "conv_bwd_weight_noalloc"}
     for n in names:
         assert hasattr(L, n), n
 
@@ -190,6 +190,26 @@ def test_bwd_checks(L):
     assert h(X, Y, W_, X, WSP, ws) == ALIAS              # db overlaps x
     assert h(X, Y, W_, None, WSP, 0) == WS
     assert h(X, Y, W_ + 4, None, WSP, ws) == ALIGN
+
+
+def test_noalloc_checks_before_any_device_use(L):
+    """conv_bwd_weight_noalloc refuses, on the host, a shape whose plan needs
+    more than the fixed scratch (96 MiB) and a bad shape; a well-formed call
+    reaches the device check."""
+    import torch
+    SCRATCH = -11
+    big = (32, 512, 28, 28, 512, 3, 3, 1, 1, 1)
+    n = m.plan_count(2, big)
+    i = max(range(n), key=lambda j: m.plan_workspace_size(2, big, j))
+    assert m.plan_workspace_size(2, big, i) > (96 << 20)
+    m.plan_set(2, big, i)
+    try:
+        assert L.conv_bwd_weight_noalloc(*big, X, Y, W_, None, None) == SCRATCH
+    finally:
+        m.plan_clear()
+    assert L.conv_bwd_weight_noalloc(*BAD_SHAPES[0], X, Y, W_, None, None) == SHAPE
+    if not torch.cuda.is_available():
+        assert L.conv_bwd_weight_noalloc(*GOOD, X, Y, W_, B, None) == DEVICE
 
 
 def test_device_check_without_gpu(L):
