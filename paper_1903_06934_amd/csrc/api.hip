@@ -240,8 +240,8 @@ int pick_img_tile(int M, long long Ncol, int Kred, int G)
 
 void img_tile_dims(int tile, int &bm, int &bn)
 {
-    static const int dims[][2] = {{64, 64}, {128, 64}, {16, 128}, {32, 64},
-                                  {48, 64}, {96, 64},  {96, 128}};
+    static const int dims[][2] = {{64, 64}, {128, 64}, {16, 128}, {32, 64}, {48, 64},
+                                  {96, 64}, {96, 128}, {128, 128}, {64, 128}};
     bm = dims[tile][0];
     bn = dims[tile][1];
 }
@@ -265,12 +265,13 @@ int images_per_launch(const Geom &g)
 // paper's framework times its convolution strategies over the first training
 // iterations before keeping the fastest), overrides the rule.
 
-constexpr int kNumImgTiles = 7;
+constexpr int kNumImgTiles = 9;
 constexpr int kNumWgradTiles = 9;
 
 const char *img_tile_name(int tile)
 {
-    static const char *names[] = {"64x64", "128x64", "16x128", "32x64", "48x64", "96x64", "96x128"};
+    static const char *names[] = {"64x64", "128x64", "16x128", "32x64", "48x64",
+                                  "96x64", "96x128", "128x128", "64x128"};
     static_assert(sizeof(names) / sizeof(names[0]) == kNumImgTiles, "one name per tile");
     return tile >= 0 && tile < kNumImgTiles ? names[tile] : "?";
 }

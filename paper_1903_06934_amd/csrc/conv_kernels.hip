@@ -117,11 +117,21 @@ __device__ __forceinline__ int xcd_tile(int hw, int total)
 // (tap, channel) decode of k is scalar work.
 // FAST: cin % 16 == 0, so a slice lies inside one filter tap; the spatial
 // bounds test and offset are then computed once per slice and column.
+// ONE (with FAST, 64-column tiles): the 1x1 direct GEMM -- one tap, stride 1,
+// no offset, the source pixel index equal to the column's pixel index and
+// pixels per image a multiple of 4 -- so each source row of a slice is 64
+// consecutive pixels in 16 aligned groups of 4 that never straddle an image.
+// B is then staged with 16-byte direct-to-LDS loads (buffer_load_dwordx4 ...
+// lds): one wave-load fills 4 rows x 64 columns, a quarter of the load
+// instructions of the one-dword gather.  LDS layout of a stage: 4-row
+// groups of 256 words plus 16 words of padding, so that the four lane groups
+// of a ds_read_b32 (rows 4 apart, i.e. one row in each group) hit distinct
+// banks.
 //
 // Pipeline: three stages (LDS buffers for B, and for A or register sets for
 // A); slices t + 1 and t + 2 are in flight while slice t computes.
 // ---------------------------------------------------------------------------
-template <int BM, int BN, int BK, int WM, int WN, int PAD, bool FAST, int NST>
+template <int BM, int BN, int BK, int WM, int WN, int PAD, bool FAST, int NST, bool ONE = false>
 __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArgs a)
 {
     constexpr int NW = WM * WN;
@@ -134,19 +144,26 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
     // rows (3-wave tiles, one 64-wide segment), the waves with a row fewer
     // issue one more load into a spare LDS row (out-of-range offset: it
     // reads zero and touches no memory), so every wave issues LB loads.
-    constexpr int LB = (BK * HB + NW - 1) / NW;
-    constexpr int BROWS = BK + ((BK * HB) % NW ? 1 : 0);
-    constexpr int LDA = 64 * HA + PAD, LDB = BN + PAD;
+    // ONE: BK / 4 wave-loads of 4 rows x 64 columns per slice; waves with a
+    // load fewer issue one into a spare group (out of range: reads zero).
+    constexpr int NG = BK / 4;
+    constexpr int LB = ONE ? (NG + NW - 1) / NW : (BK * HB + NW - 1) / NW;
+    constexpr int BROWS = ONE ? NG + (NG % NW ? 1 : 0) : BK + ((BK * HB) % NW ? 1 : 0);
+    constexpr int LDA = 64 * HA + PAD, LDB = ONE ? 4 * 64 + 16 : BN + PAD;
     static_assert(BK == 16 && NST == 3, "16-row slices, 3 stages");
     static_assert(BN % 64 == 0 && TM % 16 == 0 && TN % 16 == 0, "tile");
     static_assert(BK % NW == 0 || HB == 1, "uneven B rows need one segment per row");
     static_assert(!ASH || (BK * HA) % NW == 0, "A rows per wave");
+    static_assert(!ONE || (FAST && HB == 1 && !ASH), "1x1 direct GEMM: 64-column tiles");
 
     // One distinct array per pipeline stage, so that the compiler's alias
     // analysis can tell an in-flight direct-to-LDS load from a read of
     // another stage's buffer (it would otherwise wait for every load).
+    // B element (row k, column n) lies at [k][n], or for ONE at
+    // [k / 4][(k % 4) * 64 + n].
     __shared__ float As0[ASH ? BK : 1][LDA], As1[ASH ? BK : 1][LDA], As2[ASH ? BK : 1][LDA];
-    __shared__ float Bs0[BROWS][LDB], Bs1[BROWS][LDB], Bs2[BROWS][LDB];
+    __shared__ __attribute__((aligned(16))) float Bs0[BROWS][LDB], Bs1[BROWS][LDB],
+        Bs2[BROWS][LDB];
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -189,6 +206,20 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
     }
     const uint32_t a_gbase = (uint32_t)g * (uint32_t)a.a_ld * (uint32_t)a.M * 4u;
 
+    // ONE: lane l stages row l / 16 of a 4-row group at columns
+    // n0 + 4 (l % 16) .. + 3; byte offset of that source row segment for
+    // channel 0 of the group (or out of range past the last column).
+    uint32_t b4_base = 0;
+    if constexpr (ONE) {
+        const int n = n0 + 4 * (lane & 15);
+        const uint32_t c = n < a.Ncol ? (uint32_t)n : 0u;
+        const uint32_t img = fast_div(c, a.col_hw);
+        const uint32_t pix = c - img * a.col_hw.d;
+        b4_base = ((img * a.src_img_words + ((uint32_t)g * a.cin + (uint32_t)(lane >> 4)) *
+                                                (uint32_t)a.src_hw + pix) * 4u) |
+                  oob_mask(n < a.Ncol);
+    }
+
     // Per-lane B column data: image base offset, base coordinates, validity.
     uint32_t b_base[HB];
     int b_hb[HB], b_wb[HB];
@@ -223,7 +254,19 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
             for (int i = 0; i < FM; i++)
                 ar[i] = load4_untracked(rAw, (a_off[i] + (uint32_t)k0 * 4u) | a_msk[i]);
         }
-        if constexpr (FAST) {
+        if constexpr (ONE) {
+            // Slice k0 covers channels k0 .. k0 + 15 (one tap); group j its
+            // rows 4 j .. 4 j + 3.
+#pragma unroll
+            for (int j = 0; j < LB; j++) {
+                const int grp = wave + NW * j;
+                const bool live = grp < NG;
+                const uint32_t off =
+                    (b4_base + (uint32_t)(k0 + 4 * grp) * (uint32_t)a.src_hw * 4u) | oob_mask(live);
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rB, (LDS_AS void *)&Bd[live ? grp : NG][0],
+                                                         16, off, 0, 0, 0);
+            }
+        } else if constexpr (FAST) {
             // Slice k0 / 16 = cb * taps + tap covers channels 16 cb .. 16 cb + 15.
             const uint32_t sl = (uint32_t)k0 / 16u;
             const uint32_t cb = fast_div(sl, a.k_taps);
@@ -289,8 +332,12 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
 #pragma unroll
         for (int s = 0; s < 4; s++)
 #pragma unroll
-            for (int j = 0; j < FN; j++)
-                bf[s][j] = Bc[4 * kr + s][wn * TN + j * 16 + lc];
+            for (int j = 0; j < FN; j++) {
+                if constexpr (ONE)
+                    bf[s][j] = Bc[kr][s * 64 + wn * TN + j * 16 + lc];
+                else
+                    bf[s][j] = Bc[4 * kr + s][wn * TN + j * 16 + lc];
+            }
         f32x4 af[FM];
 #pragma unroll
         for (int i = 0; i < FM; i++) {
@@ -892,12 +939,29 @@ __global__ __launch_bounds__(RED_E * RED_J) void splitk_reduce_kernel(
 // Launchers.
 // ---------------------------------------------------------------------------
 
+// Whether a launch is a 1x1 direct GEMM the ONE variant can stage with
+// 16-byte loads: one tap, stride 1, no offset, the source pixel index equal
+// to the column's, channel-aligned slices, pixels per image a multiple of 4.
+static bool one_by_one_direct(const ImgGemmArgs &a, bool fast)
+{
+    return fast && a.k_taps.d == 1 && a.k_tw.d == 1 && a.cstep == 1 && a.coff_h == 0 &&
+           a.coff_w == 0 && a.mblock <= 1 && a.src_hw == (int)a.col_hw.d &&
+           a.src_w == (int)a.col_w.d && a.col_hw.d % 4 == 0;
+}
+
 template <int BM, int BN, int BK, int WM, int WN, int PAD>
 static hipError_t img_launch(const ImgGemmArgs &a, bool fast, hipStream_t stream)
 {
     constexpr int NST = 3;
     int tiles = ((a.M + BM - 1) / BM) * ((a.Ncol + BN - 1) / BN);
     dim3 grid(tiles * a.groups * a.nsplit);
+    if constexpr (BN == 64 && WM > 1) {
+        if (one_by_one_direct(a, fast)) {
+            hipLaunchKernelGGL((img_gemm_kernel<BM, BN, BK, WM, WN, PAD, true, NST, true>), grid,
+                               dim3(64 * WM * WN), 0, stream, a);
+            return hipGetLastError();
+        }
+    }
     if (fast)
         hipLaunchKernelGGL((img_gemm_kernel<BM, BN, BK, WM, WN, PAD, true, NST>), grid,
                            dim3(64 * WM * WN), 0, stream, a);
@@ -925,6 +989,8 @@ hipError_t launch_img_gemm(const ImgGemmArgs &a, int tile, bool fast, hipStream_
     case IMG_48x64: return img_launch<48, 64, K, 3, 1, 4>(a, fast, stream);
     case IMG_96x64: return img_launch<96, 64, K, 2, 2, 4>(a, fast, stream);
     case IMG_96x128: return img_launch<96, 128, K, 2, 2, 4>(a, fast, stream);
+    case IMG_128x128: return img_launch<128, 128, K, 2, 2, 4>(a, fast, stream);
+    case IMG_64x128: return img_launch<64, 128, K, 2, 2, 4>(a, fast, stream);
     default: return img_launch<64, 64, K, 4, 1, 4>(a, fast, stream);
     }
 }

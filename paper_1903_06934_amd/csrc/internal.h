@@ -104,7 +104,10 @@ struct WgradArgs {
 };
 
 // Image-GEMM tile shapes (BM x BN; 4 waves, 3 for 48x64).
-enum ImgTile { IMG_64x64 = 0, IMG_128x64, IMG_16x128, IMG_32x64, IMG_48x64, IMG_96x64, IMG_96x128 };
+enum ImgTile {
+    IMG_64x64 = 0, IMG_128x64, IMG_16x128, IMG_32x64, IMG_48x64, IMG_96x64, IMG_96x128,
+    IMG_128x128, IMG_64x128
+};
 // Tiles with one wave row (WM == 1 in launch_img_gemm): every wave needs the
 // same filter rows, which the kernel then shares through LDS, packed k-major.
 inline bool img_tile_shares_a(int tile) { return tile == IMG_16x128; }

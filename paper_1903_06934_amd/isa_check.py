@@ -76,7 +76,9 @@ def check_function(name: str, body: list) -> list:
     loop = _loop_lines(body)
     n = len(loop)
     for p, t in enumerate(loop):
-        if not t.startswith("buffer_load_dwordx4"):
+        # Register loads only: a direct-to-LDS load (suffix "lds") has no
+        # destination register and is tracked by the compiler.
+        if not t.startswith("buffer_load_dwordx4") or t.split()[-1] == "lds":
             continue
         X = _regs(t.split(",")[0])
         seq = [loop[(p + k) % n] for k in range(1, n)]

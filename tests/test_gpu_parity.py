@@ -102,6 +102,28 @@ def test_large_tile_paths(shape):
     full_parity(shape)
 
 
+# 1x1 stride-1 layers (and the first stride phase of a 1x1 stride-2 layer's
+# backward-data) whose pixels per image are a multiple of 4 and whose
+# channels per group are a multiple of 16 run the image GEMM's direct 1x1
+# variant (16-byte staging loads) on its 64-column tiles: each such row tile
+# class, groups, ragged column tails, a split reduction; and 7 x 7 maps
+# (49 pixels) that keep the one-dword gather.
+ONE_BY_ONE_SHAPES = [
+    (2, 32, 14, 14, 48, 1, 1, 1, 0, 1),    # 196 pixels, M = 48 (three waves), ragged columns
+    (3, 64, 6, 10, 80, 1, 1, 1, 0, 1),     # M = 80 (96-row tile), bwd-data M = 64
+    (2, 128, 8, 8, 256, 1, 1, 1, 0, 1),    # M = 256 (128x64), bwd-data M = 128
+    (3, 64, 12, 12, 32, 1, 1, 1, 0, 2),    # groups, M = 16 / 32 per group
+    (2, 64, 28, 28, 32, 1, 1, 2, 0, 1),    # stride 2: bwd-data phase (0, 0) is direct
+    (1, 3072, 4, 4, 64, 1, 1, 1, 0, 1),    # one tile, deep reduction: split
+    (2, 32, 7, 7, 32, 1, 1, 1, 0, 1),      # 49 pixels: the gather path
+]
+
+
+@pytest.mark.parametrize("shape", ONE_BY_ONE_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_one_by_one_direct(shape):
+    full_parity(shape)
+
+
 # Backward-data with few input channels: the blocked plan (b x b input pixels
 # of a block as GEMM rows, b = stride * f).  Many edge shapes above take it
 # too; these add each row-tile class and several column tiles.

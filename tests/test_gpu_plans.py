@@ -25,6 +25,7 @@ PLAN_SHAPES = [
     (32, 200, 1, 1, 72, 1, 1, 1, 0, 1),    # inner product, batch of 16s: dW as an image GEMM
     (8, 1024, 1, 1, 100, 1, 1, 1, 0, 1),   # inner product, forward fine splits
     (8, 100, 1, 1, 1024, 1, 1, 1, 0, 1),   # inner product, backward-data fine splits
+    (2, 64, 12, 12, 48, 1, 1, 1, 0, 1),    # 1x1 direct GEMM on every 64-column tile
 ]
 
 
