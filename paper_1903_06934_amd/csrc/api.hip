@@ -308,6 +308,8 @@ struct ImgPlan {
     int tile, nsplit, kchunk;  // tile -1: (backward-data phases) each phase by the rule
     int xnb = 0;               // forward: explicit plan, images per column chunk (0: implicit)
     bool bt = false;           // inner product: batch-transposed plan
+    int halo = -1;             // halo GEMM tile (HaloTile), or -1; kchunk then counts
+    int tw = 0;                // 16-channel blocks per split, tw the pixel-block width
 };
 
 // Splits for `tiles` workgroups over Kred rows: about 8 workgroups per CU,
@@ -346,7 +348,110 @@ ImgPlan img_rule(int M, long long Ncol, int Kred, int G, bool allow_split)
 
 bool same_img(const ImgPlan &a, const ImgPlan &b)
 {
-    return a.tile == b.tile && a.nsplit == b.nsplit && a.xnb == b.xnb && a.bt == b.bt;
+    return a.tile == b.tile && a.nsplit == b.nsplit && a.xnb == b.xnb && a.bt == b.bt &&
+           a.halo == b.halo && a.tw == b.tw;
+}
+
+// ------------------------------------------------------------ halo plans
+// Stride-1 3 x 3 layers with channel-aligned slices can run the halo GEMM
+// (halo_gemm_kernel): 112-column tiles that are TR x TW pixel blocks, the
+// source region of a 16-channel block staged once for all nine taps.  The
+// block width is the one of 112, 56, 28, 14 that pads the output grid
+// (P x Q) least; 0 if none can stage this source (16-byte loads need a
+// source width that is a multiple of 4).
+int halo_width(int P, int Q, int src_w)
+{
+    int best = 0;
+    long long best_cols = 0;
+    for (int tw : {112, 56, 28, 14}) {
+        if (!halo_width_supported(tw, src_w, 0))
+            continue;
+        const int tr = kHaloCols / tw;
+        const long long cols = (long long)((P + tr - 1) / tr) * ((Q + tw - 1) / tw) * kHaloCols;
+        if (!best || cols < best_cols) {
+            best = tw;
+            best_cols = cols;
+        }
+    }
+    return best;
+}
+
+long long halo_tile_count(int tile, int M, int nimg, int P, int Q, int tw, int G)
+{
+    const int bm = tile == HALO_128x112 ? 128 : 64, tr = kHaloCols / tw;
+    return (long long)((M + bm - 1) / bm) * nimg * ((P + tr - 1) / tr) * ((Q + tw - 1) / tw) * G;
+}
+
+// A halo plan over ncb channel blocks: unsplit (ns = 1), or split so that
+// about three workgroups per CU run (each split at least 4 blocks) when ns
+// is 0, or into ns splits.
+ImgPlan halo_plan(int tile, int tw, long long tiles, int ncb, int ns)
+{
+    if (ns == 0) {
+        const long long want = 3LL * num_cus();
+        ns = tiles >= want ? 1 : (int)std::min<long long>((want + tiles - 1) / tiles, ncb / 4);
+        if (ns < 2)
+            ns = 1;
+    }
+    ImgPlan p{IMG_64x64, 1, ncb};  // tile: the packed-filter layout (m-major)
+    p.halo = tile;
+    p.tw = tw;
+    if (ns > 1) {
+        p.kchunk = (ncb + ns - 1) / ns;
+        p.nsplit = (ncb + p.kchunk - 1) / p.kchunk;
+    }
+    return p;
+}
+
+// Halo candidates of a stride-1 3 x 3 GEMM with M rows over cin source
+// channels (a multiple of 16), an nimg x P x Q output grid and a src_w-wide
+// source: each tile that fits M, unsplit and (allow_split) split.
+template <class P, class Make>
+void halo_variants(int M, int cin, int nimg, int Pout, int Qout, int src_w, int G,
+                   bool allow_split, Make make, std::vector<P> &out)
+{
+    const int tw = halo_width(Pout, Qout, src_w);
+    if (!tw || cin % 16)
+        return;
+    const int ncb = cin / 16;
+    for (int tile : {HALO_128x112, HALO_64x112}) {
+        if (tile == HALO_128x112 && M <= 64)
+            continue;
+        const long long tiles = halo_tile_count(tile, M, nimg, Pout, Qout, tw, G);
+        ImgPlan cands[2] = {halo_plan(tile, tw, tiles, ncb, 1),
+                            halo_plan(tile, tw, tiles, ncb, allow_split ? 0 : 1)};
+        for (int i = 0; i < (cands[1].nsplit > 1 ? 2 : 1); i++) {
+            P p = make(cands[i]);
+            bool dup = false;
+            for (const P &q : out)
+                dup = dup || same_plan(p, q);
+            if (!dup)
+                out.push_back(p);
+        }
+    }
+}
+
+const char *halo_tile_name(int tile) { return tile == HALO_128x112 ? "128x112" : "64x112"; }
+
+// The built-in rule's use of the halo GEMM: whenever it applies and its pixel
+// blocks cover the output grid with at most 1/8 of the columns idle (every
+// map width of 224, 112, 56, 28 or 14 pixels; not 13 x 13, where the image
+// GEMM measured faster), with the 64-row tile, unsplit.  Measured on the
+// MI355X at the configurations' batches: VGG-16 conv1_2 ... conv5_3 forward
+// and backward-data 112-143 TFLOP/s against 93-126 for the image GEMM;
+// ResNet 56 x 56 / 14 x 14 3 x 3 layers 124 / 108 against 92-104 / 86.
+bool halo_rule(int cin, int Pout, int Qout, int src_w, ImgPlan *out)
+{
+    const int tw = halo_width(Pout, Qout, src_w);
+    if (!tw || cin % 16)
+        return false;
+    const int tr = kHaloCols / tw;
+    const double used = (double)Pout * Qout /
+                        ((double)((Pout + tr - 1) / tr) * ((Qout + tw - 1) / tw) * kHaloCols);
+    if (used < 0.875)
+        return false;
+    *out = halo_plan(HALO_64x112, tw, 0, cin / 16, 1);
+    return true;
 }
 
 // ------------------------------------------------------------ inner product
@@ -490,6 +595,9 @@ ImgPlan fwd_rule(const Geom &g)
         p.bt = true;
         return p;
     }
+    ImgPlan h;
+    if (g.st == 1 && g.R == 3 && g.S == 3 && halo_rule(g.Cg, g.P, g.Q, g.W, &h))
+        return h;
     const int nb = images_per_launch(g);
     return img_rule(g.Kg, (long long)(g.N < nb ? g.N : nb) * g.P * g.Q, g.Cg * g.R * g.S, g.G,
                     nb >= g.N);
@@ -511,6 +619,9 @@ void fwd_candidates(const Geom &g, std::vector<ImgPlan> &out)
     const int nb = images_per_launch(g);
     img_variants<ImgPlan>(g.Kg, (long long)(g.N < nb ? g.N : nb) * g.P * g.Q, g.Cg * g.R * g.S,
                           g.G, nb >= g.N, [](const ImgPlan &p) { return p; }, out);
+    if (g.st == 1 && g.R == 3 && g.S == 3 && !is_inner_product(g))
+        halo_variants<ImgPlan>(g.Kg, g.Cg, g.N < nb ? g.N : nb, g.P, g.Q, g.W, g.G, nb >= g.N,
+                               [](const ImgPlan &p) { return p; }, out);
     // Explicit: im2col, then the 1x1 GEMM with its own rule's tile.
     if (const int xnb = explicit_images(g)) {
         const int kred = g.Cg * g.R * g.S;
@@ -539,6 +650,12 @@ void fwd_name(const ImgPlan &p, char *buf, size_t len)
     if (p.xnb > 0)
         snprintf(buf, len, "explicit im2col (%d images a chunk), image GEMM %s", p.xnb,
                  img_tile_name(p.tile));
+    else if (p.halo >= 0 && p.nsplit > 1)
+        snprintf(buf, len, "halo GEMM %s (%dx%d pixels), %d splits", halo_tile_name(p.halo),
+                 p.tw, kHaloCols / p.tw, p.nsplit);
+    else if (p.halo >= 0)
+        snprintf(buf, len, "halo GEMM %s (%dx%d pixels)", halo_tile_name(p.halo), p.tw,
+                 kHaloCols / p.tw);
     else if (p.nsplit > 1)
         snprintf(buf, len, "%simage GEMM %s, %d splits", pre, img_tile_name(p.tile), p.nsplit);
     else
@@ -668,6 +785,8 @@ BwdPlan bwd_rule(const Geom &g)
         const int kred = g.Kg * p.bp.ntr * p.bp.nts;
         p.img = with_split(pick_img_tile(p.bp.M, (long long)n0 * p.bp.nh * p.bp.nw, kred, g.G),
                            kred, 1);
+    } else if (g.st == 1 && g.R == 3 && g.S == 3 && halo_rule(g.Kg, g.H, g.W, g.Q, &p.img)) {
+        // The one phase as a halo GEMM.
     } else if (g.st == 1) {
         // Split-K only for stride 1 (one phase covering all of dx).
         p.img = img_rule(g.Cg, (long long)n0 * g.H * g.W, g.Kg * g.R * g.S, g.G, nb >= g.N);
@@ -697,6 +816,11 @@ void bwd_candidates(const Geom &g, std::vector<BwdPlan> &out)
     img_variants<BwdPlan>(g.Cg, (long long)n0 * g.H * g.W / (g.st * g.st), kred_max, g.G,
                           g.st == 1 && nb >= g.N,
                           [](const ImgPlan &i) { return BwdPlan{false, BlockPlan{}, i, 0}; }, out);
+    // Stride 1, 3 x 3: the one phase as a halo GEMM over dx's pixel grid.
+    if (g.st == 1 && g.R == 3 && g.S == 3 && !is_inner_product(g))
+        halo_variants<BwdPlan>(g.Cg, g.Kg, n0, g.H, g.W, g.Q, g.G, nb >= g.N,
+                               [](const ImgPlan &i) { return BwdPlan{false, BlockPlan{}, i, 0}; },
+                               out);
     // Blocked, for few channels per group.
     if (g.Cg <= 16)
         for (int f = 1; f <= 8; f++) {
@@ -755,6 +879,12 @@ void bwd_name(const BwdPlan &p, char *buf, size_t len)
     else if (p.blocked)
         snprintf(buf, len, "blocked %dx%d pixels (f=%d), image GEMM %s", p.bp.b, p.bp.b, p.bp.f,
                  img_tile_name(p.img.tile));
+    else if (p.img.halo >= 0 && p.img.nsplit > 1)
+        snprintf(buf, len, "stride phases, halo GEMM %s (%dx%d pixels), %d splits",
+                 halo_tile_name(p.img.halo), p.img.tw, kHaloCols / p.img.tw, p.img.nsplit);
+    else if (p.img.halo >= 0)
+        snprintf(buf, len, "stride phases, halo GEMM %s (%dx%d pixels)", halo_tile_name(p.img.halo),
+                 p.img.tw, kHaloCols / p.img.tw);
     else if (p.img.tile < 0)
         snprintf(buf, len, "stride phases, tiles by rule");
     else if (p.img.nsplit > 1)
@@ -1085,6 +1215,57 @@ hipError_t mark(hipEvent_t ev, hipStream_t stream)
     return ev ? hipEventRecord(ev, stream) : hipSuccess;
 }
 
+// One halo GEMM launch (plan.halo >= 0) of a stride-1 3 x 3 problem: M rows
+// of the packed bank A (a_ld words each, FAST order over cin source channels),
+// source images src (src_c channels of src_h x src_w), output grid Pout x Qout
+// of out (out_c channels per image), nimg images; (coff_h, coff_w) is the
+// source coordinate of tap (0, 0) of output pixel (0, 0), flip for the
+// backward-data phase (source row p + coff_h - r).  Split partial slabs go to
+// part, split_stride apart.
+int halo_gemm(const ImgPlan &plan, int M, int groups, const float *A, int a_ld, int cin,
+              const float *src, int src_c, int src_h, int src_w, int Pout, int Qout, int out_c,
+              int nimg, int coff_h, int coff_w, bool flip, const float *bias, float *out,
+              float *part, long long split_stride, hipStream_t stream)
+{
+    const size_t fb = sizeof(float);
+    HaloGemmArgs h{};
+    h.M = M;
+    h.Kred = cin * 9;
+    h.groups = groups;
+    h.A = A;
+    h.a_ld = a_ld;
+    h.a_bytes = (uint32_t)((size_t)groups * M * a_ld * fb);
+    h.src = src;
+    h.src_bytes = (uint32_t)((size_t)nimg * src_c * src_h * src_w * fb);
+    h.cin = cin;
+    h.src_h = src_h;
+    h.src_w = src_w;
+    h.src_hw = src_h * src_w;
+    h.src_img_words = (uint32_t)((size_t)src_c * src_h * src_w);
+    h.P = Pout;
+    h.Q = Qout;
+    h.TW = plan.tw;
+    h.TR = kHaloCols / plan.tw;
+    h.row_blocks = (Pout + h.TR - 1) / h.TR;
+    h.col_segs = (Qout + h.TW - 1) / h.TW;
+    h.nimg = nimg;
+    // Halo origin: the top-left source pixel any tap of the block reads.
+    const int V = plan.tw == 14 ? 1 : 4;
+    h.row0 = flip ? coff_h - 2 : coff_h;
+    const int col_raw = flip ? coff_w - 2 : coff_w;
+    h.col0 = (col_raw >= 0 ? col_raw / V : -((-col_raw + V - 1) / V)) * V;
+    h.slack = col_raw - h.col0;
+    h.out = plan.nsplit > 1 ? part : out;
+    h.bias = bias;
+    h.out_img_stride = (long long)out_c * Pout * Qout;
+    h.out_hw = Pout * Qout;
+    h.out_w = Qout;
+    h.nsplit = plan.nsplit;
+    h.cbchunk = plan.kchunk;
+    h.split_stride = split_stride;
+    return launch_status(launch_halo_gemm(h, plan.halo, flip, stream));
+}
+
 // Forward GEMM launches over n images of geometry g (images from src, outputs
 // to y), at most images_per_launch(g) images a launch; wp is the packed
 // filter bank, part the split-K slabs (plan.nsplit > 1: n must be all of g's).
@@ -1124,6 +1305,14 @@ int fwd_gemms(const Geom &g, const ImgPlan &plan, const float *wp, const float *
     const bool fast = g.Cg % kBK == 0;
     for (int n0 = 0; n0 < n_images; n0 += nb) {
         const int n = n_images - n0 < nb ? n_images - n0 : nb;
+        if (plan.halo >= 0) {
+            int st = halo_gemm(plan, g.Kg, g.G, wp, a_ld, g.Cg, src + n0 * xi, g.C, g.H, g.W, g.P,
+                               g.Q, g.K, n, -g.pad, -g.pad, false, b, y + n0 * yi, part,
+                               (long long)n_images * yi, stream);
+            if (st != MICONV_OK)
+                return st;
+            continue;
+        }
         a.Ncol = n * g.P * g.Q;
         a.src = src + n0 * xi;
         a.src_bytes = (uint32_t)(n * xi * (long long)fb);
@@ -1464,6 +1653,14 @@ int phase_gemms(const Geom &g, const BwdPlan &plan, const float *w, char *&wsp, 
             *marked = true;
             for (int n0 = 0; n0 < n_images; n0 += nb) {
                 const int n = n_images - n0 < nb ? n_images - n0 : nb;
+                if (plan.img.halo >= 0) {  // stride 1: the one phase, flipped taps
+                    int st = halo_gemm(plan.img, g.Cg, group, wr, a_ld, g.Kg, dy + n0 * yi, K,
+                                       g.P, g.Q, H, W, g.C, n, ah.d, aw.d, true, nullptr,
+                                       dx + n0 * xi, part, (long long)n_images * xi, stream);
+                    if (st != MICONV_OK)
+                        return st;
+                    continue;
+                }
                 a.Ncol = n * ah.n * aw.n;
                 a.src = dy + n0 * yi;
                 a.src_bytes = (uint32_t)(n * yi * (long long)fb);

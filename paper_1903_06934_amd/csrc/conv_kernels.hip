@@ -472,6 +472,264 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
 }
 
 // ---------------------------------------------------------------------------
+// Halo-staged implicit GEMM for stride-1 3 x 3 layers (see HaloGemmArgs).
+//
+// A tile is BM filter rows x 112 columns, the columns being a TR x TW block of
+// output pixels of one image.  The gathered operand of a 16-channel block is
+// the same image region for all nine taps, shifted: it is staged once per
+// block (the halo, V words per lane and load, direct to LDS) and the nine
+// slices of the block read their B operands from it at per-tap offsets.  That
+// divides the staging-load lanes per MFMA by 5 to 6 (by 20 with 16-byte
+// loads) against the per-slice gather of img_gemm_kernel, whose load-issue
+// rate (one dword per lane) is what bounds it.
+//
+// The pixel block is fixed per instantiation (HaloCfg): TW = 112, 56, 28 or 14
+// columns (the map widths of the 3 x 3 layers at 224 ... 14 pixels) by
+// TR = 112 / TW rows, so every LDS offset of a tap is a compile-time constant
+// and the B reads need no address arithmetic.  LDS layout of a block:
+// halo[c][i][j] at c cs + i hw_w + j, either dense (the wave-loads fill
+// consecutive words, cs = hr hw_w) or one wave-load per channel (cs padded);
+// cs is chosen so that the four MFMA lane groups, which read channels 4 apart,
+// fall on different LDS banks.
+//
+// Four waves split the rows (BM / 4 each, FM = BM / 64 accumulator blocks
+// high) and each covers all 112 columns (7 blocks of 16).  The filter
+// operand of a slice is one 16-byte load per lane and row block, straight
+// into registers, issued two slices ahead into a ring of 3 register sets.
+// The halo has two LDS stages: the next block's loads are issued at the start
+// of a block and complete under its nine slices; one barrier per block.
+// ---------------------------------------------------------------------------
+template <int TW>
+struct HaloCfg;
+template <>
+struct HaloCfg<112> {
+    static constexpr int TR = 1, V = 4, HWW = 124, PERCH = 0, CS = 3 * 124;
+};
+template <>
+struct HaloCfg<56> {
+    static constexpr int TR = 2, V = 4, HWW = 64, PERCH = 1, CS = 260;
+};
+template <>
+struct HaloCfg<28> {
+    static constexpr int TR = 4, V = 4, HWW = 36, PERCH = 1, CS = 260;
+};
+template <>
+struct HaloCfg<14> {
+    static constexpr int TR = 8, V = 1, HWW = 18, PERCH = 0, CS = 10 * 18;
+};
+
+constexpr int kHaloStageWords = 6400;  // per stage (25 KiB): two stages, three workgroups a CU
+
+template <int BM, int TW, bool FLIP>
+__global__ __launch_bounds__(256) void halo_gemm_kernel(const HaloGemmArgs a)
+{
+    typedef HaloCfg<TW> C;
+    constexpr int R = 3, S = 3, RS = 9, NR = 3;
+    constexpr int NW = 4, BN = kHaloCols, TM = BM / NW, FM = TM / 16, FN = BN / 16;
+    constexpr int TR = C::TR, V = C::V, HWW = C::HWW, CS = C::CS;
+    constexpr int HR = TR + R - 1;
+    constexpr int GPR = HWW / V;                  // load groups per halo row
+    constexpr int EPC = HR * GPR;                 // load groups per channel
+    // Dense: wave-loads over 16 EPC groups; per channel: EPC <= 64, one each.
+    constexpr int NWL = C::PERCH ? 16 : (16 * EPC + 63) / 64;
+    constexpr int LPW = (NWL + NW - 1) / NW;      // wave-loads per wave and block
+    constexpr int SPARE = C::PERCH ? 16 * CS : NWL * 64 * V;  // slot of padding loads
+    static_assert(TR * TW == BN, "pixel block");
+    static_assert(HWW % V == 0 && HWW >= TW + S - 1, "halo row");
+    // One wave-load per channel writes all 64 lanes (masked lanes write
+    // zeros), so a channel's slot must hold 64 V words.
+    static_assert(C::PERCH ? (EPC <= 64 && CS >= 64 * V && (CS * 4) % 16 == 0)
+                           : CS == HR * HWW, "channel stride");
+    static_assert(SPARE + 64 * V <= kHaloStageWords, "halo stage");
+
+    __shared__ __attribute__((aligned(16))) float H0[kHaloStageWords], H1[kHaloStageWords];
+
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int mtiles = (a.M + BM - 1) / BM;
+    const int per_img = a.row_blocks * a.col_segs;
+    const int tiles = mtiles * a.nimg * per_img;
+    const int lin = xcd_tile(blockIdx.x, tiles * a.groups * a.nsplit);
+    const int split = lin / (tiles * a.groups);
+    const int rest = lin - split * tiles * a.groups;
+    const int g = rest / tiles, tile = rest - g * tiles;
+    const int mt = tile % mtiles, pt = tile / mtiles;
+    const int img = pt / per_img;
+    const int prem = pt - img * per_img;
+    const int rb = prem / a.col_segs, csg = prem - rb * a.col_segs;
+    const int p0 = rb * TR, q0 = csg * TW;
+    const int m0 = mt * BM;
+    const int ncb = a.Kred / (16 * RS);
+    const int cb_beg = split * a.cbchunk;
+    const int cb_end = min(ncb, cb_beg + a.cbchunk);
+    const int kr = lane >> 4, lc = lane & 15;
+
+    // Filter operand: row m = m0 + wave * TM + 16 i + lc, reduction words
+    // 16 t + 4 kr .. + 3 of slice t; rows past M read zero.
+    const __amdgpu_buffer_rsrc_t rA = make_rsrc(a.A, a.a_bytes);
+    uint32_t a_off[FM];
+#pragma unroll
+    for (int i = 0; i < FM; i++) {
+        const int m = m0 + wave * TM + i * 16 + lc;
+        a_off[i] = (((uint32_t)(g * a.M + (m < a.M ? m : 0)) * (uint32_t)a.a_ld + 4u * kr) * 4u) |
+                   oob_mask(m < a.M);
+    }
+    const int t_last = cb_end * RS - 1;  // last slice of this split
+    auto loadA = [&](int t, f32x4 (&dst)[FM]) {
+        const int tc = t < t_last ? t : t_last;  // past the end: a harmless repeat
+#pragma unroll
+        for (int i = 0; i < FM; i++)
+            dst[i] = __builtin_bit_cast(
+                f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                           rA, (int)(a_off[i] + (uint32_t)tc * 64u), 0, 0));
+    };
+
+    // Halo staging.  Wave-load i = wave + 4 j carries, per lane, load group
+    // e of channel c (dense: e + EPC c = 64 i + lane; per channel: c = i,
+    // e = lane) into LDS word c CS + V e (dense: 64 V i + V lane) of a stage.
+    // Group e = row * GPR + grp is source pixel (p0 + row0 + row,
+    // q0 + col0 + V grp) .. + V - 1 of channel 16 cb + c, zero outside the
+    // source (with V = 4 the source width and col0, q0 are multiples of 4, so
+    // a group lies inside or outside a row).  Loads past the last wave-load
+    // go to a spare slot and read zero.
+    const __amdgpu_buffer_rsrc_t rB = make_rsrc(a.src, a.src_bytes);
+    uint32_t h_off[LPW];
+#pragma unroll
+    for (int j = 0; j < LPW; j++) {
+        const int i = wave + NW * j;
+        int c, e;
+        if constexpr (C::PERCH) {
+            c = i;
+            e = lane;
+        } else {
+            const int ge = i * 64 + lane;
+            c = ge / EPC;
+            e = ge - c * EPC;
+        }
+        const int row = e / GPR, grp = e - row * GPR;
+        const int h = p0 + a.row0 + row, w = q0 + a.col0 + grp * V;
+        const bool ok = i < NWL && c < 16 && e < EPC && (unsigned)h < (unsigned)a.src_h &&
+                        w >= 0 && w + V <= a.src_w;
+        h_off[j] = ok ? ((uint32_t)img * a.src_img_words +
+                         (uint32_t)(g * a.cin + c) * (uint32_t)a.src_hw +
+                         (uint32_t)(h * a.src_w + w)) * 4u
+                      : kOob;
+    }
+    const uint32_t cb_bytes = 16u * (uint32_t)a.src_hw * 4u;
+    auto issue_halo = [&](int cb, float *Hd) {
+#pragma unroll
+        for (int j = 0; j < LPW; j++) {
+            const int i = wave + NW * j;
+            float *dst = Hd + (i >= NWL ? SPARE : C::PERCH ? i * CS : i * 64 * V);
+            const uint32_t off = h_off[j] == kOob ? kOob : h_off[j] + (uint32_t)cb * cb_bytes;
+            if constexpr (V == 4)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rB, (LDS_AS void *)dst, 16, off, 0, 0, 0);
+            else
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rB, (LDS_AS void *)dst, 4, off, 0, 0, 0);
+        }
+    };
+
+    // B operand: column n = 16 j + lc is pixel (dr, dq) = (n / TW, n % TW) of
+    // the block; for channel 4 kr + s4 and tap (rr, ss) its halo word is
+    // bofs[j] + s4 CS + rr HWW + ss, with bofs[j] = 4 kr CS + dr HWW + dq + slack
+    // (a compile-time offset from a per-lane base).  Columns outside the
+    // output read word 0 and are not stored.
+    int bofs[FN];
+    bool nok[FN];
+#pragma unroll
+    for (int j = 0; j < FN; j++) {
+        const int n = j * 16 + lc;
+        const int dr = n / TW, dq = n - (n / TW) * TW;
+        nok[j] = p0 + dr < a.P && q0 + dq < a.Q;
+        bofs[j] = nok[j] ? kr * 4 * CS + dr * HWW + dq + a.slack : 0;
+    }
+
+    f32x4 acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; i++)
+#pragma unroll
+        for (int j = 0; j < FN; j++)
+            acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    f32x4 ring[NR][FM];
+    auto block = [&](int cb, const float *Hc, float *Hn, bool stage_next) {
+        // The other stage is free (every wave passed the barrier after
+        // reading it): stage the next block into it.
+        if (stage_next)
+            issue_halo(cb + 1, Hn);
+        __asm__ volatile("" ::: "memory");
+#pragma unroll
+        for (int tap = 0; tap < RS; tap++) {
+            const int r = tap / S, sx = tap % S;
+            const int toff = (FLIP ? R - 1 - r : r) * HWW + (FLIP ? S - 1 - sx : sx);
+            loadA(cb * RS + tap + 2, ring[(tap + 2) % NR]);
+            float bf[4][FN];
+#pragma unroll
+            for (int s4 = 0; s4 < 4; s4++)
+#pragma unroll
+                for (int j = 0; j < FN; j++)
+                    bf[s4][j] = Hc[bofs[j] + s4 * CS + toff];
+#pragma unroll
+            for (int s4 = 0; s4 < 4; s4++)
+#pragma unroll
+                for (int i = 0; i < FM; i++)
+#pragma unroll
+                    for (int j = 0; j < FN; j++)
+                        acc[i][j] = mfma16(ring[tap % NR][i][s4], bf[s4][j], acc[i][j]);
+            // Keep each tap's LDS reads with its MFMAs: hoisting later taps'
+            // reads would hold their operands in registers meanwhile.
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        // The next block's halo has landed once at most the two filter loads
+        // issued last (the next block's first two slices) are outstanding.
+        __asm__ volatile("" ::: "memory");
+        __builtin_amdgcn_s_waitcnt((2 * FM & 15) | (((2 * FM) >> 4) << 14) | (7 << 4) | (15 << 8));
+        __asm__ volatile("" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        __asm__ volatile("" ::: "memory");
+    };
+
+    if (cb_beg < cb_end) {
+        issue_halo(cb_beg, H0);
+        loadA(cb_beg * RS, ring[0]);
+        loadA(cb_beg * RS + 1, ring[1]);
+        __builtin_amdgcn_s_waitcnt(0);
+        __asm__ volatile("" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        __asm__ volatile("" ::: "memory");
+    }
+    int cb = cb_beg;
+    for (; cb + 1 < cb_end; cb += 2) {
+        block(cb, H0, H1, true);
+        block(cb + 1, H1, H0, cb + 2 < cb_end);
+    }
+    if (cb < cb_end)
+        block(cb, H0, H1, false);
+
+    // Epilogue: + bias (unsplit), pixel (p0 + dr, q0 + dq) of the tile's image.
+    float *const out = a.nsplit > 1 ? a.out + (long long)split * a.split_stride : a.out;
+    const float *const bias = a.nsplit > 1 ? nullptr : a.bias;
+#pragma unroll
+    for (int i = 0; i < FM; i++)
+#pragma unroll
+        for (int v = 0; v < 4; v++) {
+            const int m = m0 + wave * TM + i * 16 + acc_row(v, lane);
+            if (m >= a.M)
+                continue;
+            const int oc = g * a.M + m;
+            const float bv = bias ? bias[oc] : 0.f;
+            const long long base = (long long)img * a.out_img_stride + (long long)oc * a.out_hw;
+#pragma unroll
+            for (int j = 0; j < FN; j++) {
+                const int n = j * 16 + lc;
+                const int dr = n / TW, dq = n - (n / TW) * TW;
+                if (nok[j])
+                    out[base + (long long)(p0 + dr) * a.out_w + (q0 + dq)] = acc[i][j][v] + bv;
+            }
+        }
+}
+
+// ---------------------------------------------------------------------------
 // Backward-weight GEMM with one pixel per lane (same WgradArgs).
 //
 // Tap-uniform tiles (PACKED = false) take dw columns in (tap, channel) order:
@@ -993,6 +1251,47 @@ hipError_t launch_img_gemm(const ImgGemmArgs &a, int tile, bool fast, hipStream_
     case IMG_64x128: return img_launch<64, 128, K, 2, 2, 4>(a, fast, stream);
     default: return img_launch<64, 64, K, 4, 1, 4>(a, fast, stream);
     }
+}
+
+template <int BM, int TW>
+static hipError_t halo_launch(const HaloGemmArgs &a, bool flip, hipStream_t stream)
+{
+    const int tiles = ((a.M + BM - 1) / BM) * a.nimg * a.row_blocks * a.col_segs;
+    dim3 grid(tiles * a.groups * a.nsplit);
+    if (flip)
+        hipLaunchKernelGGL((halo_gemm_kernel<BM, TW, true>), grid, dim3(256), 0, stream, a);
+    else
+        hipLaunchKernelGGL((halo_gemm_kernel<BM, TW, false>), grid, dim3(256), 0, stream, a);
+    return hipGetLastError();
+}
+
+template <int BM>
+static hipError_t halo_launch_tw(const HaloGemmArgs &a, bool flip, hipStream_t stream)
+{
+    switch (a.TW) {
+    case 112: return halo_launch<BM, 112>(a, flip, stream);
+    case 56: return halo_launch<BM, 56>(a, flip, stream);
+    case 28: return halo_launch<BM, 28>(a, flip, stream);
+    case 14: return halo_launch<BM, 14>(a, flip, stream);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+bool halo_width_supported(int TW, int src_w, int col0)
+{
+    if (TW == 14)
+        return true;  // one-word loads
+    return (TW == 112 || TW == 56 || TW == 28) && src_w % 4 == 0 && col0 % 4 == 0;
+}
+
+int halo_rows(int TW) { return kHaloCols / TW; }
+
+hipError_t launch_halo_gemm(const HaloGemmArgs &a, int tile, bool flip, hipStream_t stream)
+{
+    if (!halo_width_supported(a.TW, a.src_w, a.col0) || a.TR != halo_rows(a.TW))
+        return hipErrorInvalidValue;
+    return tile == HALO_128x112 ? halo_launch_tw<128>(a, flip, stream)
+                                : halo_launch_tw<64>(a, flip, stream);
 }
 
 template <int BM, int BN, int WM, int WN, bool PACKED = false>

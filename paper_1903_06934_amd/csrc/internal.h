@@ -79,6 +79,50 @@ struct ImgGemmArgs {
 };
 
 // ---------------------------------------------------------------------------
+// Halo-staged implicit GEMM for stride-1 3 x 3 layers with channel-aligned
+// slices (the forward pass, or the single stride phase of a stride-1
+// backward-data pass).  Same GEMM as ImgGemmArgs with cstep = 1, but the
+// columns of a tile are a TR x TW block of output pixels of one image (rows
+// p0 .. p0 + TR - 1, columns q0 .. q0 + TW - 1; column n of the tile is
+// (n / TW, n % TW)), TW one of 112, 56, 28, 14 and TR = 112 / TW, and for
+// each 16-channel block the source region all nine taps of the block need
+// (the halo) is staged in LDS once:
+//   halo[c][i][j] = src[img][g * cin + 16 cb + c][p0 + row0 + i][q0 + col0 + j]
+//                   (0 outside the source),
+// loaded 4 words per lane (TW >= 28: needs col0 and the source width to be
+// multiples of 4) or 1 (TW = 14).  Tap (r, s) of pixel (dr, dq) reads
+// halo[c][dr + rr][dq + slack + ss] with (rr, ss) = (r, s), or (2 - r, 2 - s)
+// for the backward-data phase (flip; its source rows are p + coff_h - r).
+// The reduction order is the channel-block-major one of the packed filter:
+// k = (cb * 9 + tap) * 16 + ci.
+// ---------------------------------------------------------------------------
+struct HaloGemmArgs {
+    int M, Kred, groups;
+    const float *A;
+    int a_ld;
+    uint32_t a_bytes;
+    const float *src;
+    uint32_t src_bytes;
+    int cin;                   // source channels per group (multiple of 16)
+    int src_h, src_w, src_hw;
+    uint32_t src_img_words;
+    int P, Q;                  // output extents (the pixel grid of the columns)
+    int TR, TW;                // pixel block of a tile
+    int row_blocks, col_segs;  // blocks per image: ceil(P / TR) x ceil(Q / TW)
+    int nimg;                  // images of this launch
+    int row0, col0, slack;     // halo origin relative to (p0, q0); slack = first tap column
+    float *out;
+    const float *bias;         // may be null
+    long long out_img_stride;
+    int out_hw, out_w;
+    // Split-K over channel blocks: split s covers blocks [s * cbchunk, ...)
+    // and, when nsplit > 1, writes its partial sums (no bias) to
+    // out + s * split_stride.
+    int nsplit, cbchunk;
+    long long split_stride;
+};
+
+// ---------------------------------------------------------------------------
 // Backward-weight GEMM, per split s and group g (both folded into the 1-D grid):
 //   out[s][g][m][n] = sum over pixels pix in split s of
 //                     dy[img][g*Kg + m][p][q] * x[img][g*Cg + c][p*st - pad + r][q*st - pad + s']
@@ -121,6 +165,13 @@ enum WgradTile {
 inline bool wgrad_tile_is_tap(int tile) { return tile <= WG_TAP_64x16 || tile >= WG_TAP_128x32; }
 
 hipError_t launch_img_gemm(const ImgGemmArgs &a, int tile, bool fast, hipStream_t stream);
+// Halo tiles: BM rows (64 or 128) x 112 columns; flip for the backward-data
+// phase.  halo_width_supported: whether TW (112, 56, 28, 14) can stage this
+// source (16-byte loads need the width and col0 to be multiples of 4).
+enum HaloTile { HALO_64x112 = 0, HALO_128x112 };
+constexpr int kHaloCols = 112;
+bool halo_width_supported(int TW, int src_w, int col0);
+hipError_t launch_halo_gemm(const HaloGemmArgs &a, int tile, bool flip, hipStream_t stream);
 hipError_t launch_wgrad_gemm(const WgradArgs &a, int tile, hipStream_t stream);
 
 // wp[(g*Kg + k) * a_ld + kk] (or, if kmajor, wp[(g*a_ld + kk) * Kg + k]) =

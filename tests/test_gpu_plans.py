@@ -26,6 +26,16 @@ PLAN_SHAPES = [
     (8, 1024, 1, 1, 100, 1, 1, 1, 0, 1),   # inner product, forward fine splits
     (8, 100, 1, 1, 1024, 1, 1, 1, 0, 1),   # inner product, backward-data fine splits
     (2, 64, 12, 12, 48, 1, 1, 1, 0, 1),    # 1x1 direct GEMM on every 64-column tile
+    # Halo GEMM (stride-1 3x3, channel-aligned): each pixel block width, padding
+    # 0-2, groups, ragged rows and columns, split channel blocks.
+    (2, 32, 10, 20, 48, 3, 3, 1, 1, 1),    # 28 x 4 blocks, 16-byte halo loads
+    (2, 16, 6, 9, 32, 3, 3, 1, 1, 1),      # 14 x 8 blocks, one-word loads (width 9)
+    (1, 32, 2, 100, 128, 3, 3, 1, 1, 1),   # 112 x 1 blocks, 100 of 112 columns used
+    (2, 16, 5, 116, 32, 3, 3, 1, 1, 1),    # 56 x 2 blocks, three segments a row
+    (1, 64, 7, 7, 64, 3, 3, 1, 1, 2),      # groups, 7 x 7 maps
+    (2, 16, 9, 12, 16, 3, 3, 1, 2, 1),     # pad 2
+    (2, 16, 8, 12, 16, 3, 3, 1, 0, 1),     # pad 0
+    (1, 256, 6, 6, 128, 3, 3, 1, 1, 1),    # few tiles, 16 channel blocks: split
 ]
 
 
