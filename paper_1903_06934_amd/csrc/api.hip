@@ -356,14 +356,16 @@ bool same_img(const ImgPlan &a, const ImgPlan &b)
 // Stride-1 3 x 3 layers with channel-aligned slices can run the halo GEMM
 // (halo_gemm_kernel): 112-column tiles that are TR x TW pixel blocks, the
 // source region of a 16-channel block staged once for all nine taps.  The
-// block width is the one of 112, 56, 28, 14 that pads the output grid
+// block width is the one of 56, 112, 28, 14 (in that order of preference:
+// 56 x 2 blocks stage the least halo per pixel of the 16-byte ones and
+// measured fastest wherever they fit, by 1-2 %) that pads the output grid
 // (P x Q) least; 0 if none can stage this source (16-byte loads need a
 // source width that is a multiple of 4).
 int halo_width(int P, int Q, int src_w)
 {
     int best = 0;
     long long best_cols = 0;
-    for (int tw : {112, 56, 28, 14}) {
+    for (int tw : {56, 112, 28, 14}) {
         if (!halo_width_supported(tw, src_w, 0))
             continue;
         const int tr = kHaloCols / tw;
@@ -405,15 +407,31 @@ ImgPlan halo_plan(int tile, int tw, long long tiles, int ncb, int ns)
 
 // Halo candidates of a stride-1 3 x 3 GEMM with M rows over cin source
 // channels (a multiple of 16), an nimg x P x Q output grid and a src_w-wide
-// source: each tile that fits M, unsplit and (allow_split) split.
+// source: each pixel-block width that pads the grid no more than the best
+// one, each tile that fits M, unsplit and (allow_split) split.
+std::vector<int> halo_widths(int P, int Q, int src_w)
+{
+    std::vector<int> out;
+    const int best = halo_width(P, Q, src_w);
+    auto blocks = [&](int tw) {
+        const int tr = kHaloCols / tw;
+        return (long long)((P + tr - 1) / tr) * ((Q + tw - 1) / tw);
+    };
+    if (best)
+        for (int tw : {112, 56, 28, 14})
+            if (halo_width_supported(tw, src_w, 0) && blocks(tw) == blocks(best))
+                out.push_back(tw);
+    return out;
+}
+
 template <class P, class Make>
 void halo_variants(int M, int cin, int nimg, int Pout, int Qout, int src_w, int G,
                    bool allow_split, Make make, std::vector<P> &out)
 {
-    const int tw = halo_width(Pout, Qout, src_w);
-    if (!tw || cin % 16)
+    if (cin % 16)
         return;
     const int ncb = cin / 16;
+    for (int tw : halo_widths(Pout, Qout, src_w))
     for (int tile : {HALO_128x112, HALO_64x112}) {
         if (tile == HALO_128x112 && M <= 64)
             continue;
@@ -906,6 +924,8 @@ struct WgradPlan {
     int xnb;  // explicit plan: images per column chunk (0: implicit); nb = xnb then
     bool bt;  // inner product: batch-transposed plan (the problem of batch_columns)
     int img = -1;  // inner product: dW = dy^T x as an image GEMM with this tile (-1: no)
+    int halo_tw = 0;  // halo backward-weight with this pixel-block width (0: no); chunk then
+                      // counts pixel blocks
 };
 
 bool is_tap_tile(int tile) { return wgrad_tile_is_tap(tile); }
@@ -1010,8 +1030,67 @@ WgradPlan wgrad_img_plan(const Geom &g, int tile)
     return p;
 }
 
+// Halo backward-weight (wgrad_halo_kernel): stride-1 3 x 3 layers with
+// channel-aligned groups whose dy and x rows are a multiple of 4 wide, in one
+// launch.  Pixel-block width: the one of 56, 28, 112 (in that order of
+// preference; the 112 x 1 blocks stage 45 % more halo per pixel and measured
+// 3-7 % slower) that pads the P x Q grid least (0: not applicable).  The rule
+// for such layers: on VGG-16 conv1_2 ... conv4_3 at batch 32 it ran at
+// 120-128 TFLOP/s against 116-122 for the best tap-tile plan.
+int wgrad_halo_width(const Geom &g)
+{
+    if (g.st != 1 || g.R != 3 || g.S != 3 || g.Cg % 16 || is_inner_product(g) ||
+        images_per_launch(g) < g.N)
+        return 0;
+    int best = 0;
+    long long best_cols = 0;
+    for (int tw : {56, 28, 112}) {
+        if (!wgrad_halo_supported(tw, g.Q, g.W))
+            continue;
+        const int tr = kHaloCols / tw;
+        const long long cols =
+            (long long)((g.P + tr - 1) / tr) * ((g.Q + tw - 1) / tw) * kHaloCols;
+        if (!best || cols < best_cols) {
+            best = tw;
+            best_cols = cols;
+        }
+    }
+    return best;
+}
+
+// Splits over the pixel blocks so that about three workgroups per CU run
+// (three fit at once), times 2^scale, each split at least 4 blocks.
+WgradPlan wgrad_halo_plan(const Geom &g, int tw, int scale = 0)
+{
+    WgradPlan p{};
+    p.tile = -1;
+    p.halo_tw = tw;
+    p.slice = kHaloCols;
+    p.nb = g.N;
+    const int tr = kHaloCols / tw;
+    const long long blocks = (long long)g.N * ((g.P + tr - 1) / tr) * ((g.Q + tw - 1) / tw);
+    const long long tiles = (long long)((g.Kg + 63) / 64) * (g.Cg / 16) * g.G;
+    long long ns = (3LL * num_cus() + tiles - 1) / tiles;
+    if (scale > 0)
+        ns <<= scale;
+    else if (scale < 0)
+        ns >>= -scale;
+    if (ns > blocks / 4)
+        ns = blocks / 4;
+    if (ns < 1)
+        ns = 1;
+    p.chunk = (int)((blocks + ns - 1) / ns);
+    p.nsplit = (int)((blocks + p.chunk - 1) / p.chunk);
+    p.via_part = true;
+    p.part_bytes = align_up((size_t)p.nsplit * g.K * g.Cg * 9 * sizeof(float));
+    p.bias_bytes = align_up((size_t)p.nsplit * g.K * sizeof(float));
+    return p;
+}
+
 WgradPlan wgrad_rule(const Geom &g)
 {
+    if (const int tw = wgrad_halo_width(g))
+        return wgrad_halo_plan(g, tw);
     if (!is_inner_product(g))
         return wgrad_plan(g);
     // With a batch of whole 16-row slices, the image GEMM over the batch
@@ -1071,7 +1150,8 @@ void wgrad_candidates(const Geom &g, std::vector<WgradPlan> &out)
             WgradPlan p = wgrad_plan(g, t, scale);
             bool dup = false;
             for (const WgradPlan &q : out)
-                dup = dup || (q.tile == p.tile && q.chunk == p.chunk && q.xnb == 0 && !q.bt);
+                dup = dup || (q.tile == p.tile && q.chunk == p.chunk && q.xnb == 0 && !q.bt &&
+                              !q.halo_tw);
             if (!dup)
                 out.push_back(p);
         }
@@ -1080,6 +1160,24 @@ void wgrad_candidates(const Geom &g, std::vector<WgradPlan> &out)
         WgradPlan e = wgrad_plan(one_by_one(g, g.N), -1, 0, xnb);
         e.xnb = xnb;
         out.push_back(e);
+    }
+    // Halo: all nine taps of a tile from one staging per pixel block; each
+    // block width that pads the grid no more than the best one.
+    if (const int best = wgrad_halo_width(g)) {
+        auto blocks = [&](int tw) {
+            const int tr = kHaloCols / tw;
+            return (long long)((g.P + tr - 1) / tr) * ((g.Q + tw - 1) / tw);
+        };
+        for (int tw : {112, 56, 28})
+            if (wgrad_halo_supported(tw, g.Q, g.W) && blocks(tw) == blocks(best))
+                for (int scale : {0, 1, -1}) {
+                    WgradPlan p = wgrad_halo_plan(g, tw, scale);
+                    bool dup = false;
+                    for (const WgradPlan &q : out)
+                        dup = dup || (q.halo_tw == p.halo_tw && q.chunk == p.chunk);
+                    if (!dup)
+                        out.push_back(p);
+                }
     }
 }
 
@@ -1097,6 +1195,9 @@ void wgrad_name(const WgradPlan &p, char *buf, size_t len)
 {
     if (p.img >= 0)
         snprintf(buf, len, "batch-transposed, image GEMM %s over the batch", img_tile_name(p.img));
+    else if (p.halo_tw)
+        snprintf(buf, len, "halo, 9 taps of 64x16 (%dx%d pixels), %d splits of %d blocks",
+                 p.halo_tw, kHaloCols / p.halo_tw, p.nsplit, p.chunk);
     else if (p.xnb > 0)
         snprintf(buf, len, "explicit im2col (%d images a chunk), %s, %d splits of %d pixels",
                  p.xnb, wgrad_tile_name(p.tile), p.nsplit, p.chunk);
@@ -1846,6 +1947,40 @@ int wgrad_exec(const Geom &g, const WgradPlan &p, const float *x, const float *d
         if ((st = wgrad_launches(batch_columns(g), p, tail, dyt, dw, db != nullptr, part, db_part,
                                  1, split0, stream)) != MICONV_OK)
             return st;
+    } else if (p.halo_tw) {
+        WgradHaloArgs h{};
+        h.Kg = g.Kg;
+        h.Cg = g.Cg;
+        h.groups = g.G;
+        h.K = K;
+        h.dy = dy;
+        h.x = x;
+        h.dy_bytes = (uint32_t)((size_t)N * K * g.P * g.Q * fb);
+        h.x_bytes = (uint32_t)((size_t)N * C * H * W * fb);
+        h.dy_img_words = (uint32_t)((size_t)K * g.P * g.Q);
+        h.x_img_words = (uint32_t)((size_t)C * H * W);
+        h.H = H;
+        h.W = W;
+        h.P = g.P;
+        h.Q = g.Q;
+        h.TW = p.halo_tw;
+        const int tr = kHaloCols / p.halo_tw;
+        h.row_blocks = (g.P + tr - 1) / tr;
+        h.col_segs = (g.Q + p.halo_tw - 1) / p.halo_tw;
+        h.nimg = N;
+        // x halo origin (p0 - pad, q0 - pad), columns from a multiple of 4.
+        h.row0 = -g.pad;
+        h.col0 = -((g.pad + 3) / 4) * 4;
+        h.slack = -g.pad - h.col0;
+        h.chunk = p.chunk;
+        h.nsplit = p.nsplit;
+        h.out = part;
+        h.split_stride = (long long)K * g.Cg * 9;
+        h.db_part = db ? db_part : nullptr;
+        if (mark(tl_events.before, stream) != hipSuccess)
+            return MICONV_ERR_LAUNCH;
+        if ((st = launch_status(launch_wgrad_halo(h, stream))) != MICONV_OK)
+            return st;
     } else if (p.xnb > 0) {
         // Explicit: im2col of a chunk of images, then the 1x1 problem over the
         // columns, whose dw[k][c'] is dw[k][c][r][s].
@@ -1873,7 +2008,7 @@ int wgrad_exec(const Geom &g, const WgradPlan &p, const float *x, const float *d
     // Tap-ordered partials go back to dw's [k][c][r][s] (a 1x1 problem has one tap).
     const int taps = p.xnb > 0 || p.bt ? 1 : R * S;
     const int ncol = g.Cg * R * S;
-    const bool tap_order = is_tap_tile(p.tile);
+    const bool tap_order = p.halo_tw || is_tap_tile(p.tile);
     if (p.via_part &&
         (st = launch_status(launch_splitk_reduce(part, p.nsplit, (long long)K * ncol, K * ncol,
                                                  dw, tap_order ? taps : 0,

@@ -943,6 +943,186 @@ __global__ __launch_bounds__(64 * WM * WN) void wgrad_kernel(const WgradArgs a)
 }
 
 // ---------------------------------------------------------------------------
+// Halo backward-weight for stride-1 3 x 3 layers (see WgradHaloArgs).
+//
+// The one-pixel-per-lane kernel above stages, per 64-pixel slice and tap
+// tile, one dword per lane and operand row: about one staging load per two
+// MFMAs.  Here a workgroup owns all nine taps of a 64-filter x 16-channel
+// tile, so each 112-pixel block's dy rows and x halo are staged once (16-byte
+// loads) and used by nine taps: about one load per twenty MFMAs.
+//
+// MFMA mapping (16x16x4, reduction over pixels): at step s (0 .. 27) lane
+// group kr takes pixel 4 s + kr of the block, so a lane's A operand
+// (filter lc of its wave's 16, dy row) and B operand (channel lc, the x halo
+// shifted by the tap) sit at a per-lane base plus a compile-time offset; rows
+// are laid out so that the 64 lanes of an LDS read hit 64 different banks.
+// Each wave keeps nine 16x16 accumulators (one per tap) of its 16 filters x
+// the 16 channels.  A single LDS stage: three workgroups fit a CU.
+// ---------------------------------------------------------------------------
+constexpr int kWhDyLd = 116;  // dy row: 112 pixels + one 4-word group of padding
+
+template <int TW>
+__global__ __launch_bounds__(256) void wgrad_halo_kernel(const WgradHaloArgs a)
+{
+    typedef HaloCfg<TW> C;
+    constexpr int TR = C::TR, HWW = C::HWW, CS = C::CS;
+    constexpr int HR = TR + 2, GPR = HWW / 4, EPC = HR * GPR;
+    constexpr int XNWL = C::PERCH ? 16 : (16 * EPC + 63) / 64;  // x halo wave-loads
+    constexpr int YNWL = 64 * (kWhDyLd / 4) / 64;                // dy wave-loads (29)
+    constexpr int XW = C::PERCH ? 16 * CS : XNWL * 64 * 4;
+    static_assert(C::V == 4 && TR * TW == kHaloCols, "16-byte halo, 112-pixel blocks");
+    static_assert((64 * (kWhDyLd / 4)) % 64 == 0, "whole dy wave-loads");
+
+    __shared__ __attribute__((aligned(16))) float Y[64 * kWhDyLd];
+    __shared__ __attribute__((aligned(16))) float X[XW];
+
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int mtiles = (a.Kg + 63) / 64, ctiles = a.Cg / 16;
+    const int tiles = mtiles * ctiles;
+    const int lin = xcd_tile(blockIdx.x, tiles * a.groups * a.nsplit);
+    const int split = lin / (tiles * a.groups);
+    const int rest = lin - split * tiles * a.groups;
+    const int g = rest / tiles, tile = rest - g * tiles;
+    const int mt = tile % mtiles, ct = tile / mtiles;
+    const int m0 = mt * 64, c0 = ct * 16;
+    const int per_img = a.row_blocks * a.col_segs;
+    const int nblocks = a.nimg * per_img;
+    const int b_beg = split * a.chunk, b_end = min(nblocks, b_beg + a.chunk);
+    const int kr = lane >> 4, lc = lane & 15;
+
+    const __amdgpu_buffer_rsrc_t rdy = make_rsrc(a.dy, a.dy_bytes);
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(a.x, a.x_bytes);
+
+    // Staging lanes.  dy: wave-load i, lane l carries group L = 64 i + l,
+    // row L / 29 (filter m0 + row), pixels 4 (L % 29) .. + 3 (group 28 is
+    // padding); LDS words 4 L ...  x: as in halo_gemm_kernel, channel c0 + c.
+    constexpr int YL = (YNWL + 3) / 4, XL = (XNWL + 3) / 4;
+    int y_row[YL], y_px[YL];
+#pragma unroll
+    for (int j = 0; j < YL; j++) {
+        const int L = (wave + 4 * j) * 64 + lane;
+        y_row[j] = L / (kWhDyLd / 4);
+        y_px[j] = 4 * (L - y_row[j] * (kWhDyLd / 4));
+    }
+    int x_c[XL], x_row[XL], x_grp[XL];
+#pragma unroll
+    for (int j = 0; j < XL; j++) {
+        const int i = wave + 4 * j;
+        int c, e;
+        if constexpr (C::PERCH) {
+            c = i;
+            e = lane;
+        } else {
+            const int ge = i * 64 + lane;
+            c = ge / EPC;
+            e = ge - c * EPC;
+        }
+        x_c[j] = (c < 16 && e < EPC) ? c : 16;  // 16: masked
+        x_row[j] = e / GPR;
+        x_grp[j] = e - x_row[j] * GPR;
+    }
+
+    // Compute-side bases: A = Y[(16 wave + lc) * 116 + kr + 4 s],
+    // B = X[lc * CS + kr + slack + (dr(s) + r) * HWW + dq(s) + sx].
+    const int ya = (16 * wave + lc) * kWhDyLd + kr;
+    const int xb = lc * CS + kr + a.slack;
+
+    f32x4 acc[9];
+#pragma unroll
+    for (int t = 0; t < 9; t++)
+        acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float bsum = 0.f;
+    const bool do_bias = a.db_part != nullptr && ct == 0;
+
+    for (int b = b_beg; b < b_end; b++) {
+        const int img = b / per_img, prem = b - img * per_img;
+        const int rb = prem / a.col_segs, csg = prem - rb * a.col_segs;
+        const int p0 = rb * TR, q0 = csg * TW;
+        // Every wave is done reading the previous block.
+        __builtin_amdgcn_s_barrier();
+        __asm__ volatile("" ::: "memory");
+#pragma unroll
+        for (int j = 0; j < YL; j++) {
+            const int i = wave + 4 * j;
+            if (i < YNWL) {
+                const int px = y_px[j], dr = px / TW, dq = px - (px / TW) * TW;
+                const int k = m0 + y_row[j];
+                const bool ok = px < kHaloCols && k < a.Kg && p0 + dr < a.P && q0 + dq < a.Q;
+                const uint32_t off =
+                    ok ? ((uint32_t)img * a.dy_img_words + (uint32_t)(g * a.Kg + k) * (uint32_t)(a.P * a.Q) +
+                          (uint32_t)((p0 + dr) * a.Q + q0 + dq)) * 4u
+                       : kOob;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rdy, (LDS_AS void *)&Y[i * 256], 16, off, 0,
+                                                         0, 0);
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < XL; j++) {
+            const int i = wave + 4 * j;
+            if (i < XNWL) {
+                const int h = p0 + a.row0 + x_row[j], w = q0 + a.col0 + 4 * x_grp[j];
+                const bool ok = x_c[j] < 16 && (unsigned)h < (unsigned)a.H && w >= 0 && w + 4 <= a.W;
+                const uint32_t off =
+                    ok ? ((uint32_t)img * a.x_img_words + (uint32_t)(g * a.Cg + c0 + x_c[j]) *
+                                                              (uint32_t)(a.H * a.W) +
+                          (uint32_t)(h * a.W + w)) * 4u
+                       : kOob;
+                float *dst = C::PERCH ? &X[i * CS] : &X[i * 256];
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (LDS_AS void *)dst, 16, off, 0, 0, 0);
+            }
+        }
+        __builtin_amdgcn_s_waitcnt(0);
+        __asm__ volatile("" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        __asm__ volatile("" ::: "memory");
+
+        float av[28];
+#pragma unroll
+        for (int s4 = 0; s4 < 28; s4++)
+            av[s4] = Y[ya + 4 * s4];
+        if (do_bias) {
+#pragma unroll
+            for (int s4 = 0; s4 < 28; s4++)
+                bsum += av[s4];
+        }
+        // Taps innermost: the nine accumulators are independent, so
+        // consecutive MFMAs never wait for each other's result.
+#pragma unroll
+        for (int s4 = 0; s4 < 28; s4++) {
+            const int px = 4 * s4, dr = px / TW, dq = px % TW;
+#pragma unroll
+            for (int tap = 0; tap < 9; tap++) {
+                const int r = tap / 3, sx = tap % 3;
+                const float bv = X[xb + (dr + r) * HWW + dq + sx];
+                acc[tap] = mfma16(av[s4], bv, acc[tap]);
+            }
+            if (s4 % 2 == 1)
+                __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+
+    // Bias gradient: the four lane groups of a filter row summed disjoint
+    // pixels; combine them in a fixed order.
+    if (do_bias) {
+        bsum += __shfl_xor(bsum, 16, 64);
+        bsum += __shfl_xor(bsum, 32, 64);
+        const int k = m0 + 16 * wave + lc;
+        if (kr == 0 && k < a.Kg)
+            a.db_part[(long long)split * a.K + g * a.Kg + k] = bsum;
+    }
+    float *outs = a.out + (long long)split * a.split_stride;
+#pragma unroll
+    for (int tap = 0; tap < 9; tap++)
+#pragma unroll
+        for (int v = 0; v < 4; v++) {
+            const int k = m0 + 16 * wave + 4 * kr + v;
+            if (k < a.Kg)
+                outs[((long long)(g * a.Kg + k) * 9 + tap) * a.Cg + c0 + lc] = acc[tap][v];
+        }
+}
+
+// ---------------------------------------------------------------------------
 // Filter packing.
 // ---------------------------------------------------------------------------
 __global__ void pack_fwd_kernel(const float *__restrict__ w, float *__restrict__ wp, int Kg,
@@ -1275,6 +1455,24 @@ static hipError_t halo_launch_tw(const HaloGemmArgs &a, bool flip, hipStream_t s
     case 14: return halo_launch<BM, 14>(a, flip, stream);
     default: return hipErrorInvalidValue;
     }
+}
+
+bool wgrad_halo_supported(int TW, int Q, int W)
+{
+    return (TW == 112 || TW == 56 || TW == 28) && Q % 4 == 0 && W % 4 == 0;
+}
+
+hipError_t launch_wgrad_halo(const WgradHaloArgs &a, hipStream_t stream)
+{
+    if (!wgrad_halo_supported(a.TW, a.Q, a.W) || a.col0 % 4)
+        return hipErrorInvalidValue;
+    const int tiles = ((a.Kg + 63) / 64) * (a.Cg / 16) * a.groups * a.nsplit;
+    switch (a.TW) {
+    case 112: hipLaunchKernelGGL(wgrad_halo_kernel<112>, dim3(tiles), dim3(256), 0, stream, a); break;
+    case 56: hipLaunchKernelGGL(wgrad_halo_kernel<56>, dim3(tiles), dim3(256), 0, stream, a); break;
+    default: hipLaunchKernelGGL(wgrad_halo_kernel<28>, dim3(tiles), dim3(256), 0, stream, a); break;
+    }
+    return hipGetLastError();
 }
 
 bool halo_width_supported(int TW, int src_w, int col0)

@@ -147,6 +147,35 @@ struct WgradArgs {
     float *db_part;          // [split][K] partial bias gradients, or null
 };
 
+// ---------------------------------------------------------------------------
+// Halo backward-weight for stride-1 3 x 3 layers (channels per group a
+// multiple of 16, dy rows a multiple of 4 wide): a workgroup computes all nine
+// taps of 64 filters x 16 input channels, its reduction running over TR x TW
+// pixel blocks of the images (TW = 112, 56 or 28, TR = 112 / TW; the same
+// blocks as HaloGemmArgs).  Per block it stages the 64 dy rows of the block
+// (dy[img][g Kg + k][p0 .. p0 + TR - 1][q0 .. q0 + TW - 1]) and the x halo of
+// its 16 channels (rows p0 - pad .., columns q0 - pad ..) in LDS once, then
+// runs the nine taps from them.  Split s covers pixel blocks
+// [s chunk, (s + 1) chunk) of the nimg x row_blocks x col_segs blocks and
+// writes partial sums out[s][g Kg + k][tap][c] (and, for the first channel
+// tile, db_part[s][g Kg + k]).
+// ---------------------------------------------------------------------------
+struct WgradHaloArgs {
+    int Kg, Cg, groups, K;
+    const float *dy, *x;
+    uint32_t dy_bytes, x_bytes;
+    uint32_t dy_img_words, x_img_words;
+    int H, W, P, Q;
+    int TW, row_blocks, col_segs, nimg;
+    int row0, col0, slack;    // x halo origin relative to (p0, q0); slack: first tap column
+    int chunk, nsplit;        // pixel blocks per split
+    float *out;               // [split][K][9][Cg]
+    long long split_stride;   // K * Cg * 9
+    float *db_part;           // [split][K], or null
+};
+bool wgrad_halo_supported(int TW, int Q, int W);
+hipError_t launch_wgrad_halo(const WgradHaloArgs &a, hipStream_t stream);
+
 // Image-GEMM tile shapes (BM x BN; 4 waves, 3 for 48x64).
 enum ImgTile {
     IMG_64x64 = 0, IMG_128x64, IMG_16x128, IMG_32x64, IMG_48x64, IMG_96x64, IMG_96x128,

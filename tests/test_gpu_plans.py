@@ -36,6 +36,10 @@ PLAN_SHAPES = [
     (2, 16, 9, 12, 16, 3, 3, 1, 2, 1),     # pad 2
     (2, 16, 8, 12, 16, 3, 3, 1, 0, 1),     # pad 0
     (1, 256, 6, 6, 128, 3, 3, 1, 1, 1),    # few tiles, 16 channel blocks: split
+    # Halo backward-weight (stride-1 3x3, dy and x rows multiples of 4 wide):
+    # filters not a multiple of 64, pad 3.
+    (2, 32, 6, 28, 80, 3, 3, 1, 1, 1),
+    (1, 16, 4, 8, 16, 3, 3, 1, 3, 1),
 ]
 
 
