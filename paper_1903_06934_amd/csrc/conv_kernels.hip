@@ -1023,10 +1023,21 @@ __global__ __launch_bounds__(256) void wgrad_halo_kernel(const WgradHaloArgs a)
         x_grp[j] = e - x_row[j] * GPR;
     }
 
-    // Compute-side bases: A = Y[(16 wave + lc) * 116 + kr + 4 s],
-    // B = X[lc * CS + kr + slack + (dr(s) + r) * HWW + dq(s) + sx].
-    const int ya = (16 * wave + lc) * kWhDyLd + kr;
-    const int xb = lc * CS + kr + a.slack;
+    // Pixel of MFMA step s = 2 t + e (t < 14, e < 2) for lane group kr: pairs
+    // of steps cover 8 pixels, lane group kr the adjacent pair 2 kr, 2 kr + 1
+    // of them (so the compiler's two-dword LDS reads of steps 2 t and 2 t + 1
+    // spread a half-wave's 16 rows x 2 lane groups over all 32 banks):
+    //   TW % 8 == 0: row-major pixel 8 t + 2 kr + e;
+    //   TW == 28:    row 2 (t / 7) + kr / 2, column 4 (t % 7) + 2 (kr % 2) + e
+    // (8-pixel runs would straddle 28-pixel rows).  The lane part goes into
+    // the bases; the (t, e) part is a compile-time offset:
+    //   A = Y[(16 wave + lc) * 116 + pix(t, e, kr)],
+    //   B = X[lc * CS + slack + (dr + r) * HWW + dq + sx].
+    constexpr bool ROWS2 = TW % 8 != 0;
+    static_assert(!ROWS2 || TW == 28, "pixel pairs");
+    const int kdr = ROWS2 ? kr >> 1 : 0, kdq = ROWS2 ? 2 * (kr & 1) : 2 * kr;
+    const int ya = (16 * wave + lc) * kWhDyLd + kdr * TW + kdq;
+    const int xb = lc * CS + a.slack + kdr * HWW + kdq;
 
     f32x4 acc[9];
 #pragma unroll
@@ -1077,27 +1088,36 @@ __global__ __launch_bounds__(256) void wgrad_halo_kernel(const WgradHaloArgs a)
         __builtin_amdgcn_s_barrier();
         __asm__ volatile("" ::: "memory");
 
+        // (dr, dq) of step s's pixel without the lane part.
+        auto step_dr = [](int st) {
+            const int t = st >> 1;
+            return ROWS2 ? 2 * (t / 7) : (8 * t) / TW;
+        };
+        auto step_dq = [](int st) {
+            const int t = st >> 1, e = st & 1;
+            return ROWS2 ? 4 * (t % 7) + e : (8 * t) % TW + e;
+        };
         float av[28];
 #pragma unroll
-        for (int s4 = 0; s4 < 28; s4++)
-            av[s4] = Y[ya + 4 * s4];
+        for (int st = 0; st < 28; st++)
+            av[st] = Y[ya + step_dr(st) * TW + step_dq(st)];
         if (do_bias) {
 #pragma unroll
-            for (int s4 = 0; s4 < 28; s4++)
-                bsum += av[s4];
+            for (int st = 0; st < 28; st++)
+                bsum += av[st];
         }
         // Taps innermost: the nine accumulators are independent, so
         // consecutive MFMAs never wait for each other's result.
 #pragma unroll
-        for (int s4 = 0; s4 < 28; s4++) {
-            const int px = 4 * s4, dr = px / TW, dq = px % TW;
+        for (int st = 0; st < 28; st++) {
+            const int dr = step_dr(st), dq = step_dq(st);
 #pragma unroll
             for (int tap = 0; tap < 9; tap++) {
                 const int r = tap / 3, sx = tap % 3;
                 const float bv = X[xb + (dr + r) * HWW + dq + sx];
-                acc[tap] = mfma16(av[s4], bv, acc[tap]);
+                acc[tap] = mfma16(av[st], bv, acc[tap]);
             }
-            if (s4 % 2 == 1)
+            if (st % 2 == 1)
                 __builtin_amdgcn_sched_barrier(0);
         }
     }
