@@ -926,6 +926,8 @@ struct WgradPlan {
     int img = -1;  // inner product: dW = dy^T x as an image GEMM with this tile (-1: no)
     int halo_tw = 0;  // halo backward-weight with this pixel-block width (0: no); chunk then
                       // counts pixel blocks
+    int halo_ct = 1;  // its 16-channel sub-tiles per workgroup (1 or 2)
+    int halo_db = 0;  // 1: the double-buffered eight-wave kernel (halo_ct 2)
 };
 
 bool is_tap_tile(int tile) { return wgrad_tile_is_tap(tile); }
@@ -1058,19 +1060,23 @@ int wgrad_halo_width(const Geom &g)
     return best;
 }
 
-// Splits over the pixel blocks so that about three workgroups per CU run
-// (three fit at once), times 2^scale, each split at least 4 blocks.
-WgradPlan wgrad_halo_plan(const Geom &g, int tw, int scale = 0)
+// Splits over the pixel blocks so that as many workgroups run as fit on the
+// CUs at once (three per CU with one 16-channel sub-tile, two with two),
+// times 2^scale, each split at least 4 blocks.
+WgradPlan wgrad_halo_plan(const Geom &g, int tw, int scale = 0, int ct = 1, int db = 0)
 {
     WgradPlan p{};
     p.tile = -1;
     p.halo_tw = tw;
+    p.halo_ct = ct;
+    p.halo_db = db;
     p.slice = kHaloCols;
     p.nb = g.N;
     const int tr = kHaloCols / tw;
     const long long blocks = (long long)g.N * ((g.P + tr - 1) / tr) * ((g.Q + tw - 1) / tw);
-    const long long tiles = (long long)((g.Kg + 63) / 64) * (g.Cg / 16) * g.G;
-    long long ns = (3LL * num_cus() + tiles - 1) / tiles;
+    const long long tiles = (long long)((g.Kg + 63) / 64) * (g.Cg / (16 * ct)) * g.G;
+    const long long resident = (db ? 1LL : ct == 1 ? 3LL : 2LL) * num_cus();
+    long long ns = (resident + tiles - 1) / tiles;
     if (scale > 0)
         ns <<= scale;
     else if (scale < 0)
@@ -1089,8 +1095,10 @@ WgradPlan wgrad_halo_plan(const Geom &g, int tw, int scale = 0)
 
 WgradPlan wgrad_rule(const Geom &g)
 {
+    // Two 16-channel sub-tiles a workgroup where the channels allow: 2-4 %
+    // faster than one on VGG-16 conv1_2 ... conv4_3 at batch 32.
     if (const int tw = wgrad_halo_width(g))
-        return wgrad_halo_plan(g, tw);
+        return wgrad_halo_plan(g, tw, 0, g.Cg % 32 == 0 ? 2 : 1);
     if (!is_inner_product(g))
         return wgrad_plan(g);
     // With a batch of whole 16-row slices, the image GEMM over the batch
@@ -1168,16 +1176,21 @@ void wgrad_candidates(const Geom &g, std::vector<WgradPlan> &out)
             const int tr = kHaloCols / tw;
             return (long long)((g.P + tr - 1) / tr) * ((g.Q + tw - 1) / tw);
         };
-        for (int tw : {112, 56, 28})
-            if (wgrad_halo_supported(tw, g.Q, g.W) && blocks(tw) == blocks(best))
-                for (int scale : {0, 1, -1}) {
-                    WgradPlan p = wgrad_halo_plan(g, tw, scale);
-                    bool dup = false;
-                    for (const WgradPlan &q : out)
-                        dup = dup || (q.halo_tw == p.halo_tw && q.chunk == p.chunk);
-                    if (!dup)
-                        out.push_back(p);
-                }
+        for (int kind : {0, 1, 2}) {  // 16 channels; 32; 32 double-buffered
+            const int ct = kind ? 2 : 1, db = kind == 2;
+            for (int tw : {112, 56, 28})
+                if (g.Cg % (16 * ct) == 0 && wgrad_halo_supported(tw, g.Q, g.W) &&
+                    blocks(tw) == blocks(best))
+                    for (int scale : {0, 1, -1}) {
+                        WgradPlan p = wgrad_halo_plan(g, tw, scale, ct, db);
+                        bool dup = false;
+                        for (const WgradPlan &q : out)
+                            dup = dup || (q.halo_tw == p.halo_tw && q.halo_ct == p.halo_ct &&
+                                          q.halo_db == p.halo_db && q.chunk == p.chunk);
+                        if (!dup)
+                            out.push_back(p);
+                    }
+        }
     }
 }
 
@@ -1196,8 +1209,9 @@ void wgrad_name(const WgradPlan &p, char *buf, size_t len)
     if (p.img >= 0)
         snprintf(buf, len, "batch-transposed, image GEMM %s over the batch", img_tile_name(p.img));
     else if (p.halo_tw)
-        snprintf(buf, len, "halo, 9 taps of 64x16 (%dx%d pixels), %d splits of %d blocks",
-                 p.halo_tw, kHaloCols / p.halo_tw, p.nsplit, p.chunk);
+        snprintf(buf, len, "halo, 9 taps of 64x%d%s (%dx%d pixels), %d splits of %d blocks",
+                 16 * p.halo_ct, p.halo_db ? " (8 waves, 2 stages)" : "", p.halo_tw,
+                 kHaloCols / p.halo_tw, p.nsplit, p.chunk);
     else if (p.xnb > 0)
         snprintf(buf, len, "explicit im2col (%d images a chunk), %s, %d splits of %d pixels",
                  p.xnb, wgrad_tile_name(p.tile), p.nsplit, p.chunk);
@@ -1964,6 +1978,8 @@ int wgrad_exec(const Geom &g, const WgradPlan &p, const float *x, const float *d
         h.P = g.P;
         h.Q = g.Q;
         h.TW = p.halo_tw;
+        h.CT = p.halo_ct;
+        h.db = p.halo_db;
         const int tr = kHaloCols / p.halo_tw;
         h.row_blocks = (g.P + tr - 1) / tr;
         h.col_segs = (g.Q + p.halo_tw - 1) / p.halo_tw;

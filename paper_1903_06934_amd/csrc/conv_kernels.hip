@@ -15,9 +15,33 @@ namespace miconv {
 // A[l % 16][l / 16]; B (4 x 16): B[l / 16][l % 16]; D (16 x 16): lane l,
 // register v holds D[4 (l / 16) + v][l % 16].
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+#define LDS_AS __attribute__((address_space(3)))
 constexpr int MF = 16;  // accumulator block edge
 
 __device__ __forceinline__ int acc_row(int v, int lane) { return 4 * (lane >> 4) + v; }
+
+// Two aligned words of LDS as one ds_read_b64 (word: even index into base).
+// The read is volatile so that the compiler does not fuse two of them into
+// one ds_read2_b64: on gfx950 a two-address LDS read (ds_read2_b32,
+// ds_read2_b64) at the operand patterns used here (16 rows a fixed stride
+// apart, two words per lane) costs 4-8 bank-conflict cycles where the
+// single ds_read_b64 costs none.
+typedef LDS_AS const volatile f32x2 lds_f32x2;
+__device__ __forceinline__ f32x2 lds_b64(const float *base, int word)
+{
+    return *(lds_f32x2 *)(base + word);
+}
+// A per-lane word offset hidden from the optimizer, so that the reads off
+// base + offset (which keep base's provenance: the compiler still knows
+// which LDS array they read) share one address register with their
+// constants in the instruction's offset field instead of each read's full
+// address being precomputed, loop-invariant, into a register of its own.
+__device__ __forceinline__ int opaque(int v)
+{
+    __asm__ volatile("" : "+v"(v));
+    return v;
+}
 
 __device__ __forceinline__ f32x4 mfma16(float a, float b, f32x4 c)
 {
@@ -37,7 +61,6 @@ __device__ __forceinline__ f32x4 mfma16(float a, float b, f32x4 c)
 // has bit 31 set and OR-ing bit 31 into an offset makes it out of range
 // (for every dword of a multi-dword load too).
 // ---------------------------------------------------------------------------
-#define LDS_AS __attribute__((address_space(3)))
 
 constexpr uint32_t kOob = 0x80000000u;  // beyond any buffer of < 2^31 bytes
 
@@ -956,20 +979,25 @@ __global__ __launch_bounds__(64 * WM * WN) void wgrad_kernel(const WgradArgs a)
 // (filter lc of its wave's 16, dy row) and B operand (channel lc, the x halo
 // shifted by the tap) sit at a per-lane base plus a compile-time offset; rows
 // are laid out so that the 64 lanes of an LDS read hit 64 different banks.
-// Each wave keeps nine 16x16 accumulators (one per tap) of its 16 filters x
-// the 16 channels.  A single LDS stage: three workgroups fit a CU.
+// Each wave keeps nine 16x16 accumulators (one per tap) of its 16 filters
+// for each of the CT 16-channel sub-tiles of the workgroup.  A single LDS
+// stage: three workgroups fit a CU with one sub-tile, two with two (which
+// stage each block's dy once for twice the MFMAs, and read dy from memory
+// half as often over the channel tiles).
 // ---------------------------------------------------------------------------
 constexpr int kWhDyLd = 116;  // dy row: 112 pixels + one 4-word group of padding
 
-template <int TW>
+template <int TW, int CT, bool SODD>
 __global__ __launch_bounds__(256) void wgrad_halo_kernel(const WgradHaloArgs a)
 {
     typedef HaloCfg<TW> C;
     constexpr int TR = C::TR, HWW = C::HWW, CS = C::CS;
     constexpr int HR = TR + 2, GPR = HWW / 4, EPC = HR * GPR;
-    constexpr int XNWL = C::PERCH ? 16 : (16 * EPC + 63) / 64;  // x halo wave-loads
-    constexpr int YNWL = 64 * (kWhDyLd / 4) / 64;                // dy wave-loads (29)
-    constexpr int XW = C::PERCH ? 16 * CS : XNWL * 64 * 4;
+    constexpr int NCH = 16 * CT;                                  // channels per workgroup
+    constexpr int XNWL = C::PERCH ? NCH : (NCH * EPC + 63) / 64;  // x halo wave-loads
+    constexpr int YNWL = 64 * (kWhDyLd / 4) / 64;                 // dy wave-loads (29)
+    constexpr int XW = C::PERCH ? NCH * CS : XNWL * 64 * 4;
+    static_assert(C::PERCH ? CS >= 256 : CS == 4 * EPC, "channel c's halo at c CS");
     static_assert(C::V == 4 && TR * TW == kHaloCols, "16-byte halo, 112-pixel blocks");
     static_assert((64 * (kWhDyLd / 4)) % 64 == 0, "whole dy wave-loads");
 
@@ -978,14 +1006,14 @@ __global__ __launch_bounds__(256) void wgrad_halo_kernel(const WgradHaloArgs a)
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int mtiles = (a.Kg + 63) / 64, ctiles = a.Cg / 16;
+    const int mtiles = (a.Kg + 63) / 64, ctiles = a.Cg / NCH;
     const int tiles = mtiles * ctiles;
     const int lin = xcd_tile(blockIdx.x, tiles * a.groups * a.nsplit);
     const int split = lin / (tiles * a.groups);
     const int rest = lin - split * tiles * a.groups;
     const int g = rest / tiles, tile = rest - g * tiles;
     const int mt = tile % mtiles, ct = tile / mtiles;
-    const int m0 = mt * 64, c0 = ct * 16;
+    const int m0 = mt * 64, c0 = ct * NCH;
     const int per_img = a.row_blocks * a.col_segs;
     const int nblocks = a.nimg * per_img;
     const int b_beg = split * a.chunk, b_end = min(nblocks, b_beg + a.chunk);
@@ -1018,31 +1046,40 @@ __global__ __launch_bounds__(256) void wgrad_halo_kernel(const WgradHaloArgs a)
             c = ge / EPC;
             e = ge - c * EPC;
         }
-        x_c[j] = (c < 16 && e < EPC) ? c : 16;  // 16: masked
+        x_c[j] = (c < NCH && e < EPC) ? c : NCH;  // NCH: masked
         x_row[j] = e / GPR;
         x_grp[j] = e - x_row[j] * GPR;
     }
 
     // Pixel of MFMA step s = 2 t + e (t < 14, e < 2) for lane group kr: pairs
     // of steps cover 8 pixels, lane group kr the adjacent pair 2 kr, 2 kr + 1
-    // of them (so the compiler's two-dword LDS reads of steps 2 t and 2 t + 1
-    // spread a half-wave's 16 rows x 2 lane groups over all 32 banks):
+    // of them (so that the two-dword LDS reads of steps 2 t and 2 t + 1
+    // spread a half-wave's 16 rows x 2 lane groups over all 64 banks):
     //   TW % 8 == 0: row-major pixel 8 t + 2 kr + e;
     //   TW == 28:    row 2 (t / 7) + kr / 2, column 4 (t % 7) + 2 (kr % 2) + e
     // (8-pixel runs would straddle 28-pixel rows).  The lane part goes into
     // the bases; the (t, e) part is a compile-time offset:
     //   A = Y[(16 wave + lc) * 116 + pix(t, e, kr)],
     //   B = X[lc * CS + slack + (dr + r) * HWW + dq + sx].
+    // Per step pair and filter row r a lane needs the four B words
+    // w[e + sx] = X[x0 .. x0 + 3], x0 = lc CS + slack + (lane part) + (dr + r)
+    // HWW + (the pair's column), whose parity is the parity of slack (the
+    // rest is even).  They are read as aligned two-word reads (ds_read_b64):
+    // two when slack is even, three (from x0 - 1) when it is odd (SODD); the
+    // A operand of a step pair is one such read too.
     constexpr bool ROWS2 = TW % 8 != 0;
     static_assert(!ROWS2 || TW == 28, "pixel pairs");
+    static_assert(CS % 2 == 0 && HWW % 2 == 0, "even row and channel strides");
     const int kdr = ROWS2 ? kr >> 1 : 0, kdq = ROWS2 ? 2 * (kr & 1) : 2 * kr;
     const int ya = (16 * wave + lc) * kWhDyLd + kdr * TW + kdq;
-    const int xb = lc * CS + a.slack + kdr * HWW + kdq;
+    const int xw = lc * CS + a.slack - (SODD ? 1 : 0) + kdr * HWW + kdq;  // even
 
-    f32x4 acc[9];
+    f32x4 acc[CT][9];
 #pragma unroll
-    for (int t = 0; t < 9; t++)
-        acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < CT; j++)
+#pragma unroll
+        for (int t = 0; t < 9; t++)
+            acc[j][t] = f32x4{0.f, 0.f, 0.f, 0.f};
     float bsum = 0.f;
     const bool do_bias = a.db_part != nullptr && ct == 0;
 
@@ -1073,7 +1110,7 @@ __global__ __launch_bounds__(256) void wgrad_halo_kernel(const WgradHaloArgs a)
             const int i = wave + 4 * j;
             if (i < XNWL) {
                 const int h = p0 + a.row0 + x_row[j], w = q0 + a.col0 + 4 * x_grp[j];
-                const bool ok = x_c[j] < 16 && (unsigned)h < (unsigned)a.H && w >= 0 && w + 4 <= a.W;
+                const bool ok = x_c[j] < NCH && (unsigned)h < (unsigned)a.H && w >= 0 && w + 4 <= a.W;
                 const uint32_t off =
                     ok ? ((uint32_t)img * a.x_img_words + (uint32_t)(g * a.Cg + c0 + x_c[j]) *
                                                               (uint32_t)(a.H * a.W) +
@@ -1099,26 +1136,47 @@ __global__ __launch_bounds__(256) void wgrad_halo_kernel(const WgradHaloArgs a)
         };
         float av[28];
 #pragma unroll
-        for (int st = 0; st < 28; st++)
-            av[st] = Y[ya + step_dr(st) * TW + step_dq(st)];
+        for (int t = 0; t < 14; t++) {
+            const f32x2 v = lds_b64(Y, ya + step_dr(2 * t) * TW + step_dq(2 * t));
+            av[2 * t] = v.x;
+            av[2 * t + 1] = v.y;
+        }
         if (do_bias) {
 #pragma unroll
             for (int st = 0; st < 28; st++)
                 bsum += av[st];
         }
-        // Taps innermost: the nine accumulators are independent, so
+        // B words of step pair t, read one pair ahead of their MFMAs.
+        constexpr int NRD = SODD ? 3 : 2;  // two-word reads per filter row
+        f32x2 wb[2][CT][3][NRD];
+        auto load_b = [&](f32x2 (&dst)[CT][3][NRD], int t) {
+            const int dr = step_dr(2 * t), dq = step_dq(2 * t);
+#pragma unroll
+            for (int j = 0; j < CT; j++)
+#pragma unroll
+                for (int r = 0; r < 3; r++)
+#pragma unroll
+                    for (int k = 0; k < NRD; k++)
+                        dst[j][r][k] = lds_b64(X, xw + j * 16 * CS + (dr + r) * HWW + dq + 2 * k);
+        };
+        load_b(wb[0], 0);
+        // Taps innermost: the 9 CT accumulators are independent, so
         // consecutive MFMAs never wait for each other's result.
 #pragma unroll
-        for (int st = 0; st < 28; st++) {
-            const int dr = step_dr(st), dq = step_dq(st);
+        for (int t = 0; t < 14; t++) {
+            if (t + 1 < 14)
+                load_b(wb[(t + 1) & 1], t + 1);
+            const f32x2(&wc)[CT][3][NRD] = wb[t & 1];
 #pragma unroll
-            for (int tap = 0; tap < 9; tap++) {
-                const int r = tap / 3, sx = tap % 3;
-                const float bv = X[xb + (dr + r) * HWW + dq + sx];
-                acc[tap] = mfma16(av[st], bv, acc[tap]);
-            }
-            if (st % 2 == 1)
-                __builtin_amdgcn_sched_barrier(0);
+            for (int e = 0; e < 2; e++)
+#pragma unroll
+                for (int j = 0; j < CT; j++)
+#pragma unroll
+                    for (int tap = 0; tap < 9; tap++) {
+                        const int r = tap / 3, i = e + tap % 3 + (SODD ? 1 : 0);  // word of the row
+                        acc[j][tap] = mfma16(av[2 * t + e], wc[j][r][i >> 1][i & 1], acc[j][tap]);
+                    }
+            __builtin_amdgcn_sched_barrier(0);
         }
     }
 
@@ -1133,12 +1191,237 @@ __global__ __launch_bounds__(256) void wgrad_halo_kernel(const WgradHaloArgs a)
     }
     float *outs = a.out + (long long)split * a.split_stride;
 #pragma unroll
+    for (int j = 0; j < CT; j++)
+#pragma unroll
+        for (int tap = 0; tap < 9; tap++)
+#pragma unroll
+            for (int v = 0; v < 4; v++) {
+                const int k = m0 + 16 * wave + 4 * kr + v;
+                if (k < a.Kg)
+                    outs[((long long)(g * a.Kg + k) * 9 + tap) * a.Cg + c0 + 16 * j + lc] =
+                        acc[j][tap][v];
+            }
+}
+
+// ---------------------------------------------------------------------------
+// Double-buffered halo backward-weight: eight waves (two per SIMD), 64 filters
+// x 32 channels, pixel blocks staged one ahead.  Wave w computes the nine taps
+// of filters 16 (w % 4) .. + 15 and channels 16 (w / 4) .. + 15 of the tile.
+// While the waves run the MFMAs of block b from one LDS stage, the DMA of
+// block b + 1 fills the other, so a block costs one barrier and no exposed
+// load latency.  Two stages of dy rows and x halos for 32 channels take 123-
+// 152 KiB of LDS: one workgroup a CU.  The two stages are distinct arrays
+// (blocks are taken in pairs), so the compiler's wait for in-flight DMA
+// before an LDS read only ever covers the stage being read.
+// ---------------------------------------------------------------------------
+template <int TW, bool SODD>
+__global__ __launch_bounds__(512) void wgrad_halo_db_kernel(const WgradHaloArgs a)
+{
+    typedef HaloCfg<TW> C;
+    constexpr int TR = C::TR, HWW = C::HWW, CS = C::CS;
+    constexpr int HR = TR + 2, GPR = HWW / 4, EPC = HR * GPR;
+    constexpr int NCH = 32, NWV = 8;
+    constexpr int XNWL = C::PERCH ? NCH : (NCH * EPC + 63) / 64;  // x halo wave-loads
+    constexpr int YNWL = 64 * (kWhDyLd / 4) / 64;                 // dy wave-loads (29)
+    constexpr int XW = C::PERCH ? NCH * CS : XNWL * 64 * 4;
+    constexpr int YW = 64 * kWhDyLd;
+    static_assert(C::PERCH ? CS >= 256 : CS == 4 * EPC, "channel c's halo at c CS");
+    static_assert(C::V == 4 && TR * TW == kHaloCols, "16-byte halo, 112-pixel blocks");
+    static_assert(2 * (YW + XW) * 4 <= 160 * 1024, "two stages in LDS");
+
+    __shared__ __attribute__((aligned(16))) float Y0[YW];
+    __shared__ __attribute__((aligned(16))) float X0[XW];
+    __shared__ __attribute__((aligned(16))) float Y1[YW];
+    __shared__ __attribute__((aligned(16))) float X1[XW];
+
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wm = wave & 3, wj = wave >> 2;
+    const int mtiles = (a.Kg + 63) / 64, ctiles = a.Cg / NCH;
+    const int tiles = mtiles * ctiles;
+    const int lin = xcd_tile(blockIdx.x, tiles * a.groups * a.nsplit);
+    const int split = lin / (tiles * a.groups);
+    const int rest = lin - split * tiles * a.groups;
+    const int g = rest / tiles, tile = rest - g * tiles;
+    const int mt = tile % mtiles, ct = tile / mtiles;
+    const int m0 = mt * 64, c0 = ct * NCH;
+    const int per_img = a.row_blocks * a.col_segs;
+    const int nblocks = a.nimg * per_img;
+    const int b_beg = split * a.chunk, b_end = min(nblocks, b_beg + a.chunk);
+    const int kr = lane >> 4, lc = lane & 15;
+
+    const __amdgpu_buffer_rsrc_t rdy = make_rsrc(a.dy, a.dy_bytes);
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(a.x, a.x_bytes);
+
+    // Staging lanes, as in wgrad_halo_kernel with eight waves: wave-load i
+    // of a block is issued by wave i % 8.
+    constexpr int YL = (YNWL + NWV - 1) / NWV, XL = (XNWL + NWV - 1) / NWV;
+    int y_row[YL], y_px[YL];
+#pragma unroll
+    for (int j = 0; j < YL; j++) {
+        const int L = (wave + NWV * j) * 64 + lane;
+        y_row[j] = L / (kWhDyLd / 4);
+        y_px[j] = 4 * (L - y_row[j] * (kWhDyLd / 4));
+    }
+    int x_c[XL], x_row[XL], x_grp[XL];
+#pragma unroll
+    for (int j = 0; j < XL; j++) {
+        const int i = wave + NWV * j;
+        int c, e;
+        if constexpr (C::PERCH) {
+            c = i;
+            e = lane;
+        } else {
+            const int ge = i * 64 + lane;
+            c = ge / EPC;
+            e = ge - c * EPC;
+        }
+        x_c[j] = (c < NCH && e < EPC) ? c : NCH;  // NCH: masked
+        x_row[j] = e / GPR;
+        x_grp[j] = e - x_row[j] * GPR;
+    }
+
+    // DMA of pixel block b into one stage.
+    auto stage = [&](int b, float *Yd, float *Xd) {
+        const int img = b / per_img, prem = b - img * per_img;
+        const int rb = prem / a.col_segs, csg = prem - rb * a.col_segs;
+        const int p0 = rb * TR, q0 = csg * TW;
+#pragma unroll
+        for (int j = 0; j < YL; j++) {
+            const int i = wave + NWV * j;
+            if (i < YNWL) {
+                const int px = y_px[j], dr = px / TW, dq = px - (px / TW) * TW;
+                const int k = m0 + y_row[j];
+                const bool ok = px < kHaloCols && k < a.Kg && p0 + dr < a.P && q0 + dq < a.Q;
+                const uint32_t off =
+                    ok ? ((uint32_t)img * a.dy_img_words + (uint32_t)(g * a.Kg + k) * (uint32_t)(a.P * a.Q) +
+                          (uint32_t)((p0 + dr) * a.Q + q0 + dq)) * 4u
+                       : kOob;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rdy, (LDS_AS void *)&Yd[i * 256], 16, off, 0, 0, 0);
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < XL; j++) {
+            const int i = wave + NWV * j;
+            if (i < XNWL) {
+                const int h = p0 + a.row0 + x_row[j], w = q0 + a.col0 + 4 * x_grp[j];
+                const bool ok = x_c[j] < NCH && (unsigned)h < (unsigned)a.H && w >= 0 && w + 4 <= a.W;
+                const uint32_t off =
+                    ok ? ((uint32_t)img * a.x_img_words + (uint32_t)(g * a.Cg + c0 + x_c[j]) *
+                                                              (uint32_t)(a.H * a.W) +
+                          (uint32_t)(h * a.W + w)) * 4u
+                       : kOob;
+                float *dst = C::PERCH ? &Xd[i * CS] : &Xd[i * 256];
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (LDS_AS void *)dst, 16, off, 0, 0, 0);
+            }
+        }
+    };
+
+    // Operand mapping as in wgrad_halo_kernel (pixel pairs per lane group,
+    // B words by aligned two-word reads), for this wave's filter rows and
+    // channel sub-tile.
+    constexpr bool ROWS2 = TW % 8 != 0;
+    static_assert(!ROWS2 || TW == 28, "pixel pairs");
+    static_assert(CS % 2 == 0 && HWW % 2 == 0, "even row and channel strides");
+    const int kdr = ROWS2 ? kr >> 1 : 0, kdq = ROWS2 ? 2 * (kr & 1) : 2 * kr;
+    const int ya = (16 * wm + lc) * kWhDyLd + kdr * TW + kdq;
+    const int xw = (16 * wj + lc) * CS + a.slack - (SODD ? 1 : 0) + kdr * HWW + kdq;  // even
+    auto step_dr = [](int st) {
+        const int t = st >> 1;
+        return ROWS2 ? 2 * (t / 7) : (8 * t) / TW;
+    };
+    auto step_dq = [](int st) {
+        const int t = st >> 1, e = st & 1;
+        return ROWS2 ? 4 * (t % 7) + e : (8 * t) % TW + e;
+    };
+
+    f32x4 acc[9];
+#pragma unroll
+    for (int t = 0; t < 9; t++)
+        acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float bsum = 0.f;
+    const bool do_bias = a.db_part != nullptr && ct == 0 && wj == 0;
+
+    // MFMAs of one staged block.
+    auto compute = [&](const float *Yc, const float *Xc) {
+        const float *yp = Yc + opaque(ya), *xp = Xc + opaque(xw);
+        float av[28];
+#pragma unroll
+        for (int t = 0; t < 14; t++) {
+            const f32x2 v = lds_b64(yp, step_dr(2 * t) * TW + step_dq(2 * t));
+            av[2 * t] = v.x;
+            av[2 * t + 1] = v.y;
+        }
+        if (do_bias) {
+#pragma unroll
+            for (int st = 0; st < 28; st++)
+                bsum += av[st];
+        }
+        constexpr int NRD = SODD ? 3 : 2;
+        f32x2 wb[2][3][NRD];
+        auto load_b = [&](f32x2 (&dst)[3][NRD], int t) {
+            const int dr = step_dr(2 * t), dq = step_dq(2 * t);
+#pragma unroll
+            for (int r = 0; r < 3; r++)
+#pragma unroll
+                for (int k = 0; k < NRD; k++)
+                    dst[r][k] = lds_b64(xp, (dr + r) * HWW + dq + 2 * k);
+        };
+        load_b(wb[0], 0);
+#pragma unroll
+        for (int t = 0; t < 14; t++) {
+            if (t + 1 < 14)
+                load_b(wb[(t + 1) & 1], t + 1);
+            const f32x2(&wc)[3][NRD] = wb[t & 1];
+#pragma unroll
+            for (int e = 0; e < 2; e++)
+#pragma unroll
+                for (int tap = 0; tap < 9; tap++) {
+                    const int r = tap / 3, i = e + tap % 3 + (SODD ? 1 : 0);
+                    acc[tap] = mfma16(av[2 * t + e], wc[r][i >> 1][i & 1], acc[tap]);
+                }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
+
+    // One block: wait for this wave's DMA of it, barrier (every wave's DMA
+    // has landed and every wave is done with the other stage), start the DMA
+    // of the next block into the other stage, compute.
+    auto block = [&](int b, const float *Yc, const float *Xc, float *Yn, float *Xn) {
+        __builtin_amdgcn_s_waitcnt(0);
+        __asm__ volatile("" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        __asm__ volatile("" ::: "memory");
+        if (b + 1 < b_end)
+            stage(b + 1, Yn, Xn);
+        compute(Yc, Xc);
+    };
+
+    if (b_beg < b_end)
+        stage(b_beg, Y0, X0);
+    int b = b_beg;
+    for (; b + 1 < b_end; b += 2) {
+        block(b, Y0, X0, Y1, X1);
+        block(b + 1, Y1, X1, Y0, X0);
+    }
+    if (b < b_end)
+        block(b, Y0, X0, Y1, X1);
+
+    if (do_bias) {
+        bsum += __shfl_xor(bsum, 16, 64);
+        bsum += __shfl_xor(bsum, 32, 64);
+        const int k = m0 + 16 * wm + lc;
+        if (kr == 0 && k < a.Kg)
+            a.db_part[(long long)split * a.K + g * a.Kg + k] = bsum;
+    }
+    float *outs = a.out + (long long)split * a.split_stride;
+#pragma unroll
     for (int tap = 0; tap < 9; tap++)
 #pragma unroll
         for (int v = 0; v < 4; v++) {
-            const int k = m0 + 16 * wave + 4 * kr + v;
+            const int k = m0 + 16 * wm + 4 * kr + v;
             if (k < a.Kg)
-                outs[((long long)(g * a.Kg + k) * 9 + tap) * a.Cg + c0 + lc] = acc[tap][v];
+                outs[((long long)(g * a.Kg + k) * 9 + tap) * a.Cg + c0 + 16 * wj + lc] = acc[tap][v];
         }
 }
 
@@ -1482,17 +1765,43 @@ bool wgrad_halo_supported(int TW, int Q, int W)
     return (TW == 112 || TW == 56 || TW == 28) && Q % 4 == 0 && W % 4 == 0;
 }
 
+template <bool SODD>
+static hipError_t wgrad_halo_launch_par(const WgradHaloArgs &a, int tiles, hipStream_t stream)
+{
+    const dim3 grid(tiles), block(256);
+    if (a.db) {
+        const dim3 block8(512);
+        switch (a.TW) {
+        case 112: hipLaunchKernelGGL((wgrad_halo_db_kernel<112, SODD>), grid, block8, 0, stream, a); break;
+        case 56: hipLaunchKernelGGL((wgrad_halo_db_kernel<56, SODD>), grid, block8, 0, stream, a); break;
+        default: hipLaunchKernelGGL((wgrad_halo_db_kernel<28, SODD>), grid, block8, 0, stream, a); break;
+        }
+    } else if (a.CT == 2) {
+        switch (a.TW) {
+        case 112: hipLaunchKernelGGL((wgrad_halo_kernel<112, 2, SODD>), grid, block, 0, stream, a); break;
+        case 56: hipLaunchKernelGGL((wgrad_halo_kernel<56, 2, SODD>), grid, block, 0, stream, a); break;
+        default: hipLaunchKernelGGL((wgrad_halo_kernel<28, 2, SODD>), grid, block, 0, stream, a); break;
+        }
+    } else {
+        switch (a.TW) {
+        case 112: hipLaunchKernelGGL((wgrad_halo_kernel<112, 1, SODD>), grid, block, 0, stream, a); break;
+        case 56: hipLaunchKernelGGL((wgrad_halo_kernel<56, 1, SODD>), grid, block, 0, stream, a); break;
+        default: hipLaunchKernelGGL((wgrad_halo_kernel<28, 1, SODD>), grid, block, 0, stream, a); break;
+        }
+    }
+    return hipGetLastError();
+}
+
 hipError_t launch_wgrad_halo(const WgradHaloArgs &a, hipStream_t stream)
 {
     if (!wgrad_halo_supported(a.TW, a.Q, a.W) || a.col0 % 4)
         return hipErrorInvalidValue;
-    const int tiles = ((a.Kg + 63) / 64) * (a.Cg / 16) * a.groups * a.nsplit;
-    switch (a.TW) {
-    case 112: hipLaunchKernelGGL(wgrad_halo_kernel<112>, dim3(tiles), dim3(256), 0, stream, a); break;
-    case 56: hipLaunchKernelGGL(wgrad_halo_kernel<56>, dim3(tiles), dim3(256), 0, stream, a); break;
-    default: hipLaunchKernelGGL(wgrad_halo_kernel<28>, dim3(tiles), dim3(256), 0, stream, a); break;
-    }
-    return hipGetLastError();
+    if ((a.CT != 1 && a.CT != 2) || a.Cg % (16 * a.CT) || a.slack < 0 || a.slack > 3 ||
+        (a.db && a.CT != 2))
+        return hipErrorInvalidValue;
+    const int tiles = ((a.Kg + 63) / 64) * (a.Cg / (16 * a.CT)) * a.groups * a.nsplit;
+    return (a.slack & 1) ? wgrad_halo_launch_par<true>(a, tiles, stream)
+                         : wgrad_halo_launch_par<false>(a, tiles, stream);
 }
 
 bool halo_width_supported(int TW, int src_w, int col0)

@@ -150,11 +150,11 @@ struct WgradArgs {
 // ---------------------------------------------------------------------------
 // Halo backward-weight for stride-1 3 x 3 layers (channels per group a
 // multiple of 16, dy rows a multiple of 4 wide): a workgroup computes all nine
-// taps of 64 filters x 16 input channels, its reduction running over TR x TW
+// taps of 64 filters x 16 CT input channels, its reduction running over TR x TW
 // pixel blocks of the images (TW = 112, 56 or 28, TR = 112 / TW; the same
 // blocks as HaloGemmArgs).  Per block it stages the 64 dy rows of the block
 // (dy[img][g Kg + k][p0 .. p0 + TR - 1][q0 .. q0 + TW - 1]) and the x halo of
-// its 16 channels (rows p0 - pad .., columns q0 - pad ..) in LDS once, then
+// its 16 CT channels (rows p0 - pad .., columns q0 - pad ..) in LDS once, then
 // runs the nine taps from them.  Split s covers pixel blocks
 // [s chunk, (s + 1) chunk) of the nimg x row_blocks x col_segs blocks and
 // writes partial sums out[s][g Kg + k][tap][c] (and, for the first channel
@@ -166,7 +166,8 @@ struct WgradHaloArgs {
     uint32_t dy_bytes, x_bytes;
     uint32_t dy_img_words, x_img_words;
     int H, W, P, Q;
-    int TW, row_blocks, col_segs, nimg;
+    int TW, CT, row_blocks, col_segs, nimg;  // CT: 16-channel sub-tiles per workgroup (1, 2)
+    int db;                   // 1: eight waves, two LDS stages (CT = 2)
     int row0, col0, slack;    // x halo origin relative to (p0, q0); slack: first tap column
     int chunk, nsplit;        // pixel blocks per split
     float *out;               // [split][K][9][Cg]

@@ -40,6 +40,7 @@ PLAN_SHAPES = [
     # filters not a multiple of 64, pad 3.
     (2, 32, 6, 28, 80, 3, 3, 1, 1, 1),
     (1, 16, 4, 8, 16, 3, 3, 1, 3, 1),
+    (2, 64, 6, 12, 48, 3, 3, 1, 1, 2),     # two 16-channel sub-tiles a workgroup, groups
 ]
 
 
