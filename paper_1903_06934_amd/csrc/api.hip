@@ -1033,12 +1033,13 @@ WgradPlan wgrad_img_plan(const Geom &g, int tile)
 }
 
 // Halo backward-weight (wgrad_halo_kernel): stride-1 3 x 3 layers with
-// channel-aligned groups whose dy and x rows are a multiple of 4 wide, in one
-// launch.  Pixel-block width: the one of 56, 28, 112 (in that order of
-// preference; the 112 x 1 blocks stage 45 % more halo per pixel and measured
-// 3-7 % slower) that pads the P x Q grid least (0: not applicable).  The rule
-// for such layers: on VGG-16 conv1_2 ... conv4_3 at batch 32 it ran at
-// 120-128 TFLOP/s against 116-122 for the best tap-tile plan.
+// channel-aligned groups whose dy and x rows are a multiple of 4 wide, or
+// 14-wide maps of an even number of rows, in one launch.  Pixel-block width:
+// the one of 56, 28, 112, 14 (in that order of preference; the 112 x 1
+// blocks stage 45 % more halo per pixel and measured 3-7 % slower) that pads
+// the P x Q grid least (0: not applicable).  The rule for such layers: on
+// VGG-16 conv1_2 ... conv4_3 at batch 32 it ran at 120-128 TFLOP/s against
+// 116-122 for the best tap-tile plan.
 int wgrad_halo_width(const Geom &g)
 {
     if (g.st != 1 || g.R != 3 || g.S != 3 || g.Cg % 16 || is_inner_product(g) ||
@@ -1046,8 +1047,8 @@ int wgrad_halo_width(const Geom &g)
         return 0;
     int best = 0;
     long long best_cols = 0;
-    for (int tw : {56, 28, 112}) {
-        if (!wgrad_halo_supported(tw, g.Q, g.W))
+    for (int tw : {56, 28, 112, 14}) {
+        if (!wgrad_halo_supported(tw, g.P, g.Q, g.W))
             continue;
         const int tr = kHaloCols / tw;
         const long long cols =
@@ -1095,10 +1096,13 @@ WgradPlan wgrad_halo_plan(const Geom &g, int tw, int scale = 0, int ct = 1, int 
 
 WgradPlan wgrad_rule(const Geom &g)
 {
-    // Two 16-channel sub-tiles a workgroup where the channels allow: 2-4 %
-    // faster than one on VGG-16 conv1_2 ... conv4_3 at batch 32.
+    // Where the channels allow, the double-buffered eight-wave kernel (64 x
+    // 32 tiles): on VGG-16 at batch 32 2-6 % faster than the single-stage
+    // 64 x 32 one on conv1_2 ... conv2_2 and even on conv3_x, conv4_x, itself
+    // 2-4 % faster than 64 x 16; on the 14 x 14 layers of ResNet-50 and
+    // GoogLeNet 3-5 % faster than the best tap tile.
     if (const int tw = wgrad_halo_width(g))
-        return wgrad_halo_plan(g, tw, 0, g.Cg % 32 == 0 ? 2 : 1);
+        return g.Cg % 32 == 0 ? wgrad_halo_plan(g, tw, 0, 2, 1) : wgrad_halo_plan(g, tw);
     if (!is_inner_product(g))
         return wgrad_plan(g);
     // With a batch of whole 16-row slices, the image GEMM over the batch
@@ -1178,8 +1182,8 @@ void wgrad_candidates(const Geom &g, std::vector<WgradPlan> &out)
         };
         for (int kind : {0, 1, 2}) {  // 16 channels; 32; 32 double-buffered
             const int ct = kind ? 2 : 1, db = kind == 2;
-            for (int tw : {112, 56, 28})
-                if (g.Cg % (16 * ct) == 0 && wgrad_halo_supported(tw, g.Q, g.W) &&
+            for (int tw : {112, 56, 28, 14})
+                if (g.Cg % (16 * ct) == 0 && wgrad_halo_supported(tw, g.P, g.Q, g.W) &&
                     blocks(tw) == blocks(best))
                     for (int scale : {0, 1, -1}) {
                         WgradPlan p = wgrad_halo_plan(g, tw, scale, ct, db);
@@ -1984,9 +1988,10 @@ int wgrad_exec(const Geom &g, const WgradPlan &p, const float *x, const float *d
         h.row_blocks = (g.P + tr - 1) / tr;
         h.col_segs = (g.Q + p.halo_tw - 1) / p.halo_tw;
         h.nimg = N;
-        // x halo origin (p0 - pad, q0 - pad), columns from a multiple of 4.
+        // x halo origin (p0 - pad, q0 - pad); for 16-byte loads the
+        // columns start at a multiple of 4.
         h.row0 = -g.pad;
-        h.col0 = -((g.pad + 3) / 4) * 4;
+        h.col0 = p.halo_tw == 14 ? -g.pad : -((g.pad + 3) / 4) * 4;
         h.slack = -g.pad - h.col0;
         h.chunk = p.chunk;
         h.nsplit = p.nsplit;

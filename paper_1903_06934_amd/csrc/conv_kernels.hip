@@ -970,319 +970,105 @@ __global__ __launch_bounds__(64 * WM * WN) void wgrad_kernel(const WgradArgs a)
 //
 // The one-pixel-per-lane kernel above stages, per 64-pixel slice and tap
 // tile, one dword per lane and operand row: about one staging load per two
-// MFMAs.  Here a workgroup owns all nine taps of a 64-filter x 16-channel
-// tile, so each 112-pixel block's dy rows and x halo are staged once (16-byte
-// loads) and used by nine taps: about one load per twenty MFMAs.
+// MFMAs.  Here a workgroup owns all nine taps of a 64-filter x 16 CT-channel
+// tile, so each 112-pixel block's dy rows and x halo are staged once and used
+// by nine taps: about one load per twenty MFMAs.
 //
-// MFMA mapping (16x16x4, reduction over pixels): at step s (0 .. 27) lane
-// group kr takes pixel 4 s + kr of the block, so a lane's A operand
-// (filter lc of its wave's 16, dy row) and B operand (channel lc, the x halo
-// shifted by the tap) sit at a per-lane base plus a compile-time offset; rows
-// are laid out so that the 64 lanes of an LDS read hit 64 different banks.
-// Each wave keeps nine 16x16 accumulators (one per tap) of its 16 filters
-// for each of the CT 16-channel sub-tiles of the workgroup.  A single LDS
-// stage: three workgroups fit a CU with one sub-tile, two with two (which
-// stage each block's dy once for twice the MFMAs, and read dy from memory
-// half as often over the channel tiles).
+// Pixel blocks (WgHaloCfg): TW = 112, 56, 28 or 14 columns by TR = 112 / TW
+// rows.  dy rows are staged as 16-byte groups of 4 pixels (29 groups a row,
+// the last padding); for TW = 14 a block is 8 whole rows of a 14-wide map,
+// which lie contiguously in dy.  x halo of a channel: HR = TR + 2 rows of HWW
+// columns from (p0 - pad, q0 + col0), 16-byte loads (V = 4; col0 rounded down
+// to a multiple of 4, the tap columns then start slack words in) or one-word
+// loads (V = 1; col0 = -pad, slack 0).  Layout: channel c at c CS, either
+// dense (consecutive wave-loads, CS = the channel's words) or WPC wave-loads
+// per channel with CS padded.  CS and HWW are chosen so that the operand
+// reads below hit all 64 banks.
 // ---------------------------------------------------------------------------
 constexpr int kWhDyLd = 116;  // dy row: 112 pixels + one 4-word group of padding
 
-template <int TW, int CT, bool SODD>
-__global__ __launch_bounds__(256) void wgrad_halo_kernel(const WgradHaloArgs a)
-{
-    typedef HaloCfg<TW> C;
-    constexpr int TR = C::TR, HWW = C::HWW, CS = C::CS;
-    constexpr int HR = TR + 2, GPR = HWW / 4, EPC = HR * GPR;
-    constexpr int NCH = 16 * CT;                                  // channels per workgroup
-    constexpr int XNWL = C::PERCH ? NCH : (NCH * EPC + 63) / 64;  // x halo wave-loads
-    constexpr int YNWL = 64 * (kWhDyLd / 4) / 64;                 // dy wave-loads (29)
-    constexpr int XW = C::PERCH ? NCH * CS : XNWL * 64 * 4;
-    static_assert(C::PERCH ? CS >= 256 : CS == 4 * EPC, "channel c's halo at c CS");
-    static_assert(C::V == 4 && TR * TW == kHaloCols, "16-byte halo, 112-pixel blocks");
-    static_assert((64 * (kWhDyLd / 4)) % 64 == 0, "whole dy wave-loads");
+template <int TW>
+struct WgHaloCfg;
+template <>
+struct WgHaloCfg<112> {
+    static constexpr int TR = 1, V = 4, HWW = 124, CS = 3 * 124, WPC = 0;
+};
+template <>
+struct WgHaloCfg<56> {
+    static constexpr int TR = 2, V = 4, HWW = 64, CS = 260, WPC = 1;
+};
+template <>
+struct WgHaloCfg<28> {
+    static constexpr int TR = 4, V = 4, HWW = 36, CS = 260, WPC = 1;
+};
+template <>
+struct WgHaloCfg<14> {
+    static constexpr int TR = 8, V = 1, HWW = 16, CS = 194, WPC = 3;
+};
 
-    __shared__ __attribute__((aligned(16))) float Y[64 * kWhDyLd];
-    __shared__ __attribute__((aligned(16))) float X[XW];
+// Staging of one pixel block (dy rows of 64 filters, x halo of NCH channels)
+// by NWV waves into LDS.  dy: wave-load i is issued by wave i % NWV.  x, WPC
+// wave-loads per channel: wave w loads channels w, w + NWV, ..., so a lane's
+// element of part p (p < WPC) of a channel is the same for every channel;
+// dense layout: wave-load i by wave i % NWV.
+template <int TW, int NCH, int NWV>
+struct WgHaloStage {
+    typedef WgHaloCfg<TW> C;
+    static constexpr int TR = C::TR, V = C::V, HWW = C::HWW, CS = C::CS, WPC = C::WPC;
+    static constexpr int HR = TR + 2, GPR = HWW / V, EPC = HR * GPR;  // elements of V words
+    static constexpr int XNWL = WPC ? NCH * WPC : (NCH * EPC * V + 255) / 256;
+    static constexpr int YNWL = 64 * (kWhDyLd / 4) / 64;  // 29
+    static constexpr int XW = WPC ? NCH * CS : XNWL * 256;
+    static constexpr int YW = 64 * kWhDyLd;
+    static constexpr int YL = (YNWL + NWV - 1) / NWV;
+    static constexpr int XL = WPC ? WPC : (XNWL + NWV - 1) / NWV;  // per-lane x slots
+    static constexpr int NCC = (NCH + NWV - 1) / NWV;              // channels per wave (WPC > 0)
+    static_assert(TR * TW == kHaloCols && HWW % V == 0, "112-pixel blocks");
+    static_assert(WPC ? CS >= WPC * 64 * V && WPC * 64 >= EPC : CS == EPC * V,
+                  "channel c's halo at c CS, regions disjoint");
+    static_assert(V == 4 || V == 1, "16-byte or one-word halo loads");
 
-    const int lane = threadIdx.x & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int mtiles = (a.Kg + 63) / 64, ctiles = a.Cg / NCH;
-    const int tiles = mtiles * ctiles;
-    const int lin = xcd_tile(blockIdx.x, tiles * a.groups * a.nsplit);
-    const int split = lin / (tiles * a.groups);
-    const int rest = lin - split * tiles * a.groups;
-    const int g = rest / tiles, tile = rest - g * tiles;
-    const int mt = tile % mtiles, ct = tile / mtiles;
-    const int m0 = mt * 64, c0 = ct * NCH;
-    const int per_img = a.row_blocks * a.col_segs;
-    const int nblocks = a.nimg * per_img;
-    const int b_beg = split * a.chunk, b_end = min(nblocks, b_beg + a.chunk);
-    const int kr = lane >> 4, lc = lane & 15;
-
-    const __amdgpu_buffer_rsrc_t rdy = make_rsrc(a.dy, a.dy_bytes);
-    const __amdgpu_buffer_rsrc_t rx = make_rsrc(a.x, a.x_bytes);
-
-    // Staging lanes.  dy: wave-load i, lane l carries group L = 64 i + l,
-    // row L / 29 (filter m0 + row), pixels 4 (L % 29) .. + 3 (group 28 is
-    // padding); LDS words 4 L ...  x: as in halo_gemm_kernel, channel c0 + c.
-    constexpr int YL = (YNWL + 3) / 4, XL = (XNWL + 3) / 4;
     int y_row[YL], y_px[YL];
-#pragma unroll
-    for (int j = 0; j < YL; j++) {
-        const int L = (wave + 4 * j) * 64 + lane;
-        y_row[j] = L / (kWhDyLd / 4);
-        y_px[j] = 4 * (L - y_row[j] * (kWhDyLd / 4));
-    }
-    int x_c[XL], x_row[XL], x_grp[XL];
-#pragma unroll
-    for (int j = 0; j < XL; j++) {
-        const int i = wave + 4 * j;
-        int c, e;
-        if constexpr (C::PERCH) {
-            c = i;
-            e = lane;
-        } else {
-            const int ge = i * 64 + lane;
-            c = ge / EPC;
-            e = ge - c * EPC;
-        }
-        x_c[j] = (c < NCH && e < EPC) ? c : NCH;  // NCH: masked
-        x_row[j] = e / GPR;
-        x_grp[j] = e - x_row[j] * GPR;
-    }
+    int x_c[XL], x_row[XL], x_col[XL];  // x_c: dense layout's channel, or 0 / NCH (masked)
 
-    // Pixel of MFMA step s = 2 t + e (t < 14, e < 2) for lane group kr: pairs
-    // of steps cover 8 pixels, lane group kr the adjacent pair 2 kr, 2 kr + 1
-    // of them (so that the two-dword LDS reads of steps 2 t and 2 t + 1
-    // spread a half-wave's 16 rows x 2 lane groups over all 64 banks):
-    //   TW % 8 == 0: row-major pixel 8 t + 2 kr + e;
-    //   TW == 28:    row 2 (t / 7) + kr / 2, column 4 (t % 7) + 2 (kr % 2) + e
-    // (8-pixel runs would straddle 28-pixel rows).  The lane part goes into
-    // the bases; the (t, e) part is a compile-time offset:
-    //   A = Y[(16 wave + lc) * 116 + pix(t, e, kr)],
-    //   B = X[lc * CS + slack + (dr + r) * HWW + dq + sx].
-    // Per step pair and filter row r a lane needs the four B words
-    // w[e + sx] = X[x0 .. x0 + 3], x0 = lc CS + slack + (lane part) + (dr + r)
-    // HWW + (the pair's column), whose parity is the parity of slack (the
-    // rest is even).  They are read as aligned two-word reads (ds_read_b64):
-    // two when slack is even, three (from x0 - 1) when it is odd (SODD); the
-    // A operand of a step pair is one such read too.
-    constexpr bool ROWS2 = TW % 8 != 0;
-    static_assert(!ROWS2 || TW == 28, "pixel pairs");
-    static_assert(CS % 2 == 0 && HWW % 2 == 0, "even row and channel strides");
-    const int kdr = ROWS2 ? kr >> 1 : 0, kdq = ROWS2 ? 2 * (kr & 1) : 2 * kr;
-    const int ya = (16 * wave + lc) * kWhDyLd + kdr * TW + kdq;
-    const int xw = lc * CS + a.slack - (SODD ? 1 : 0) + kdr * HWW + kdq;  // even
-
-    f32x4 acc[CT][9];
-#pragma unroll
-    for (int j = 0; j < CT; j++)
-#pragma unroll
-        for (int t = 0; t < 9; t++)
-            acc[j][t] = f32x4{0.f, 0.f, 0.f, 0.f};
-    float bsum = 0.f;
-    const bool do_bias = a.db_part != nullptr && ct == 0;
-
-    for (int b = b_beg; b < b_end; b++) {
-        const int img = b / per_img, prem = b - img * per_img;
-        const int rb = prem / a.col_segs, csg = prem - rb * a.col_segs;
-        const int p0 = rb * TR, q0 = csg * TW;
-        // Every wave is done reading the previous block.
-        __builtin_amdgcn_s_barrier();
-        __asm__ volatile("" ::: "memory");
+    __device__ void init(int wave, int lane)
+    {
 #pragma unroll
         for (int j = 0; j < YL; j++) {
-            const int i = wave + 4 * j;
-            if (i < YNWL) {
-                const int px = y_px[j], dr = px / TW, dq = px - (px / TW) * TW;
-                const int k = m0 + y_row[j];
-                const bool ok = px < kHaloCols && k < a.Kg && p0 + dr < a.P && q0 + dq < a.Q;
-                const uint32_t off =
-                    ok ? ((uint32_t)img * a.dy_img_words + (uint32_t)(g * a.Kg + k) * (uint32_t)(a.P * a.Q) +
-                          (uint32_t)((p0 + dr) * a.Q + q0 + dq)) * 4u
-                       : kOob;
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rdy, (LDS_AS void *)&Y[i * 256], 16, off, 0,
-                                                         0, 0);
-            }
+            const int L = (wave + NWV * j) * 64 + lane;
+            y_row[j] = L / (kWhDyLd / 4);
+            y_px[j] = 4 * (L - y_row[j] * (kWhDyLd / 4));
         }
 #pragma unroll
         for (int j = 0; j < XL; j++) {
-            const int i = wave + 4 * j;
-            if (i < XNWL) {
-                const int h = p0 + a.row0 + x_row[j], w = q0 + a.col0 + 4 * x_grp[j];
-                const bool ok = x_c[j] < NCH && (unsigned)h < (unsigned)a.H && w >= 0 && w + 4 <= a.W;
-                const uint32_t off =
-                    ok ? ((uint32_t)img * a.x_img_words + (uint32_t)(g * a.Cg + c0 + x_c[j]) *
-                                                              (uint32_t)(a.H * a.W) +
-                          (uint32_t)(h * a.W + w)) * 4u
-                       : kOob;
-                float *dst = C::PERCH ? &X[i * CS] : &X[i * 256];
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (LDS_AS void *)dst, 16, off, 0, 0, 0);
+            int c, e;
+            if constexpr (WPC > 0) {
+                c = 0;
+                e = j * 64 + lane;
+            } else {
+                const int ge = (wave + NWV * j) * 64 + lane;
+                c = ge / EPC;
+                e = ge - c * EPC;
             }
-        }
-        __builtin_amdgcn_s_waitcnt(0);
-        __asm__ volatile("" ::: "memory");
-        __builtin_amdgcn_s_barrier();
-        __asm__ volatile("" ::: "memory");
-
-        // (dr, dq) of step s's pixel without the lane part.
-        auto step_dr = [](int st) {
-            const int t = st >> 1;
-            return ROWS2 ? 2 * (t / 7) : (8 * t) / TW;
-        };
-        auto step_dq = [](int st) {
-            const int t = st >> 1, e = st & 1;
-            return ROWS2 ? 4 * (t % 7) + e : (8 * t) % TW + e;
-        };
-        float av[28];
-#pragma unroll
-        for (int t = 0; t < 14; t++) {
-            const f32x2 v = lds_b64(Y, ya + step_dr(2 * t) * TW + step_dq(2 * t));
-            av[2 * t] = v.x;
-            av[2 * t + 1] = v.y;
-        }
-        if (do_bias) {
-#pragma unroll
-            for (int st = 0; st < 28; st++)
-                bsum += av[st];
-        }
-        // B words of step pair t, read one pair ahead of their MFMAs.
-        constexpr int NRD = SODD ? 3 : 2;  // two-word reads per filter row
-        f32x2 wb[2][CT][3][NRD];
-        auto load_b = [&](f32x2 (&dst)[CT][3][NRD], int t) {
-            const int dr = step_dr(2 * t), dq = step_dq(2 * t);
-#pragma unroll
-            for (int j = 0; j < CT; j++)
-#pragma unroll
-                for (int r = 0; r < 3; r++)
-#pragma unroll
-                    for (int k = 0; k < NRD; k++)
-                        dst[j][r][k] = lds_b64(X, xw + j * 16 * CS + (dr + r) * HWW + dq + 2 * k);
-        };
-        load_b(wb[0], 0);
-        // Taps innermost: the 9 CT accumulators are independent, so
-        // consecutive MFMAs never wait for each other's result.
-#pragma unroll
-        for (int t = 0; t < 14; t++) {
-            if (t + 1 < 14)
-                load_b(wb[(t + 1) & 1], t + 1);
-            const f32x2(&wc)[CT][3][NRD] = wb[t & 1];
-#pragma unroll
-            for (int e = 0; e < 2; e++)
-#pragma unroll
-                for (int j = 0; j < CT; j++)
-#pragma unroll
-                    for (int tap = 0; tap < 9; tap++) {
-                        const int r = tap / 3, i = e + tap % 3 + (SODD ? 1 : 0);  // word of the row
-                        acc[j][tap] = mfma16(av[2 * t + e], wc[j][r][i >> 1][i & 1], acc[j][tap]);
-                    }
-            __builtin_amdgcn_sched_barrier(0);
+            x_c[j] = (c < NCH && e < EPC) ? c : NCH;  // NCH: masked
+            x_row[j] = e / GPR;
+            x_col[j] = V * (e - x_row[j] * GPR);
         }
     }
 
-    // Bias gradient: the four lane groups of a filter row summed disjoint
-    // pixels; combine them in a fixed order.
-    if (do_bias) {
-        bsum += __shfl_xor(bsum, 16, 64);
-        bsum += __shfl_xor(bsum, 32, 64);
-        const int k = m0 + 16 * wave + lc;
-        if (kr == 0 && k < a.Kg)
-            a.db_part[(long long)split * a.K + g * a.Kg + k] = bsum;
-    }
-    float *outs = a.out + (long long)split * a.split_stride;
-#pragma unroll
-    for (int j = 0; j < CT; j++)
-#pragma unroll
-        for (int tap = 0; tap < 9; tap++)
-#pragma unroll
-            for (int v = 0; v < 4; v++) {
-                const int k = m0 + 16 * wave + 4 * kr + v;
-                if (k < a.Kg)
-                    outs[((long long)(g * a.Kg + k) * 9 + tap) * a.Cg + c0 + 16 * j + lc] =
-                        acc[j][tap][v];
-            }
-}
-
-// ---------------------------------------------------------------------------
-// Double-buffered halo backward-weight: eight waves (two per SIMD), 64 filters
-// x 32 channels, pixel blocks staged one ahead.  Wave w computes the nine taps
-// of filters 16 (w % 4) .. + 15 and channels 16 (w / 4) .. + 15 of the tile.
-// While the waves run the MFMAs of block b from one LDS stage, the DMA of
-// block b + 1 fills the other, so a block costs one barrier and no exposed
-// load latency.  Two stages of dy rows and x halos for 32 channels take 123-
-// 152 KiB of LDS: one workgroup a CU.  The two stages are distinct arrays
-// (blocks are taken in pairs), so the compiler's wait for in-flight DMA
-// before an LDS read only ever covers the stage being read.
-// ---------------------------------------------------------------------------
-template <int TW, bool SODD>
-__global__ __launch_bounds__(512) void wgrad_halo_db_kernel(const WgradHaloArgs a)
-{
-    typedef HaloCfg<TW> C;
-    constexpr int TR = C::TR, HWW = C::HWW, CS = C::CS;
-    constexpr int HR = TR + 2, GPR = HWW / 4, EPC = HR * GPR;
-    constexpr int NCH = 32, NWV = 8;
-    constexpr int XNWL = C::PERCH ? NCH : (NCH * EPC + 63) / 64;  // x halo wave-loads
-    constexpr int YNWL = 64 * (kWhDyLd / 4) / 64;                 // dy wave-loads (29)
-    constexpr int XW = C::PERCH ? NCH * CS : XNWL * 64 * 4;
-    constexpr int YW = 64 * kWhDyLd;
-    static_assert(C::PERCH ? CS >= 256 : CS == 4 * EPC, "channel c's halo at c CS");
-    static_assert(C::V == 4 && TR * TW == kHaloCols, "16-byte halo, 112-pixel blocks");
-    static_assert(2 * (YW + XW) * 4 <= 160 * 1024, "two stages in LDS");
-
-    __shared__ __attribute__((aligned(16))) float Y0[YW];
-    __shared__ __attribute__((aligned(16))) float X0[XW];
-    __shared__ __attribute__((aligned(16))) float Y1[YW];
-    __shared__ __attribute__((aligned(16))) float X1[XW];
-
-    const int lane = threadIdx.x & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int wm = wave & 3, wj = wave >> 2;
-    const int mtiles = (a.Kg + 63) / 64, ctiles = a.Cg / NCH;
-    const int tiles = mtiles * ctiles;
-    const int lin = xcd_tile(blockIdx.x, tiles * a.groups * a.nsplit);
-    const int split = lin / (tiles * a.groups);
-    const int rest = lin - split * tiles * a.groups;
-    const int g = rest / tiles, tile = rest - g * tiles;
-    const int mt = tile % mtiles, ct = tile / mtiles;
-    const int m0 = mt * 64, c0 = ct * NCH;
-    const int per_img = a.row_blocks * a.col_segs;
-    const int nblocks = a.nimg * per_img;
-    const int b_beg = split * a.chunk, b_end = min(nblocks, b_beg + a.chunk);
-    const int kr = lane >> 4, lc = lane & 15;
-
-    const __amdgpu_buffer_rsrc_t rdy = make_rsrc(a.dy, a.dy_bytes);
-    const __amdgpu_buffer_rsrc_t rx = make_rsrc(a.x, a.x_bytes);
-
-    // Staging lanes, as in wgrad_halo_kernel with eight waves: wave-load i
-    // of a block is issued by wave i % 8.
-    constexpr int YL = (YNWL + NWV - 1) / NWV, XL = (XNWL + NWV - 1) / NWV;
-    int y_row[YL], y_px[YL];
-#pragma unroll
-    for (int j = 0; j < YL; j++) {
-        const int L = (wave + NWV * j) * 64 + lane;
-        y_row[j] = L / (kWhDyLd / 4);
-        y_px[j] = 4 * (L - y_row[j] * (kWhDyLd / 4));
-    }
-    int x_c[XL], x_row[XL], x_grp[XL];
-#pragma unroll
-    for (int j = 0; j < XL; j++) {
-        const int i = wave + NWV * j;
-        int c, e;
-        if constexpr (C::PERCH) {
-            c = i;
-            e = lane;
-        } else {
-            const int ge = i * 64 + lane;
-            c = ge / EPC;
-            e = ge - c * EPC;
-        }
-        x_c[j] = (c < NCH && e < EPC) ? c : NCH;  // NCH: masked
-        x_row[j] = e / GPR;
-        x_grp[j] = e - x_row[j] * GPR;
+    __device__ void load_x(__amdgpu_buffer_rsrc_t rx, uint32_t off, float *dst) const
+    {
+        if constexpr (V == 4)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (LDS_AS void *)dst, 16, off, 0, 0, 0);
+        else
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (LDS_AS void *)dst, 4, off, 0, 0, 0);
     }
 
-    // DMA of pixel block b into one stage.
-    auto stage = [&](int b, float *Yd, float *Xd) {
+    // DMA of pixel block b into Yd, Xd.
+    __device__ void issue(const WgradHaloArgs &a, __amdgpu_buffer_rsrc_t rdy, __amdgpu_buffer_rsrc_t rx,
+                          int wave, int b, int g, int m0, int c0, float *Yd, float *Xd) const
+    {
+        const int per_img = a.row_blocks * a.col_segs;
         const int img = b / per_img, prem = b - img * per_img;
         const int rb = prem / a.col_segs, csg = prem - rb * a.col_segs;
         const int p0 = rb * TR, q0 = csg * TW;
@@ -1300,89 +1086,268 @@ __global__ __launch_bounds__(512) void wgrad_halo_db_kernel(const WgradHaloArgs 
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(rdy, (LDS_AS void *)&Yd[i * 256], 16, off, 0, 0, 0);
             }
         }
+        const uint32_t xim = (uint32_t)img * a.x_img_words, hw = (uint32_t)(a.H * a.W);
+        if constexpr (WPC > 0) {
+            // The lane's pixel offset and validity of each part, then one
+            // wave-load per channel and part.
+            uint32_t poff[WPC];
+            bool pok[WPC];
 #pragma unroll
-        for (int j = 0; j < XL; j++) {
-            const int i = wave + NWV * j;
-            if (i < XNWL) {
-                const int h = p0 + a.row0 + x_row[j], w = q0 + a.col0 + 4 * x_grp[j];
-                const bool ok = x_c[j] < NCH && (unsigned)h < (unsigned)a.H && w >= 0 && w + 4 <= a.W;
-                const uint32_t off =
-                    ok ? ((uint32_t)img * a.x_img_words + (uint32_t)(g * a.Cg + c0 + x_c[j]) *
-                                                              (uint32_t)(a.H * a.W) +
-                          (uint32_t)(h * a.W + w)) * 4u
-                       : kOob;
-                float *dst = C::PERCH ? &Xd[i * CS] : &Xd[i * 256];
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (LDS_AS void *)dst, 16, off, 0, 0, 0);
+            for (int j = 0; j < WPC; j++) {
+                const int h = p0 + a.row0 + x_row[j], w = q0 + a.col0 + x_col[j];
+                pok[j] = x_c[j] < NCH && (unsigned)h < (unsigned)a.H && w >= 0 && w + V <= a.W;
+                poff[j] = (uint32_t)(h * a.W + w);
+            }
+#pragma unroll
+            for (int cc = 0; cc < NCC; cc++) {
+                const int c = wave + NWV * cc;
+                if (c < NCH) {
+                    const uint32_t cb = xim + (uint32_t)(g * a.Cg + c0 + c) * hw;
+#pragma unroll
+                    for (int j = 0; j < WPC; j++)
+                        load_x(rx, pok[j] ? (cb + poff[j]) * 4u : kOob, &Xd[c * CS + j * 64 * V]);
+                }
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < XL; j++) {
+                const int i = wave + NWV * j;
+                if (i < XNWL) {
+                    const int h = p0 + a.row0 + x_row[j], w = q0 + a.col0 + x_col[j];
+                    const bool ok = x_c[j] < NCH && (unsigned)h < (unsigned)a.H && w >= 0 && w + V <= a.W;
+                    const uint32_t off =
+                        ok ? (xim + (uint32_t)(g * a.Cg + c0 + x_c[j]) * hw + (uint32_t)(h * a.W + w)) * 4u
+                           : kOob;
+                    load_x(rx, off, &Xd[i * 64 * V]);
+                }
             }
         }
-    };
+    }
+};
 
-    // Operand mapping as in wgrad_halo_kernel (pixel pairs per lane group,
-    // B words by aligned two-word reads), for this wave's filter rows and
-    // channel sub-tile.
-    constexpr bool ROWS2 = TW % 8 != 0;
-    static_assert(!ROWS2 || TW == 28, "pixel pairs");
-    static_assert(CS % 2 == 0 && HWW % 2 == 0, "even row and channel strides");
-    const int kdr = ROWS2 ? kr >> 1 : 0, kdq = ROWS2 ? 2 * (kr & 1) : 2 * kr;
-    const int ya = (16 * wm + lc) * kWhDyLd + kdr * TW + kdq;
-    const int xw = (16 * wj + lc) * CS + a.slack - (SODD ? 1 : 0) + kdr * HWW + kdq;  // even
-    auto step_dr = [](int st) {
-        const int t = st >> 1;
-        return ROWS2 ? 2 * (t / 7) : (8 * t) / TW;
+// MFMA mapping (16x16x4, reduction over pixels): 28 steps s = 2 t + e (t <
+// 14, e < 2) of 4 pixels, lane group kr taking one of them; pairs of steps
+// cover 8 pixels, lane group kr an adjacent pair of columns, so that a lane's
+// A operands of steps 2 t and 2 t + 1 (dy, filter lc of its wave's 16) are one
+// aligned two-word LDS read, and its B operands (x of channel lc, shifted by
+// the tap) for the three columns sx of filter row r are the four words
+// x0 .. x0 + 3, x0 = lc CS + slack + (lane part) + (dr + r) HWW + (the pair's
+// column), read as two aligned two-word reads when slack is even and three
+// from x0 - 1 when it is odd (SODD).  Pixel of step pair t, lane group kr:
+//   TW % 8 == 0: row-major pixel 8 t + 2 kr + e;
+//   TW == 28:    row 2 (t / 7) + kr / 2, column 4 (t % 7) + 2 (kr % 2) + e;
+//   TW == 14:    row 2 kr + t / 7, column 2 (t % 7) + e
+// (pairs never straddle a row).  The lane part goes into the bases, the (t,
+// e) part is a compile-time offset.
+template <int TW>
+struct WgHaloMap {
+    static constexpr int kdr(int kr) { return TW == 28 ? kr >> 1 : TW == 14 ? 2 * kr : 0; }
+    static constexpr int kdq(int kr) { return TW == 28 ? 2 * (kr & 1) : TW == 14 ? 0 : 2 * kr; }
+    static constexpr int dr(int t) { return TW == 28 ? 2 * (t / 7) : TW == 14 ? t / 7 : (8 * t) / TW; }
+    static constexpr int dq(int t) { return TW == 28 ? 4 * (t % 7) : TW == 14 ? 2 * (t % 7) : (8 * t) % TW; }
+    static_assert(TW % 8 == 0 || TW == 28 || TW == 14, "pixel pairs");
+};
+
+// Nine taps of 16 filters x 16 channels from one staged block: A from Yc at
+// lane offset ya, B from Xc at lane offset xw (both even), into acc[tap];
+// the A values are summed into bsum when do_bias.  mid() runs after the
+// MFMAs of step pair MIDT (a place for the next block's DMA that does not
+// compete with the first LDS reads of the block).
+struct WgNoMid {
+    __device__ void operator()() const {}
+};
+template <int TW, bool SODD, int MIDT = -1, class Mid = WgNoMid>
+__device__ __forceinline__ void wg_halo_block_mfma(const float *Yc, const float *Xc, int ya, int xw,
+                                                   f32x4 (&acc)[9], bool do_bias, float &bsum,
+                                                   const Mid &mid = Mid())
+{
+    typedef WgHaloCfg<TW> C;
+    typedef WgHaloMap<TW> M;
+    const float *yp = Yc + opaque(ya), *xp = Xc + opaque(xw);
+    float av[28];
+#pragma unroll
+    for (int t = 0; t < 14; t++) {
+        const f32x2 v = lds_b64(yp, M::dr(t) * TW + M::dq(t));
+        av[2 * t] = v.x;
+        av[2 * t + 1] = v.y;
+    }
+    if (do_bias) {
+#pragma unroll
+        for (int st = 0; st < 28; st++)
+            bsum += av[st];
+    }
+    // B words of step pair t, read one pair ahead of their MFMAs.
+    constexpr int NRD = SODD ? 3 : 2;
+    f32x2 wb[2][3][NRD];
+    auto load_b = [&](f32x2 (&dst)[3][NRD], int t) {
+#pragma unroll
+        for (int r = 0; r < 3; r++)
+#pragma unroll
+            for (int k = 0; k < NRD; k++)
+                dst[r][k] = lds_b64(xp, (M::dr(t) + r) * C::HWW + M::dq(t) + 2 * k);
     };
-    auto step_dq = [](int st) {
-        const int t = st >> 1, e = st & 1;
-        return ROWS2 ? 4 * (t % 7) + e : (8 * t) % TW + e;
-    };
+    load_b(wb[0], 0);
+    // Taps innermost: the nine accumulators are independent, so consecutive
+    // MFMAs never wait for each other's result.
+#pragma unroll
+    for (int t = 0; t < 14; t++) {
+        if (t + 1 < 14)
+            load_b(wb[(t + 1) & 1], t + 1);
+        const f32x2(&wc)[3][NRD] = wb[t & 1];
+#pragma unroll
+        for (int e = 0; e < 2; e++)
+#pragma unroll
+            for (int tap = 0; tap < 9; tap++) {
+                const int r = tap / 3, i = e + tap % 3 + (SODD ? 1 : 0);  // word of the row
+                acc[tap] = mfma16(av[2 * t + e], wc[r][i >> 1][i & 1], acc[tap]);
+            }
+        __builtin_amdgcn_sched_barrier(0);
+        if (t == MIDT) {
+            mid();
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+}
+
+// Work item of a workgroup: split, group, filter tile m0, channel tile c0
+// (NCH channels) and the split's pixel blocks [b_beg, b_end).
+struct WgHaloTile {
+    int split, g, m0, c0, b_beg, b_end;
+    __device__ WgHaloTile(const WgradHaloArgs &a, int nch)
+    {
+        const int mtiles = (a.Kg + 63) / 64, ctiles = a.Cg / nch;
+        const int tiles = mtiles * ctiles;
+        const int lin = xcd_tile(blockIdx.x, tiles * a.groups * a.nsplit);
+        split = lin / (tiles * a.groups);
+        const int rest = lin - split * tiles * a.groups;
+        g = rest / tiles;
+        const int tile = rest - g * tiles;
+        m0 = (tile % mtiles) * 64;
+        c0 = (tile / mtiles) * nch;
+        const int nblocks = a.nimg * a.row_blocks * a.col_segs;
+        b_beg = split * a.chunk;
+        b_end = min(nblocks, b_beg + a.chunk);
+    }
+};
+
+// Partial sums of a wave's nine 16 x 16 tiles (filters m0 + fk .., channels
+// c0 + fc ..) and, when do_bias, of its 16 filters' bias gradient.
+__device__ __forceinline__ void wg_halo_store(const WgradHaloArgs &a, const WgHaloTile &w, int fk, int fc,
+                                              const f32x4 (&acc)[9], bool do_bias, float bsum)
+{
+    const int lane = threadIdx.x & 63, kr = lane >> 4, lc = lane & 15;
+    if (do_bias) {
+        // The four lane groups of a filter row summed disjoint pixels;
+        // combine them in a fixed order.
+        bsum += __shfl_xor(bsum, 16, 64);
+        bsum += __shfl_xor(bsum, 32, 64);
+        const int k = w.m0 + fk + lc;
+        if (kr == 0 && k < a.Kg)
+            a.db_part[(long long)w.split * a.K + w.g * a.Kg + k] = bsum;
+    }
+    float *outs = a.out + (long long)w.split * a.split_stride;
+#pragma unroll
+    for (int tap = 0; tap < 9; tap++)
+#pragma unroll
+        for (int v = 0; v < 4; v++) {
+            const int k = w.m0 + fk + 4 * kr + v;
+            if (k < a.Kg)
+                outs[((long long)(w.g * a.Kg + k) * 9 + tap) * a.Cg + w.c0 + fc + lc] = acc[tap][v];
+        }
+}
+
+// Single-stage kernel: four waves, each the nine taps of 16 filters x the CT
+// 16-channel sub-tiles of the workgroup's 64 x 16 CT tile.  Per block: barrier,
+// DMA, wait, barrier, MFMAs.  Three workgroups fit a CU with one sub-tile, two
+// with two (which stage each block's dy once for twice the MFMAs, and read dy
+// from memory half as often over the channel tiles).
+template <int TW, int CT, bool SODD>
+__global__ __launch_bounds__(256) void wgrad_halo_kernel(const WgradHaloArgs a)
+{
+    typedef WgHaloStage<TW, 16 * CT, 4> St;
+    typedef WgHaloMap<TW> M;
+    __shared__ __attribute__((aligned(16))) float Y[St::YW];
+    __shared__ __attribute__((aligned(16))) float X[St::XW];
+
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int kr = lane >> 4, lc = lane & 15;
+    const WgHaloTile w(a, 16 * CT);
+    const __amdgpu_buffer_rsrc_t rdy = make_rsrc(a.dy, a.dy_bytes);
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(a.x, a.x_bytes);
+    St st;
+    st.init(wave, lane);
+
+    const int ya = (16 * wave + lc) * kWhDyLd + M::kdr(kr) * TW + M::kdq(kr);
+    const int xw = lc * St::CS + a.slack - (SODD ? 1 : 0) + M::kdr(kr) * St::HWW + M::kdq(kr);  // even
+
+    f32x4 acc[CT][9];
+#pragma unroll
+    for (int j = 0; j < CT; j++)
+#pragma unroll
+        for (int t = 0; t < 9; t++)
+            acc[j][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float bsum = 0.f;
+    const bool do_bias = a.db_part != nullptr && w.c0 == 0;
+
+    for (int b = w.b_beg; b < w.b_end; b++) {
+        // Every wave is done reading the previous block.
+        __builtin_amdgcn_s_barrier();
+        __asm__ volatile("" ::: "memory");
+        st.issue(a, rdy, rx, wave, b, w.g, w.m0, w.c0, Y, X);
+        __builtin_amdgcn_s_waitcnt(0);
+        __asm__ volatile("" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        __asm__ volatile("" ::: "memory");
+#pragma unroll
+        for (int j = 0; j < CT; j++)
+            wg_halo_block_mfma<TW, SODD>(Y, X + j * 16 * St::CS, ya, xw, acc[j], do_bias && j == 0, bsum);
+    }
+#pragma unroll
+    for (int j = 0; j < CT; j++)
+        wg_halo_store(a, w, 16 * wave, 16 * j, acc[j], do_bias && j == 0, bsum);
+}
+
+// Double-buffered kernel: eight waves (two per SIMD), 64 filters x 32
+// channels, pixel blocks staged one ahead.  Wave w computes the nine taps of
+// filters 16 (w % 4) .. + 15 and channels 16 (w / 4) .. + 15 of the tile.
+// While the waves run the MFMAs of block b from one LDS stage, the DMA of
+// block b + 1 fills the other, so a block costs one barrier and no exposed
+// load latency.  Two stages take 99-152 KiB of LDS: one workgroup a CU.  The
+// two stages are distinct arrays (blocks are taken in pairs), so the
+// compiler's wait for in-flight DMA before an LDS read only ever covers the
+// stage being read.
+template <int TW, bool SODD>
+__global__ __launch_bounds__(512) void wgrad_halo_db_kernel(const WgradHaloArgs a)
+{
+    typedef WgHaloStage<TW, 32, 8> St;
+    typedef WgHaloMap<TW> M;
+    static_assert(2 * (St::YW + St::XW) * 4 <= 160 * 1024, "two stages in LDS");
+    __shared__ __attribute__((aligned(16))) float Y0[St::YW];
+    __shared__ __attribute__((aligned(16))) float X0[St::XW];
+    __shared__ __attribute__((aligned(16))) float Y1[St::YW];
+    __shared__ __attribute__((aligned(16))) float X1[St::XW];
+
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wm = wave & 3, wj = wave >> 2;
+    const int kr = lane >> 4, lc = lane & 15;
+    const WgHaloTile w(a, 32);
+    const __amdgpu_buffer_rsrc_t rdy = make_rsrc(a.dy, a.dy_bytes);
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(a.x, a.x_bytes);
+    St st;
+    st.init(wave, lane);
+
+    const int ya = (16 * wm + lc) * kWhDyLd + M::kdr(kr) * TW + M::kdq(kr);
+    const int xw = (16 * wj + lc) * St::CS + a.slack - (SODD ? 1 : 0) + M::kdr(kr) * St::HWW +
+                   M::kdq(kr);  // even
 
     f32x4 acc[9];
 #pragma unroll
     for (int t = 0; t < 9; t++)
         acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
     float bsum = 0.f;
-    const bool do_bias = a.db_part != nullptr && ct == 0 && wj == 0;
-
-    // MFMAs of one staged block.
-    auto compute = [&](const float *Yc, const float *Xc) {
-        const float *yp = Yc + opaque(ya), *xp = Xc + opaque(xw);
-        float av[28];
-#pragma unroll
-        for (int t = 0; t < 14; t++) {
-            const f32x2 v = lds_b64(yp, step_dr(2 * t) * TW + step_dq(2 * t));
-            av[2 * t] = v.x;
-            av[2 * t + 1] = v.y;
-        }
-        if (do_bias) {
-#pragma unroll
-            for (int st = 0; st < 28; st++)
-                bsum += av[st];
-        }
-        constexpr int NRD = SODD ? 3 : 2;
-        f32x2 wb[2][3][NRD];
-        auto load_b = [&](f32x2 (&dst)[3][NRD], int t) {
-            const int dr = step_dr(2 * t), dq = step_dq(2 * t);
-#pragma unroll
-            for (int r = 0; r < 3; r++)
-#pragma unroll
-                for (int k = 0; k < NRD; k++)
-                    dst[r][k] = lds_b64(xp, (dr + r) * HWW + dq + 2 * k);
-        };
-        load_b(wb[0], 0);
-#pragma unroll
-        for (int t = 0; t < 14; t++) {
-            if (t + 1 < 14)
-                load_b(wb[(t + 1) & 1], t + 1);
-            const f32x2(&wc)[3][NRD] = wb[t & 1];
-#pragma unroll
-            for (int e = 0; e < 2; e++)
-#pragma unroll
-                for (int tap = 0; tap < 9; tap++) {
-                    const int r = tap / 3, i = e + tap % 3 + (SODD ? 1 : 0);
-                    acc[tap] = mfma16(av[2 * t + e], wc[r][i >> 1][i & 1], acc[tap]);
-                }
-            __builtin_amdgcn_sched_barrier(0);
-        }
-    };
+    const bool do_bias = a.db_part != nullptr && w.c0 == 0 && wj == 0;
 
     // One block: wait for this wave's DMA of it, barrier (every wave's DMA
     // has landed and every wave is done with the other stage), start the DMA
@@ -1392,37 +1357,23 @@ __global__ __launch_bounds__(512) void wgrad_halo_db_kernel(const WgradHaloArgs 
         __asm__ volatile("" ::: "memory");
         __builtin_amdgcn_s_barrier();
         __asm__ volatile("" ::: "memory");
-        if (b + 1 < b_end)
-            stage(b + 1, Yn, Xn);
-        compute(Yc, Xc);
+        auto next = [&]() {
+            if (b + 1 < w.b_end)
+                st.issue(a, rdy, rx, wave, b + 1, w.g, w.m0, w.c0, Yn, Xn);
+        };
+        wg_halo_block_mfma<TW, SODD, 3>(Yc, Xc, ya, xw, acc, do_bias, bsum, next);
     };
 
-    if (b_beg < b_end)
-        stage(b_beg, Y0, X0);
-    int b = b_beg;
-    for (; b + 1 < b_end; b += 2) {
+    if (w.b_beg < w.b_end)
+        st.issue(a, rdy, rx, wave, w.b_beg, w.g, w.m0, w.c0, Y0, X0);
+    int b = w.b_beg;
+    for (; b + 1 < w.b_end; b += 2) {
         block(b, Y0, X0, Y1, X1);
         block(b + 1, Y1, X1, Y0, X0);
     }
-    if (b < b_end)
+    if (b < w.b_end)
         block(b, Y0, X0, Y1, X1);
-
-    if (do_bias) {
-        bsum += __shfl_xor(bsum, 16, 64);
-        bsum += __shfl_xor(bsum, 32, 64);
-        const int k = m0 + 16 * wm + lc;
-        if (kr == 0 && k < a.Kg)
-            a.db_part[(long long)split * a.K + g * a.Kg + k] = bsum;
-    }
-    float *outs = a.out + (long long)split * a.split_stride;
-#pragma unroll
-    for (int tap = 0; tap < 9; tap++)
-#pragma unroll
-        for (int v = 0; v < 4; v++) {
-            const int k = m0 + 16 * wm + 4 * kr + v;
-            if (k < a.Kg)
-                outs[((long long)(g * a.Kg + k) * 9 + tap) * a.Cg + c0 + 16 * wj + lc] = acc[tap][v];
-        }
+    wg_halo_store(a, w, 16 * wm, 16 * wj, acc, do_bias, bsum);
 }
 
 // ---------------------------------------------------------------------------
@@ -1760,8 +1711,10 @@ static hipError_t halo_launch_tw(const HaloGemmArgs &a, bool flip, hipStream_t s
     }
 }
 
-bool wgrad_halo_supported(int TW, int Q, int W)
+bool wgrad_halo_supported(int TW, int P, int Q, int W)
 {
+    if (TW == 14)  // whole rows of a 14-wide map (contiguous in dy), one-word x loads
+        return Q == 14 && P % 2 == 0;
     return (TW == 112 || TW == 56 || TW == 28) && Q % 4 == 0 && W % 4 == 0;
 }
 
@@ -1774,19 +1727,22 @@ static hipError_t wgrad_halo_launch_par(const WgradHaloArgs &a, int tiles, hipSt
         switch (a.TW) {
         case 112: hipLaunchKernelGGL((wgrad_halo_db_kernel<112, SODD>), grid, block8, 0, stream, a); break;
         case 56: hipLaunchKernelGGL((wgrad_halo_db_kernel<56, SODD>), grid, block8, 0, stream, a); break;
-        default: hipLaunchKernelGGL((wgrad_halo_db_kernel<28, SODD>), grid, block8, 0, stream, a); break;
+        case 28: hipLaunchKernelGGL((wgrad_halo_db_kernel<28, SODD>), grid, block8, 0, stream, a); break;
+        default: hipLaunchKernelGGL((wgrad_halo_db_kernel<14, false>), grid, block8, 0, stream, a); break;
         }
     } else if (a.CT == 2) {
         switch (a.TW) {
         case 112: hipLaunchKernelGGL((wgrad_halo_kernel<112, 2, SODD>), grid, block, 0, stream, a); break;
         case 56: hipLaunchKernelGGL((wgrad_halo_kernel<56, 2, SODD>), grid, block, 0, stream, a); break;
-        default: hipLaunchKernelGGL((wgrad_halo_kernel<28, 2, SODD>), grid, block, 0, stream, a); break;
+        case 28: hipLaunchKernelGGL((wgrad_halo_kernel<28, 2, SODD>), grid, block, 0, stream, a); break;
+        default: hipLaunchKernelGGL((wgrad_halo_kernel<14, 2, false>), grid, block, 0, stream, a); break;
         }
     } else {
         switch (a.TW) {
         case 112: hipLaunchKernelGGL((wgrad_halo_kernel<112, 1, SODD>), grid, block, 0, stream, a); break;
         case 56: hipLaunchKernelGGL((wgrad_halo_kernel<56, 1, SODD>), grid, block, 0, stream, a); break;
-        default: hipLaunchKernelGGL((wgrad_halo_kernel<28, 1, SODD>), grid, block, 0, stream, a); break;
+        case 28: hipLaunchKernelGGL((wgrad_halo_kernel<28, 1, SODD>), grid, block, 0, stream, a); break;
+        default: hipLaunchKernelGGL((wgrad_halo_kernel<14, 1, false>), grid, block, 0, stream, a); break;
         }
     }
     return hipGetLastError();
@@ -1794,7 +1750,9 @@ static hipError_t wgrad_halo_launch_par(const WgradHaloArgs &a, int tiles, hipSt
 
 hipError_t launch_wgrad_halo(const WgradHaloArgs &a, hipStream_t stream)
 {
-    if (!wgrad_halo_supported(a.TW, a.Q, a.W) || a.col0 % 4)
+    // col0: the x halo's first column relative to q0, -pad for one-word
+    // loads, rounded down to a multiple of 4 for 16-byte ones.
+    if (!wgrad_halo_supported(a.TW, a.P, a.Q, a.W) || (a.TW == 14 ? a.slack != 0 : a.col0 % 4 != 0))
         return hipErrorInvalidValue;
     if ((a.CT != 1 && a.CT != 2) || a.Cg % (16 * a.CT) || a.slack < 0 || a.slack > 3 ||
         (a.db && a.CT != 2))

@@ -174,7 +174,7 @@ struct WgradHaloArgs {
     long long split_stride;   // K * Cg * 9
     float *db_part;           // [split][K], or null
 };
-bool wgrad_halo_supported(int TW, int Q, int W);
+bool wgrad_halo_supported(int TW, int P, int Q, int W);
 hipError_t launch_wgrad_halo(const WgradHaloArgs &a, hipStream_t stream);
 
 // Image-GEMM tile shapes (BM x BN; 4 waves, 3 for 48x64).

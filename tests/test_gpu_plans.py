@@ -41,6 +41,9 @@ PLAN_SHAPES = [
     (2, 32, 6, 28, 80, 3, 3, 1, 1, 1),
     (1, 16, 4, 8, 16, 3, 3, 1, 3, 1),
     (2, 64, 6, 12, 48, 3, 3, 1, 1, 2),     # two 16-channel sub-tiles a workgroup, groups
+    (2, 32, 14, 14, 80, 3, 3, 1, 1, 1),    # 14-wide maps: whole-row blocks, one-word x loads
+    (2, 16, 12, 16, 32, 3, 3, 1, 0, 1),    # 14 wide by pad 0, 10 rows
+    (1, 32, 8, 12, 32, 3, 3, 1, 2, 1),     # 14 wide by pad 2
 ]
 
 
