@@ -904,28 +904,34 @@ __global__ __launch_bounds__(64 * WM * WN) void wgrad_kernel(const WgradArgs a)
                 bsum += v.w;
             }
         }
-        float4 af[FM][PB / 4], bf[FN][PB / 4];
+        // MFMA step (u, e) of lane group kr takes pixel 8 u + 2 kr + e of the
+        // slice: a lane's operands of steps (u, 0), (u, 1) are one aligned
+        // ds_read_b64, and with 68-word rows the 32 lanes of a pass (16 rows
+        // x lane groups 0, 1) hit all 64 banks.  (Sixteen consecutive pixels
+        // a lane group read as ds_read_b128 cost bank conflicts.)
+        static_assert(PB == 16 && LDR % 64 == 4, "pixel pairs over 68-word rows");
+        f32x2 af[FM][PB / 2], bf[FN][PB / 2];
 #pragma unroll
         for (int i = 0; i < FM; i++) {
-            const float *rowp = &L[(wm * TM + i * MF + lc) * LDR + kr * PB];
+            const float *rowp = &L[(wm * TM + i * MF + lc) * LDR + 2 * kr];
 #pragma unroll
-            for (int u = 0; u < PB / 4; u++)
-                af[i][u] = *(const float4 *)&rowp[4 * u];
+            for (int u = 0; u < PB / 2; u++)
+                af[i][u] = lds_b64(rowp, 8 * u);
         }
 #pragma unroll
         for (int j = 0; j < FN; j++) {
-            const float *rowp = &L[(BM + wn * TN + j * MF + lc) * LDR + kr * PB];
+            const float *rowp = &L[(BM + wn * TN + j * MF + lc) * LDR + 2 * kr];
 #pragma unroll
-            for (int u = 0; u < PB / 4; u++)
-                bf[j][u] = *(const float4 *)&rowp[4 * u];
+            for (int u = 0; u < PB / 2; u++)
+                bf[j][u] = lds_b64(rowp, 8 * u);
         }
         __syncthreads();  // every wave holds its operands: the tile is free
         if (t + 1 < nslices)
             issue(kbeg + (t + 1) * BK);
 #pragma unroll
-        for (int u = 0; u < PB / 4; u++)
+        for (int u = 0; u < PB / 2; u++)
 #pragma unroll
-            for (int e = 0; e < 4; e++)
+            for (int e = 0; e < 2; e++)
 #pragma unroll
                 for (int i = 0; i < FM; i++)
 #pragma unroll
