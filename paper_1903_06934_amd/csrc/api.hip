@@ -353,20 +353,22 @@ bool same_img(const ImgPlan &a, const ImgPlan &b)
 }
 
 // ------------------------------------------------------------ halo plans
-// Stride-1 3 x 3 layers with channel-aligned slices can run the halo GEMM
-// (halo_gemm_kernel): 112-column tiles that are TR x TW pixel blocks, the
-// source region of a 16-channel block staged once for all nine taps.  The
-// block width is the one of 56, 112, 28, 14 (in that order of preference:
-// 56 x 2 blocks stage the least halo per pixel of the 16-byte ones and
-// measured fastest wherever they fit, by 1-2 %) that pads the output grid
-// (P x Q) least; 0 if none can stage this source (16-byte loads need a
-// source width that is a multiple of 4).
-int halo_width(int P, int Q, int src_w)
+// Stride-1 3 x 3 and 5 x 5 layers with channel-aligned slices can run the
+// halo GEMM (halo_gemm_kernel): 112-column tiles that are TR x TW pixel
+// blocks, the source region of a 16-channel block staged once for all R R
+// taps.  The block width is the one of 56, 112, 28, 14 (3 x 3, in that order
+// of preference: 56 x 2 blocks stage the least halo per pixel of the 16-byte
+// ones and measured fastest wherever they fit, by 1-2 %) or of 28, 14 (5 x 5)
+// that pads the output grid (P x Q) least; 0 if none can stage this source
+// (16-byte loads need a source width that is a multiple of 4).
+bool halo_filter(const Geom &g) { return g.st == 1 && g.R == g.S && (g.R == 3 || g.R == 5); }
+
+int halo_width(int P, int Q, int src_w, int R)
 {
     int best = 0;
     long long best_cols = 0;
     for (int tw : {56, 112, 28, 14}) {
-        if (!halo_width_supported(tw, src_w, 0))
+        if (!halo_width_supported(tw, R, src_w, 0))
             continue;
         const int tr = kHaloCols / tw;
         const long long cols = (long long)((P + tr - 1) / tr) * ((Q + tw - 1) / tw) * kHaloCols;
@@ -409,29 +411,29 @@ ImgPlan halo_plan(int tile, int tw, long long tiles, int ncb, int ns)
 // channels (a multiple of 16), an nimg x P x Q output grid and a src_w-wide
 // source: each pixel-block width that pads the grid no more than the best
 // one, each tile that fits M, unsplit and (allow_split) split.
-std::vector<int> halo_widths(int P, int Q, int src_w)
+std::vector<int> halo_widths(int P, int Q, int src_w, int R)
 {
     std::vector<int> out;
-    const int best = halo_width(P, Q, src_w);
+    const int best = halo_width(P, Q, src_w, R);
     auto blocks = [&](int tw) {
         const int tr = kHaloCols / tw;
         return (long long)((P + tr - 1) / tr) * ((Q + tw - 1) / tw);
     };
     if (best)
         for (int tw : {112, 56, 28, 14})
-            if (halo_width_supported(tw, src_w, 0) && blocks(tw) == blocks(best))
+            if (halo_width_supported(tw, R, src_w, 0) && blocks(tw) == blocks(best))
                 out.push_back(tw);
     return out;
 }
 
 template <class P, class Make>
-void halo_variants(int M, int cin, int nimg, int Pout, int Qout, int src_w, int G,
+void halo_variants(int M, int cin, int nimg, int Pout, int Qout, int src_w, int R, int G,
                    bool allow_split, Make make, std::vector<P> &out)
 {
     if (cin % 16)
         return;
     const int ncb = cin / 16;
-    for (int tw : halo_widths(Pout, Qout, src_w))
+    for (int tw : halo_widths(Pout, Qout, src_w, R))
     for (int tile : {HALO_128x112, HALO_64x112}) {
         if (tile == HALO_128x112 && M <= 64)
             continue;
@@ -458,9 +460,18 @@ const char *halo_tile_name(int tile) { return tile == HALO_128x112 ? "128x112" :
 // MI355X at the configurations' batches: VGG-16 conv1_2 ... conv5_3 forward
 // and backward-data 112-143 TFLOP/s against 93-126 for the image GEMM;
 // ResNet 56 x 56 / 14 x 14 3 x 3 layers 124 / 108 against 92-104 / 86.
-bool halo_rule(int cin, int Pout, int Qout, int src_w, ImgPlan *out)
+// 5 x 5 layers take it with M >= 48 (at most one idle wave) when the tiles,
+// split over channel blocks as halo_plan does if they are fewer than three
+// workgroups a CU, give every CU one: AlexNet conv2 forward 130 TFLOP/s
+// against 120 for the image GEMM and backward-data 106 against 104,
+// GoogLeNet's 14 x 14 5 x 5 with 128 filters forward 87 against 64 and
+// backward-data 60 (two splits) against 52; its 64-filter and 32-filter
+// 5 x 5 layers (128 tiles, two channel blocks; M = 32) measured slower than
+// the image GEMM and keep it.
+bool halo_rule(int M, int cin, int nimg, int Pout, int Qout, int src_w, int R, int G,
+               ImgPlan *out)
 {
-    const int tw = halo_width(Pout, Qout, src_w);
+    const int tw = halo_width(Pout, Qout, src_w, R);
     if (!tw || cin % 16)
         return false;
     const int tr = kHaloCols / tw;
@@ -468,6 +479,14 @@ bool halo_rule(int cin, int Pout, int Qout, int src_w, ImgPlan *out)
                         ((double)((Pout + tr - 1) / tr) * ((Qout + tw - 1) / tw) * kHaloCols);
     if (used < 0.875)
         return false;
+    if (R == 5) {
+        const long long tiles = halo_tile_count(HALO_64x112, M, nimg, Pout, Qout, tw, G);
+        const ImgPlan p = halo_plan(HALO_64x112, tw, tiles, cin / 16, 0);
+        if (M < 48 || tiles * p.nsplit < num_cus())
+            return false;
+        *out = p;
+        return true;
+    }
     *out = halo_plan(HALO_64x112, tw, 0, cin / 16, 1);
     return true;
 }
@@ -614,9 +633,9 @@ ImgPlan fwd_rule(const Geom &g)
         return p;
     }
     ImgPlan h;
-    if (g.st == 1 && g.R == 3 && g.S == 3 && halo_rule(g.Cg, g.P, g.Q, g.W, &h))
-        return h;
     const int nb = images_per_launch(g);
+    if (halo_filter(g) && halo_rule(g.Kg, g.Cg, g.N < nb ? g.N : nb, g.P, g.Q, g.W, g.R, g.G, &h))
+        return h;
     return img_rule(g.Kg, (long long)(g.N < nb ? g.N : nb) * g.P * g.Q, g.Cg * g.R * g.S, g.G,
                     nb >= g.N);
 }
@@ -637,8 +656,8 @@ void fwd_candidates(const Geom &g, std::vector<ImgPlan> &out)
     const int nb = images_per_launch(g);
     img_variants<ImgPlan>(g.Kg, (long long)(g.N < nb ? g.N : nb) * g.P * g.Q, g.Cg * g.R * g.S,
                           g.G, nb >= g.N, [](const ImgPlan &p) { return p; }, out);
-    if (g.st == 1 && g.R == 3 && g.S == 3 && !is_inner_product(g))
-        halo_variants<ImgPlan>(g.Kg, g.Cg, g.N < nb ? g.N : nb, g.P, g.Q, g.W, g.G, nb >= g.N,
+    if (halo_filter(g))
+        halo_variants<ImgPlan>(g.Kg, g.Cg, g.N < nb ? g.N : nb, g.P, g.Q, g.W, g.R, g.G, nb >= g.N,
                                [](const ImgPlan &p) { return p; }, out);
     // Explicit: im2col, then the 1x1 GEMM with its own rule's tile.
     if (const int xnb = explicit_images(g)) {
@@ -803,7 +822,7 @@ BwdPlan bwd_rule(const Geom &g)
         const int kred = g.Kg * p.bp.ntr * p.bp.nts;
         p.img = with_split(pick_img_tile(p.bp.M, (long long)n0 * p.bp.nh * p.bp.nw, kred, g.G),
                            kred, 1);
-    } else if (g.st == 1 && g.R == 3 && g.S == 3 && halo_rule(g.Kg, g.H, g.W, g.Q, &p.img)) {
+    } else if (halo_filter(g) && halo_rule(g.Cg, g.Kg, n0, g.H, g.W, g.Q, g.R, g.G, &p.img)) {
         // The one phase as a halo GEMM.
     } else if (g.st == 1) {
         // Split-K only for stride 1 (one phase covering all of dx).
@@ -834,9 +853,9 @@ void bwd_candidates(const Geom &g, std::vector<BwdPlan> &out)
     img_variants<BwdPlan>(g.Cg, (long long)n0 * g.H * g.W / (g.st * g.st), kred_max, g.G,
                           g.st == 1 && nb >= g.N,
                           [](const ImgPlan &i) { return BwdPlan{false, BlockPlan{}, i, 0}; }, out);
-    // Stride 1, 3 x 3: the one phase as a halo GEMM over dx's pixel grid.
-    if (g.st == 1 && g.R == 3 && g.S == 3 && !is_inner_product(g))
-        halo_variants<BwdPlan>(g.Cg, g.Kg, n0, g.H, g.W, g.Q, g.G, nb >= g.N,
+    // Stride 1, 3 x 3 or 5 x 5: the one phase as a halo GEMM over dx's pixel grid.
+    if (halo_filter(g))
+        halo_variants<BwdPlan>(g.Cg, g.Kg, n0, g.H, g.W, g.Q, g.R, g.G, nb >= g.N,
                                [](const ImgPlan &i) { return BwdPlan{false, BlockPlan{}, i, 0}; },
                                out);
     // Blocked, for few channels per group.
@@ -1334,14 +1353,14 @@ hipError_t mark(hipEvent_t ev, hipStream_t stream)
     return ev ? hipEventRecord(ev, stream) : hipSuccess;
 }
 
-// One halo GEMM launch (plan.halo >= 0) of a stride-1 3 x 3 problem: M rows
+// One halo GEMM launch (plan.halo >= 0) of a stride-1 R x R problem: M rows
 // of the packed bank A (a_ld words each, FAST order over cin source channels),
 // source images src (src_c channels of src_h x src_w), output grid Pout x Qout
 // of out (out_c channels per image), nimg images; (coff_h, coff_w) is the
 // source coordinate of tap (0, 0) of output pixel (0, 0), flip for the
 // backward-data phase (source row p + coff_h - r).  Split partial slabs go to
 // part, split_stride apart.
-int halo_gemm(const ImgPlan &plan, int M, int groups, const float *A, int a_ld, int cin,
+int halo_gemm(const ImgPlan &plan, int M, int groups, const float *A, int a_ld, int cin, int R,
               const float *src, int src_c, int src_h, int src_w, int Pout, int Qout, int out_c,
               int nimg, int coff_h, int coff_w, bool flip, const float *bias, float *out,
               float *part, long long split_stride, hipStream_t stream)
@@ -1349,7 +1368,8 @@ int halo_gemm(const ImgPlan &plan, int M, int groups, const float *A, int a_ld, 
     const size_t fb = sizeof(float);
     HaloGemmArgs h{};
     h.M = M;
-    h.Kred = cin * 9;
+    h.R = R;
+    h.Kred = cin * R * R;
     h.groups = groups;
     h.A = A;
     h.a_ld = a_ld;
@@ -1369,9 +1389,9 @@ int halo_gemm(const ImgPlan &plan, int M, int groups, const float *A, int a_ld, 
     h.col_segs = (Qout + h.TW - 1) / h.TW;
     h.nimg = nimg;
     // Halo origin: the top-left source pixel any tap of the block reads.
-    const int V = plan.tw == 14 ? 1 : 4;
-    h.row0 = flip ? coff_h - 2 : coff_h;
-    const int col_raw = flip ? coff_w - 2 : coff_w;
+    const int V = halo_load_words(plan.tw, R);
+    h.row0 = flip ? coff_h - (R - 1) : coff_h;
+    const int col_raw = flip ? coff_w - (R - 1) : coff_w;
     h.col0 = (col_raw >= 0 ? col_raw / V : -((-col_raw + V - 1) / V)) * V;
     h.slack = col_raw - h.col0;
     h.out = plan.nsplit > 1 ? part : out;
@@ -1425,7 +1445,7 @@ int fwd_gemms(const Geom &g, const ImgPlan &plan, const float *wp, const float *
     for (int n0 = 0; n0 < n_images; n0 += nb) {
         const int n = n_images - n0 < nb ? n_images - n0 : nb;
         if (plan.halo >= 0) {
-            int st = halo_gemm(plan, g.Kg, g.G, wp, a_ld, g.Cg, src + n0 * xi, g.C, g.H, g.W, g.P,
+            int st = halo_gemm(plan, g.Kg, g.G, wp, a_ld, g.Cg, g.R, src + n0 * xi, g.C, g.H, g.W, g.P,
                                g.Q, g.K, n, -g.pad, -g.pad, false, b, y + n0 * yi, part,
                                (long long)n_images * yi, stream);
             if (st != MICONV_OK)
@@ -1773,7 +1793,7 @@ int phase_gemms(const Geom &g, const BwdPlan &plan, const float *w, char *&wsp, 
             for (int n0 = 0; n0 < n_images; n0 += nb) {
                 const int n = n_images - n0 < nb ? n_images - n0 : nb;
                 if (plan.img.halo >= 0) {  // stride 1: the one phase, flipped taps
-                    int st = halo_gemm(plan.img, g.Cg, group, wr, a_ld, g.Kg, dy + n0 * yi, K,
+                    int st = halo_gemm(plan.img, g.Cg, group, wr, a_ld, g.Kg, g.R, dy + n0 * yi, K,
                                        g.P, g.Q, H, W, g.C, n, ah.d, aw.d, true, nullptr,
                                        dx + n0 * xi, part, (long long)n_images * xi, stream);
                     if (st != MICONV_OK)

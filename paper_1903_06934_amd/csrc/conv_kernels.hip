@@ -495,77 +495,106 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
 }
 
 // ---------------------------------------------------------------------------
-// Halo-staged implicit GEMM for stride-1 3 x 3 layers (see HaloGemmArgs).
+// Halo-staged implicit GEMM for stride-1 R x R layers, R = 3 or 5 (see
+// HaloGemmArgs).
 //
 // A tile is BM filter rows x 112 columns, the columns being a TR x TW block of
 // output pixels of one image.  The gathered operand of a 16-channel block is
-// the same image region for all nine taps, shifted: it is staged once per
-// block (the halo, V words per lane and load, direct to LDS) and the nine
-// slices of the block read their B operands from it at per-tap offsets.  That
-// divides the staging-load lanes per MFMA by 5 to 6 (by 20 with 16-byte
-// loads) against the per-slice gather of img_gemm_kernel, whose load-issue
-// rate (one dword per lane) is what bounds it.
+// the same image region for all R R taps, shifted: it is staged once per
+// block (the halo, V words per lane and load, direct to LDS) and the R R
+// slices of the block read their B operands from it at per-tap offsets.  For
+// 3 x 3 that divides the staging-load lanes per MFMA by 5 to 6 (by 20 with
+// 16-byte loads) against the per-slice gather of img_gemm_kernel, whose
+// load-issue rate (one dword per lane) is what bounds it; for 5 x 5 by 15 or
+// more, even with one-word loads.
 //
 // The pixel block is fixed per instantiation (HaloCfg): TW = 112, 56, 28 or 14
-// columns (the map widths of the 3 x 3 layers at 224 ... 14 pixels) by
-// TR = 112 / TW rows, so every LDS offset of a tap is a compile-time constant
-// and the B reads need no address arithmetic.  LDS layout of a block:
-// halo[c][i][j] at c cs + i hw_w + j, either dense (the wave-loads fill
-// consecutive words, cs = hr hw_w) or one wave-load per channel (cs padded);
-// cs is chosen so that the four MFMA lane groups, which read channels 4 apart,
-// fall on different LDS banks.
+// columns (the map widths of the 3 x 3 layers at 224 ... 14 pixels; 28 or 14
+// for 5 x 5, whose maps of 27 or 28 and 14 pixels fit them) by TR = 112 / TW
+// rows, so every LDS offset of a tap is a compile-time constant and the B
+// reads need no address arithmetic.  LDS layout of a block: halo[c][i][j] at
+// c CS + i HWW + j, either dense (the wave-loads fill consecutive words,
+// CS = HR HWW) or LPC whole wave-loads per channel in a padded slot of CS
+// words; CS is chosen so that the four MFMA lane groups, which read channels 4
+// apart, fall on different LDS banks.  5 x 5 blocks use one-word loads, so any
+// map width can be staged (AlexNet's 27-wide maps included).
 //
 // Four waves split the rows (BM / 4 each, FM = BM / 64 accumulator blocks
-// high) and each covers all 112 columns (7 blocks of 16).  The filter
+// high) and each covers all 112 columns (7 blocks of 16); in 5 x 5 tiles a
+// wave whose rows all lie past M (M = 48 on the 64-row tile) stages its share
+// of the halo and skips the MFMAs.  The filter
 // operand of a slice is one 16-byte load per lane and row block, straight
-// into registers, issued two slices ahead into a ring of 3 register sets.
-// The halo has two LDS stages: the next block's loads are issued at the start
-// of a block and complete under its nine slices; one barrier per block.
+// into registers, issued two slices ahead into a ring of NR register sets
+// (NR = 3, or 5 for 5 x 5: NR divides R R, so slice t always sits in set
+// t mod NR).  The halo has two LDS stages: the next block's loads are issued
+// at the start of a block and complete under its R R slices; one barrier per
+// block.
 // ---------------------------------------------------------------------------
-template <int TW>
+template <int TW, int R>
 struct HaloCfg;
 template <>
-struct HaloCfg<112> {
-    static constexpr int TR = 1, V = 4, HWW = 124, PERCH = 0, CS = 3 * 124;
+struct HaloCfg<112, 3> {
+    static constexpr int TR = 1, V = 4, HWW = 124, LPC = 0, CS = 3 * 124;
 };
 template <>
-struct HaloCfg<56> {
-    static constexpr int TR = 2, V = 4, HWW = 64, PERCH = 1, CS = 260;
+struct HaloCfg<56, 3> {
+    static constexpr int TR = 2, V = 4, HWW = 64, LPC = 1, CS = 260;
 };
 template <>
-struct HaloCfg<28> {
-    static constexpr int TR = 4, V = 4, HWW = 36, PERCH = 1, CS = 260;
+struct HaloCfg<28, 3> {
+    static constexpr int TR = 4, V = 4, HWW = 36, LPC = 1, CS = 260;
 };
 template <>
-struct HaloCfg<14> {
-    static constexpr int TR = 8, V = 1, HWW = 18, PERCH = 0, CS = 10 * 18;
+struct HaloCfg<14, 3> {
+    static constexpr int TR = 8, V = 1, HWW = 18, LPC = 0, CS = 10 * 18;
+};
+template <>
+struct HaloCfg<28, 5> {  // 8 x 32 words a channel: four wave-loads
+    static constexpr int TR = 4, V = 1, HWW = 32, LPC = 4, CS = 260;
+};
+template <>
+struct HaloCfg<14, 5> {  // 12 x 18 words a channel in four wave-loads
+    static constexpr int TR = 8, V = 1, HWW = 18, LPC = 4, CS = 260;
 };
 
 constexpr int kHaloStageWords = 6400;  // per stage (25 KiB): two stages, three workgroups a CU
 
-template <int BM, int TW, bool FLIP>
-__global__ __launch_bounds__(256) void halo_gemm_kernel(const HaloGemmArgs a)
+// Waves per SIMD the register allocation must allow: three for 3 x 3 tiles
+// (which the LDS of three workgroups a CU also allows), four for 64-row 5 x 5
+// ones (four workgroups a CU); 128-row 5 x 5 tiles fit three without the
+// bound.
+template <int BM, int R>
+constexpr int halo_min_waves() { return R == 3 ? 3 : BM == 64 ? 4 : 1; }
+
+template <int BM, int TW, int R, bool FLIP>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(halo_min_waves<BM, R>())))
+void halo_gemm_kernel(const HaloGemmArgs a)
 {
-    typedef HaloCfg<TW> C;
-    constexpr int R = 3, S = 3, RS = 9, NR = 3;
+    typedef HaloCfg<TW, R> C;
+    constexpr int S = R, RS = R * S, NR = RS % 3 == 0 ? 3 : 5, DIST = 2;
     constexpr int NW = 4, BN = kHaloCols, TM = BM / NW, FM = TM / 16, FN = BN / 16;
-    constexpr int TR = C::TR, V = C::V, HWW = C::HWW, CS = C::CS;
+    constexpr int TR = C::TR, V = C::V, HWW = C::HWW, CS = C::CS, LPC = C::LPC;
     constexpr int HR = TR + R - 1;
     constexpr int GPR = HWW / V;                  // load groups per halo row
     constexpr int EPC = HR * GPR;                 // load groups per channel
-    // Dense: wave-loads over 16 EPC groups; per channel: EPC <= 64, one each.
-    constexpr int NWL = C::PERCH ? 16 : (16 * EPC + 63) / 64;
+    // Dense: wave-loads over 16 EPC groups; per channel: LPC each.
+    constexpr int NWL = LPC ? 16 * LPC : (16 * EPC + 63) / 64;
     constexpr int LPW = (NWL + NW - 1) / NW;      // wave-loads per wave and block
-    constexpr int SPARE = C::PERCH ? 16 * CS : NWL * 64 * V;  // slot of padding loads
+    constexpr int SPARE = LPC ? 16 * CS : NWL * 64 * V;  // slot of padding loads
+    // Words per LDS stage: 3 x 3 blocks take the common 25 KiB (three
+    // workgroups a CU); 5 x 5 ones only what they use (17 KiB: four).
+    constexpr int STG = R == 3 ? kHaloStageWords : SPARE + 64 * V;
+    static_assert(RS % NR == 0, "filter ring");
+    static_assert(BM == 64 || BM == 128, "tile rows");
     static_assert(TR * TW == BN, "pixel block");
     static_assert(HWW % V == 0 && HWW >= TW + S - 1, "halo row");
-    // One wave-load per channel writes all 64 lanes (masked lanes write
-    // zeros), so a channel's slot must hold 64 V words.
-    static_assert(C::PERCH ? (EPC <= 64 && CS >= 64 * V && (CS * 4) % 16 == 0)
-                           : CS == HR * HWW, "channel stride");
-    static_assert(SPARE + 64 * V <= kHaloStageWords, "halo stage");
+    // A wave-load writes all 64 lanes (masked lanes write zeros), so a
+    // channel's slot must hold LPC 64 V words.
+    static_assert(LPC ? (EPC <= 64 * LPC && CS >= 64 * V * LPC && (CS * 4) % 16 == 0)
+                      : CS == HR * HWW, "channel stride");
+    static_assert(SPARE + 64 * V <= STG && STG <= kHaloStageWords && STG % 4 == 0, "halo stage");
 
-    __shared__ __attribute__((aligned(16))) float H0[kHaloStageWords], H1[kHaloStageWords];
+    __shared__ __attribute__((aligned(16))) float H0[STG], H1[STG];
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -586,14 +615,18 @@ __global__ __launch_bounds__(256) void halo_gemm_kernel(const HaloGemmArgs a)
     const int cb_beg = split * a.cbchunk;
     const int cb_end = min(ncb, cb_beg + a.cbchunk);
     const int kr = lane >> 4, lc = lane & 15;
+    // Wave-uniform: some row of this wave is real (checked for 5 x 5 only,
+    // whose M = 48 backward-data phases leave a 64-row tile's last wave idle).
+    const int wrow = wave;  // the wave's row block of the tile
+    const bool live = R == 3 || m0 + wrow * TM < a.M;
 
-    // Filter operand: row m = m0 + wave * TM + 16 i + lc, reduction words
+    // Filter operand: row m = m0 + wrow * TM + 16 i + lc, reduction words
     // 16 t + 4 kr .. + 3 of slice t; rows past M read zero.
     const __amdgpu_buffer_rsrc_t rA = make_rsrc(a.A, a.a_bytes);
     uint32_t a_off[FM];
 #pragma unroll
     for (int i = 0; i < FM; i++) {
-        const int m = m0 + wave * TM + i * 16 + lc;
+        const int m = m0 + wrow * TM + i * 16 + lc;
         a_off[i] = (((uint32_t)(g * a.M + (m < a.M ? m : 0)) * (uint32_t)a.a_ld + 4u * kr) * 4u) |
                    oob_mask(m < a.M);
     }
@@ -608,22 +641,27 @@ __global__ __launch_bounds__(256) void halo_gemm_kernel(const HaloGemmArgs a)
     };
 
     // Halo staging.  Wave-load i = wave + 4 j carries, per lane, load group
-    // e of channel c (dense: e + EPC c = 64 i + lane; per channel: c = i,
-    // e = lane) into LDS word c CS + V e (dense: 64 V i + V lane) of a stage.
+    // e of channel c (dense: e + EPC c = 64 i + lane; per channel: c = i / LPC,
+    // e = 64 (i mod LPC) + lane) into LDS word c CS + V e (dense: 64 V i +
+    // V lane) of a stage.
     // Group e = row * GPR + grp is source pixel (p0 + row0 + row,
     // q0 + col0 + V grp) .. + V - 1 of channel 16 cb + c, zero outside the
     // source (with V = 4 the source width and col0, q0 are multiples of 4, so
     // a group lies inside or outside a row).  Loads past the last wave-load
     // go to a spare slot and read zero.
+    // With as many wave-loads per channel as waves (LPC = NW), wave w loads
+    // part w of every channel, wave-load j being channel j: one lane offset
+    // then serves all of them, plus j channel strides.
+    constexpr bool PARTS = LPC == NW;
     const __amdgpu_buffer_rsrc_t rB = make_rsrc(a.src, a.src_bytes);
-    uint32_t h_off[LPW];
+    uint32_t h_off[PARTS ? 1 : LPW];
 #pragma unroll
-    for (int j = 0; j < LPW; j++) {
+    for (int j = 0; j < (PARTS ? 1 : LPW); j++) {
         const int i = wave + NW * j;
         int c, e;
-        if constexpr (C::PERCH) {
-            c = i;
-            e = lane;
+        if constexpr (LPC) {
+            c = i / LPC;
+            e = (i % LPC) * 64 + lane;
         } else {
             const int ge = i * 64 + lane;
             c = ge / EPC;
@@ -638,13 +676,17 @@ __global__ __launch_bounds__(256) void halo_gemm_kernel(const HaloGemmArgs a)
                          (uint32_t)(h * a.src_w + w)) * 4u
                       : kOob;
     }
-    const uint32_t cb_bytes = 16u * (uint32_t)a.src_hw * 4u;
+    const uint32_t ch_bytes = (uint32_t)a.src_hw * 4u, cb_bytes = 16u * ch_bytes;
     auto issue_halo = [&](int cb, float *Hd) {
 #pragma unroll
         for (int j = 0; j < LPW; j++) {
             const int i = wave + NW * j;
-            float *dst = Hd + (i >= NWL ? SPARE : C::PERCH ? i * CS : i * 64 * V);
-            const uint32_t off = h_off[j] == kOob ? kOob : h_off[j] + (uint32_t)cb * cb_bytes;
+            float *dst = Hd + (i >= NWL ? SPARE
+                               : LPC ? (i / LPC) * CS + (i % LPC) * 64 * V
+                                     : i * 64 * V);
+            const uint32_t h = h_off[PARTS ? 0 : j];
+            const uint32_t off =
+                h == kOob ? kOob : h + (uint32_t)cb * cb_bytes + (PARTS ? (uint32_t)j * ch_bytes : 0u);
             if constexpr (V == 4)
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(rB, (LDS_AS void *)dst, 16, off, 0, 0, 0);
             else
@@ -656,7 +698,8 @@ __global__ __launch_bounds__(256) void halo_gemm_kernel(const HaloGemmArgs a)
     // the block; for channel 4 kr + s4 and tap (rr, ss) its halo word is
     // bofs[j] + s4 CS + rr HWW + ss, with bofs[j] = 4 kr CS + dr HWW + dq + slack
     // (a compile-time offset from a per-lane base).  Columns outside the
-    // output read word 0 and are not stored.
+    // output read word 0 and are not stored (reading their own halo words
+    // instead measured 8 % slower on AlexNet conv2's backward-data phase).
     int bofs[FN];
     bool nok[FN];
 #pragma unroll
@@ -675,38 +718,56 @@ __global__ __launch_bounds__(256) void halo_gemm_kernel(const HaloGemmArgs a)
             acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     f32x4 ring[NR][FM];
-    auto block = [&](int cb, const float *Hc, float *Hn, bool stage_next) {
+    auto block = [&](int cb, const float *Hc, float *Hn, bool stage_next) __attribute__((always_inline)) {
         // The other stage is free (every wave passed the barrier after
         // reading it): stage the next block into it.
         if (stage_next)
             issue_halo(cb + 1, Hn);
         __asm__ volatile("" ::: "memory");
-#pragma unroll
-        for (int tap = 0; tap < RS; tap++) {
+        if (!live) {
+            // Only this wave's halo loads are outstanding.
+            __builtin_amdgcn_s_waitcnt(0);
+            __asm__ volatile("" ::: "memory");
+            __builtin_amdgcn_s_barrier();
+            __asm__ volatile("" ::: "memory");
+            return;
+        }
+        // MFMA step u = 4 tap + s4 takes channels 4 kr + s4 of the tap.  Its
+        // FN B values are read one step ahead, into bq[u & 1] while the MFMAs
+        // of step u - 1 run, so a step's MFMAs wait only for reads issued a
+        // whole step earlier (at most 2 FN reads in flight); the scheduling
+        // barriers keep the compiler from sinking each read onto its MFMA.
+        constexpr int NSTEP = 4 * RS;
+        float bq[2][FN];
+        auto readB = [&](int u, float (&dst)[FN]) __attribute__((always_inline)) {
+            const int tap = u >> 2, s4 = u & 3;
             const int r = tap / S, sx = tap % S;
-            const int toff = (FLIP ? R - 1 - r : r) * HWW + (FLIP ? S - 1 - sx : sx);
-            loadA(cb * RS + tap + 2, ring[(tap + 2) % NR]);
-            float bf[4][FN];
+            const int toff = (FLIP ? R - 1 - r : r) * HWW + (FLIP ? S - 1 - sx : sx) + s4 * CS;
 #pragma unroll
-            for (int s4 = 0; s4 < 4; s4++)
+            for (int j = 0; j < FN; j++)
+                dst[j] = Hc[bofs[j] + toff];
+        };
+        readB(0, bq[0]);
+#pragma unroll
+        for (int u = 0; u < NSTEP; u++) {
+            const int tap = u >> 2, s4 = u & 3;
+            if (s4 == 0)
+                loadA(cb * RS + tap + DIST, ring[(tap + DIST) % NR]);
+            if (u + 1 < NSTEP)
+                readB(u + 1, bq[(u + 1) & 1]);
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int i = 0; i < FM; i++)
 #pragma unroll
                 for (int j = 0; j < FN; j++)
-                    bf[s4][j] = Hc[bofs[j] + s4 * CS + toff];
-#pragma unroll
-            for (int s4 = 0; s4 < 4; s4++)
-#pragma unroll
-                for (int i = 0; i < FM; i++)
-#pragma unroll
-                    for (int j = 0; j < FN; j++)
-                        acc[i][j] = mfma16(ring[tap % NR][i][s4], bf[s4][j], acc[i][j]);
-            // Keep each tap's LDS reads with its MFMAs: hoisting later taps'
-            // reads would hold their operands in registers meanwhile.
+                    acc[i][j] = mfma16(ring[tap % NR][i][s4], bq[u & 1][j], acc[i][j]);
             __builtin_amdgcn_sched_barrier(0);
         }
-        // The next block's halo has landed once at most the two filter loads
-        // issued last (the next block's first two slices) are outstanding.
+        // The next block's halo has landed once at most the DIST filter loads
+        // issued last (the next block's first DIST slices) are outstanding.
         __asm__ volatile("" ::: "memory");
-        __builtin_amdgcn_s_waitcnt((2 * FM & 15) | (((2 * FM) >> 4) << 14) | (7 << 4) | (15 << 8));
+        __builtin_amdgcn_s_waitcnt((DIST * FM & 15) | (((DIST * FM) >> 4) << 14) | (7 << 4) |
+                                   (15 << 8));
         __asm__ volatile("" ::: "memory");
         __builtin_amdgcn_s_barrier();
         __asm__ volatile("" ::: "memory");
@@ -714,8 +775,9 @@ __global__ __launch_bounds__(256) void halo_gemm_kernel(const HaloGemmArgs a)
 
     if (cb_beg < cb_end) {
         issue_halo(cb_beg, H0);
-        loadA(cb_beg * RS, ring[0]);
-        loadA(cb_beg * RS + 1, ring[1]);
+#pragma unroll
+        for (int d = 0; d < DIST; d++)
+            loadA(cb_beg * RS + d, ring[d]);
         __builtin_amdgcn_s_waitcnt(0);
         __asm__ volatile("" ::: "memory");
         __builtin_amdgcn_s_barrier();
@@ -736,7 +798,7 @@ __global__ __launch_bounds__(256) void halo_gemm_kernel(const HaloGemmArgs a)
     for (int i = 0; i < FM; i++)
 #pragma unroll
         for (int v = 0; v < 4; v++) {
-            const int m = m0 + wave * TM + i * 16 + acc_row(v, lane);
+            const int m = m0 + wrow * TM + i * 16 + acc_row(v, lane);
             if (m >= a.M)
                 continue;
             const int oc = g * a.M + m;
@@ -1693,26 +1755,32 @@ hipError_t launch_img_gemm(const ImgGemmArgs &a, int tile, bool fast, hipStream_
     }
 }
 
-template <int BM, int TW>
+template <int BM, int TW, int R>
 static hipError_t halo_launch(const HaloGemmArgs &a, bool flip, hipStream_t stream)
 {
     const int tiles = ((a.M + BM - 1) / BM) * a.nimg * a.row_blocks * a.col_segs;
-    dim3 grid(tiles * a.groups * a.nsplit);
+    const dim3 grid(tiles * a.groups * a.nsplit), block(256);
     if (flip)
-        hipLaunchKernelGGL((halo_gemm_kernel<BM, TW, true>), grid, dim3(256), 0, stream, a);
+        hipLaunchKernelGGL((halo_gemm_kernel<BM, TW, R, true>), grid, block, 0, stream, a);
     else
-        hipLaunchKernelGGL((halo_gemm_kernel<BM, TW, false>), grid, dim3(256), 0, stream, a);
+        hipLaunchKernelGGL((halo_gemm_kernel<BM, TW, R, false>), grid, block, 0, stream, a);
     return hipGetLastError();
 }
 
 template <int BM>
 static hipError_t halo_launch_tw(const HaloGemmArgs &a, bool flip, hipStream_t stream)
 {
+    if (a.R == 5)
+        switch (a.TW) {
+        case 28: return halo_launch<BM, 28, 5>(a, flip, stream);
+        case 14: return halo_launch<BM, 14, 5>(a, flip, stream);
+        default: return hipErrorInvalidValue;
+        }
     switch (a.TW) {
-    case 112: return halo_launch<BM, 112>(a, flip, stream);
-    case 56: return halo_launch<BM, 56>(a, flip, stream);
-    case 28: return halo_launch<BM, 28>(a, flip, stream);
-    case 14: return halo_launch<BM, 14>(a, flip, stream);
+    case 112: return halo_launch<BM, 112, 3>(a, flip, stream);
+    case 56: return halo_launch<BM, 56, 3>(a, flip, stream);
+    case 28: return halo_launch<BM, 28, 3>(a, flip, stream);
+    case 14: return halo_launch<BM, 14, 3>(a, flip, stream);
     default: return hipErrorInvalidValue;
     }
 }
@@ -1768,8 +1836,14 @@ hipError_t launch_wgrad_halo(const WgradHaloArgs &a, hipStream_t stream)
                          : wgrad_halo_launch_par<false>(a, tiles, stream);
 }
 
-bool halo_width_supported(int TW, int src_w, int col0)
+int halo_load_words(int TW, int R) { return R == 3 && TW != 14 ? 4 : 1; }
+
+bool halo_width_supported(int TW, int R, int src_w, int col0)
 {
+    if (R == 5)
+        return TW == 28 || TW == 14;  // one-word loads
+    if (R != 3)
+        return false;
     if (TW == 14)
         return true;  // one-word loads
     return (TW == 112 || TW == 56 || TW == 28) && src_w % 4 == 0 && col0 % 4 == 0;
@@ -1779,7 +1853,10 @@ int halo_rows(int TW) { return kHaloCols / TW; }
 
 hipError_t launch_halo_gemm(const HaloGemmArgs &a, int tile, bool flip, hipStream_t stream)
 {
-    if (!halo_width_supported(a.TW, a.src_w, a.col0) || a.TR != halo_rows(a.TW))
+    // slack (the first tap's column in the halo row) must lie within one
+    // load group: the halo rows hold slack + TW + R - 1 words.
+    if (!halo_width_supported(a.TW, a.R, a.src_w, a.col0) || a.TR != halo_rows(a.TW) ||
+        a.Kred != a.cin * a.R * a.R || a.slack < 0 || a.slack >= halo_load_words(a.TW, a.R))
         return hipErrorInvalidValue;
     return tile == HALO_128x112 ? halo_launch_tw<128>(a, flip, stream)
                                 : halo_launch_tw<64>(a, flip, stream);

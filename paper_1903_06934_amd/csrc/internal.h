@@ -79,25 +79,26 @@ struct ImgGemmArgs {
 };
 
 // ---------------------------------------------------------------------------
-// Halo-staged implicit GEMM for stride-1 3 x 3 layers with channel-aligned
-// slices (the forward pass, or the single stride phase of a stride-1
-// backward-data pass).  Same GEMM as ImgGemmArgs with cstep = 1, but the
-// columns of a tile are a TR x TW block of output pixels of one image (rows
-// p0 .. p0 + TR - 1, columns q0 .. q0 + TW - 1; column n of the tile is
-// (n / TW, n % TW)), TW one of 112, 56, 28, 14 and TR = 112 / TW, and for
-// each 16-channel block the source region all nine taps of the block need
-// (the halo) is staged in LDS once:
+// Halo-staged implicit GEMM for stride-1 R x R layers (R = 3 or 5) with
+// channel-aligned slices (the forward pass, or the single stride phase of a
+// stride-1 backward-data pass).  Same GEMM as ImgGemmArgs with cstep = 1, but
+// the columns of a tile are a TR x TW block of output pixels of one image
+// (rows p0 .. p0 + TR - 1, columns q0 .. q0 + TW - 1; column n of the tile is
+// (n / TW, n % TW)), TW one of 112, 56, 28, 14 (R = 3) or 28, 14 (R = 5) and
+// TR = 112 / TW, and for each 16-channel block the source region all R R taps
+// of the block need (the halo) is staged in LDS once:
 //   halo[c][i][j] = src[img][g * cin + 16 cb + c][p0 + row0 + i][q0 + col0 + j]
 //                   (0 outside the source),
-// loaded 4 words per lane (TW >= 28: needs col0 and the source width to be
-// multiples of 4) or 1 (TW = 14).  Tap (r, s) of pixel (dr, dq) reads
-// halo[c][dr + rr][dq + slack + ss] with (rr, ss) = (r, s), or (2 - r, 2 - s)
-// for the backward-data phase (flip; its source rows are p + coff_h - r).
-// The reduction order is the channel-block-major one of the packed filter:
-// k = (cb * 9 + tap) * 16 + ci.
+// loaded 4 words per lane (R = 3, TW >= 28: needs col0 and the source width
+// to be multiples of 4) or 1 (R = 3, TW = 14, and R = 5).  Tap (r, s) of
+// pixel (dr, dq) reads halo[c][dr + rr][dq + slack + ss] with (rr, ss) =
+// (r, s), or (R - 1 - r, R - 1 - s) for the backward-data phase (flip; its
+// source rows are p + coff_h - r).  The reduction order is the
+// channel-block-major one of the packed filter: k = (cb * R R + tap) * 16 + ci.
 // ---------------------------------------------------------------------------
 struct HaloGemmArgs {
     int M, Kred, groups;
+    int R;                     // filter rows = columns: 3 or 5
     const float *A;
     int a_ld;
     uint32_t a_bytes;
@@ -196,11 +197,14 @@ inline bool wgrad_tile_is_tap(int tile) { return tile <= WG_TAP_64x16 || tile >=
 
 hipError_t launch_img_gemm(const ImgGemmArgs &a, int tile, bool fast, hipStream_t stream);
 // Halo tiles: BM rows (64 or 128) x 112 columns; flip for the backward-data
-// phase.  halo_width_supported: whether TW (112, 56, 28, 14) can stage this
-// source (16-byte loads need the width and col0 to be multiples of 4).
+// phase.  halo_width_supported: whether pixel blocks TW wide (112, 56, 28, 14
+// for R = 3; 28, 14 for R = 5) can stage this source (16-byte loads need the
+// width and col0 to be multiples of 4); halo_load_words: the words per lane
+// and load (4 or 1).
 enum HaloTile { HALO_64x112 = 0, HALO_128x112 };
 constexpr int kHaloCols = 112;
-bool halo_width_supported(int TW, int src_w, int col0);
+bool halo_width_supported(int TW, int R, int src_w, int col0);
+int halo_load_words(int TW, int R);
 hipError_t launch_halo_gemm(const HaloGemmArgs &a, int tile, bool flip, hipStream_t stream);
 hipError_t launch_wgrad_gemm(const WgradArgs &a, int tile, hipStream_t stream);
 

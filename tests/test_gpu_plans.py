@@ -36,6 +36,15 @@ PLAN_SHAPES = [
     (2, 16, 9, 12, 16, 3, 3, 1, 2, 1),     # pad 2
     (2, 16, 8, 12, 16, 3, 3, 1, 0, 1),     # pad 0
     (1, 256, 6, 6, 128, 3, 3, 1, 1, 1),    # few tiles, 16 channel blocks: split
+    # Halo GEMM of 5x5 layers (one-word loads, 28- and 14-wide blocks): a
+    # 27-wide map with groups and 48 channels per group (the backward-data
+    # phase's 48 rows leave the 64-row tile's last wave idle), padding 0, 1
+    # and 3, 14-wide maps.  The first two shapes above are 5x5 too.
+    (2, 96, 27, 27, 128, 5, 5, 1, 2, 2),
+    (2, 16, 10, 30, 32, 5, 5, 1, 1, 1),
+    (1, 32, 9, 18, 16, 5, 5, 1, 0, 1),
+    (1, 16, 7, 7, 32, 5, 5, 1, 3, 1),
+    (2, 48, 14, 14, 128, 5, 5, 1, 2, 1),
     # Halo backward-weight (stride-1 3x3, dy and x rows multiples of 4 wide):
     # filters not a multiple of 64, pad 3.
     (2, 32, 6, 28, 80, 3, 3, 1, 1, 1),

@@ -42,7 +42,9 @@ def test_rule_names_for_alexnet():
     by = {L.name: L.shape for L in layers}
     assert m.plan_name(m.PASS_BWD_DATA, by["conv1"], 0) == \
         "blocked 4x4 pixels (f=1), image GEMM 48x64"
-    assert m.plan_name(m.PASS_BWD_DATA, by["conv2"], 0) == "stride phases, image GEMM 48x64"
+    assert m.plan_name(m.PASS_BWD_DATA, by["conv2"], 0) == \
+        "stride phases, halo GEMM 64x112 (28x4 pixels)"
+    assert m.plan_name(m.PASS_FWD, by["conv2"], 0) == "halo GEMM 64x112 (28x4 pixels)"
     assert m.plan_name(m.PASS_FWD, by["conv1"], 0) == "image GEMM 96x128"
     assert m.plan_name(m.PASS_BWD_WEIGHT, by["conv2"], 0).startswith("tap 64x48, ")
     assert m.plan_name(m.PASS_BWD_WEIGHT, by["conv1"], 0).startswith("pixel 96x64, ")
