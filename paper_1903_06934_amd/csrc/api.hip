@@ -946,7 +946,7 @@ struct WgradPlan {
     int halo_tw = 0;  // halo backward-weight with this pixel-block width (0: no); chunk then
                       // counts pixel blocks
     int halo_ct = 1;  // its 16-channel sub-tiles per workgroup (1 or 2)
-    int halo_db = 0;  // 1: the double-buffered eight-wave kernel (halo_ct 2)
+    int halo_db = 0;  // halo_ct 2: 1 the double-buffered eight-wave kernel, 2 single-stage eight waves
 };
 
 bool is_tap_tile(int tile) { return wgrad_tile_is_tap(tile); }
@@ -1081,8 +1081,9 @@ int wgrad_halo_width(const Geom &g)
 }
 
 // Splits over the pixel blocks so that as many workgroups run as fit on the
-// CUs at once (three per CU with one 16-channel sub-tile, two with two),
-// times 2^scale, each split at least 4 blocks.
+// CUs at once (three per CU with one 16-channel sub-tile, two with two or
+// with eight single-stage waves, one double-buffered), times 2^scale, each
+// split at least 4 blocks.
 WgradPlan wgrad_halo_plan(const Geom &g, int tw, int scale = 0, int ct = 1, int db = 0)
 {
     WgradPlan p{};
@@ -1095,7 +1096,7 @@ WgradPlan wgrad_halo_plan(const Geom &g, int tw, int scale = 0, int ct = 1, int 
     const int tr = kHaloCols / tw;
     const long long blocks = (long long)g.N * ((g.P + tr - 1) / tr) * ((g.Q + tw - 1) / tw);
     const long long tiles = (long long)((g.Kg + 63) / 64) * (g.Cg / (16 * ct)) * g.G;
-    const long long resident = (db ? 1LL : ct == 1 ? 3LL : 2LL) * num_cus();
+    const long long resident = (db == 1 ? 1LL : ct == 1 ? 3LL : 2LL) * num_cus();
     long long ns = (resident + tiles - 1) / tiles;
     if (scale > 0)
         ns <<= scale;
@@ -1115,13 +1116,15 @@ WgradPlan wgrad_halo_plan(const Geom &g, int tw, int scale = 0, int ct = 1, int 
 
 WgradPlan wgrad_rule(const Geom &g)
 {
-    // Where the channels allow, the double-buffered eight-wave kernel (64 x
-    // 32 tiles): on VGG-16 at batch 32 2-6 % faster than the single-stage
-    // 64 x 32 one on conv1_2 ... conv2_2 and even on conv3_x, conv4_x, itself
-    // 2-4 % faster than 64 x 16; on the 14 x 14 layers of ResNet-50 and
-    // GoogLeNet 3-5 % faster than the best tap tile.
+    // Where the channels allow, 64 x 32 tiles over eight waves: on maps of 112
+    // rows or more the double-buffered kernel (VGG-16 at batch 32: conv1_2 ...
+    // conv2_2 2-6 % faster than the four-wave single-stage 64 x 32 one, itself
+    // 2-4 % faster than 64 x 16), on smaller ones the single-stage one with
+    // two workgroups a CU (conv3_1 ... conv5_x 3-4 % faster than the
+    // double-buffered one; ResNet-50's 56 x 56 and 28 x 28 3 x 3 layers 1-7 %).
     if (const int tw = wgrad_halo_width(g))
-        return g.Cg % 32 == 0 ? wgrad_halo_plan(g, tw, 0, 2, 1) : wgrad_halo_plan(g, tw);
+        return g.Cg % 32 == 0 ? wgrad_halo_plan(g, tw, 0, 2, g.P >= 112 ? 1 : 2)
+                              : wgrad_halo_plan(g, tw);
     if (!is_inner_product(g))
         return wgrad_plan(g);
     // With a batch of whole 16-row slices, the image GEMM over the batch
@@ -1199,8 +1202,9 @@ void wgrad_candidates(const Geom &g, std::vector<WgradPlan> &out)
             const int tr = kHaloCols / tw;
             return (long long)((g.P + tr - 1) / tr) * ((g.Q + tw - 1) / tw);
         };
-        for (int kind : {0, 1, 2}) {  // 16 channels; 32; 32 double-buffered
-            const int ct = kind ? 2 : 1, db = kind == 2;
+        // 16 channels; 32; 32 double-buffered; 32 over eight single-stage waves
+        for (int kind : {0, 1, 2, 3}) {
+            const int ct = kind ? 2 : 1, db = kind == 2 ? 1 : kind == 3 ? 2 : 0;
             for (int tw : {112, 56, 28, 14})
                 if (g.Cg % (16 * ct) == 0 && wgrad_halo_supported(tw, g.P, g.Q, g.W) &&
                     blocks(tw) == blocks(best))
@@ -1233,7 +1237,8 @@ void wgrad_name(const WgradPlan &p, char *buf, size_t len)
         snprintf(buf, len, "batch-transposed, image GEMM %s over the batch", img_tile_name(p.img));
     else if (p.halo_tw)
         snprintf(buf, len, "halo, 9 taps of 64x%d%s (%dx%d pixels), %d splits of %d blocks",
-                 16 * p.halo_ct, p.halo_db ? " (8 waves, 2 stages)" : "", p.halo_tw,
+                 16 * p.halo_ct, p.halo_db == 1 ? " (8 waves, 2 stages)" : p.halo_db ? " (8 waves)" : "",
+                 p.halo_tw,
                  kHaloCols / p.halo_tw, p.nsplit, p.chunk);
     else if (p.xnb > 0)
         snprintf(buf, len, "explicit im2col (%d images a chunk), %s, %d splits of %d pixels",

@@ -560,17 +560,17 @@ struct HaloCfg<14, 5> {  // 12 x 18 words a channel in four wave-loads
 constexpr int kHaloStageWords = 6400;  // largest stage (25 KiB, 112-wide blocks): three workgroups a CU
 
 // Waves per SIMD the register allocation must allow: four for 64-row tiles
-// (four workgroups a CU, where the LDS stages allow: all but 112-wide
-// blocks), three for 128-row 3 x 3 ones; 128-row 5 x 5 tiles fit three
+// (four workgroups a CU) whose LDS stages allow it (all but 112-wide 3 x 3
+// blocks), three for the rest of 3 x 3; 128-row 5 x 5 tiles fit three
 // without the bound.  The waves are latency-bound (each issues an MFMA only
 // every few slots), so a SIMD's throughput grows with its waves: four
 // workgroups instead of three measured 1-3 % faster on VGG-16's 224- to
 // 28-pixel layers.
-template <int BM, int R>
-constexpr int halo_min_waves() { return BM == 64 ? 4 : R == 3 ? 3 : 1; }
+template <int BM, int TW, int R>
+constexpr int halo_min_waves() { return BM == 64 && (TW != 112 || R != 3) ? 4 : R == 3 ? 3 : 1; }
 
 template <int BM, int TW, int R, bool FLIP>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(halo_min_waves<BM, R>())))
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(halo_min_waves<BM, TW, R>())))
 void halo_gemm_kernel(const HaloGemmArgs a)
 {
     typedef HaloCfg<TW, R> C;
@@ -1328,21 +1328,26 @@ __device__ __forceinline__ void wg_halo_store(const WgradHaloArgs &a, const WgHa
         }
 }
 
-// Single-stage kernel: four waves, each the nine taps of 16 filters x the CT
-// 16-channel sub-tiles of the workgroup's 64 x 16 CT tile.  Per block: barrier,
-// DMA, wait, barrier, MFMAs.  Three workgroups fit a CU with one sub-tile, two
-// with two (which stage each block's dy once for twice the MFMAs, and read dy
-// from memory half as often over the channel tiles).
-template <int TW, int CT, bool SODD>
-__global__ __launch_bounds__(256) void wgrad_halo_kernel(const WgradHaloArgs a)
+// Single-stage kernel: NW = 4 waves, each the nine taps of 16 filters x the
+// CT 16-channel sub-tiles of the workgroup's 64 x 16 CT tile, or NW = 8 waves
+// (CT = 2), each one sub-tile.  Per block: barrier, DMA, wait, barrier, MFMAs.
+// Three four-wave workgroups fit a CU with one sub-tile, two with two (which
+// stage each block's dy once for twice the MFMAs, and read dy from memory
+// half as often over the channel tiles); two eight-wave ones, four waves a
+// SIMD, each workgroup's DMA wait covered by the other's MFMAs.
+template <int TW, int CT, bool SODD, int NW = 4>
+__global__ __launch_bounds__(NW * 64) void wgrad_halo_kernel(const WgradHaloArgs a)
 {
-    typedef WgHaloStage<TW, 16 * CT, 4> St;
+    typedef WgHaloStage<TW, 16 * CT, NW> St;
     typedef WgHaloMap<TW> M;
+    constexpr int CTW = CT * 4 / NW;  // sub-tiles of a wave
+    static_assert(NW == 4 || (NW == 8 && CT == 2), "four waves, or eight over two sub-tiles");
     __shared__ __attribute__((aligned(16))) float Y[St::YW];
     __shared__ __attribute__((aligned(16))) float X[St::XW];
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wm = wave & 3, wj = wave >> 2;  // filters 16 wm .., sub-tiles wj CTW ..
     const int kr = lane >> 4, lc = lane & 15;
     const WgHaloTile w(a, 16 * CT);
     const __amdgpu_buffer_rsrc_t rdy = make_rsrc(a.dy, a.dy_bytes);
@@ -1350,17 +1355,18 @@ __global__ __launch_bounds__(256) void wgrad_halo_kernel(const WgradHaloArgs a)
     St st;
     st.init(wave, lane);
 
-    const int ya = (16 * wave + lc) * kWhDyLd + M::kdr(kr) * TW + M::kdq(kr);
-    const int xw = lc * St::CS + a.slack - (SODD ? 1 : 0) + M::kdr(kr) * St::HWW + M::kdq(kr);  // even
+    const int ya = (16 * wm + lc) * kWhDyLd + M::kdr(kr) * TW + M::kdq(kr);
+    const int xw = (16 * wj * CTW + lc) * St::CS + a.slack - (SODD ? 1 : 0) + M::kdr(kr) * St::HWW +
+                   M::kdq(kr);  // even
 
-    f32x4 acc[CT][9];
+    f32x4 acc[CTW][9];
 #pragma unroll
-    for (int j = 0; j < CT; j++)
+    for (int j = 0; j < CTW; j++)
 #pragma unroll
         for (int t = 0; t < 9; t++)
             acc[j][t] = f32x4{0.f, 0.f, 0.f, 0.f};
     float bsum = 0.f;
-    const bool do_bias = a.db_part != nullptr && w.c0 == 0;
+    const bool do_bias = a.db_part != nullptr && w.c0 == 0 && wj == 0;
 
     for (int b = w.b_beg; b < w.b_end; b++) {
         // Every wave is done reading the previous block.
@@ -1372,12 +1378,12 @@ __global__ __launch_bounds__(256) void wgrad_halo_kernel(const WgradHaloArgs a)
         __builtin_amdgcn_s_barrier();
         __asm__ volatile("" ::: "memory");
 #pragma unroll
-        for (int j = 0; j < CT; j++)
+        for (int j = 0; j < CTW; j++)
             wg_halo_block_mfma<TW, SODD>(Y, X + j * 16 * St::CS, ya, xw, acc[j], do_bias && j == 0, bsum);
     }
 #pragma unroll
-    for (int j = 0; j < CT; j++)
-        wg_halo_store(a, w, 16 * wave, 16 * j, acc[j], do_bias && j == 0, bsum);
+    for (int j = 0; j < CTW; j++)
+        wg_halo_store(a, w, 16 * wm, 16 * (wj * CTW + j), acc[j], do_bias && j == 0, bsum);
 }
 
 // Double-buffered kernel: eight waves (two per SIMD), 64 filters x 32
@@ -1799,9 +1805,15 @@ bool wgrad_halo_supported(int TW, int P, int Q, int W)
 template <bool SODD>
 static hipError_t wgrad_halo_launch_par(const WgradHaloArgs &a, int tiles, hipStream_t stream)
 {
-    const dim3 grid(tiles), block(256);
-    if (a.db) {
-        const dim3 block8(512);
+    const dim3 grid(tiles), block(256), block8(512);
+    if (a.db == 2) {
+        switch (a.TW) {
+        case 112: hipLaunchKernelGGL((wgrad_halo_kernel<112, 2, SODD, 8>), grid, block8, 0, stream, a); break;
+        case 56: hipLaunchKernelGGL((wgrad_halo_kernel<56, 2, SODD, 8>), grid, block8, 0, stream, a); break;
+        case 28: hipLaunchKernelGGL((wgrad_halo_kernel<28, 2, SODD, 8>), grid, block8, 0, stream, a); break;
+        default: hipLaunchKernelGGL((wgrad_halo_kernel<14, 2, false, 8>), grid, block8, 0, stream, a); break;
+        }
+    } else if (a.db) {
         switch (a.TW) {
         case 112: hipLaunchKernelGGL((wgrad_halo_db_kernel<112, SODD>), grid, block8, 0, stream, a); break;
         case 56: hipLaunchKernelGGL((wgrad_halo_db_kernel<56, SODD>), grid, block8, 0, stream, a); break;
@@ -1833,7 +1845,7 @@ hipError_t launch_wgrad_halo(const WgradHaloArgs &a, hipStream_t stream)
     if (!wgrad_halo_supported(a.TW, a.P, a.Q, a.W) || (a.TW == 14 ? a.slack != 0 : a.col0 % 4 != 0))
         return hipErrorInvalidValue;
     if ((a.CT != 1 && a.CT != 2) || a.Cg % (16 * a.CT) || a.slack < 0 || a.slack > 3 ||
-        (a.db && a.CT != 2))
+        a.db < 0 || a.db > 2 || (a.db && a.CT != 2))
         return hipErrorInvalidValue;
     const int tiles = ((a.Kg + 63) / 64) * (a.Cg / (16 * a.CT)) * a.groups * a.nsplit;
     return (a.slack & 1) ? wgrad_halo_launch_par<true>(a, tiles, stream)

@@ -168,7 +168,7 @@ struct WgradHaloArgs {
     uint32_t dy_img_words, x_img_words;
     int H, W, P, Q;
     int TW, CT, row_blocks, col_segs, nimg;  // CT: 16-channel sub-tiles per workgroup (1, 2)
-    int db;                   // 1: eight waves, two LDS stages (CT = 2)
+    int db;                   // CT = 2 only: 1 eight waves, two LDS stages; 2 eight waves, one stage
     int row0, col0, slack;    // x halo origin relative to (p0, q0); slack: first tap column
     int chunk, nsplit;        // pixel blocks per split
     float *out;               // [split][K][9][Cg]
