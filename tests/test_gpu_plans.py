@@ -45,6 +45,9 @@ PLAN_SHAPES = [
     (1, 32, 9, 18, 16, 5, 5, 1, 0, 1),
     (1, 16, 7, 7, 32, 5, 5, 1, 3, 1),
     (2, 48, 14, 14, 128, 5, 5, 1, 2, 1),
+    # Split reductions of 2^18 elements or more (their 16-byte form): dw of
+    # 128 x 256 x 9 over split pixels, split-K y of 8 x 128 x 256.
+    (8, 256, 16, 16, 128, 3, 3, 1, 1, 1),
     # Halo backward-weight (stride-1 3x3, dy and x rows multiples of 4 wide):
     # filters not a multiple of 64, pad 3.
     (2, 32, 6, 28, 80, 3, 3, 1, 1, 1),
