@@ -59,6 +59,32 @@ PLAN_SHAPES = [
 ]
 
 
+def _random_halo_shapes(count=8, seed=20261202):
+    """Seeded stride-1 3x3 and 5x5 shapes with channels per group a multiple
+    of 16 (so the halo GEMM is a candidate of forward and backward-data, and
+    for 3x3 the halo backward-weight where the rows allow): random maps 5-40
+    pixels a side, pads 0..R, one or two groups, filters per group 16-96."""
+    rng = np.random.default_rng(seed)
+    out = []
+    while len(out) < count:
+        R = int(rng.choice([3, 5]))
+        G = int(rng.choice([1, 2]))
+        N = int(rng.integers(1, 4))
+        C = G * 16 * int(rng.integers(1, 4))
+        K = G * int(rng.choice([16, 32, 48, 64, 80, 96]))
+        H, W = int(rng.integers(5, 41)), int(rng.integers(5, 41))
+        pad = int(rng.integers(0, R + 1))
+        if H + 2 * pad < R or W + 2 * pad < R:
+            continue
+        out.append((N, C, H, W, K, R, R, 1, pad, G))
+    return out
+
+
+@pytest.mark.parametrize("shape", _random_halo_shapes(), ids=lambda s: "x".join(map(str, s)))
+def test_random_halo_shapes_every_candidate(shape):
+    test_every_candidate_matches_oracle(shape)
+
+
 @pytest.fixture(autouse=True)
 def _clean():
     import paper_1903_06934_amd as m
