@@ -609,7 +609,13 @@ void halo_gemm_kernel(const HaloGemmArgs a)
     const int split = lin / (tiles * a.groups);
     const int rest = lin - split * tiles * a.groups;
     const int g = rest / tiles, tile = rest - g * tiles;
-    const int mt = tile % mtiles, pt = tile / mtiles;
+    // Pixel blocks fastest: an XCD's range of tiles is then one or two
+    // filter-row tiles over many pixel blocks, so the filter rows it re-reads
+    // stay in its L2 (filter-row tiles fastest made every XCD stream the
+    // whole bank, 9.4 MB for VGG-16's 512-channel layers, past its 4 MB L2:
+    // 0.3-2.8 % slower).
+    const int ptiles = a.nimg * per_img;
+    const int pt = tile % ptiles, mt = tile / ptiles;
     const int img = pt / per_img;
     const int prem = pt - img * per_img;
     const int rb = prem / a.col_segs, csg = prem - rb * a.col_segs;
