@@ -310,7 +310,12 @@ struct ImgPlan {
     bool bt = false;           // inner product: batch-transposed plan
     int halo = -1;             // halo GEMM tile (HaloTile), or -1; kchunk then counts
     int tw = 0;                // 16-channel blocks per split, tw the pixel-block width
+    int th = 0;                // pixel-block rows: 0 for 112 / tw, else a whole th x tw map
 };
+
+// Rows and columns (pixels rounded up to 16) of a halo pixel block.
+int halo_th(int tw, int th) { return th ? th : kHaloCols / tw; }
+int halo_cols(int tw, int th) { return th ? (tw * th + 15) / 16 * 16 : kHaloCols; }
 
 // Splits for `tiles` workgroups over Kred rows: about 8 workgroups per CU,
 // each split at least kSplitRows rows and 8 slices; 1 if that is under two.
@@ -349,7 +354,7 @@ ImgPlan img_rule(int M, long long Ncol, int Kred, int G, bool allow_split)
 bool same_img(const ImgPlan &a, const ImgPlan &b)
 {
     return a.tile == b.tile && a.nsplit == b.nsplit && a.xnb == b.xnb && a.bt == b.bt &&
-           a.halo == b.halo && a.tw == b.tw;
+           a.halo == b.halo && a.tw == b.tw && a.th == b.th;
 }
 
 // ------------------------------------------------------------ halo plans
@@ -368,7 +373,7 @@ int halo_width(int P, int Q, int src_w, int R)
     int best = 0;
     long long best_cols = 0;
     for (int tw : {56, 112, 28, 14}) {
-        if (!halo_width_supported(tw, R, src_w, 0))
+        if (!halo_block_supported(tw, kHaloCols / tw, R, src_w, 0))
             continue;
         const int tr = kHaloCols / tw;
         const long long cols = (long long)((P + tr - 1) / tr) * ((Q + tw - 1) / tw) * kHaloCols;
@@ -380,16 +385,16 @@ int halo_width(int P, int Q, int src_w, int R)
     return best;
 }
 
-long long halo_tile_count(int tile, int M, int nimg, int P, int Q, int tw, int G)
+long long halo_tile_count(int tile, int M, int nimg, int P, int Q, int tw, int G, int th = 0)
 {
-    const int bm = tile == HALO_128x112 ? 128 : 64, tr = kHaloCols / tw;
+    const int bm = tile == HALO_128x112 ? 128 : 64, tr = halo_th(tw, th);
     return (long long)((M + bm - 1) / bm) * nimg * ((P + tr - 1) / tr) * ((Q + tw - 1) / tw) * G;
 }
 
 // A halo plan over ncb channel blocks: unsplit (ns = 1), or split so that
 // about three workgroups per CU run (each split at least 4 blocks) when ns
 // is 0, or into ns splits.
-ImgPlan halo_plan(int tile, int tw, long long tiles, int ncb, int ns)
+ImgPlan halo_plan(int tile, int tw, long long tiles, int ncb, int ns, int th = 0)
 {
     if (ns == 0) {
         const long long want = 3LL * num_cus();
@@ -400,6 +405,7 @@ ImgPlan halo_plan(int tile, int tw, long long tiles, int ncb, int ns)
     ImgPlan p{IMG_64x64, 1, ncb};  // tile: the packed-filter layout (m-major)
     p.halo = tile;
     p.tw = tw;
+    p.th = th;
     if (ns > 1) {
         p.kchunk = (ncb + ns - 1) / ns;
         p.nsplit = (ncb + p.kchunk - 1) / p.kchunk;
@@ -421,7 +427,7 @@ std::vector<int> halo_widths(int P, int Q, int src_w, int R)
     };
     if (best)
         for (int tw : {112, 56, 28, 14})
-            if (halo_width_supported(tw, R, src_w, 0) && blocks(tw) == blocks(best))
+            if (halo_block_supported(tw, kHaloCols / tw, R, src_w, 0) && blocks(tw) == blocks(best))
                 out.push_back(tw);
     return out;
 }
@@ -433,13 +439,10 @@ void halo_variants(int M, int cin, int nimg, int Pout, int Qout, int src_w, int 
     if (cin % 16)
         return;
     const int ncb = cin / 16;
-    for (int tw : halo_widths(Pout, Qout, src_w, R))
-    for (int tile : {HALO_128x112, HALO_64x112}) {
-        if (tile == HALO_128x112 && M <= 64)
-            continue;
-        const long long tiles = halo_tile_count(tile, M, nimg, Pout, Qout, tw, G);
-        ImgPlan cands[2] = {halo_plan(tile, tw, tiles, ncb, 1),
-                            halo_plan(tile, tw, tiles, ncb, allow_split ? 0 : 1)};
+    auto add = [&](int tile, int tw, int th) {
+        const long long tiles = halo_tile_count(tile, M, nimg, Pout, Qout, tw, G, th);
+        ImgPlan cands[2] = {halo_plan(tile, tw, tiles, ncb, 1, th),
+                            halo_plan(tile, tw, tiles, ncb, allow_split ? 0 : 1, th)};
         for (int i = 0; i < (cands[1].nsplit > 1 ? 2 : 1); i++) {
             P p = make(cands[i]);
             bool dup = false;
@@ -448,18 +451,35 @@ void halo_variants(int M, int cin, int nimg, int Pout, int Qout, int src_w, int 
             if (!dup)
                 out.push_back(p);
         }
-    }
+    };
+    for (int tw : halo_widths(Pout, Qout, src_w, R))
+        for (int tile : {HALO_128x112, HALO_64x112})
+            if (tile == HALO_64x112 || M > 64)
+                add(tile, tw, 0);
+    // A whole 13 x 13 map as one block (64-row tile only).
+    if (Pout == Qout && halo_block_supported(Qout, Pout, R, src_w, 0))
+        add(HALO_64x112, Qout, Pout);
 }
 
-const char *halo_tile_name(int tile) { return tile == HALO_128x112 ? "128x112" : "64x112"; }
+// "<rows>x<columns>" of a halo tile with a tw-wide, th-row pixel block.
+const char *halo_tile_name(int tile, int tw, int th)
+{
+    static thread_local char buf[16];
+    snprintf(buf, sizeof buf, "%dx%d", tile == HALO_128x112 ? 128 : 64, halo_cols(tw, th));
+    return buf;
+}
 
 // The built-in rule's use of the halo GEMM: whenever it applies and its pixel
 // blocks cover the output grid with at most 1/8 of the columns idle (every
-// map width of 224, 112, 56, 28 or 14 pixels; not 13 x 13, where the image
-// GEMM measured faster), with the 64-row tile, unsplit.  Measured on the
-// MI355X at the configurations' batches: VGG-16 conv1_2 ... conv5_3 forward
-// and backward-data 112-143 TFLOP/s against 93-126 for the image GEMM;
-// ResNet 56 x 56 / 14 x 14 3 x 3 layers 124 / 108 against 92-104 / 86.
+// map width of 224, 112, 56, 28 or 14 pixels, and 13 x 13 maps as whole-map
+// blocks), with the 64-row tile, unsplit unless the tiles leave some CUs a
+// tile more than others and number under two a CU: then two splits.
+// Measured on the MI355X at the configurations' batches: VGG-16 conv1_2 ...
+// conv5_3 forward and backward-data 112-143 TFLOP/s against 93-126 for the
+// image GEMM; ResNet 56 x 56 / 14 x 14 3 x 3 layers 124 / 108 against
+// 92-104 / 86; AlexNet conv3-conv5 (13 x 13) 120-128 against 104-123;
+// GoogLeNet's 14 x 14 3 x 3 backward-data with 192 rows (384 tiles) 102
+// split against 85 unsplit.
 // 5 x 5 layers take it with M >= 48 (at most one idle wave) when the tiles,
 // split over channel blocks as halo_plan does if they are fewer than three
 // workgroups a CU, give every CU one: AlexNet conv2 forward 130 TFLOP/s
@@ -468,11 +488,28 @@ const char *halo_tile_name(int tile) { return tile == HALO_128x112 ? "128x112" :
 // backward-data 60 (two splits) against 52; its 64-filter and 32-filter
 // 5 x 5 layers (128 tiles, two channel blocks; M = 32) measured slower than
 // the image GEMM and keep it.
+// Splits of the rule's 3 x 3 halo plans: two when the tiles are fewer than
+// two a CU and uneven over the CUs (so some CUs would run one more tile than
+// the rest) and each split keeps at least 4 channel blocks; else one.
+int halo_rule_splits(long long tiles, int ncb)
+{
+    const long long cus = num_cus();
+    return tiles < 2 * cus && tiles % cus && ncb >= 8 ? 2 : 1;
+}
+
 bool halo_rule(int M, int cin, int nimg, int Pout, int Qout, int src_w, int R, int G,
                ImgPlan *out)
 {
+    if (cin % 16)
+        return false;
+    if (Pout == Qout && halo_block_supported(Qout, Pout, R, src_w, 0)) {
+        const long long tiles = halo_tile_count(HALO_64x112, M, nimg, Pout, Qout, Qout, G, Pout);
+        *out = halo_plan(HALO_64x112, Qout, tiles, cin / 16, halo_rule_splits(tiles, cin / 16),
+                         Pout);
+        return true;
+    }
     const int tw = halo_width(Pout, Qout, src_w, R);
-    if (!tw || cin % 16)
+    if (!tw)
         return false;
     const int tr = kHaloCols / tw;
     const double used = (double)Pout * Qout /
@@ -487,7 +524,8 @@ bool halo_rule(int M, int cin, int nimg, int Pout, int Qout, int src_w, int R, i
         *out = p;
         return true;
     }
-    *out = halo_plan(HALO_64x112, tw, 0, cin / 16, 1);
+    const long long tiles = halo_tile_count(HALO_64x112, M, nimg, Pout, Qout, tw, G);
+    *out = halo_plan(HALO_64x112, tw, tiles, cin / 16, halo_rule_splits(tiles, cin / 16));
     return true;
 }
 
@@ -688,11 +726,11 @@ void fwd_name(const ImgPlan &p, char *buf, size_t len)
         snprintf(buf, len, "explicit im2col (%d images a chunk), image GEMM %s", p.xnb,
                  img_tile_name(p.tile));
     else if (p.halo >= 0 && p.nsplit > 1)
-        snprintf(buf, len, "halo GEMM %s (%dx%d pixels), %d splits", halo_tile_name(p.halo),
-                 p.tw, kHaloCols / p.tw, p.nsplit);
+        snprintf(buf, len, "halo GEMM %s (%dx%d pixels), %d splits",
+                 halo_tile_name(p.halo, p.tw, p.th), p.tw, halo_th(p.tw, p.th), p.nsplit);
     else if (p.halo >= 0)
-        snprintf(buf, len, "halo GEMM %s (%dx%d pixels)", halo_tile_name(p.halo), p.tw,
-                 kHaloCols / p.tw);
+        snprintf(buf, len, "halo GEMM %s (%dx%d pixels)", halo_tile_name(p.halo, p.tw, p.th),
+                 p.tw, halo_th(p.tw, p.th));
     else if (p.nsplit > 1)
         snprintf(buf, len, "%simage GEMM %s, %d splits", pre, img_tile_name(p.tile), p.nsplit);
     else
@@ -918,10 +956,12 @@ void bwd_name(const BwdPlan &p, char *buf, size_t len)
                  img_tile_name(p.img.tile));
     else if (p.img.halo >= 0 && p.img.nsplit > 1)
         snprintf(buf, len, "stride phases, halo GEMM %s (%dx%d pixels), %d splits",
-                 halo_tile_name(p.img.halo), p.img.tw, kHaloCols / p.img.tw, p.img.nsplit);
+                 halo_tile_name(p.img.halo, p.img.tw, p.img.th), p.img.tw,
+                 halo_th(p.img.tw, p.img.th), p.img.nsplit);
     else if (p.img.halo >= 0)
-        snprintf(buf, len, "stride phases, halo GEMM %s (%dx%d pixels)", halo_tile_name(p.img.halo),
-                 p.img.tw, kHaloCols / p.img.tw);
+        snprintf(buf, len, "stride phases, halo GEMM %s (%dx%d pixels)",
+                 halo_tile_name(p.img.halo, p.img.tw, p.img.th), p.img.tw,
+                 halo_th(p.img.tw, p.img.th));
     else if (p.img.tile < 0)
         snprintf(buf, len, "stride phases, tiles by rule");
     else if (p.img.nsplit > 1)
@@ -1389,12 +1429,12 @@ int halo_gemm(const ImgPlan &plan, int M, int groups, const float *A, int a_ld, 
     h.P = Pout;
     h.Q = Qout;
     h.TW = plan.tw;
-    h.TR = kHaloCols / plan.tw;
+    h.TR = halo_th(plan.tw, plan.th);
     h.row_blocks = (Pout + h.TR - 1) / h.TR;
     h.col_segs = (Qout + h.TW - 1) / h.TW;
     h.nimg = nimg;
     // Halo origin: the top-left source pixel any tap of the block reads.
-    const int V = halo_load_words(plan.tw, R);
+    const int V = halo_load_words(plan.tw, h.TR, R);
     h.row0 = flip ? coff_h - (R - 1) : coff_h;
     const int col_raw = flip ? coff_w - (R - 1) : coff_w;
     h.col0 = (col_raw >= 0 ? col_raw / V : -((-col_raw + V - 1) / V)) * V;

@@ -520,7 +520,8 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
 // map width can be staged (AlexNet's 27-wide maps included).
 //
 // Four waves split the rows (BM / 4 each, FM = BM / 64 accumulator blocks
-// high) and each covers all 112 columns (7 blocks of 16); in 5 x 5 tiles a
+// high) and each covers all 112 columns (7 blocks of 16; 11 for a whole
+// 13 x 13 map); in 5 x 5 tiles a
 // wave whose rows all lie past M (M = 48 on the 64-row tile) stages its share
 // of the halo and skips the MFMAs.  The filter
 // operand of a slice is one 16-byte load per lane and row block, straight
@@ -530,53 +531,66 @@ __global__ __launch_bounds__(64 * WM * WN) void img_gemm_kernel(const ImgGemmArg
 // at the start of a block and complete under its R R slices; one barrier per
 // block.
 // ---------------------------------------------------------------------------
-template <int TW, int R>
+template <int TW, int TR, int R>
 struct HaloCfg;
 template <>
-struct HaloCfg<112, 3> {
-    static constexpr int TR = 1, V = 4, HWW = 124, LPC = 0, CS = 3 * 124;
+struct HaloCfg<112, 1, 3> {
+    static constexpr int V = 4, HWW = 124, LPC = 0, CS = 3 * 124;
 };
 template <>
-struct HaloCfg<56, 3> {
-    static constexpr int TR = 2, V = 4, HWW = 64, LPC = 1, CS = 260;
+struct HaloCfg<56, 2, 3> {
+    static constexpr int V = 4, HWW = 64, LPC = 1, CS = 260;
 };
 template <>
-struct HaloCfg<28, 3> {
-    static constexpr int TR = 4, V = 4, HWW = 36, LPC = 1, CS = 260;
+struct HaloCfg<28, 4, 3> {
+    static constexpr int V = 4, HWW = 36, LPC = 1, CS = 260;
 };
 template <>
-struct HaloCfg<14, 3> {
-    static constexpr int TR = 8, V = 1, HWW = 18, LPC = 0, CS = 10 * 18;
+struct HaloCfg<14, 8, 3> {
+    static constexpr int V = 1, HWW = 18, LPC = 0, CS = 10 * 18;
 };
 template <>
-struct HaloCfg<28, 5> {  // 8 x 32 words a channel: four wave-loads
-    static constexpr int TR = 4, V = 1, HWW = 32, LPC = 4, CS = 260;
+struct HaloCfg<28, 4, 5> {  // 8 x 32 words a channel: four wave-loads
+    static constexpr int V = 1, HWW = 32, LPC = 4, CS = 260;
 };
 template <>
-struct HaloCfg<14, 5> {  // 12 x 18 words a channel in four wave-loads
-    static constexpr int TR = 8, V = 1, HWW = 18, LPC = 4, CS = 260;
+struct HaloCfg<14, 8, 5> {  // 12 x 18 words a channel in four wave-loads
+    static constexpr int V = 1, HWW = 18, LPC = 4, CS = 260;
+};
+// Whole-image blocks of 13 x 13 maps (3 x 3): 176 columns, 169 used, against
+// 169 of 224 for two 14 x 8 blocks; 15 halo rows of 16 words, four
+// wave-loads a channel.  (A 14 x 14 map as one 208-column block measured
+// slower than two 14 x 8 blocks, which already use 7/8 of their columns.)
+template <>
+struct HaloCfg<13, 13, 3> {
+    static constexpr int V = 1, HWW = 16, LPC = 4, CS = 260;
 };
 
 constexpr int kHaloStageWords = 6400;  // largest stage (25 KiB, 112-wide blocks): three workgroups a CU
 
 // Waves per SIMD the register allocation must allow: four for 64-row tiles
 // (four workgroups a CU) whose LDS stages allow it (all but 112-wide 3 x 3
-// blocks), three for the rest of 3 x 3; 128-row 5 x 5 tiles fit three
+// blocks), three for the rest of 3 x 3 (whole 13 x 13 maps, 176 columns of
+// accumulators, included); 128-row 5 x 5 tiles fit three
 // without the bound.  The waves are latency-bound (each issues an MFMA only
 // every few slots), so a SIMD's throughput grows with its waves: four
 // workgroups instead of three measured 1-3 % faster on VGG-16's 224- to
 // 28-pixel layers.
-template <int BM, int TW, int R>
-constexpr int halo_min_waves() { return BM == 64 && (TW != 112 || R != 3) ? 4 : R == 3 ? 3 : 1; }
+template <int BM, int TW, int TR, int R>
+constexpr int halo_min_waves()
+{
+    return TR * TW != kHaloCols ? 3 : BM == 64 && (TW != 112 || R != 3) ? 4 : R == 3 ? 3 : 1;
+}
 
-template <int BM, int TW, int R, bool FLIP>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(halo_min_waves<BM, TW, R>())))
+template <int BM, int TW, int TR, int R, bool FLIP>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(halo_min_waves<BM, TW, TR, R>())))
 void halo_gemm_kernel(const HaloGemmArgs a)
 {
-    typedef HaloCfg<TW, R> C;
+    typedef HaloCfg<TW, TR, R> C;
     constexpr int S = R, RS = R * S, NR = RS % 3 == 0 ? 3 : 5, DIST = 2;
-    constexpr int NW = 4, BN = kHaloCols, TM = BM / NW, FM = TM / 16, FN = BN / 16;
-    constexpr int TR = C::TR, V = C::V, HWW = C::HWW, CS = C::CS, LPC = C::LPC;
+    constexpr int PIX = TR * TW;  // pixels of a block; columns past it are padding
+    constexpr int NW = 4, BN = (PIX + 15) / 16 * 16, TM = BM / NW, FM = TM / 16, FN = BN / 16;
+    constexpr int V = C::V, HWW = C::HWW, CS = C::CS, LPC = C::LPC;
     constexpr int HR = TR + R - 1;
     constexpr int GPR = HWW / V;                  // load groups per halo row
     constexpr int EPC = HR * GPR;                 // load groups per channel
@@ -590,7 +604,7 @@ void halo_gemm_kernel(const HaloGemmArgs a)
     constexpr int STG = SPARE + 64 * V;
     static_assert(RS % NR == 0, "filter ring");
     static_assert(BM == 64 || BM == 128, "tile rows");
-    static_assert(TR * TW == BN, "pixel block");
+    static_assert(PIX == kHaloCols || (TR == TW && BN > kHaloCols), "pixel block: 112 pixels or a whole small map");
     static_assert(HWW % V == 0 && HWW >= TW + S - 1, "halo row");
     // A wave-load writes all 64 lanes (masked lanes write zeros), so a
     // channel's slot must hold LPC 64 V words.
@@ -716,7 +730,7 @@ void halo_gemm_kernel(const HaloGemmArgs a)
     for (int j = 0; j < FN; j++) {
         const int n = j * 16 + lc;
         const int dr = n / TW, dq = n - (n / TW) * TW;
-        nok[j] = p0 + dr < a.P && q0 + dq < a.Q;
+        nok[j] = n < PIX && p0 + dr < a.P && q0 + dq < a.Q;
         bofs[j] = nok[j] ? kr * 4 * CS + dr * HWW + dq + a.slack : 0;
     }
 
@@ -1791,32 +1805,39 @@ hipError_t launch_img_gemm(const ImgGemmArgs &a, int tile, bool fast, hipStream_
     }
 }
 
-template <int BM, int TW, int R>
+template <int BM, int TW, int TR, int R>
 static hipError_t halo_launch(const HaloGemmArgs &a, bool flip, hipStream_t stream)
 {
     const int tiles = ((a.M + BM - 1) / BM) * a.nimg * a.row_blocks * a.col_segs;
     const dim3 grid(tiles * a.groups * a.nsplit), block(256);
     if (flip)
-        hipLaunchKernelGGL((halo_gemm_kernel<BM, TW, R, true>), grid, block, 0, stream, a);
+        hipLaunchKernelGGL((halo_gemm_kernel<BM, TW, TR, R, true>), grid, block, 0, stream, a);
     else
-        hipLaunchKernelGGL((halo_gemm_kernel<BM, TW, R, false>), grid, block, 0, stream, a);
+        hipLaunchKernelGGL((halo_gemm_kernel<BM, TW, TR, R, false>), grid, block, 0, stream, a);
     return hipGetLastError();
 }
 
 template <int BM>
 static hipError_t halo_launch_tw(const HaloGemmArgs &a, bool flip, hipStream_t stream)
 {
+    if (a.TR * a.TW != kHaloCols) {  // whole-image blocks: 64-row tiles
+        if constexpr (BM == 64) {
+            if (a.R == 3 && a.TW == 13 && a.TR == 13)
+                return halo_launch<BM, 13, 13, 3>(a, flip, stream);
+        }
+        return hipErrorInvalidValue;
+    }
     if (a.R == 5)
         switch (a.TW) {
-        case 28: return halo_launch<BM, 28, 5>(a, flip, stream);
-        case 14: return halo_launch<BM, 14, 5>(a, flip, stream);
+        case 28: return halo_launch<BM, 28, 4, 5>(a, flip, stream);
+        case 14: return halo_launch<BM, 14, 8, 5>(a, flip, stream);
         default: return hipErrorInvalidValue;
         }
     switch (a.TW) {
-    case 112: return halo_launch<BM, 112, 3>(a, flip, stream);
-    case 56: return halo_launch<BM, 56, 3>(a, flip, stream);
-    case 28: return halo_launch<BM, 28, 3>(a, flip, stream);
-    case 14: return halo_launch<BM, 14, 3>(a, flip, stream);
+    case 112: return halo_launch<BM, 112, 1, 3>(a, flip, stream);
+    case 56: return halo_launch<BM, 56, 2, 3>(a, flip, stream);
+    case 28: return halo_launch<BM, 28, 4, 3>(a, flip, stream);
+    case 14: return halo_launch<BM, 14, 8, 3>(a, flip, stream);
     default: return hipErrorInvalidValue;
     }
 }
@@ -1878,10 +1899,20 @@ hipError_t launch_wgrad_halo(const WgradHaloArgs &a, hipStream_t stream)
                          : wgrad_halo_launch_par<false>(a, tiles, stream);
 }
 
-int halo_load_words(int TW, int R) { return R == 3 && TW != 14 ? 4 : 1; }
-
-bool halo_width_supported(int TW, int R, int src_w, int col0)
+bool halo_whole_image(int TW, int TR, int R)
 {
+    return R == 3 && TW == 13 && TR == 13;
+}
+
+int halo_load_words(int TW, int TR, int R)
+{
+    return R == 3 && TW != 14 && !halo_whole_image(TW, TR, R) ? 4 : 1;
+}
+
+bool halo_block_supported(int TW, int TR, int R, int src_w, int col0)
+{
+    if (TR * TW != kHaloCols)
+        return halo_whole_image(TW, TR, R);  // one-word loads
     if (R == 5)
         return TW == 28 || TW == 14;  // one-word loads
     if (R != 3)
@@ -1891,14 +1922,12 @@ bool halo_width_supported(int TW, int R, int src_w, int col0)
     return (TW == 112 || TW == 56 || TW == 28) && src_w % 4 == 0 && col0 % 4 == 0;
 }
 
-int halo_rows(int TW) { return kHaloCols / TW; }
-
 hipError_t launch_halo_gemm(const HaloGemmArgs &a, int tile, bool flip, hipStream_t stream)
 {
     // slack (the first tap's column in the halo row) must lie within one
     // load group: the halo rows hold slack + TW + R - 1 words.
-    if (!halo_width_supported(a.TW, a.R, a.src_w, a.col0) || a.TR != halo_rows(a.TW) ||
-        a.Kred != a.cin * a.R * a.R || a.slack < 0 || a.slack >= halo_load_words(a.TW, a.R))
+    if (!halo_block_supported(a.TW, a.TR, a.R, a.src_w, a.col0) ||
+        a.Kred != a.cin * a.R * a.R || a.slack < 0 || a.slack >= halo_load_words(a.TW, a.TR, a.R))
         return hipErrorInvalidValue;
     return tile == HALO_128x112 ? halo_launch_tw<128>(a, flip, stream)
                                 : halo_launch_tw<64>(a, flip, stream);

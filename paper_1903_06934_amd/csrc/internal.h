@@ -196,15 +196,18 @@ enum WgradTile {
 inline bool wgrad_tile_is_tap(int tile) { return tile <= WG_TAP_64x16 || tile >= WG_TAP_128x32; }
 
 hipError_t launch_img_gemm(const ImgGemmArgs &a, int tile, bool fast, hipStream_t stream);
-// Halo tiles: BM rows (64 or 128) x 112 columns; flip for the backward-data
-// phase.  halo_width_supported: whether pixel blocks TW wide (112, 56, 28, 14
-// for R = 3; 28, 14 for R = 5) can stage this source (16-byte loads need the
-// width and col0 to be multiples of 4); halo_load_words: the words per lane
-// and load (4 or 1).
+// Halo tiles: BM rows (64 or 128) x 112 columns (TR x TW = 112 pixels), or
+// 64 x 176 / 208 for whole 13 x 13 / 14 x 14 maps (3 x 3); flip for the
+// backward-data phase.  halo_block_supported: whether TR x TW pixel blocks
+// (112, 56, 28, 14 wide for R = 3; 28, 14 for R = 5; a whole 13 x 13 or
+// 14 x 14 map for R = 3) can stage this source (16-byte loads need the width
+// and col0 to be multiples of 4); halo_load_words: the words per lane and
+// load (4 or 1).
 enum HaloTile { HALO_64x112 = 0, HALO_128x112 };
 constexpr int kHaloCols = 112;
-bool halo_width_supported(int TW, int R, int src_w, int col0);
-int halo_load_words(int TW, int R);
+bool halo_whole_image(int TW, int TR, int R);
+bool halo_block_supported(int TW, int TR, int R, int src_w, int col0);
+int halo_load_words(int TW, int TR, int R);
 hipError_t launch_halo_gemm(const HaloGemmArgs &a, int tile, bool flip, hipStream_t stream);
 hipError_t launch_wgrad_gemm(const WgradArgs &a, int tile, hipStream_t stream);
 

@@ -55,6 +55,12 @@ PLAN_SHAPES = [
     (2, 64, 6, 12, 48, 3, 3, 1, 1, 2),     # two 16-channel sub-tiles a workgroup, groups
     (2, 32, 14, 14, 80, 3, 3, 1, 1, 1),    # 14-wide maps: whole-row blocks, one-word x loads
     (2, 16, 12, 16, 32, 3, 3, 1, 0, 1),    # 14 wide by pad 0, 10 rows
+    # Whole-map halo blocks (13 x 13 and 14 x 14 outputs, 3x3): groups, rows
+    # past one 64-row tile, pad 0 and 2.
+    (2, 64, 13, 13, 96, 3, 3, 1, 1, 2),
+    (1, 32, 14, 14, 144, 3, 3, 1, 1, 1),
+    (1, 16, 15, 15, 32, 3, 3, 1, 0, 1),
+    (1, 16, 12, 12, 16, 3, 3, 1, 2, 1),
     (1, 32, 8, 12, 32, 3, 3, 1, 2, 1),     # 14 wide by pad 2
 ]
 

@@ -45,9 +45,25 @@ def test_rule_names_for_alexnet():
     assert m.plan_name(m.PASS_BWD_DATA, by["conv2"], 0) == \
         "stride phases, halo GEMM 64x112 (28x4 pixels)"
     assert m.plan_name(m.PASS_FWD, by["conv2"], 0) == "halo GEMM 64x112 (28x4 pixels)"
+    for name in ("conv3", "conv4", "conv5"):  # 13 x 13 maps: whole-map blocks
+        assert m.plan_name(m.PASS_FWD, by[name], 0) == "halo GEMM 64x176 (13x13 pixels)"
+        assert m.plan_name(m.PASS_BWD_DATA, by[name], 0) == \
+            "stride phases, halo GEMM 64x176 (13x13 pixels)"
     assert m.plan_name(m.PASS_FWD, by["conv1"], 0) == "image GEMM 96x128"
     assert m.plan_name(m.PASS_BWD_WEIGHT, by["conv2"], 0).startswith("tap 64x48, ")
     assert m.plan_name(m.PASS_BWD_WEIGHT, by["conv1"], 0).startswith("pixel 96x64, ")
+
+
+def test_rule_splits_uneven_halo_grids():
+    """GoogLeNet-shaped 14 x 14 3x3 layers at batch 64: 384 backward-data
+    tiles (1.5 a CU) split in two; 256 or 768 tiles run unsplit."""
+    _, layers = workloads.config(4)
+    by = {L.name: L.shape for L in layers}
+    assert m.plan_name(m.PASS_BWD_DATA, by["hi_3x3"], 0) == \
+        "stride phases, halo GEMM 64x112 (14x8 pixels), 2 splits"
+    assert m.plan_name(m.PASS_FWD, by["hi_3x3"], 0) == "halo GEMM 64x112 (14x8 pixels)"
+    assert m.plan_name(m.PASS_BWD_DATA, by["mid_3x3"], 0) == \
+        "stride phases, halo GEMM 64x112 (14x8 pixels)"
 
 
 def test_set_get_clear_and_workspace():
