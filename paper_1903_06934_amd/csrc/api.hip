@@ -1120,9 +1120,9 @@ int wgrad_halo_width(const Geom &g)
     return best;
 }
 
-// Splits over the pixel blocks so that as many workgroups run as fit on the
-// CUs at once (three per CU with one 16-channel sub-tile, two with two or
-// with eight single-stage waves, one double-buffered), times 2^scale, each
+// Splits over the pixel blocks so that at most as many workgroups run as fit
+// on the CUs at once (three per CU with one 16-channel sub-tile, two with two
+// or with eight single-stage waves, one double-buffered), times 2^scale, each
 // split at least 4 blocks.
 WgradPlan wgrad_halo_plan(const Geom &g, int tw, int scale = 0, int ct = 1, int db = 0)
 {
@@ -1137,7 +1137,7 @@ WgradPlan wgrad_halo_plan(const Geom &g, int tw, int scale = 0, int ct = 1, int 
     const long long blocks = (long long)g.N * ((g.P + tr - 1) / tr) * ((g.Q + tw - 1) / tw);
     const long long tiles = (long long)((g.Kg + 63) / 64) * (g.Cg / (16 * ct)) * g.G;
     const long long resident = (db == 1 ? 1LL : ct == 1 ? 3LL : 2LL) * num_cus();
-    long long ns = (resident + tiles - 1) / tiles;
+    long long ns = resident / tiles;  // rounded down: no second, partial round of workgroups
     if (scale > 0)
         ns <<= scale;
     else if (scale < 0)
@@ -1278,8 +1278,7 @@ void wgrad_name(const WgradPlan &p, char *buf, size_t len)
     else if (p.halo_tw)
         snprintf(buf, len, "halo, 9 taps of 64x%d%s (%dx%d pixels), %d splits of %d blocks",
                  16 * p.halo_ct, p.halo_db == 1 ? " (8 waves, 2 stages)" : p.halo_db ? " (8 waves)" : "",
-                 p.halo_tw,
-                 kHaloCols / p.halo_tw, p.nsplit, p.chunk);
+                 p.halo_tw, kHaloCols / p.halo_tw, p.nsplit, p.chunk);
     else if (p.xnb > 0)
         snprintf(buf, len, "explicit im2col (%d images a chunk), %s, %d splits of %d pixels",
                  p.xnb, wgrad_tile_name(p.tile), p.nsplit, p.chunk);

@@ -152,7 +152,7 @@ struct WgradArgs {
 // Halo backward-weight for stride-1 3 x 3 layers (channels per group a
 // multiple of 16, dy rows a multiple of 4 wide): a workgroup computes all nine
 // taps of 64 filters x 16 CT input channels, its reduction running over TR x TW
-// pixel blocks of the images (TW = 112, 56 or 28, TR = 112 / TW; the same
+// pixel blocks of the images (TW = 112, 56, 28 or 14, TR = 112 / TW; the same
 // blocks as HaloGemmArgs).  Per block it stages the 64 dy rows of the block
 // (dy[img][g Kg + k][p0 .. p0 + TR - 1][q0 .. q0 + TW - 1]) and the x halo of
 // its 16 CT channels (rows p0 - pad .., columns q0 - pad ..) in LDS once, then
@@ -197,12 +197,11 @@ inline bool wgrad_tile_is_tap(int tile) { return tile <= WG_TAP_64x16 || tile >=
 
 hipError_t launch_img_gemm(const ImgGemmArgs &a, int tile, bool fast, hipStream_t stream);
 // Halo tiles: BM rows (64 or 128) x 112 columns (TR x TW = 112 pixels), or
-// 64 x 176 / 208 for whole 13 x 13 / 14 x 14 maps (3 x 3); flip for the
-// backward-data phase.  halo_block_supported: whether TR x TW pixel blocks
-// (112, 56, 28, 14 wide for R = 3; 28, 14 for R = 5; a whole 13 x 13 or
-// 14 x 14 map for R = 3) can stage this source (16-byte loads need the width
-// and col0 to be multiples of 4); halo_load_words: the words per lane and
-// load (4 or 1).
+// 64 x 176 for a whole 13 x 13 map (3 x 3); flip for the backward-data
+// phase.  halo_block_supported: whether TR x TW pixel blocks (112, 56, 28, 14
+// wide for R = 3; 28, 14 for R = 5; a whole 13 x 13 map for R = 3) can stage
+// this source (16-byte loads need the width and col0 to be multiples of 4);
+// halo_load_words: the words per lane and load (4 or 1).
 enum HaloTile { HALO_64x112 = 0, HALO_128x112 };
 constexpr int kHaloCols = 112;
 bool halo_whole_image(int TW, int TR, int R);

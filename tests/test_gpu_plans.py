@@ -55,9 +55,10 @@ PLAN_SHAPES = [
     (2, 64, 6, 12, 48, 3, 3, 1, 1, 2),     # two 16-channel sub-tiles a workgroup, groups
     (2, 32, 14, 14, 80, 3, 3, 1, 1, 1),    # 14-wide maps: whole-row blocks, one-word x loads
     (2, 16, 12, 16, 32, 3, 3, 1, 0, 1),    # 14 wide by pad 0, 10 rows
-    # Whole-map halo blocks (13 x 13 and 14 x 14 outputs, 3x3): groups, rows
-    # past one 64-row tile, pad 0 and 2.
+    # Whole-map halo blocks (13 x 13 outputs, 3x3; 14 x 14 ones keep the 14 x 8
+    # blocks): groups, rows past one 64-row tile, a batch of 12, pad 0 and 2.
     (2, 64, 13, 13, 96, 3, 3, 1, 1, 2),
+    (12, 32, 13, 13, 80, 3, 3, 1, 1, 1),
     (1, 32, 14, 14, 144, 3, 3, 1, 1, 1),
     (1, 16, 15, 15, 32, 3, 3, 1, 0, 1),
     (1, 16, 12, 12, 16, 3, 3, 1, 2, 1),
