@@ -92,6 +92,26 @@ def test_random_halo_shapes_every_candidate(shape):
     test_every_candidate_matches_oracle(shape)
 
 
+def _random_whole_map_shapes(count=4, seed=20261203):
+    """Seeded stride-1 3x3 shapes whose forward output is 13 x 13 (the
+    whole-map halo block): pads 0..2 (source 15 - 2 pad a side), one or two
+    groups, 16-48 channels and 16-96 filters a group."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(count):
+        G = int(rng.choice([1, 2]))
+        pad = int(rng.integers(0, 3))
+        H = 15 - 2 * pad
+        out.append((int(rng.integers(1, 4)), G * 16 * int(rng.integers(1, 4)), H, H,
+                    G * int(rng.choice([16, 32, 48, 64, 80, 96])), 3, 3, 1, pad, G))
+    return out
+
+
+@pytest.mark.parametrize("shape", _random_whole_map_shapes(), ids=lambda s: "x".join(map(str, s)))
+def test_random_whole_map_shapes_every_candidate(shape):
+    test_every_candidate_matches_oracle(shape)
+
+
 @pytest.fixture(autouse=True)
 def _clean():
     import paper_1903_06934_amd as m
