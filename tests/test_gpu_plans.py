@@ -59,6 +59,7 @@ PLAN_SHAPES = [
     # blocks): groups, rows past one 64-row tile, a batch of 12, pad 0 and 2.
     (2, 64, 13, 13, 96, 3, 3, 1, 1, 2),
     (12, 32, 13, 13, 80, 3, 3, 1, 1, 1),
+    (1, 128, 13, 13, 128, 3, 3, 1, 1, 1),  # 8 channel blocks: split whole-map plans
     (1, 32, 14, 14, 144, 3, 3, 1, 1, 1),
     (1, 16, 15, 15, 32, 3, 3, 1, 0, 1),
     (1, 16, 12, 12, 16, 3, 3, 1, 2, 1),
