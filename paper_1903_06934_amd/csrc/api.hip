@@ -311,6 +311,7 @@ struct ImgPlan {
     int halo = -1;             // halo GEMM tile (HaloTile), or -1; kchunk then counts
     int tw = 0;                // 16-channel blocks per split, tw the pixel-block width
     int th = 0;                // pixel-block rows: 0 for 112 / tw, else a whole th x tw map
+    int ks = 1;                // halo wave groups: 2 = eight waves over two halves of the blocks
 };
 
 // Rows and columns (pixels rounded up to 16) of a halo pixel block.
@@ -354,7 +355,7 @@ ImgPlan img_rule(int M, long long Ncol, int Kred, int G, bool allow_split)
 bool same_img(const ImgPlan &a, const ImgPlan &b)
 {
     return a.tile == b.tile && a.nsplit == b.nsplit && a.xnb == b.xnb && a.bt == b.bt &&
-           a.halo == b.halo && a.tw == b.tw && a.th == b.th;
+           a.halo == b.halo && a.tw == b.tw && a.th == b.th && a.ks == b.ks;
 }
 
 // ------------------------------------------------------------ halo plans
@@ -454,8 +455,22 @@ void halo_variants(int M, int cin, int nimg, int Pout, int Qout, int src_w, int 
     };
     for (int tw : halo_widths(Pout, Qout, src_w, R))
         for (int tile : {HALO_128x112, HALO_64x112})
-            if (tile == HALO_64x112 || M > 64)
+            if (tile == HALO_64x112 || M > 64) {
                 add(tile, tw, 0);
+                // Two wave groups where the tiles are at most two a CU (3 x 3,
+                // 56- to 14-wide blocks, an even number of channel blocks).
+                const long long tiles = halo_tile_count(tile, M, nimg, Pout, Qout, tw, G);
+                if (R == 3 && tw != 112 && ncb % 2 == 0 && tiles <= 2LL * num_cus()) {
+                    ImgPlan q = halo_plan(tile, tw, tiles, ncb, 1);
+                    q.ks = 2;
+                    P p = make(q);
+                    bool dup = false;
+                    for (const P &o : out)
+                        dup = dup || same_plan(p, o);
+                    if (!dup)
+                        out.push_back(p);
+                }
+            }
     // A whole 13 x 13 map as one block (64-row tile only).
     if (Pout == Qout && halo_block_supported(Qout, Pout, R, src_w, 0))
         add(HALO_64x112, Qout, Pout);
@@ -473,7 +488,10 @@ const char *halo_tile_name(int tile, int tw, int th)
 // blocks cover the output grid with at most 1/8 of the columns idle (every
 // map width of 224, 112, 56, 28 or 14 pixels, and 13 x 13 maps as whole-map
 // blocks), with the 64-row tile, unsplit unless the tiles leave some CUs a
-// tile more than others and number under two a CU: then two splits.
+// tile more than others and number under two a CU: then two splits; tiles
+// that fill one or two slots of every CU evenly run two wave groups (VGG-16
+// conv5_x at batch 32, 512 tiles: 0.258 against 0.272 ms forward; ResNet
+// s14_3x3 and GoogLeNet mid_3x3 backward-data 2-4 % faster).
 // Measured on the MI355X at the configurations' batches: VGG-16 conv1_2 ...
 // conv5_3 forward and backward-data 112-143 TFLOP/s against 93-126 for the
 // image GEMM; ResNet 56 x 56 / 14 x 14 3 x 3 layers 124 / 108 against
@@ -526,6 +544,10 @@ bool halo_rule(int M, int cin, int nimg, int Pout, int Qout, int src_w, int R, i
     }
     const long long tiles = halo_tile_count(HALO_64x112, M, nimg, Pout, Qout, tw, G);
     *out = halo_plan(HALO_64x112, tw, tiles, cin / 16, halo_rule_splits(tiles, cin / 16));
+    // Tiles that fill one or two slots of every CU evenly: two wave groups.
+    const long long cus = num_cus();
+    if (out->nsplit == 1 && tw != 112 && (cin / 16) % 2 == 0 && tiles <= 2 * cus && tiles % cus == 0)
+        out->ks = 2;
     return true;
 }
 
@@ -729,8 +751,8 @@ void fwd_name(const ImgPlan &p, char *buf, size_t len)
         snprintf(buf, len, "halo GEMM %s (%dx%d pixels), %d splits",
                  halo_tile_name(p.halo, p.tw, p.th), p.tw, halo_th(p.tw, p.th), p.nsplit);
     else if (p.halo >= 0)
-        snprintf(buf, len, "halo GEMM %s (%dx%d pixels)", halo_tile_name(p.halo, p.tw, p.th),
-                 p.tw, halo_th(p.tw, p.th));
+        snprintf(buf, len, "halo GEMM %s (%dx%d pixels)%s", halo_tile_name(p.halo, p.tw, p.th),
+                 p.tw, halo_th(p.tw, p.th), p.ks == 2 ? ", 8 waves" : "");
     else if (p.nsplit > 1)
         snprintf(buf, len, "%simage GEMM %s, %d splits", pre, img_tile_name(p.tile), p.nsplit);
     else
@@ -959,9 +981,9 @@ void bwd_name(const BwdPlan &p, char *buf, size_t len)
                  halo_tile_name(p.img.halo, p.img.tw, p.img.th), p.img.tw,
                  halo_th(p.img.tw, p.img.th), p.img.nsplit);
     else if (p.img.halo >= 0)
-        snprintf(buf, len, "stride phases, halo GEMM %s (%dx%d pixels)",
+        snprintf(buf, len, "stride phases, halo GEMM %s (%dx%d pixels)%s",
                  halo_tile_name(p.img.halo, p.img.tw, p.img.th), p.img.tw,
-                 halo_th(p.img.tw, p.img.th));
+                 halo_th(p.img.tw, p.img.th), p.img.ks == 2 ? ", 8 waves" : "");
     else if (p.img.tile < 0)
         snprintf(buf, len, "stride phases, tiles by rule");
     else if (p.img.nsplit > 1)
@@ -1446,6 +1468,7 @@ int halo_gemm(const ImgPlan &plan, int M, int groups, const float *A, int a_ld, 
     h.nsplit = plan.nsplit;
     h.cbchunk = plan.kchunk;
     h.split_stride = split_stride;
+    h.ks = plan.ks;
     return launch_status(launch_halo_gemm(h, plan.halo, flip, stream));
 }
 

@@ -576,14 +576,22 @@ constexpr int kHaloStageWords = 6400;  // largest stage (25 KiB, 112-wide blocks
 // every few slots), so a SIMD's throughput grows with its waves: four
 // workgroups instead of three measured 1-3 % faster on VGG-16's 224- to
 // 28-pixel layers.
-template <int BM, int TW, int TR, int R>
+//
+// KS = 2 (small grids): eight waves, two groups of four over the two halves of
+// the channel blocks, each group with its own two halo stages; the second
+// group's partial sums are added to the first's through LDS before the
+// epilogue.  This doubles the waves a SIMD holds where the tiles are too few to
+// fill the CU slots, without the partial-sum round trip through memory of a
+// split plan.
+template <int BM, int TW, int TR, int R, int KS = 1>
 constexpr int halo_min_waves()
 {
-    return TR * TW != kHaloCols ? 3 : BM == 64 && (TW != 112 || R != 3) ? 4 : R == 3 ? 3 : 1;
+    return KS == 2 ? (BM == 64 ? 4 : 2)
+           : TR * TW != kHaloCols ? 3 : BM == 64 && (TW != 112 || R != 3) ? 4 : R == 3 ? 3 : 1;
 }
 
-template <int BM, int TW, int TR, int R, bool FLIP>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(halo_min_waves<BM, TW, TR, R>())))
+template <int BM, int TW, int TR, int R, bool FLIP, int KS = 1>
+__global__ __launch_bounds__(256 * KS) __attribute__((amdgpu_waves_per_eu(halo_min_waves<BM, TW, TR, R, KS>())))
 void halo_gemm_kernel(const HaloGemmArgs a)
 {
     typedef HaloCfg<TW, TR, R> C;
@@ -611,11 +619,15 @@ void halo_gemm_kernel(const HaloGemmArgs a)
     static_assert(LPC ? (EPC <= 64 * LPC && CS >= 64 * V * LPC && (CS * 4) % 16 == 0)
                       : CS == HR * HWW, "channel stride");
     static_assert(SPARE + 64 * V <= STG && STG <= kHaloStageWords && STG % 4 == 0, "halo stage");
+    static_assert(KS == 1 || (KS == 2 && R == 3 && PIX == kHaloCols && TW != 112), "wave groups");
 
-    __shared__ __attribute__((aligned(16))) float H0[STG], H1[STG];
+    // Stages of wave group kh: H0[kh], H1[kh].
+    __shared__ __attribute__((aligned(16))) float H0[KS][STG], H1[KS][STG];
+    static_assert(KS == 1 || NW * 4 * 64 * 4 <= KS * STG, "partial sums of four column blocks fit H0");
 
     const int lane = threadIdx.x & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) & (NW - 1);
+    const int kh = KS == 2 ? __builtin_amdgcn_readfirstlane(threadIdx.x >> 8) : 0;
     const int mtiles = (a.M + BM - 1) / BM;
     const int per_img = a.row_blocks * a.col_segs;
     const int tiles = mtiles * a.nimg * per_img;
@@ -636,8 +648,12 @@ void halo_gemm_kernel(const HaloGemmArgs a)
     const int p0 = rb * TR, q0 = csg * TW;
     const int m0 = mt * BM;
     const int ncb = a.Kred / (16 * RS);
-    const int cb_beg = split * a.cbchunk;
-    const int cb_end = min(ncb, cb_beg + a.cbchunk);
+    // The split's channel blocks; with KS = 2 the group's half of them (the
+    // host makes their count even).
+    const int cb_lo = split * a.cbchunk;
+    const int cb_n = (min(ncb, cb_lo + a.cbchunk) - cb_lo) / KS;
+    const int cb_beg = cb_lo + kh * cb_n;
+    const int cb_end = cb_beg + cb_n;
     const int kr = lane >> 4, lc = lane & 15;
     // Wave-uniform: some row of this wave is real (checked for 5 x 5 only,
     // whose M = 48 backward-data phases leave a 64-row tile's last wave idle).
@@ -797,8 +813,9 @@ void halo_gemm_kernel(const HaloGemmArgs a)
         __asm__ volatile("" ::: "memory");
     };
 
+    float *const G0 = H0[kh], *const G1 = H1[kh];
     if (cb_beg < cb_end) {
-        issue_halo(cb_beg, H0);
+        issue_halo(cb_beg, G0);
 #pragma unroll
         for (int d = 0; d < DIST; d++)
             loadA(cb_beg * RS + d, ring[d]);
@@ -809,11 +826,45 @@ void halo_gemm_kernel(const HaloGemmArgs a)
     }
     int cb = cb_beg;
     for (; cb + 1 < cb_end; cb += 2) {
-        block(cb, H0, H1, true);
-        block(cb + 1, H1, H0, cb + 2 < cb_end);
+        block(cb, G0, G1, true);
+        block(cb + 1, G1, G0, cb + 2 < cb_end);
     }
     if (cb < cb_end)
-        block(cb, H0, H1, false);
+        block(cb, G0, G1, false);
+
+    if constexpr (KS == 2) {
+        // Group 1's sums into group 0's, four column blocks of one row block
+        // at a time through H0 (free: the last block ended with a barrier and
+        // staged nothing), in a fixed order (each group summed its own half
+        // of the channel blocks first).
+        f32x4 *const red = reinterpret_cast<f32x4 *>(&H0[0][0]);
+#pragma unroll
+        for (int i = 0; i < FM; i++)
+#pragma unroll
+            for (int j0 = 0; j0 < FN; j0 += 4) {
+                if (kh == 1) {
+#pragma unroll
+                    for (int j = j0; j < min(FN, j0 + 4); j++)
+                        red[(wrow * 4 + j - j0) * 64 + lane] = acc[i][j];
+                }
+                __asm__ volatile("" ::: "memory");
+                __builtin_amdgcn_s_barrier();
+                __asm__ volatile("" ::: "memory");
+                if (kh == 0) {
+#pragma unroll
+                    for (int j = j0; j < min(FN, j0 + 4); j++) {
+                        const f32x4 o = red[(wrow * 4 + j - j0) * 64 + lane];
+                        acc[i][j] = f32x4{acc[i][j][0] + o[0], acc[i][j][1] + o[1],
+                                          acc[i][j][2] + o[2], acc[i][j][3] + o[3]};
+                    }
+                }
+                __asm__ volatile("" ::: "memory");
+                __builtin_amdgcn_s_barrier();
+                __asm__ volatile("" ::: "memory");
+            }
+        if (kh == 1)
+            return;
+    }
 
     // Epilogue: + bias (unsplit), pixel (p0 + dr, q0 + dq) of the tile's image.
     float *const out = a.nsplit > 1 ? a.out + (long long)split * a.split_stride : a.out;
@@ -1810,6 +1861,17 @@ static hipError_t halo_launch(const HaloGemmArgs &a, bool flip, hipStream_t stre
 {
     const int tiles = ((a.M + BM - 1) / BM) * a.nimg * a.row_blocks * a.col_segs;
     const dim3 grid(tiles * a.groups * a.nsplit), block(256);
+    if constexpr (R == 3 && TR * TW == kHaloCols && TW != 112) {
+        if (a.ks == 2) {
+            if (flip)
+                hipLaunchKernelGGL((halo_gemm_kernel<BM, TW, TR, R, true, 2>), grid, dim3(512), 0, stream, a);
+            else
+                hipLaunchKernelGGL((halo_gemm_kernel<BM, TW, TR, R, false, 2>), grid, dim3(512), 0, stream, a);
+            return hipGetLastError();
+        }
+    }
+    if (a.ks != 1)
+        return hipErrorInvalidValue;
     if (flip)
         hipLaunchKernelGGL((halo_gemm_kernel<BM, TW, TR, R, true>), grid, block, 0, stream, a);
     else
@@ -1928,6 +1990,11 @@ hipError_t launch_halo_gemm(const HaloGemmArgs &a, int tile, bool flip, hipStrea
     // load group: the halo rows hold slack + TW + R - 1 words.
     if (!halo_block_supported(a.TW, a.TR, a.R, a.src_w, a.col0) ||
         a.Kred != a.cin * a.R * a.R || a.slack < 0 || a.slack >= halo_load_words(a.TW, a.TR, a.R))
+        return hipErrorInvalidValue;
+    // Two wave groups: 3 x 3 blocks 56, 28 or 14 wide, unsplit, an even number
+    // of channel blocks (one half per group).
+    if (a.ks == 2 && (a.R != 3 || a.TR * a.TW != kHaloCols || a.TW == 112 || a.nsplit != 1 ||
+                      (a.cin / 16) % 2 != 0 || a.cbchunk != a.cin / 16))
         return hipErrorInvalidValue;
     return tile == HALO_128x112 ? halo_launch_tw<128>(a, flip, stream)
                                 : halo_launch_tw<64>(a, flip, stream);

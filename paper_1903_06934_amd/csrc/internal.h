@@ -121,6 +121,9 @@ struct HaloGemmArgs {
     // out + s * split_stride.
     int nsplit, cbchunk;
     long long split_stride;
+    // Wave groups of a workgroup (halo_gemm_kernel KS): 1, or 2 (eight waves,
+    // each group of four over half the channel blocks; unsplit plans only).
+    int ks;
 };
 
 // ---------------------------------------------------------------------------

@@ -56,14 +56,28 @@ def test_rule_names_for_alexnet():
 
 def test_rule_splits_uneven_halo_grids():
     """GoogLeNet-shaped 14 x 14 3x3 layers at batch 64: 384 backward-data
-    tiles (1.5 a CU) split in two; 256 or 768 tiles run unsplit."""
+    tiles (1.5 a CU) split in two; 768 tiles run unsplit, 256 or 512 (one or
+    two a CU, evenly) with two wave groups."""
     _, layers = workloads.config(4)
     by = {L.name: L.shape for L in layers}
     assert m.plan_name(m.PASS_BWD_DATA, by["hi_3x3"], 0) == \
         "stride phases, halo GEMM 64x112 (14x8 pixels), 2 splits"
     assert m.plan_name(m.PASS_FWD, by["hi_3x3"], 0) == "halo GEMM 64x112 (14x8 pixels)"
     assert m.plan_name(m.PASS_BWD_DATA, by["mid_3x3"], 0) == \
-        "stride phases, halo GEMM 64x112 (14x8 pixels)"
+        "stride phases, halo GEMM 64x112 (14x8 pixels), 8 waves"
+    assert m.plan_name(m.PASS_FWD, by["mid_3x3"], 0) == "halo GEMM 64x112 (14x8 pixels), 8 waves"
+
+
+def test_rule_two_wave_groups_for_vgg_conv5():
+    """VGG-16-shaped conv5_x at batch 32 (512 tiles of 64 rows, two a CU):
+    two wave groups over the 32 channel blocks; conv4_x (1024 tiles) and the
+    224-wide conv1_2 keep four waves."""
+    _, layers = workloads.config(2)
+    by = {L.name: L.shape for L in layers}
+    for p in (m.PASS_FWD, m.PASS_BWD_DATA):
+        assert m.plan_name(p, by["conv5_1"], 0).endswith("(14x8 pixels), 8 waves")
+        assert "8 waves" not in m.plan_name(p, by["conv4_2"], 0)
+        assert "8 waves" not in m.plan_name(p, by["conv1_2"], 0)
 
 
 def test_set_get_clear_and_workspace():
