@@ -80,6 +80,20 @@ def test_rule_two_wave_groups_for_vgg_conv5():
         assert "8 waves" not in m.plan_name(p, by["conv1_2"], 0)
 
 
+def test_two_wave_group_candidates_need_even_channel_blocks():
+    """Two wave groups split a tile's channel blocks in halves: offered for
+    3x3 halo plans with an even number of 16-channel blocks and few tiles,
+    never with an odd number, for 112-wide blocks or with a split."""
+    even = (2, 64, 14, 14, 32, 3, 3, 1, 1, 1)   # 4 channel blocks
+    odd = (2, 48, 14, 14, 32, 3, 3, 1, 1, 1)    # 3 channel blocks
+    wide = (1, 64, 4, 112, 32, 3, 3, 1, 1, 1)   # 112-wide blocks
+    names = lambda sh: [m.plan_name(m.PASS_FWD, sh, i) for i in range(m.plan_count(m.PASS_FWD, sh))]
+    assert any(n.endswith("8 waves") for n in names(even))
+    assert not any("8 waves" in n for n in names(odd))
+    assert not any("112x1 pixels), 8 waves" in n for n in names(wide))
+    assert not any("splits, 8 waves" in n or ("8 waves" in n and "splits" in n) for n in names(even))
+
+
 def test_set_get_clear_and_workspace():
     shape = (8, 3, 67, 67, 32, 11, 11, 4, 2, 1)
     n = m.plan_count(m.PASS_BWD_DATA, shape)
