@@ -490,8 +490,8 @@ const char *halo_tile_name(int tile, int tw, int th)
 // blocks), with the 64-row tile, unsplit unless the tiles leave some CUs a
 // tile more than others and number under two a CU: then two splits; tiles
 // that fill one or two slots of every CU evenly run two wave groups (VGG-16
-// conv5_x at batch 32, 512 tiles: 0.258 against 0.272 ms forward; ResNet
-// s14_3x3 and GoogLeNet mid_3x3 backward-data 2-4 % faster).
+// conv5_x at batch 32, 512 tiles: 1-5 % faster forward, 0-3 % backward-data;
+// ResNet s14_3x3 and GoogLeNet mid_3x3 backward-data 2-4 %).
 // Measured on the MI355X at the configurations' batches: VGG-16 conv1_2 ...
 // conv5_3 forward and backward-data 112-143 TFLOP/s against 93-126 for the
 // image GEMM; ResNet 56 x 56 / 14 x 14 3 x 3 layers 124 / 108 against
