@@ -440,37 +440,33 @@ void halo_variants(int M, int cin, int nimg, int Pout, int Qout, int src_w, int 
     if (cin % 16)
         return;
     const int ncb = cin / 16;
+    auto push = [&](const ImgPlan &c) {
+        P p = make(c);
+        bool dup = false;
+        for (const P &q : out)
+            dup = dup || same_plan(p, q);
+        if (!dup)
+            out.push_back(p);
+    };
+    // Per tile and pixel block: unsplit, split (allow_split), and two wave
+    // groups where the tiles are at most two a CU (3 x 3, 56- to 14-wide
+    // blocks, an even number of channel blocks).
     auto add = [&](int tile, int tw, int th) {
         const long long tiles = halo_tile_count(tile, M, nimg, Pout, Qout, tw, G, th);
-        ImgPlan cands[2] = {halo_plan(tile, tw, tiles, ncb, 1, th),
-                            halo_plan(tile, tw, tiles, ncb, allow_split ? 0 : 1, th)};
-        for (int i = 0; i < (cands[1].nsplit > 1 ? 2 : 1); i++) {
-            P p = make(cands[i]);
-            bool dup = false;
-            for (const P &q : out)
-                dup = dup || same_plan(p, q);
-            if (!dup)
-                out.push_back(p);
+        push(halo_plan(tile, tw, tiles, ncb, 1, th));
+        const ImgPlan split = halo_plan(tile, tw, tiles, ncb, allow_split ? 0 : 1, th);
+        if (split.nsplit > 1)
+            push(split);
+        if (!th && R == 3 && tw != 112 && ncb % 2 == 0 && tiles <= 2LL * num_cus()) {
+            ImgPlan q = halo_plan(tile, tw, tiles, ncb, 1);
+            q.ks = 2;
+            push(q);
         }
     };
     for (int tw : halo_widths(Pout, Qout, src_w, R))
         for (int tile : {HALO_128x112, HALO_64x112})
-            if (tile == HALO_64x112 || M > 64) {
+            if (tile == HALO_64x112 || M > 64)
                 add(tile, tw, 0);
-                // Two wave groups where the tiles are at most two a CU (3 x 3,
-                // 56- to 14-wide blocks, an even number of channel blocks).
-                const long long tiles = halo_tile_count(tile, M, nimg, Pout, Qout, tw, G);
-                if (R == 3 && tw != 112 && ncb % 2 == 0 && tiles <= 2LL * num_cus()) {
-                    ImgPlan q = halo_plan(tile, tw, tiles, ncb, 1);
-                    q.ks = 2;
-                    P p = make(q);
-                    bool dup = false;
-                    for (const P &o : out)
-                        dup = dup || same_plan(p, o);
-                    if (!dup)
-                        out.push_back(p);
-                }
-            }
     // A whole 13 x 13 map as one block (64-row tile only).
     if (Pout == Qout && halo_block_supported(Qout, Pout, R, src_w, 0))
         add(HALO_64x112, Qout, Pout);
@@ -482,6 +478,15 @@ const char *halo_tile_name(int tile, int tw, int th)
     static thread_local char buf[16];
     snprintf(buf, sizeof buf, "%dx%d", tile == HALO_128x112 ? 128 : 64, halo_cols(tw, th));
     return buf;
+}
+
+// Splits of the rule's 3 x 3 halo plans: two when the tiles are fewer than
+// two a CU and uneven over the CUs (so some CUs would run one more tile than
+// the rest) and each split keeps at least 4 channel blocks; else one.
+int halo_rule_splits(long long tiles, int ncb)
+{
+    const long long cus = num_cus();
+    return tiles < 2 * cus && tiles % cus && ncb >= 8 ? 2 : 1;
 }
 
 // The built-in rule's use of the halo GEMM: whenever it applies and its pixel
@@ -506,15 +511,6 @@ const char *halo_tile_name(int tile, int tw, int th)
 // backward-data 60 (two splits) against 52; its 64-filter and 32-filter
 // 5 x 5 layers (128 tiles, two channel blocks; M = 32) measured slower than
 // the image GEMM and keep it.
-// Splits of the rule's 3 x 3 halo plans: two when the tiles are fewer than
-// two a CU and uneven over the CUs (so some CUs would run one more tile than
-// the rest) and each split keeps at least 4 channel blocks; else one.
-int halo_rule_splits(long long tiles, int ncb)
-{
-    const long long cus = num_cus();
-    return tiles < 2 * cus && tiles % cus && ncb >= 8 ? 2 : 1;
-}
-
 bool halo_rule(int M, int cin, int nimg, int Pout, int Qout, int src_w, int R, int G,
                ImgPlan *out)
 {
